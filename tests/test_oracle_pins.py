@@ -1,0 +1,619 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix (no GPU).
+
+Each test checks the oracle against a source other than itself: closed forms,
+torch autograd on the same network, central finite differences, Parareal written
+from its textbook definition, and the finite-step exactness and fixed-point
+properties of MGRIT (Section 3.1).
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from workloads import WORKLOADS, generate, random_state
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-300))
+
+
+def tiny_dense(seed=0, B=7, q=5, N=12, nf=3, nc=4, act="tanh", kscale=0.3):
+    r = np.random.default_rng(seed)
+    return dict(y=r.standard_normal((B, nf)), L_in=0.5 * r.standard_normal((q, nf)),
+                K=kscale * r.standard_normal((N, q, q)), b=0.1 * r.standard_normal((N, q)),
+                W=0.5 * r.standard_normal((nc, q)), mu=0.1 * r.standard_normal(nc),
+                onehot=np.eye(nc)[r.integers(0, nc, B)], h=0.7 / N * 4, act=act)
+
+
+def tiny_conv(seed=0, B=2, C=3, H=5, W=6, N=4, nc=3, act="tanh"):
+    r = np.random.default_rng(seed)
+    return dict(y=r.standard_normal((B, 1, H, W)), L_in=0.4 * r.standard_normal((C, 1, 3, 3)),
+                K=0.3 * r.standard_normal((N, C, C, 3, 3)), b=0.1 * r.standard_normal((N, C)),
+                W=0.3 * r.standard_normal((nc, C * H * W)), mu=0.1 * r.standard_normal(nc),
+                onehot=np.eye(nc)[r.integers(0, nc, B)], h=0.25, act=act)
+
+
+def full_objective(p, opening):
+    u0 = O.open_forward(p["y"], p["L_in"], p["act"], opening)
+    U = O.serial_forward(u0, p["K"], p["b"], p["h"], p["act"])
+    J, lamN, dW, dmu = O.loss_terminal(U[-1], p["W"], p["mu"], p["onehot"])
+    return J, U, lamN, dW, dmu
+
+
+def full_gradient(p, opening):
+    J, U, lamN, dW, dmu = full_objective(p, opening)
+    Lam = O.serial_adjoint(U, lamN, p["K"], p["b"], p["h"], p["act"])
+    dK, db = O.gradient(U, Lam, p["K"], p["b"], p["h"], p["act"])
+    dL = O.open_grad(p["y"], p["L_in"], Lam[0], p["act"], opening)
+    return dict(K=dK, b=db, W=dW, mu=dmu, L_in=dL), U, Lam
+
+
+# ---------------------------------------------------------------- activations
+
+def test_smoothrelu_golden_values():
+    tab = np.loadtxt(os.path.join(GOLDEN, "smoothrelu.txt"))
+    x, s, ds = tab[:, 0], tab[:, 1], tab[:, 2]
+    assert np.allclose(O.act(x, "smoothrelu"), s, rtol=0, atol=1e-15)
+    assert np.allclose(O.dact(x, "smoothrelu"), ds, rtol=0, atol=1e-15)
+
+
+def test_smoothrelu_is_c1():
+    # value and slope agree from both sides of the branch points +-0.1
+    for x0 in (-0.1, 0.1):
+        for e in (1e-7, 1e-9):
+            lo, hi = O.act(np.array([x0 - e, x0 + e]), "smoothrelu")
+            assert abs(hi - lo) < 3 * e
+            dlo, dhi = O.dact(np.array([x0 - e, x0 + e]), "smoothrelu")
+            assert abs(dhi - dlo) < 1e-5
+
+
+@pytest.mark.parametrize("kind", ["tanh", "relu", "smoothrelu", "identity"])
+def test_dact_matches_autograd(kind):
+    z = np.linspace(-2.0, 2.0, 401) + 1e-3  # stay off the ReLU kink at 0
+    t = torch.tensor(z, dtype=torch.float64, requires_grad=True)
+    if kind == "tanh":
+        y = torch.tanh(t)
+    elif kind == "relu":
+        y = torch.relu(t)
+    elif kind == "identity":
+        y = t * 1.0
+    else:
+        y = torch.where(t.abs() <= 0.1, 2.5 * t * t + 0.5 * t + 0.025, torch.relu(t))
+    y.sum().backward()
+    assert np.allclose(O.act(z, kind), y.detach().numpy(), rtol=0, atol=1e-15)
+    assert np.allclose(O.dact(z, kind), t.grad.numpy(), rtol=0, atol=1e-14)
+
+
+def test_relu_derivative_at_zero_is_zero():
+    assert O.dact(np.array([0.0]), "relu")[0] == 0.0
+
+
+# ---------------------------------------------------------------- convolution
+
+def test_conv_matches_torch_conv2d():
+    r = np.random.default_rng(3)
+    v = r.standard_normal((3, 4, 7, 9))
+    Kn = r.standard_normal((5, 4, 3, 3))
+    ref = torch.nn.functional.conv2d(torch.tensor(v), torch.tensor(Kn), padding=1).numpy()
+    assert rel(O.conv3x3(Kn, v), ref) < 1e-14
+
+
+def test_conv_transpose_and_weight_grad_match_autograd():
+    r = np.random.default_rng(4)
+    v = r.standard_normal((3, 4, 7, 9))
+    Kn = r.standard_normal((4, 4, 3, 3))
+    s = r.standard_normal((3, 4, 7, 9))
+    tv = torch.tensor(v, requires_grad=True)
+    tk = torch.tensor(Kn, requires_grad=True)
+    (torch.nn.functional.conv2d(tv, tk, padding=1) * torch.tensor(s)).sum().backward()
+    assert rel(O.conv3x3_transpose(Kn, s), tv.grad.numpy()) < 1e-14
+    assert rel(O.conv3x3_weight_grad(s, v), tk.grad.numpy()) < 1e-14
+
+
+# ---------------------------------------------------------------- serial closed forms
+
+@pytest.mark.parametrize("kind", ["tanh", "relu", "smoothrelu"])
+def test_serial_forward_zero_weights_closed_form(kind):
+    # K = 0: u^{n} = u^0 + n h sigma(b) when b is the same in every layer
+    r = np.random.default_rng(1)
+    N, B, q, h = 9, 4, 6, 0.3
+    u0 = r.standard_normal((B, q))
+    b1 = 0.5 * r.standard_normal(q)
+    U = O.serial_forward(u0, np.zeros((N, q, q)), np.tile(b1, (N, 1)), h, kind)
+    sig = {"tanh": np.tanh(b1), "relu": np.maximum(b1, 0),
+           "smoothrelu": np.where(np.abs(b1) <= 0.1, 2.5 * b1 ** 2 + 0.5 * b1 + 0.025, np.maximum(b1, 0))}[kind]
+    for n in range(N + 1):
+        assert rel(U[n], u0 + n * h * sig[None, :]) < 1e-14
+
+
+def test_serial_forward_linear_closed_form():
+    # identity activation, constant K, b = 0: u^N = (I + h K)^N u^0
+    r = np.random.default_rng(2)
+    N, B, q, h = 17, 5, 6, 0.1
+    u0 = r.standard_normal((B, q))
+    K1 = r.standard_normal((q, q))
+    U = O.serial_forward(u0, np.tile(K1, (N, 1, 1)), np.zeros((N, q)), h, "identity")
+    M = np.linalg.matrix_power(np.eye(q) + h * K1, N)
+    assert rel(U[N], u0 @ M.T) < 1e-13
+
+
+def test_serial_adjoint_linear_closed_form():
+    r = np.random.default_rng(5)
+    N, B, q, h = 11, 3, 4, 0.2
+    u0 = r.standard_normal((B, q))
+    K1 = r.standard_normal((q, q))
+    K = np.tile(K1, (N, 1, 1))
+    U = O.serial_forward(u0, K, np.zeros((N, q)), h, "identity")
+    lamN = r.standard_normal((B, q))
+    Lam = O.serial_adjoint(U, lamN, K, np.zeros((N, q)), h, "identity")
+    M = np.linalg.matrix_power(np.eye(q) + h * K1, N)
+    assert rel(Lam[0], lamN @ M) < 1e-13
+
+
+# ---------------------------------------------------------------- autograd / backprop
+
+@pytest.mark.parametrize("kind", ["tanh", "relu", "smoothrelu"])
+def test_adjoint_and_gradient_match_torch_autograd_dense(kind):
+    p = tiny_dense(seed=7, act=kind)
+    g, U, Lam = full_gradient(p, "dense_act")
+    t = {k: torch.tensor(p[k], requires_grad=True) for k in ("L_in", "K", "b", "W", "mu")}
+
+    def sig(z):
+        if kind == "tanh":
+            return torch.tanh(z)
+        if kind == "relu":
+            return torch.relu(z)
+        return torch.where(z.abs() <= 0.1, 2.5 * z * z + 0.5 * z + 0.025, torch.relu(z))
+
+    u = sig(torch.tensor(p["y"]) @ t["L_in"].T)
+    us = [u]
+    for n in range(p["K"].shape[0]):
+        u = u + p["h"] * sig(u @ t["K"][n].T + t["b"][n])
+        u.retain_grad()
+        us.append(u)
+    us[0].retain_grad()
+    z = u @ t["W"].T + t["mu"]
+    J = -(torch.tensor(p["onehot"]) * torch.log_softmax(z, dim=1)).sum() / z.shape[0]
+    J.backward()
+    for k in g:
+        assert rel(g[k], t[k].grad.numpy()) < 1e-12, k
+    for n in range(len(us)):
+        assert rel(Lam[n], us[n].grad.numpy()) < 1e-12, n
+
+
+def test_adjoint_and_gradient_match_torch_autograd_conv():
+    p = tiny_conv(seed=8, act="tanh")
+    g, U, Lam = full_gradient(p, "conv_act")
+    t = {k: torch.tensor(p[k], requires_grad=True) for k in ("L_in", "K", "b", "W", "mu")}
+    u = torch.tanh(torch.nn.functional.conv2d(torch.tensor(p["y"]), t["L_in"], padding=1))
+    for n in range(p["K"].shape[0]):
+        u = u + p["h"] * torch.tanh(torch.nn.functional.conv2d(u, t["K"][n], t["b"][n], padding=1))
+    z = u.reshape(u.shape[0], -1) @ t["W"].T + t["mu"]
+    J = -(torch.tensor(p["onehot"]) * torch.log_softmax(z, dim=1)).sum() / z.shape[0]
+    J.backward()
+    for k in g:
+        assert rel(g[k], t[k].grad.numpy()) < 1e-12, k
+
+
+# ---------------------------------------------------------------- finite differences
+
+def test_gradient_central_finite_differences_dense():
+    # config-1-sized tanh net (width 8, 32 layers, 2 input features, 5 classes)
+    wl = WORKLOADS[1].with_overrides(B=16)
+    d = generate(wl)
+    p = dict(y=d["y"].astype(np.float64), L_in=d["L_in"].astype(np.float64),
+             K=d["K"].astype(np.float64), b=0.05 * np.random.default_rng(9).standard_normal((wl.N, wl.q)),
+             W=d["W"].astype(np.float64), mu=0.1 * np.ones(wl.n_classes),
+             onehot=d["onehot"], h=wl.h, act="tanh")
+    g, _, _ = full_gradient(p, "dense_act")
+    eps = 1e-6
+    r = np.random.default_rng(10)
+
+    def J_at(pp):
+        return full_objective(pp, "dense_act")[0]
+
+    # random directional derivative over all parameters at once
+    dirs = {k: r.standard_normal(p[k].shape) for k in g}
+    pp = {**p, **{k: p[k] + eps * dirs[k] for k in g}}
+    pm = {**p, **{k: p[k] - eps * dirs[k] for k in g}}
+    fd = (J_at(pp) - J_at(pm)) / (2 * eps)
+    an = sum(float(np.sum(g[k] * dirs[k])) for k in g)
+    assert abs(fd - an) <= 1e-7 * abs(an)
+    # single entries of every parameter block
+    for k, idx in (("K", (3, 2, 5)), ("K", (31, 7, 0)), ("b", (0, 4)), ("b", (20, 1)),
+                   ("W", (2, 6)), ("mu", (4,)), ("L_in", (5, 1))):
+        e = np.zeros_like(p[k])
+        e[idx] = eps
+        fd = (J_at({**p, k: p[k] + e}) - J_at({**p, k: p[k] - e})) / (2 * eps)
+        assert abs(fd - g[k][idx]) <= 1e-7 * max(abs(g[k][idx]), 1e-3), (k, idx, fd, g[k][idx])
+
+
+def test_gradient_central_finite_differences_conv():
+    p = tiny_conv(seed=11, act="tanh")
+    g, _, _ = full_gradient(p, "conv_act")
+    eps = 1e-6
+    r = np.random.default_rng(12)
+    dirs = {k: r.standard_normal(p[k].shape) for k in g}
+    Jp = full_objective({**p, **{k: p[k] + eps * dirs[k] for k in g}}, "conv_act")[0]
+    Jm = full_objective({**p, **{k: p[k] - eps * dirs[k] for k in g}}, "conv_act")[0]
+    an = sum(float(np.sum(g[k] * dirs[k])) for k in g)
+    assert abs((Jp - Jm) / (2 * eps) - an) <= 1e-7 * abs(an)
+
+
+# ---------------------------------------------------------------- residual norms
+
+def test_residual_norm_of_serial_solution_is_zero():
+    p = tiny_dense(seed=13)
+    U = O.serial_forward(np.random.default_rng(0).standard_normal((7, 5)), p["K"], p["b"], p["h"], "tanh")
+    assert O.residual_norm_state(U, p["K"], p["b"], p["h"], "tanh") == 0.0
+    Lam = O.serial_adjoint(U, np.ones((7, 5)), p["K"], p["b"], p["h"], "tanh")
+    assert O.residual_norm_adjoint(U, Lam, p["K"], p["b"], p["h"], "tanh") == 0.0
+
+
+def test_residual_norm_single_perturbation_closed_form():
+    # K = 0: a perturbation delta at one interior point gives rho = sqrt(2) ||delta||
+    r = np.random.default_rng(14)
+    N, B, q, h = 10, 3, 4, 0.3
+    K = np.zeros((N, q, q))
+    b = np.tile(r.standard_normal(q), (N, 1))
+    U = O.serial_forward(r.standard_normal((B, q)), K, b, h, "tanh")
+    delta = r.standard_normal((B, q))
+    U2 = U.copy()
+    U2[4] += delta
+    rho = O.residual_norm_state(U2, K, b, h, "tanh")
+    assert abs(rho - np.sqrt(2) * np.linalg.norm(delta)) < 1e-13 * rho
+    U3 = U.copy()
+    U3[N] += delta  # last point enters one residual row only
+    assert abs(O.residual_norm_state(U3, K, b, h, "tanh") - np.linalg.norm(delta)) < 1e-12
+
+
+# ---------------------------------------------------------------- MGRIT
+
+def _mgrit_case(seed=20, N=32, B=6, q=5, act="tanh", kscale=0.4):
+    r = np.random.default_rng(seed)
+    K = kscale * r.standard_normal((N, q, q))
+    b = 0.2 * r.standard_normal((N, q))
+    u0 = r.standard_normal((B, q))
+    return K, b, u0, 5.0 / N
+
+
+@pytest.mark.parametrize("relax,gain", [("F", 1), ("FCF", 2)])
+def test_two_level_finite_step_exactness_forward(relax, gain):
+    # two-level F: after m iterations points n <= (m+1)c-1 are exact; FCF: n <= (2m+1)c-1
+    K, b, u0, h = _mgrit_case()
+    N, c = K.shape[0], 4
+    S = O.serial_forward(u0, K, b, h, "tanh")
+    U = np.zeros_like(S)
+    U[0] = u0
+    full = N // c if relax == "F" else -(-N // (2 * c))
+    for m in range(1, full + 1):
+        Um, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=c, max_levels=2, relax=relax, max_iter=m)
+        exact = min((gain * m + 1) * c - 1, N)
+        err = np.abs(Um - S).reshape(N + 1, -1).max(axis=1)
+        assert err[:exact + 1].max() < 1e-14, (m, exact)
+        if exact < N:
+            assert err[exact + 1:].max() > 1e-8  # not exact beyond the front
+    assert np.abs(Um - S).max() < 1e-14
+
+
+@pytest.mark.parametrize("relax,gain", [("F", 1), ("FCF", 2)])
+def test_two_level_finite_step_exactness_adjoint(relax, gain):
+    K, b, u0, h = _mgrit_case(seed=21)
+    N, c = K.shape[0], 4
+    U = O.serial_forward(u0, K, b, h, "tanh")
+    lamN = np.random.default_rng(0).standard_normal(u0.shape)
+    S = O.serial_adjoint(U, lamN, K, b, h, "tanh")
+    L = np.zeros_like(S)
+    L[N] = lamN
+    full = N // c if relax == "F" else -(-N // (2 * c))
+    for m in range(1, full + 1):
+        Lm, _, _ = O.mgrit_adjoint(U, L, K, b, h, "tanh", cf=c, max_levels=2, relax=relax, max_iter=m)
+        exact = min((gain * m + 1) * c - 1, N)
+        err = np.abs(Lm - S).reshape(N + 1, -1).max(axis=1)[::-1]  # distance from the end
+        assert err[:exact + 1].max() < 1e-14, (m, exact)
+        if exact < N:
+            assert err[exact + 1:].max() > 1e-8
+    assert np.abs(Lm - S).max() < 1e-14
+
+
+def _parareal(u0, K, b, h, c, iters, kind):
+    """Parareal (Gander & Vandewalle 2007), the equivalent of two-level MGRIT with
+    F-relaxation: fine propagator F_k = c fine steps from T_k, coarse propagator
+    G_k = one step of size c h with the weights of layer k c. Iteration:
+        U_{k+1}^{new} = G_k(U_k^{new}) + F_k(U_k^{old}) - G_k(U_k^{old}),
+    then the fine points are filled by fine propagation from the new C-points."""
+    N = K.shape[0]
+    Nc = N // c
+
+    def fine(k, v):
+        for j in range(c):
+            n = k * c + j
+            v = v + h * O.act(v @ K[n].T + b[n], kind)
+        return v
+
+    def coarse(k, v):
+        n = k * c
+        return v + c * h * O.act(v @ K[n].T + b[n], kind)
+
+    Uc = [u0] * (Nc + 1)  # cold start: every C-point is u0
+    for _ in range(iters):
+        Fold = [fine(k, Uc[k]) for k in range(Nc)]
+        new = [u0]
+        for k in range(Nc):
+            new.append(coarse(k, new[k]) + Fold[k] - coarse(k, Uc[k]))
+        Uc = new
+    out = np.zeros((N + 1,) + u0.shape)
+    for k in range(Nc):
+        v = Uc[k]
+        out[k * c] = v
+        for j in range(1, c):
+            n = k * c + j - 1
+            v = v + h * O.act(v @ K[n].T + b[n], kind)
+            out[k * c + j] = v
+    out[N] = Uc[Nc]
+    return out
+
+
+@pytest.mark.parametrize("iters", [1, 2, 3])
+def test_two_level_F_equals_parareal(iters):
+    K, b, u0, h = _mgrit_case(seed=22, kscale=0.6)
+    U = np.zeros((K.shape[0] + 1,) + u0.shape)
+    U[0] = u0
+    Um, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=2, relax="F", max_iter=iters)
+    P = _parareal(u0, K, b, h, 4, iters, "tanh")
+    assert rel(Um, P) < 1e-13
+
+
+@pytest.mark.parametrize("levels,relax", [(2, "F"), (3, "FCF"), (4, "FCF"), (3, "F")])
+def test_coarse_propagator_exact_when_layers_are_constant_increments(levels, relax):
+    # K = 0 and the same bias in every layer: c fine steps of size h equal one coarse step
+    # of size c h on every level, so one V-cycle solves the problem exactly.
+    r = np.random.default_rng(23)
+    N, B, q, h = 64, 3, 4, 0.05
+    K = np.zeros((N, q, q))
+    b = np.tile(r.standard_normal(q), (N, 1))
+    u0 = r.standard_normal((B, q))
+    S = O.serial_forward(u0, K, b, h, "tanh")
+    U = np.zeros_like(S)
+    U[0] = u0
+    Um, hist, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=levels, relax=relax, max_iter=1)
+    assert rel(Um, S) < 1e-14
+    lamN = r.standard_normal((B, q))
+    Ls = O.serial_adjoint(S, lamN, K, b, h, "tanh")
+    L0 = np.zeros_like(S)
+    L0[N] = lamN
+    Lm, _, _ = O.mgrit_adjoint(S, L0, K, b, h, "tanh", cf=4, max_levels=levels, relax=relax, max_iter=1)
+    assert rel(Lm, Ls) < 1e-14
+
+
+@pytest.mark.parametrize("levels", [2, 3, 4])
+@pytest.mark.parametrize("kind", ["tanh", "relu"])
+def test_fixed_point_is_serial_solution(levels, kind):
+    K, b, u0, h = _mgrit_case(seed=24, N=64, act=kind)
+    S = O.serial_forward(u0, K, b, h, kind)
+    Um, hist, _ = O.mgrit_forward(S, K, b, h, kind, cf=4, max_levels=levels, relax="FCF",
+                                  max_iter=1, warm_start=True)
+    assert np.abs(Um - S).max() <= 1e-14 * np.abs(S).max()
+    assert hist[0] <= 1e-14 * np.linalg.norm(S)
+    lamN = np.random.default_rng(1).standard_normal(u0.shape)
+    Ls = O.serial_adjoint(S, lamN, K, b, h, kind)
+    Lm, hist, _ = O.mgrit_adjoint(S, Ls, K, b, h, kind, cf=4, max_levels=levels, relax="FCF",
+                                  max_iter=1, warm_start=True)
+    assert np.abs(Lm - Ls).max() <= 1e-14 * np.abs(Ls).max()
+
+
+@pytest.mark.parametrize("levels,kind", [(3, "tanh"), (4, "relu"), (5, "smoothrelu")])
+def test_multilevel_converges_to_serial(levels, kind):
+    K, b, u0, h = _mgrit_case(seed=25, N=256, act=kind, kscale=0.3)
+    S = O.serial_forward(u0, K, b, h, kind)
+    U = np.zeros_like(S)
+    U[0] = u0
+    Um, hist, it = O.mgrit_forward(U, K, b, h, kind, cf=4, max_levels=levels, relax="FCF",
+                                   max_iter=30, rtol=1e-13)
+    assert rel(Um, S) < 1e-11, (it, hist)
+    lamN = np.random.default_rng(2).standard_normal(u0.shape)
+    Ls = O.serial_adjoint(S, lamN, K, b, h, kind)
+    L0 = np.zeros_like(S)
+    L0[-1] = lamN
+    Lm, hist, it = O.mgrit_adjoint(S, L0, K, b, h, kind, cf=4, max_levels=levels, relax="FCF",
+                                   max_iter=30, rtol=1e-13)
+    assert rel(Lm, Ls) < 1e-11, (it, hist)
+
+
+def test_degenerate_hierarchies_exact_in_one_iteration():
+    K, b, u0, h = _mgrit_case(seed=26, N=16)
+    S = O.serial_forward(u0, K, b, h, "tanh")
+    U = np.zeros_like(S)
+    U[0] = u0
+    # one level: the coarsest-level solve is serial propagation
+    Um, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=1, max_iter=1)
+    assert np.abs(Um - S).max() == 0.0
+    # c = N with two levels: one interval; F-relaxation plus the exact coarse solve
+    Um, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=16, max_levels=2, relax="F", max_iter=1)
+    assert np.abs(Um - S).max() < 1e-14
+
+
+def test_monotone_residual_on_tiny_config():
+    wl = WORKLOADS[1]
+    d = generate(wl)
+    u0 = O.open_forward(d["y"], d["L_in"], wl.act, wl.opening)
+    U = np.zeros((wl.N + 1,) + u0.shape)
+    U[0] = u0
+    _, hist, _ = O.mgrit_forward(U, d["K"], d["b"], wl.h, wl.act, cf=wl.cf, max_levels=wl.max_levels,
+                                 relax=wl.relax, max_iter=8)
+    for m in range(len(hist) - 1):
+        if hist[m] > 1e-12 * hist[0]:
+            assert hist[m + 1] < hist[m], hist
+    # two-level FCF with N/c = 8 intervals is exact after 4 iterations
+    assert hist[4] <= 1e-13 * hist[0]
+    S = O.serial_forward(u0, d["K"], d["b"], wl.h, wl.act)
+    lamN = O.loss_terminal(S[-1], d["W"], d["mu"], d["onehot"])[1]
+    L0 = np.zeros_like(S)
+    L0[-1] = lamN
+    _, hist, _ = O.mgrit_adjoint(S, L0, d["K"], d["b"], wl.h, wl.act, cf=wl.cf,
+                                 max_levels=wl.max_levels, relax=wl.relax, max_iter=8)
+    for m in range(len(hist) - 1):
+        if hist[m] > 1e-12 * hist[0]:
+            assert hist[m + 1] < hist[m], hist
+
+
+def test_adjoint_mgrit_is_linear_in_terminal_value():
+    K, b, u0, h = _mgrit_case(seed=27, N=64)
+    U = O.serial_forward(u0, K, b, h, "tanh")
+    lamN = np.random.default_rng(3).standard_normal(u0.shape)
+    L0 = np.zeros_like(U)
+    L0[-1] = lamN
+    L1, _, _ = O.mgrit_adjoint(U, L0, K, b, h, "tanh", cf=4, max_levels=3, max_iter=2)
+    L2, _, _ = O.mgrit_adjoint(U, 2.5 * L0, K, b, h, "tanh", cf=4, max_levels=3, max_iter=2)
+    assert rel(L2, 2.5 * L1) < 1e-14
+
+
+def test_converged_mgrit_gradient_equals_serial_gradient():
+    # Remark after Section 3.3: converged state and adjoint MGRIT give the reduced gradient
+    K, b, u0, h = _mgrit_case(seed=28, N=64)
+    S = O.serial_forward(u0, K, b, h, "tanh")
+    lamN = np.random.default_rng(4).standard_normal(u0.shape)
+    Ls = O.serial_adjoint(S, lamN, K, b, h, "tanh")
+    U = np.zeros_like(S)
+    U[0] = u0
+    Um, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=3, max_iter=20, rtol=1e-14)
+    L0 = np.zeros_like(S)
+    L0[-1] = lamN
+    Lm, _, _ = O.mgrit_adjoint(Um, L0, K, b, h, "tanh", cf=4, max_levels=3, max_iter=20, rtol=1e-14)
+    dK, db = O.gradient(S, Ls, K, b, h, "tanh")
+    dKm, dbm = O.gradient(Um, Lm, K, b, h, "tanh")
+    assert rel(dKm, dK) < 1e-11 and rel(dbm, db) < 1e-11
+
+
+def test_one_shot_with_many_inner_iterations_is_serial_training():
+    # Section 4: for large m1, m2 the simultaneous method recovers layer-serial training
+    wl = WORKLOADS[5].with_overrides(N=16, B=24, n_features=6)
+    d = generate(wl)
+    args = (d["y"], d["onehot"], d["L_in"], d["K"], d["b"], d["W"], d["mu"], wl.h, wl.act, wl.opening)
+    ls, ws = O.serial_training(*args, updates=4, lr=0.5)
+    lo, wo = O.one_shot(*args, cf=4, max_levels=2, min_coarse=1, relax="FCF", updates=4, lr=0.5,
+                        m1=4, m2=4)
+    assert np.allclose(lo, ls, rtol=1e-12, atol=0)
+    for k in ws:
+        assert rel(wo[k], ws[k]) < 1e-12
+    # with one inner iteration the trajectory differs but the loss still decreases
+    l1, _ = O.one_shot(*args, cf=4, max_levels=2, min_coarse=1, relax="FCF", updates=4, lr=0.5)
+    assert l1[0] == pytest.approx(ls[0], rel=1e-2) and l1[-1] < l1[0]
+
+
+def test_level_sizes_of_workloads():
+    expect = {1: [32, 8], 2: [256, 64, 16], 3: [2048, 512, 128, 32, 8], 4: [512, 128, 32, 8],
+              5: [1024, 256, 64]}
+    for cfg, sizes in expect.items():
+        wl = WORKLOADS[cfg]
+        assert O.level_sizes(wl.N, wl.cf, wl.max_levels, wl.min_coarse) == sizes
+    with pytest.raises(ValueError):
+        O.level_sizes(18, 4, 3, 1)
+
+
+def test_workload_generator_is_deterministic_and_rounded():
+    wl = WORKLOADS[2].with_overrides(N=8, B=10)
+    a, b = generate(wl), generate(wl)
+    for k in a:
+        if a[k] is not None:
+            assert np.array_equal(a[k], b[k])
+    assert a["K"].dtype == np.float32 and a["y"].dtype == np.float32
+    s = random_state(wl, 3)
+    assert s.shape == (1, 10, 32) and s.dtype == np.float32
+
+
+@pytest.mark.parametrize("levels,relax", [(2, "F"), (3, "F"), (3, "FCF"), (4, "FCF")])
+def test_exact_coarse_propagators_solve_in_one_vcycle(levels, relax):
+    # Affine steps with a nilpotent K (K^2 = 0) and a bias in K's null space: c^l fine
+    # steps of size h equal exactly one step of size c^l h, so the coarse grids of every
+    # level represent their fine grids exactly and one V-cycle reaches the serial
+    # solution (to rounding) from any initial guess. The guess is random (a cold start
+    # leaves errors in range(K), which K annihilates, and would hide a wrong h_l).
+    r = np.random.default_rng(29)
+    N, B, q, h = 128, 3, 4, 0.07
+    K1 = np.zeros((q, q))
+    K1[0, 1] = 2.0
+    K1[2, 3] = -1.5
+    assert not np.any(K1 @ K1)
+    b1 = np.array([0.3, 0.0, -0.2, 0.0])
+    assert not np.any(K1 @ b1)
+    K, b = np.tile(K1, (N, 1, 1)), np.tile(b1, (N, 1))
+    u0 = r.standard_normal((B, q))
+    S = O.serial_forward(u0, K, b, h, "identity")
+    U = r.standard_normal(S.shape)
+    U[0] = u0
+    Um, _, _ = O.mgrit_forward(U, K, b, h, "identity", cf=4, max_levels=levels, relax=relax,
+                               max_iter=1, warm_start=True)
+    assert rel(Um, S) < 1e-13
+    lamN = r.standard_normal((B, q))
+    Ls = O.serial_adjoint(S, lamN, K, b, h, "identity")
+    L0 = r.standard_normal(S.shape)
+    L0[N] = lamN
+    Lm, _, _ = O.mgrit_adjoint(S, L0, K, b, h, "identity", cf=4, max_levels=levels, relax=relax,
+                               max_iter=1, warm_start=True)
+    assert rel(Lm, Ls) < 1e-13
+
+
+def _relax_by_hand(U, K, b, h, kind, c, relax):
+    """F- (and C-) relaxation on the finest grid, written from eqs. Frelax / Crelax."""
+    U = U.copy()
+    N = K.shape[0]
+
+    def F():
+        for k in range(N // c):
+            for n in range(k * c + 1, (k + 1) * c):
+                U[n] = O.phi(U[n - 1], K[n - 1], b[n - 1], h, kind)
+
+    F()
+    if relax == "FCF":
+        newC = {k * c: O.phi(U[k * c - 1], K[k * c - 1], b[k * c - 1], h, kind) for k in range(1, N // c + 1)}
+        for n, v in newC.items():
+            U[n] = v
+        F()
+    return U
+
+
+@pytest.mark.parametrize("levels,relax,kind", [(2, "F", "tanh"), (2, "FCF", "tanh"), (3, "FCF", "relu")])
+def test_reported_residual_is_full_grid_residual_of_relaxed_iterate(levels, relax, kind):
+    # rho_m (Algorithm 1, step 2) is ||G - A(U)|| of the iterate after the relaxation of
+    # iteration m; F-point rows of the residual vanish after F-relaxation.
+    K, b, u0, h = _mgrit_case(seed=30, N=64, act=kind)
+    U = np.zeros((K.shape[0] + 1,) + u0.shape)
+    U[0] = u0
+    for k in range(1, 64 // 4 + 1):
+        U[4 * k] = u0
+    _, hist, _ = O.mgrit_forward(U, K, b, h, kind, cf=4, max_levels=levels, relax=relax, max_iter=3)
+    prev = U
+    for m in range(3):
+        R = _relax_by_hand(prev, K, b, h, kind, 4, relax)
+        assert abs(hist[m] - O.residual_norm_state(R, K, b, h, kind)) <= 1e-12 * hist[m]
+        prev, _, _ = O.mgrit_forward(U, K, b, h, kind, cf=4, max_levels=levels, relax=relax,
+                                     max_iter=m + 1)
+    # adjoint: same statement on the reversed system
+    S = O.serial_forward(u0, K, b, h, kind)
+    lamN = np.random.default_rng(5).standard_normal(u0.shape)
+    L0 = np.zeros_like(S)
+    L0[-1] = lamN
+    _, hist, _ = O.mgrit_adjoint(S, L0, K, b, h, kind, cf=4, max_levels=levels, relax=relax, max_iter=2)
+    cold = L0.copy()
+    for k in range(64 // 4):
+        cold[4 * k] = lamN
+    Nn = 64
+    Lr = cold.copy()
+    for k in range(Nn // 4):
+        for n in range((k + 1) * 4 - 1, k * 4, -1):
+            Lr[n] = O.phibar(Lr[n + 1], S[n], K[n], b[n], h, kind)
+    if relax == "FCF":
+        newC = {k * 4: O.phibar(Lr[k * 4 + 1], S[k * 4], K[k * 4], b[k * 4], h, kind) for k in range(Nn // 4)}
+        for n, v in newC.items():
+            Lr[n] = v
+        for k in range(Nn // 4):
+            for n in range((k + 1) * 4 - 1, k * 4, -1):
+                Lr[n] = O.phibar(Lr[n + 1], S[n], K[n], b[n], h, kind)
+    assert abs(hist[0] - O.residual_norm_adjoint(S, Lr, K, b, h, kind)) <= 1e-12 * hist[0]
