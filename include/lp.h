@@ -1,0 +1,202 @@
+/*
+ * lp.h - C ABI of the MI355X layer-parallel ResNet library.
+ *
+ * The library solves the discrete state and adjoint equations of a residual
+ * network viewed as forward Euler time stepping (Guenther, Ruthotto, Schroder,
+ * Cyr, Gauger: "Layer-parallel training of deep residual neural networks",
+ * arXiv:1812.04352), either layer-serially or with nonlinear multigrid reduction
+ * in time (MGRIT with FAS, Section 3, Algorithm 1), and assembles the reduced
+ * gradient with respect to the layer weights.
+ *
+ * Model (Section 2): per example, u^{n+1} = Phi(u^n, theta^n) = u^n + h sigma(K_n u^n + b_n),
+ * n = 0..N-1, with K_n a dense q x q matrix or a 3x3 convolution with C channels
+ * (zero "same" padding, cross-correlation), b_n a per-feature (dense) or
+ * per-channel (conv) bias, sigma applied componentwise.
+ *
+ * Conventions for every call:
+ *   - Pointers are DEVICE pointers unless the argument is marked (host).
+ *   - The caller owns every buffer. The library never allocates device memory;
+ *     calls that need scratch memory take a caller-provided workspace `ws` of
+ *     `ws_bytes` bytes (see lp_workspace_bytes) and return LP_EWORKSPACE if it is
+ *     too small or not 256-byte aligned.
+ *   - All device work is enqueued on `stream` (a hipStream_t; NULL is the default
+ *     stream). A call that returns a host value (res_hist, iters, norm) waits for
+ *     `stream` before returning; other calls return without waiting.
+ *   - All floating-point arrays of one call have the problem's dtype
+ *     (LP_F32: float, LP_F64: double). Layouts are row-major, contiguous:
+ *       trajectory U, Lam  [N+1][B][q]     (conv: [N+1][B][C][H][W]); q = C*H*W
+ *       weights K          [N][q][q]       K[n][i][j] maps input j to output i
+ *                          (conv: [N][C][C][3][3], K[n][co][ci][ty][tx])
+ *       bias b             [N][q]          (conv: [N][C])
+ *   - U and Lam must not alias each other or the workspace.
+ *   - Calls are re-entrant when given distinct workspaces and outputs.
+ *   - Error behaviour: an argument check failing returns LP_EINVAL (or
+ *     LP_EUNSUPPORTED for a valid but unimplemented combination) before any work
+ *     is enqueued; lp_last_error() then names the argument. A HIP runtime failure
+ *     returns LP_EHIP. A non-finite residual norm returns LP_ENONFINITE after the
+ *     iteration that produced it (outputs then hold that iterate).
+ */
+#ifndef LP_H
+#define LP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LP_ABI_VERSION 1
+
+typedef enum {
+  LP_OK = 0,
+  LP_EINVAL = 1,        /* bad argument (null pointer, bad size, bad enum, N_l % cf != 0) */
+  LP_EUNSUPPORTED = 2,  /* valid but not implemented (e.g. a dense width with no kernel) */
+  LP_EWORKSPACE = 3,    /* workspace too small or misaligned */
+  LP_EHIP = 4,          /* HIP runtime error */
+  LP_ENONFINITE = 5     /* residual norm became NaN or Inf */
+} lp_status;
+
+enum { LP_F32 = 0, LP_F64 = 1 };                       /* dtype */
+enum { LP_DENSE = 0, LP_CONV3X3 = 1 };                 /* layer */
+enum { LP_TANH = 0, LP_RELU = 1, LP_SMOOTHRELU = 2, LP_IDENTITY = 3 }; /* activation sigma */
+enum { LP_RELAX_F = 0, LP_RELAX_FCF = 1 };             /* MGRIT relaxation */
+enum { LP_STATE = 0, LP_ADJOINT = 1 };                 /* which system */
+enum { LP_OPEN_IDENTITY = 0, LP_OPEN_DENSE_ACT = 1, LP_OPEN_CONV_ACT = 2 }; /* opening layer */
+
+/* The network and batch (Section 2.2). Dense: C = width q, H = W = 1.
+ * Conv: C channels of H x W pixels. h = T / N is the step size. */
+typedef struct {
+  int32_t abi_version;   /* must equal LP_ABI_VERSION */
+  int32_t dtype;         /* LP_F32 | LP_F64 */
+  int32_t layer;         /* LP_DENSE | LP_CONV3X3 */
+  int32_t act;           /* LP_TANH | LP_RELU | LP_SMOOTHRELU | LP_IDENTITY */
+  int32_t N;             /* residual layers (time steps), >= 1 */
+  int32_t B;             /* batch size, >= 0 (0: calls do nothing) */
+  int32_t C, H, W;       /* width / channels and image size */
+  double h;              /* step size */
+} lp_problem;
+
+/* MGRIT schedule (Section 3.1, Algorithm 1, as a recursive V-cycle).
+ * Level l has N_l = N / cf^l steps of size cf^l h and uses the injected weights
+ * theta^{i cf^l}. Levels are added while l+1 < max_levels and N_l > min_coarse;
+ * every coarsened level must satisfy N_l % cf == 0 (else LP_EINVAL). The
+ * coarsest level is solved by forward (adjoint: backward) substitution. */
+typedef struct {
+  int32_t cf;            /* coarsening factor c >= 2 */
+  int32_t max_levels;    /* >= 1; 1 means a serial solve */
+  int32_t min_coarse;    /* stop coarsening at N_l <= min_coarse (>= 1) */
+  int32_t relax;         /* LP_RELAX_F | LP_RELAX_FCF, on every non-coarsest level */
+  int32_t max_iter;      /* >= 1 V-cycles */
+  int32_t warm_start;    /* 0: C-points start as copies of u^0 (adjoint: lam^N); 1: caller's array is the guess */
+  double rtol;           /* stop after iteration m when rho_m <= rtol * rho_1 (0: off) */
+  double stag;           /* stop after iteration m > 1 when rho_m > stag * rho_{m-1} (0: off) */
+} lp_mgrit;
+
+int32_t lp_abi_version(void);
+const char* lp_status_string(int32_t status);
+/* Message of the last failing call on this host thread ("" if none). */
+const char* lp_last_error(void);
+
+/* Workspace bytes that lp_mgrit_forward, lp_mgrit_adjoint, lp_gradient and
+ * lp_residual_norm need for this problem and schedule (mg may be NULL: then only
+ * the gradient and residual-norm needs are counted). Returns 0 for an invalid
+ * problem. The workspace holds the coarse levels (U_l and the FAS right-hand
+ * side G_l for l >= 1), the relaxed C-points of every non-coarsest level,
+ * per-workgroup residual partials (fp64) and per-chunk gradient partials. */
+size_t lp_workspace_bytes(const lp_problem* prob, const lp_mgrit* mg);
+
+/* Layer-serial forward propagation (Section 2.3, state equations; the baseline
+ * method): U[n+1] = Phi(U[n], theta^n) for n = 0..N-1.
+ * U [N+1][B][q]: row 0 is read (u^0 = L_in y), rows 1..N are written. */
+int32_t lp_serial_forward(const lp_problem* prob, const void* K, const void* b, void* U,
+                          void* stream);
+
+/* Layer-serial adjoint propagation (Section 2.3, adjoint equations; this is
+ * backpropagation): Lam[n] = (d_u Phi(U[n], theta^n))^T Lam[n+1]
+ *                          = Lam[n+1] + h K_n^T (sigma'(K_n U[n] + b_n) * Lam[n+1]),
+ * n = N-1..0. Lam row N is read (terminal value), rows 0..N-1 are written.
+ * U is read only. */
+int32_t lp_serial_adjoint(const lp_problem* prob, const void* K, const void* b, const void* U,
+                          void* Lam, void* stream);
+
+/* MGRIT solve of the state equations A(U, theta) = G (Section 3.1, the
+ * space-time system and Algorithm 1 with FAS).
+ * U [N+1][B][q]: row 0 is u^0 (read, never written); with warm_start the other
+ * rows are the initial guess (only rows at multiples of cf are read), else they
+ * are ignored; on return they hold the iterate after *iters V-cycles (every row
+ * written, the last sweep being an F-relaxation).
+ * res_hist (host, nullable, length >= max_iter): rho_m, m = 1..*iters, the fp64
+ * norm ||G - A(U)|| over all examples and features, taken at the finest level's
+ * C-points after the relaxation of iteration m (Algorithm 1, step 2).
+ * iters (host, nullable): V-cycles run. Not converging within max_iter is not
+ * an error. */
+int32_t lp_mgrit_forward(const lp_problem* prob, const lp_mgrit* mg, const void* K,
+                         const void* b, void* U, void* ws, size_t ws_bytes, double* res_hist,
+                         int32_t* iters, void* stream);
+
+/* MGRIT solve of the adjoint equations (Section 3.2, the adjoint space-time
+ * system), linearised at the trajectory U (read only).
+ * Lam [N+1][B][q]: row N is the terminal value (read, never written); with
+ * warm_start the other rows are the initial guess (rows at multiples of cf are
+ * read), else ignored; on return they hold the iterate. Coarse levels take the
+ * adjoint step of size cf^l h linearised at the injected fine state U[i cf^l].
+ * res_hist, iters as for lp_mgrit_forward, on the adjoint residual. */
+int32_t lp_mgrit_adjoint(const lp_problem* prob, const lp_mgrit* mg, const void* K,
+                         const void* b, const void* U, void* Lam, void* ws, size_t ws_bytes,
+                         double* res_hist, int32_t* iters, void* stream);
+
+/* Reduced gradient with respect to the layer weights (Section 2.3, design
+ * equations, without regularisation):
+ *   s_k^n = sigma'(K_n u_k^n + b_n) * lam_k^{n+1}
+ *   dK[n] = h sum_k s_k^n (u_k^n)^T   (conv: the weight gradient of the 3x3 cross-correlation)
+ *   db[n] = h sum_k s_k^n             (conv: summed over pixels per channel)
+ * summed over the batch in a fixed order (bitwise reproducible).
+ * dK like K, db like b; both written. The 1/B factor of the mean loss is
+ * expected inside Lam (it is part of the terminal value). */
+int32_t lp_gradient(const lp_problem* prob, const void* K, const void* b, const void* U,
+                    const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes, void* stream);
+
+/* Full-grid residual norm (fp64, host result; the stopping quantity ||G - A(U)||):
+ *   which = LP_STATE:   (sum_{n=1..N} ||Phi(U[n-1], theta^{n-1}) - U[n]||^2)^{1/2}
+ *   which = LP_ADJOINT: (sum_{n=0..N-1} ||Lam[n+1] + h K_n^T(sigma'(z_n) * Lam[n+1]) - Lam[n]||^2)^{1/2}
+ * Lam may be NULL for LP_STATE. */
+int32_t lp_residual_norm(const lp_problem* prob, int32_t which, const void* K, const void* b,
+                         const void* U, const void* Lam, void* ws, size_t ws_bytes, double* norm,
+                         void* stream);
+
+/* ---- boundary helpers (outside the per-iteration hot path) ---- */
+
+/* Opening layer u^0 = L_in y (Section 2.1), written to u0 [B][q]:
+ *   LP_OPEN_IDENTITY:  u0 = y                       (y [B][q])
+ *   LP_OPEN_DENSE_ACT: u0 = sigma(L_in y)           (y [B][nf], L_in [q][nf])
+ *   LP_OPEN_CONV_ACT:  u0 = sigma(conv3x3(L_in, y)) (y [B][1][H][W], L_in [C][1][3][3], no bias)
+ * nf is the input feature count (ignored for the conv opening). */
+int32_t lp_open_forward(const lp_problem* prob, int32_t opening, int32_t nf, const void* y,
+                        const void* L_in, void* u0, void* stream);
+
+/* Gradient of the opening weights, dL_in = sum_k (sigma'(L_in y_k) * lam_k^0) y_k^T
+ * (conv: weight gradient of the opening convolution); dL_in like L_in. */
+int32_t lp_open_grad(const lp_problem* prob, int32_t opening, int32_t nf, const void* y,
+                     const void* L_in, const void* lam0, void* dL_in, void* stream);
+
+/* Softmax cross-entropy at the network output (Section 2.1) for class-probability
+ * rows c [B][nc] (one-hot in all workloads), z = W u^N + mu, W [nc][q], mu [nc]:
+ *   J      = (1/B) sum_k -c_k^T log softmax(z_k)          (fp64, written to J[0] on the device)
+ *   lamN   = (1/B) W^T (softmax(z_k) - c_k)   [B][q]      (the adjoint terminal value)
+ *   dW     = (1/B) sum_k (softmax(z_k) - c_k) (u_k^N)^T   [nc][q]
+ *   dmu    = (1/B) sum_k (softmax(z_k) - c_k)             [nc]
+ * Requires 1 <= nc <= min(64, q) (lamN's rows hold the softmax residual between passes). */
+int32_t lp_loss_terminal(const lp_problem* prob, int32_t nc, const void* uN, const void* W,
+                         const void* mu, const void* c, double* J, void* lamN, void* dW,
+                         void* dmu, void* stream);
+
+/* Plain gradient step x <- x - lr * g on n elements of the given dtype (the
+ * design update of Algorithm 2 with a scaled-identity Hessian approximation). */
+int32_t lp_sgd_update(int32_t dtype, size_t n, double lr, const void* g, void* x, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LP_H */

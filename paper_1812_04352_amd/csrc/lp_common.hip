@@ -1,0 +1,330 @@
+// Kernels shared by every layer family: row copies (the MGRIT cold start), the
+// fixed-order residual-norm reduction, and the boundary helpers of the network
+// (opening layer, softmax cross-entropy and its adjoint terminal value, the
+// plain gradient step). The helpers sit outside the per-iteration hot path.
+#include <math.h>
+
+#include <type_traits>
+
+#include "lp_device.h"
+#include "lp_internal.h"
+
+namespace lp {
+namespace {
+
+constexpr int NT = 256;
+
+// X[dst_row0 + t*dst_step] = X[src_row] for t = 0..count-1 (16-byte units).
+__global__ __launch_bounds__(NT) void k_copy_rows(uint4* X, size_t units, long src_row,
+                                                  long dst_row0, long dst_step, long count) {
+  const size_t tot = units * (size_t)count;
+  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < tot; i += (size_t)gridDim.x * NT) {
+    const size_t t = i / units, u = i - t * units;
+    X[(size_t)(dst_row0 + (long)t * dst_step) * units + u] = X[(size_t)src_row * units + u];
+  }
+}
+
+// out[0] = sqrt(sum of partial[0..n)), summed in a fixed order.
+__global__ __launch_bounds__(NT) void k_norm_reduce(const double* partial, int n, double* out) {
+  __shared__ double sh[NT];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < n; i += NT) s += partial[i];
+  s = block_sum<NT>(s, sh);
+  if (threadIdx.x == 0) out[0] = sqrt(s);
+}
+
+__global__ __launch_bounds__(NT) void k_zero(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < n; i += (size_t)gridDim.x * NT) p[i] = 0u;
+}
+
+unsigned grid_for(size_t work) {
+  size_t g = (work + NT - 1) / NT;
+  if (g > 65535u * 8u) g = 65535u * 8u;
+  return (unsigned)(g ? g : 1);
+}
+
+// ---------------------------------------------------------------- opening layer
+
+template <typename T, int ACT>
+__global__ __launch_bounds__(NT) void k_open_dense(const T* y, const T* L, T* u0, int B, int q, int nf) {
+  const size_t tot = (size_t)B * q;
+  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < tot; i += (size_t)gridDim.x * NT) {
+    const size_t e = i / q, r = i - e * q;
+    T acc = T(0);
+    for (int f = 0; f < nf; ++f) acc = fma(L[r * nf + f], y[e * nf + f], acc);
+    u0[i] = act_f<T, ACT>(acc);
+  }
+}
+
+// u0[e][co][y][x] = sigma(sum_{ty,tx} L[co][0][ty][tx] y[e][0][y+ty-1][x+tx-1]), zero padded.
+template <typename T, int ACT>
+__global__ __launch_bounds__(NT) void k_open_conv(const T* y, const T* L, T* u0, int B, int C, int H, int W) {
+  const size_t tot = (size_t)B * C * H * W;
+  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < tot; i += (size_t)gridDim.x * NT) {
+    size_t t = i;
+    const int x = (int)(t % W); t /= W;
+    const int yy = (int)(t % H); t /= H;
+    const int co = (int)(t % C);
+    const size_t e = t / C;
+    T acc = T(0);
+    for (int ty = 0; ty < 3; ++ty) {
+      const int sy = yy + ty - 1;
+      if (sy < 0 || sy >= H) continue;
+      for (int tx = 0; tx < 3; ++tx) {
+        const int sx = x + tx - 1;
+        if (sx < 0 || sx >= W) continue;
+        acc = fma(L[co * 9 + ty * 3 + tx], y[e * H * W + (size_t)sy * W + sx], acc);
+      }
+    }
+    u0[i] = act_f<T, ACT>(acc);
+  }
+}
+
+// dL[r][f] = sum_e sigma'(z_er) lam0[e][r] y[e][f]; one workgroup per row r,
+// examples in order, z recomputed once per (e, r).
+template <typename T, int ACT>
+__global__ __launch_bounds__(NT) void k_open_grad_dense(const T* y, const T* L, const T* lam0, T* dL,
+                                                        int B, int q, int nf) {
+  __shared__ T sv[NT];
+  const int r = blockIdx.x;
+  // each thread owns features f = threadIdx.x + k*NT
+  T acc[4] = {T(0), T(0), T(0), T(0)};  // nf <= 4*NT
+  for (int e0 = 0; e0 < B; e0 += NT) {
+    const int e = e0 + threadIdx.x;
+    T s = T(0);
+    if (e < B) {
+      T z = T(0);
+      for (int f = 0; f < nf; ++f) z = fma(L[(size_t)r * nf + f], y[(size_t)e * nf + f], z);
+      s = dact_f<T, ACT>(z) * lam0[(size_t)e * q + r];
+    }
+    sv[threadIdx.x] = s;
+    __syncthreads();
+    const int ne = min(NT, B - e0);
+    for (int k = 0; k < 4; ++k) {
+      const int f = threadIdx.x + k * NT;
+      if (f < nf)
+        for (int t = 0; t < ne; ++t) acc[k] = fma(sv[t], y[(size_t)(e0 + t) * nf + f], acc[k]);
+    }
+    __syncthreads();
+  }
+  for (int k = 0; k < 4; ++k) {
+    const int f = threadIdx.x + k * NT;
+    if (f < nf) dL[(size_t)r * nf + f] = acc[k];
+  }
+}
+
+// dL[co][0][ty][tx] = sum_e sum_p sigma'(z[e,co,p]) lam0[e,co,p] y[e, p + t]: one
+// workgroup per output channel; thread t accumulates over pixels t, t+NT, ... of
+// every example for all 9 taps, then a fixed-order tree combines the threads.
+template <typename T, int ACT>
+__global__ __launch_bounds__(NT) void k_open_grad_conv(const T* y, const T* L, const T* lam0, T* dL,
+                                                       int B, int C, int H, int W) {
+  __shared__ double sh[NT];
+  const int co = blockIdx.x;
+  T acc[9];
+  for (int t = 0; t < 9; ++t) acc[t] = T(0);
+  const int P = H * W;
+  for (int e = 0; e < B; ++e) {
+    const T* ye = y + (size_t)e * P;
+    for (int p = threadIdx.x; p < P; p += NT) {
+      const int yy = p / W, x = p - yy * W;
+      T win[9];
+      T z = T(0);
+      for (int ty = 0; ty < 3; ++ty)
+        for (int tx = 0; tx < 3; ++tx) {
+          const int sy = yy + ty - 1, sx = x + tx - 1;
+          T v = (sy >= 0 && sy < H && sx >= 0 && sx < W) ? ye[sy * W + sx] : T(0);
+          win[ty * 3 + tx] = v;
+          z = fma(L[co * 9 + ty * 3 + tx], v, z);
+        }
+      const T s = dact_f<T, ACT>(z) * lam0[((size_t)e * C + co) * P + p];
+      for (int t = 0; t < 9; ++t) acc[t] = fma(s, win[t], acc[t]);
+    }
+  }
+  for (int t = 0; t < 9; ++t) {
+    double v = block_sum<NT>((double)acc[t], sh);
+    if (threadIdx.x == 0) dL[co * 9 + t] = (T)v;
+  }
+}
+
+// ---------------------------------------------------------------- loss and terminal value
+
+constexpr int MAXNC = 64;
+
+// Pass 1 (one workgroup): per example z = W u + mu, softmax, loss; the row
+// d_e = (softmax - c)/B is parked in the first nc entries of lamN's row e.
+template <typename T>
+__global__ __launch_bounds__(1024) void k_loss_pass1(const T* uN, const T* Wc, const T* mu, const T* c,
+                                                     double* J, T* lamN, int B, int q, int nc) {
+  __shared__ double sh[1024];
+  double lsum = 0.0;
+  for (int e = threadIdx.x; e < B; e += 1024) {
+    double z[MAXNC];
+    double zmax = -INFINITY;
+    for (int j = 0; j < nc; ++j) {
+      T acc = T(0);
+      for (int i = 0; i < q; ++i) acc = fma(Wc[(size_t)j * q + i], uN[(size_t)e * q + i], acc);
+      z[j] = (double)(acc + mu[j]);
+      zmax = z[j] > zmax ? z[j] : zmax;
+    }
+    double den = 0.0;
+    for (int j = 0; j < nc; ++j) den += exp(z[j] - zmax);
+    const double lden = log(den);
+    for (int j = 0; j < nc; ++j) {
+      const double cj = (double)c[(size_t)e * nc + j];
+      const double logp = (z[j] - zmax) - lden;
+      lsum -= cj * logp;
+      lamN[(size_t)e * q + j] = (T)((exp(logp) - cj) / (double)B);
+    }
+  }
+  lsum = block_sum<1024>(lsum, sh);
+  if (threadIdx.x == 0) J[0] = lsum / (double)B;
+}
+
+// Pass 2: dW[j][i] = sum_e d[e][j] u[e][i], dmu[j] = sum_e d[e][j] (examples in order).
+template <typename T>
+__global__ __launch_bounds__(NT) void k_loss_pass2(const T* uN, const T* lamN, T* dW, T* dmu, int B, int q,
+                                                   int nc) {
+  const size_t o = (size_t)blockIdx.x * NT + threadIdx.x;
+  const size_t nw = (size_t)nc * q;
+  if (o >= nw + nc) return;
+  T acc = T(0);
+  if (o < nw) {
+    const size_t j = o / q, i = o - j * q;
+    for (int e = 0; e < B; ++e) acc = fma(lamN[(size_t)e * q + j], uN[(size_t)e * q + i], acc);
+    dW[o] = acc;
+  } else {
+    const size_t j = o - nw;
+    for (int e = 0; e < B; ++e) acc += lamN[(size_t)e * q + j];
+    dmu[j] = acc;
+  }
+}
+
+// Pass 3: lamN[e] = W^T d_e (the row's first nc entries hold d_e on entry).
+template <typename T>
+__global__ __launch_bounds__(NT) void k_loss_pass3(const T* Wc, T* lamN, int B, int q, int nc) {
+  const int e = blockIdx.x * NT + threadIdx.x;
+  if (e >= B) return;
+  T d[MAXNC];
+  for (int j = 0; j < nc; ++j) d[j] = lamN[(size_t)e * q + j];
+  for (int i = 0; i < q; ++i) {
+    T acc = T(0);
+    for (int j = 0; j < nc; ++j) acc = fma(Wc[(size_t)j * q + i], d[j], acc);
+    lamN[(size_t)e * q + i] = acc;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(NT) void k_sgd(size_t n, T lr, const T* g, T* x) {
+  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < n; i += (size_t)gridDim.x * NT)
+    x[i] = x[i] - lr * g[i];
+}
+
+template <typename T, typename F>
+hipError_t with_act(int act, F&& f) {
+  switch (act) {
+    case ACT_TANH: return f(std::integral_constant<int, ACT_TANH>{});
+    case ACT_RELU: return f(std::integral_constant<int, ACT_RELU>{});
+    case ACT_SMOOTHRELU: return f(std::integral_constant<int, ACT_SMOOTHRELU>{});
+    case ACT_IDENTITY: return f(std::integral_constant<int, ACT_IDENTITY>{});
+  }
+  return hipErrorNotSupported;
+}
+
+template <typename T>
+hipError_t open_fwd_t(const Shape& s, int opening, int nf, int B, const void* y, const void* L, void* u0,
+                      hipStream_t st) {
+  const int q = s.C * s.H * s.W;
+  if (opening == 0) {
+    return hipMemcpyAsync(u0, y, (size_t)B * q * sizeof(T), hipMemcpyDeviceToDevice, st);
+  }
+  return with_act<T>(s.act, [&](auto ac) -> hipError_t {
+    constexpr int ACT = decltype(ac)::value;
+    if (opening == 1)
+      k_open_dense<T, ACT><<<grid_for((size_t)B * q), NT, 0, st>>>((const T*)y, (const T*)L, (T*)u0, B, q, nf);
+    else
+      k_open_conv<T, ACT><<<grid_for((size_t)B * q), NT, 0, st>>>((const T*)y, (const T*)L, (T*)u0, B, s.C,
+                                                                  s.H, s.W);
+    return hipGetLastError();
+  });
+}
+
+template <typename T>
+hipError_t open_grad_t(const Shape& s, int opening, int nf, int B, const void* y, const void* L,
+                       const void* lam0, void* dL, hipStream_t st) {
+  const int q = s.C * s.H * s.W;
+  return with_act<T>(s.act, [&](auto ac) -> hipError_t {
+    constexpr int ACT = decltype(ac)::value;
+    if (opening == 1)
+      k_open_grad_dense<T, ACT><<<q, NT, 0, st>>>((const T*)y, (const T*)L, (const T*)lam0, (T*)dL, B, q, nf);
+    else
+      k_open_grad_conv<T, ACT><<<s.C, NT, 0, st>>>((const T*)y, (const T*)L, (const T*)lam0, (T*)dL, B, s.C,
+                                                   s.H, s.W);
+    return hipGetLastError();
+  });
+}
+
+template <typename T>
+hipError_t loss_t(int B, int q, int nc, const void* uN, const void* Wc, const void* mu, const void* c,
+                  double* J, void* lamN, void* dW, void* dmu, hipStream_t st) {
+  k_loss_pass1<T><<<1, 1024, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu, (const T*)c, J, (T*)lamN, B,
+                                      q, nc);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const size_t no = (size_t)nc * q + nc;
+  k_loss_pass2<T><<<(unsigned)((no + NT - 1) / NT), NT, 0, st>>>((const T*)uN, (const T*)lamN, (T*)dW,
+                                                                 (T*)dmu, B, q, nc);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  k_loss_pass3<T><<<(B + NT - 1) / NT, NT, 0, st>>>((const T*)Wc, (T*)lamN, B, q, nc);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_row0, long dst_step,
+                            long count, hipStream_t st) {
+  if (count <= 0 || slice_bytes == 0) return hipSuccess;
+  const size_t units = slice_bytes / 16;
+  k_copy_rows<<<grid_for(units * (size_t)count), NT, 0, st>>>(static_cast<uint4*>(X), units, src_row,
+                                                              dst_row0, dst_step, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_reduce(const double* partial, int n, double* out, hipStream_t st) {
+  k_norm_reduce<<<1, NT, 0, st>>>(partial, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return hipSuccess;
+  k_zero<<<grid_for(bytes / 4), NT, 0, st>>>(static_cast<uint32_t*>(p), bytes / 4);
+  return hipGetLastError();
+}
+
+hipError_t launch_open_forward(const Shape& s, int opening, int nf, int B, const void* y, const void* L,
+                               void* u0, hipStream_t st) {
+  return s.dtype == 0 ? open_fwd_t<float>(s, opening, nf, B, y, L, u0, st)
+                      : open_fwd_t<double>(s, opening, nf, B, y, L, u0, st);
+}
+
+hipError_t launch_open_grad(const Shape& s, int opening, int nf, int B, const void* y, const void* L,
+                            const void* lam0, void* dL, hipStream_t st) {
+  return s.dtype == 0 ? open_grad_t<float>(s, opening, nf, B, y, L, lam0, dL, st)
+                      : open_grad_t<double>(s, opening, nf, B, y, L, lam0, dL, st);
+}
+
+hipError_t launch_loss(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,
+                       const void* c, double* J, void* lamN, void* dW, void* dmu, hipStream_t st) {
+  return dtype == 0 ? loss_t<float>(B, q, nc, uN, Wc, mu, c, J, lamN, dW, dmu, st)
+                    : loss_t<double>(B, q, nc, uN, Wc, mu, c, J, lamN, dW, dmu, st);
+}
+
+hipError_t launch_sgd(int dtype, size_t n, double lr, const void* g, void* x, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  if (dtype == 0) k_sgd<float><<<grid_for(n), NT, 0, st>>>(n, (float)lr, (const float*)g, (float*)x);
+  else k_sgd<double><<<grid_for(n), NT, 0, st>>>(n, lr, (const double*)g, (double*)x);
+  return hipGetLastError();
+}
+
+}  // namespace lp

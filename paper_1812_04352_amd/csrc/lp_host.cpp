@@ -1,0 +1,518 @@
+// Host side of the C ABI (include/lp.h): argument checks, the MGRIT level
+// hierarchy carved out of the caller's workspace, and the V-cycle schedule of
+// Algorithm 1 (Section 3.1) applied recursively, for the state and the adjoint
+// systems. Every step of the computation runs in the HIP kernels; this file
+// only validates, lays out memory and enqueues launches on the caller's stream.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "../../include/lp.h"
+#include "lp_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  if (e == hipErrorNotSupported) return fail(LP_EUNSUPPORTED, "%s: no kernel for this shape", what);
+  return fail(LP_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define LP_TRY(expr, what)                       \
+  do {                                           \
+    hipError_t _e = (expr);                      \
+    if (_e != hipSuccess) return hip_fail(_e, what); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+size_t esize(const lp_problem* p) { return p->dtype == LP_F64 ? 8 : 4; }
+size_t qdim(const lp_problem* p) { return (size_t)p->C * p->H * p->W; }
+size_t slice_bytes(const lp_problem* p) { return (size_t)p->B * qdim(p) * esize(p); }
+
+lp::Shape shape_of(const lp_problem* p) {
+  lp::Shape s;
+  s.dtype = p->dtype;
+  s.layer = p->layer;
+  s.act = p->act;
+  s.C = p->C;
+  s.H = p->H;
+  s.W = p->W;
+  return s;
+}
+
+int check_problem(const lp_problem* p) {
+  if (!p) return fail(LP_EINVAL, "problem is NULL");
+  if (p->abi_version != LP_ABI_VERSION)
+    return fail(LP_EINVAL, "abi_version %d != %d", p->abi_version, LP_ABI_VERSION);
+  if (p->dtype != LP_F32 && p->dtype != LP_F64) return fail(LP_EINVAL, "bad dtype %d", p->dtype);
+  if (p->layer != LP_DENSE && p->layer != LP_CONV3X3) return fail(LP_EINVAL, "bad layer %d", p->layer);
+  if (p->act < LP_TANH || p->act > LP_IDENTITY) return fail(LP_EINVAL, "bad activation %d", p->act);
+  if (p->N < 1) return fail(LP_EINVAL, "N = %d < 1", p->N);
+  if (p->B < 0) return fail(LP_EINVAL, "B = %d < 0", p->B);
+  if (p->C < 1 || p->H < 1 || p->W < 1) return fail(LP_EINVAL, "bad C/H/W %d/%d/%d", p->C, p->H, p->W);
+  if (p->layer == LP_DENSE && (p->H != 1 || p->W != 1)) return fail(LP_EINVAL, "dense layers need H = W = 1");
+  if (!(p->h > 0.0) || !isfinite(p->h)) return fail(LP_EINVAL, "step size h must be finite and > 0");
+  if (!lp::shape_supported(shape_of(p)))
+    return fail(LP_EUNSUPPORTED, "no kernel for dtype %d layer %d C=%d H=%d W=%d", p->dtype, p->layer, p->C,
+                p->H, p->W);
+  return LP_OK;
+}
+
+int check_mgrit(const lp_problem* p, const lp_mgrit* m, std::vector<int>& sizes) {
+  if (!m) return fail(LP_EINVAL, "mgrit options are NULL");
+  if (m->cf < 2) return fail(LP_EINVAL, "coarsening factor %d < 2", m->cf);
+  if (m->max_levels < 1) return fail(LP_EINVAL, "max_levels %d < 1", m->max_levels);
+  if (m->min_coarse < 1) return fail(LP_EINVAL, "min_coarse %d < 1", m->min_coarse);
+  if (m->relax != LP_RELAX_F && m->relax != LP_RELAX_FCF) return fail(LP_EINVAL, "bad relax %d", m->relax);
+  if (m->max_iter < 1) return fail(LP_EINVAL, "max_iter %d < 1", m->max_iter);
+  if (!(m->rtol >= 0.0) || !(m->stag >= 0.0)) return fail(LP_EINVAL, "rtol and stag must be >= 0");
+  sizes.assign(1, p->N);
+  while ((int)sizes.size() < m->max_levels && sizes.back() > m->min_coarse) {
+    if (sizes.back() % m->cf)
+      return fail(LP_EINVAL, "level %d has N_l = %d, not divisible by cf = %d", (int)sizes.size() - 1,
+                  sizes.back(), m->cf);
+    sizes.push_back(sizes.back() / m->cf);
+  }
+  return LP_OK;
+}
+
+// Workspace layout for one MGRIT solve.
+struct Layout {
+  std::vector<size_t> X, G, S;  // byte offsets per level (X[0], G[0] unused)
+  size_t partial = 0, rho = 0, total = 0;
+  int partial_cap = 0;
+};
+
+int partial_capacity(const lp_problem* p) {
+  const int tile = lp::min_tile(shape_of(p));
+  const long tiles = (p->B + tile - 1) / tile;
+  return (int)((long)(p->N + 1) * (tiles > 0 ? tiles : 1));
+}
+
+Layout mgrit_layout(const lp_problem* p, const lp_mgrit* m, const std::vector<int>& sizes) {
+  Layout L;
+  const size_t sl = slice_bytes(p);
+  const int nl = (int)sizes.size();
+  L.X.assign(nl, 0);
+  L.G.assign(nl, 0);
+  L.S.assign(nl, 0);
+  size_t off = 0;
+  for (int l = 1; l < nl; ++l) {
+    L.X[l] = off;
+    off = up(off + (size_t)(sizes[l] + 1) * sl);
+    L.G[l] = off;
+    off = up(off + (size_t)(sizes[l] + 1) * sl);
+  }
+  if (m->relax == LP_RELAX_FCF) {
+    for (int l = 0; l + 1 < nl; ++l) {
+      L.S[l] = off;
+      off = up(off + (size_t)(sizes[l + 1] + 1) * sl);
+    }
+  }
+  L.partial_cap = partial_capacity(p);
+  L.partial = off;
+  off = up(off + (size_t)L.partial_cap * sizeof(double));
+  L.rho = off;
+  off = up(off + (size_t)(m->max_iter + 1) * sizeof(double));
+  L.total = off;
+  return L;
+}
+
+size_t grad_bytes(const lp_problem* p) {
+  const lp::Shape s = shape_of(p);
+  const size_t nch = (size_t)lp::grad_chunks(s, p->B, p->N);
+  return up((size_t)p->N * nch * lp::grad_nout(s) * esize(p));
+}
+
+size_t resid_bytes(const lp_problem* p) {
+  return up((size_t)partial_capacity(p) * sizeof(double)) + up(sizeof(double));
+}
+
+int check_ws(const void* ws, size_t have, size_t need) {
+  if (need == 0) return LP_OK;
+  if (!ws) return fail(LP_EWORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if ((uintptr_t)ws % kAlign) return fail(LP_EWORKSPACE, "workspace is not %zu-byte aligned", kAlign);
+  if (have < need) return fail(LP_EWORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return LP_OK;
+}
+
+// One MGRIT solve (state or adjoint) over the hierarchy.
+struct Solver {
+  const lp_problem* p;
+  const lp_mgrit* m;
+  lp::Shape sh;
+  int dir;
+  const void* K;
+  const void* b;
+  const void* Uf;  // fine primal trajectory (adjoint)
+  std::vector<int> sizes;
+  std::vector<void*> X, G, S;
+  double* partial;
+  hipStream_t st;
+  int partials_used = 0;
+
+  long stride(int l) const {
+    long s = 1;
+    for (int i = 0; i < l; ++i) s *= m->cf;
+    return s;
+  }
+
+  int cycle(int l) {
+    const int L = (int)sizes.size();
+    const double hl = p->h * (double)stride(l);
+    if (l == L - 1) {
+      lp::SerialArgs a{p->act, K, b, Uf, p->B, sizes[l], stride(l), hl, X[l], G[l]};
+      LP_TRY(lp::launch_serial(sh, dir, a, st), "coarsest-level solve");
+      return LP_OK;
+    }
+    const bool fcf = m->relax == LP_RELAX_FCF;
+    lp::SweepArgs a{};
+    a.act = p->act;
+    a.K = K;
+    a.b = b;
+    a.Uf = Uf;
+    a.B = p->B;
+    a.Nl = sizes[l];
+    a.c = m->cf;
+    a.stride = stride(l);
+    a.hl = hl;
+    a.hc = hl * (double)m->cf;
+    a.X = X[l];
+    a.G = G[l];
+    a.S = S[l];
+    a.finest = l == 0;
+    a.mode = lp::SWEEP_FC;
+    if (fcf) LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "FC-relaxation");
+    a.Cs = fcf ? S[l] : X[l];
+    a.cs_stride = fcf ? 1 : m->cf;
+    a.Xn = X[l + 1];
+    a.Gn = G[l + 1];
+    a.xn_every = (l + 1 < L - 1) ? m->cf : 0;
+    a.partial = l == 0 ? partial : nullptr;
+    int np = 0;
+    a.mode = lp::SWEEP_FRES;
+    LP_TRY(lp::launch_sweep(sh, dir, a, st, &np), "F-relaxation and restriction");
+    if (l == 0) partials_used = np;
+    int rc = cycle(l + 1);
+    if (rc != LP_OK) return rc;
+    a.V = X[l + 1];
+    a.mode = lp::SWEEP_CORRF;
+    a.partial = nullptr;
+    LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "correction and F-relaxation");
+    return LP_OK;
+  }
+};
+
+int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, const void* b,
+                const void* U, void* Xuser, void* ws, size_t ws_bytes, double* res_hist, int32_t* iters,
+                void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  std::vector<int> sizes;
+  rc = check_mgrit(p, m, sizes);
+  if (rc) return rc;
+  if (!K || !b || (p->B && (!Xuser || (dir == lp::DIR_ADJ && !U))))
+    return fail(LP_EINVAL, "NULL array argument");
+  if (p->B && dir == lp::DIR_ADJ && U == Xuser) return fail(LP_EINVAL, "U and Lam alias");
+  if (iters) *iters = 0;
+  if (p->B == 0) return LP_OK;
+  const Layout lay = mgrit_layout(p, m, sizes);
+  rc = check_ws(ws, ws_bytes, lay.total);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  const int L = (int)sizes.size();
+  Solver s;
+  s.p = p;
+  s.m = m;
+  s.sh = shape_of(p);
+  s.dir = dir;
+  s.K = K;
+  s.b = b;
+  s.Uf = U;
+  s.sizes = sizes;
+  s.X.assign(L, nullptr);
+  s.G.assign(L, nullptr);
+  s.S.assign(L, nullptr);
+  s.X[0] = Xuser;
+  for (int l = 1; l < L; ++l) {
+    s.X[l] = w + lay.X[l];
+    s.G[l] = w + lay.G[l];
+  }
+  if (m->relax == LP_RELAX_FCF)
+    for (int l = 0; l + 1 < L; ++l) s.S[l] = w + lay.S[l];
+  s.partial = reinterpret_cast<double*>(w + lay.partial);
+  s.st = st;
+  double* rho = reinterpret_cast<double*>(w + lay.rho);
+  const size_t sl = slice_bytes(p);
+  const int c = m->cf;
+  const int Nc = p->N / c;
+
+  if (!m->warm_start && L > 1) {
+    // cold start: every C-point is a copy of the fixed boundary row
+    if (dir == lp::DIR_FWD) LP_TRY(lp::launch_copy_rows(Xuser, sl, 0, c, c, Nc, st), "cold start");
+    else LP_TRY(lp::launch_copy_rows(Xuser, sl, p->N, 0, c, Nc, st), "cold start");
+  }
+  const bool early = m->rtol > 0.0 || m->stag > 0.0;
+  std::vector<double> hist;
+  int it = 0;
+  for (int mi = 0; mi < m->max_iter; ++mi) {
+    rc = s.cycle(0);
+    if (rc) return rc;
+    if (L > 1) LP_TRY(lp::launch_norm_reduce(s.partial, s.partials_used, rho + mi, st), "residual norm");
+    else LP_TRY(lp::launch_zero(rho + mi, sizeof(double), st), "residual norm");
+    it = mi + 1;
+    if (early) {
+      double r = 0.0;
+      LP_TRY(hipMemcpyAsync(&r, rho + mi, sizeof(double), hipMemcpyDeviceToHost, st), "read residual");
+      LP_TRY(hipStreamSynchronize(st), "stream sync");
+      hist.push_back(r);
+      if (!isfinite(r)) break;
+      if (m->rtol > 0.0 && r <= m->rtol * hist[0]) break;
+      if (m->stag > 0.0 && mi > 0 && r > m->stag * hist[mi - 1]) break;
+    }
+  }
+  if (!early) {
+    hist.assign(it, 0.0);
+    LP_TRY(hipMemcpyAsync(hist.data(), rho, it * sizeof(double), hipMemcpyDeviceToHost, st), "read residuals");
+    LP_TRY(hipStreamSynchronize(st), "stream sync");
+  }
+  if (res_hist) memcpy(res_hist, hist.data(), it * sizeof(double));
+  if (iters) *iters = it;
+  for (double r : hist)
+    if (!isfinite(r)) return fail(LP_ENONFINITE, "residual norm is not finite");
+  return LP_OK;
+}
+
+}  // namespace
+
+namespace lp {
+
+bool dense_width_supported(int q) { return q == 8 || q == 16 || q == 32 || q == 64; }
+
+int dense_grad_chunks(int B, int N) {
+  // enough workgroups to fill the chip when N is small; at least 64 examples per chunk
+  const int want = (2048 + N - 1) / N;
+  const int most = (B + 63) / 64;
+  const int ch = want < most ? want : most;
+  return ch < 1 ? 1 : ch;
+}
+
+bool shape_supported(const Shape& s) {
+  if (s.layer == 0) return s.H == 1 && s.W == 1 && dense_width_supported(s.C);
+  return conv_supported(s);
+}
+
+int min_tile(const Shape& s) { return s.layer == 0 ? 32 : conv_tile(s); }
+
+int grad_chunks(const Shape& s, int B, int N) {
+  return s.layer == 0 ? dense_grad_chunks(B, N) : conv_grad_chunks(B, N);
+}
+
+int grad_nout(const Shape& s) { return s.layer == 0 ? s.C * s.C + s.C : s.C * s.C * 9 + s.C; }
+
+hipError_t launch_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials) {
+  if (s.layer != 0) return conv_sweep(s, dir, a, st, partials);
+  return s.dtype == 0 ? dense_sweep_f32(s.C, dir, a, st, partials) : dense_sweep_f64(s.C, dir, a, st, partials);
+}
+
+hipError_t launch_serial(const Shape& s, int dir, const SerialArgs& a, hipStream_t st) {
+  if (s.layer != 0) return conv_serial(s, dir, a, st);
+  return s.dtype == 0 ? dense_serial_f32(s.C, dir, a, st) : dense_serial_f64(s.C, dir, a, st);
+}
+
+hipError_t launch_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t st, int* partials) {
+  if (s.layer != 0) return conv_resid(s, dir, a, st, partials);
+  return s.dtype == 0 ? dense_resid_f32(s.C, dir, a, st, partials) : dense_resid_f64(s.C, dir, a, st, partials);
+}
+
+hipError_t launch_grad(const Shape& s, const GradArgs& a, hipStream_t st) {
+  if (s.layer != 0) return conv_grad(s, a, st);
+  return s.dtype == 0 ? dense_grad_f32(s.C, a, st) : dense_grad_f64(s.C, a, st);
+}
+
+}  // namespace lp
+
+extern "C" {
+
+int32_t lp_abi_version(void) { return LP_ABI_VERSION; }
+
+const char* lp_status_string(int32_t s) {
+  switch (s) {
+    case LP_OK: return "ok";
+    case LP_EINVAL: return "invalid argument";
+    case LP_EUNSUPPORTED: return "unsupported";
+    case LP_EWORKSPACE: return "workspace too small or misaligned";
+    case LP_EHIP: return "HIP runtime error";
+    case LP_ENONFINITE: return "non-finite residual";
+  }
+  return "unknown status";
+}
+
+const char* lp_last_error(void) { return g_err.c_str(); }
+
+size_t lp_workspace_bytes(const lp_problem* p, const lp_mgrit* m) {
+  if (check_problem(p) != LP_OK) return 0;
+  size_t need = std::max(grad_bytes(p), resid_bytes(p));
+  if (m) {
+    std::vector<int> sizes;
+    if (check_mgrit(p, m, sizes) != LP_OK) return 0;
+    need = std::max(need, mgrit_layout(p, m, sizes).total);
+  }
+  g_err.clear();
+  return need;
+}
+
+int32_t lp_serial_forward(const lp_problem* p, const void* K, const void* b, void* U, void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  if (!K || !b || (p->B && !U)) return fail(LP_EINVAL, "NULL array argument");
+  if (p->B == 0) return LP_OK;
+  lp::SerialArgs a{p->act, K, b, nullptr, p->B, p->N, 1, p->h, U, nullptr};
+  LP_TRY(lp::launch_serial(shape_of(p), lp::DIR_FWD, a, static_cast<hipStream_t>(stream)), "serial forward");
+  return LP_OK;
+}
+
+int32_t lp_serial_adjoint(const lp_problem* p, const void* K, const void* b, const void* U, void* Lam,
+                          void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  if (!K || !b || (p->B && (!U || !Lam))) return fail(LP_EINVAL, "NULL array argument");
+  if (p->B && U == Lam) return fail(LP_EINVAL, "U and Lam alias");
+  if (p->B == 0) return LP_OK;
+  lp::SerialArgs a{p->act, K, b, U, p->B, p->N, 1, p->h, Lam, nullptr};
+  LP_TRY(lp::launch_serial(shape_of(p), lp::DIR_ADJ, a, static_cast<hipStream_t>(stream)), "serial adjoint");
+  return LP_OK;
+}
+
+int32_t lp_mgrit_forward(const lp_problem* p, const lp_mgrit* m, const void* K, const void* b, void* U,
+                         void* ws, size_t ws_bytes, double* res_hist, int32_t* iters, void* stream) {
+  return mgrit_solve(p, m, lp::DIR_FWD, K, b, nullptr, U, ws, ws_bytes, res_hist, iters, stream);
+}
+
+int32_t lp_mgrit_adjoint(const lp_problem* p, const lp_mgrit* m, const void* K, const void* b, const void* U,
+                         void* Lam, void* ws, size_t ws_bytes, double* res_hist, int32_t* iters,
+                         void* stream) {
+  return mgrit_solve(p, m, lp::DIR_ADJ, K, b, U, Lam, ws, ws_bytes, res_hist, iters, stream);
+}
+
+int32_t lp_gradient(const lp_problem* p, const void* K, const void* b, const void* U, const void* Lam,
+                    void* dK, void* db, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  if (!K || !b || !dK || !db || (p->B && (!U || !Lam))) return fail(LP_EINVAL, "NULL array argument");
+  const lp::Shape s = shape_of(p);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (p->B == 0) {
+    const size_t nw = (size_t)p->N * (lp::grad_nout(s) - p->C) * esize(p);
+    LP_TRY(lp::launch_zero(dK, nw, st), "zero gradient");
+    LP_TRY(lp::launch_zero(db, (size_t)p->N * p->C * esize(p), st), "zero gradient");
+    return LP_OK;
+  }
+  rc = check_ws(ws, ws_bytes, grad_bytes(p));
+  if (rc) return rc;
+  lp::GradArgs a{p->act, K, b, U, Lam, p->B, p->N, p->h, ws, lp::grad_chunks(s, p->B, p->N), dK, db};
+  LP_TRY(lp::launch_grad(s, a, st), "gradient");
+  return LP_OK;
+}
+
+int32_t lp_residual_norm(const lp_problem* p, int32_t which, const void* K, const void* b, const void* U,
+                         const void* Lam, void* ws, size_t ws_bytes, double* norm, void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  if (which != LP_STATE && which != LP_ADJOINT) return fail(LP_EINVAL, "bad system %d", which);
+  if (!K || !b || !norm || (p->B && (!U || (which == LP_ADJOINT && !Lam))))
+    return fail(LP_EINVAL, "NULL array argument");
+  if (p->B == 0) {
+    *norm = 0.0;
+    return LP_OK;
+  }
+  rc = check_ws(ws, ws_bytes, resid_bytes(p));
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  double* partial = static_cast<double*>(ws);
+  double* out = reinterpret_cast<double*>(static_cast<char*>(ws) + up((size_t)partial_capacity(p) * sizeof(double)));
+  lp::ResidArgs a{p->act, K, b, U, Lam, p->B, p->N, p->h, partial};
+  int np = 0;
+  LP_TRY(lp::launch_resid(shape_of(p), which == LP_STATE ? lp::DIR_FWD : lp::DIR_ADJ, a, st, &np), "residual");
+  LP_TRY(lp::launch_norm_reduce(partial, np, out, st), "residual norm");
+  LP_TRY(hipMemcpyAsync(norm, out, sizeof(double), hipMemcpyDeviceToHost, st), "read residual norm");
+  LP_TRY(hipStreamSynchronize(st), "stream sync");
+  if (!isfinite(*norm)) return fail(LP_ENONFINITE, "residual norm is not finite");
+  return LP_OK;
+}
+
+int32_t lp_open_forward(const lp_problem* p, int32_t opening, int32_t nf, const void* y, const void* L_in,
+                        void* u0, void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  if (opening < LP_OPEN_IDENTITY || opening > LP_OPEN_CONV_ACT) return fail(LP_EINVAL, "bad opening %d", opening);
+  if ((p->B && (!y || !u0)) || (opening != LP_OPEN_IDENTITY && !L_in)) return fail(LP_EINVAL, "NULL array argument");
+  if (opening == LP_OPEN_DENSE_ACT && (p->layer != LP_DENSE || nf < 1))
+    return fail(LP_EINVAL, "dense opening needs a dense problem and nf >= 1");
+  if (opening == LP_OPEN_CONV_ACT && p->layer != LP_CONV3X3) return fail(LP_EINVAL, "conv opening needs a conv problem");
+  if (p->B == 0) return LP_OK;
+  LP_TRY(lp::launch_open_forward(shape_of(p), opening, nf, p->B, y, L_in, u0, static_cast<hipStream_t>(stream)),
+         "opening layer");
+  return LP_OK;
+}
+
+int32_t lp_open_grad(const lp_problem* p, int32_t opening, int32_t nf, const void* y, const void* L_in,
+                     const void* lam0, void* dL_in, void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  if (opening != LP_OPEN_DENSE_ACT && opening != LP_OPEN_CONV_ACT)
+    return fail(LP_EINVAL, "opening %d has no weights", opening);
+  if (!L_in || !dL_in || (p->B && (!y || !lam0))) return fail(LP_EINVAL, "NULL array argument");
+  if (opening == LP_OPEN_DENSE_ACT && (p->layer != LP_DENSE || nf < 1 || nf > 1024))
+    return fail(LP_EINVAL, "dense opening needs a dense problem and 1 <= nf <= 1024");
+  if (opening == LP_OPEN_CONV_ACT && p->layer != LP_CONV3X3) return fail(LP_EINVAL, "conv opening needs a conv problem");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (p->B == 0) {
+    const size_t n = opening == LP_OPEN_DENSE_ACT ? (size_t)p->C * nf : (size_t)p->C * 9;
+    LP_TRY(lp::launch_zero(dL_in, n * esize(p), st), "zero gradient");
+    return LP_OK;
+  }
+  LP_TRY(lp::launch_open_grad(shape_of(p), opening, nf, p->B, y, L_in, lam0, dL_in, st), "opening gradient");
+  return LP_OK;
+}
+
+int32_t lp_loss_terminal(const lp_problem* p, int32_t nc, const void* uN, const void* W, const void* mu,
+                         const void* c, double* J, void* lamN, void* dW, void* dmu, void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  if (nc < 1 || nc > 64 || (size_t)nc > qdim(p)) return fail(LP_EINVAL, "need 1 <= nc <= min(64, q), nc = %d", nc);
+  if (!uN || !W || !mu || !c || !J || !lamN || !dW || !dmu) return fail(LP_EINVAL, "NULL array argument");
+  if (p->B == 0) return fail(LP_EINVAL, "the mean loss needs B >= 1");
+  LP_TRY(lp::launch_loss(p->dtype, p->B, (int)qdim(p), nc, uN, W, mu, c, J, lamN, dW, dmu,
+                         static_cast<hipStream_t>(stream)),
+         "loss");
+  return LP_OK;
+}
+
+int32_t lp_sgd_update(int32_t dtype, size_t n, double lr, const void* g, void* x, void* stream) {
+  if (dtype != LP_F32 && dtype != LP_F64) return fail(LP_EINVAL, "bad dtype %d", dtype);
+  if (n && (!g || !x)) return fail(LP_EINVAL, "NULL array argument");
+  LP_TRY(lp::launch_sgd(dtype, n, lr, g, x, static_cast<hipStream_t>(stream)), "sgd update");
+  return LP_OK;
+}
+
+}  // extern "C"

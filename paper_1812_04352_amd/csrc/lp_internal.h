@@ -1,0 +1,137 @@
+// Internal interface between the host scheduler (lp_host.cpp) and the kernel
+// launchers. Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lp {
+
+enum Dir { DIR_FWD = 0, DIR_ADJ = 1 };
+
+// One interval sweep on MGRIT level l. Interval k covers level points kc..(k+1)c.
+enum SweepMode {
+  SWEEP_FC = 0,    // F- then C-relaxation from the C-points of X; relaxed C-points -> S
+  SWEEP_FRES = 1,  // F-relaxation from the relaxed C-points, residual, FAS restriction
+  SWEEP_CORRF = 2  // coarse-grid correction of the C-points, then F-relaxation writing X
+};
+
+struct SweepArgs {
+  int act;             // activation (uniform)
+  int mode;            // SweepMode
+  const void* K;       // fine weights [N][q][q] (conv [N][C][C][3][3])
+  const void* b;       // fine bias [N][q] (conv [N][C])
+  const void* Uf;      // fine primal trajectory [N+1][B][q] (adjoint steps only)
+  int B;               // batch
+  int Nl;              // steps on this level
+  int c;               // coarsening factor
+  long stride;         // c^l: level point i uses fine weights (and adjoint state) i*stride
+  double hl, hc;       // step on this level and on the next coarser level
+  void* X;             // level trajectory: forward U_l, adjoint Lam_l
+  const void* G;       // level right-hand side (nullptr: zero rows, the finest level)
+  const void* Cs;      // relaxed C-points: C_k at Cs + k * cs_stride slices
+  long cs_stride;
+  void* S;             // FC: staging of the relaxed C-points, N_l/c + 1 slices
+  void* Xn;            // FRES: next level trajectory
+  void* Gn;            // FRES: next level right-hand side
+  int xn_every;        // FRES: write Xn[k] when k % xn_every == 0 (<= 0: boundary point only)
+  const void* V;       // CORRF: next level solution
+  double* partial;     // FRES: per-workgroup sum of squared residuals (nullable)
+  int finest;          // 1 on level 0: the fixed boundary row (u^0 or lam^N) is never written
+};
+
+// Serial (coarsest level or layer-serial) solve of X over Nl steps.
+struct SerialArgs {
+  int act;
+  const void* K;
+  const void* b;
+  const void* Uf;      // adjoint only
+  int B;
+  int Nl;
+  long stride;
+  double hl;
+  void* X;
+  const void* G;       // nullable
+};
+
+struct ResidArgs {
+  int act;
+  const void* K;
+  const void* b;
+  const void* U;
+  const void* Lam;     // adjoint only
+  int B;
+  int N;
+  double h;
+  double* partial;     // one per workgroup
+};
+
+struct GradArgs {
+  int act;
+  const void* K;
+  const void* b;
+  const void* U;
+  const void* Lam;
+  int B;
+  int N;
+  double h;
+  void* partial;       // [N][nchunks][nout] in the problem dtype
+  int nchunks;
+  void* dK;
+  void* db;
+};
+
+struct Shape {
+  int dtype;   // 0 f32, 1 f64
+  int layer;   // 0 dense, 1 conv
+  int act;
+  int C, H, W; // dense: C = q
+};
+
+// Launchers. Each returns hipSuccess, hipErrorNotSupported for a shape with no
+// kernel, or the launch error. *partials (when non-null) receives the number of
+// residual partials the launch writes.
+hipError_t launch_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials);
+hipError_t launch_serial(const Shape& s, int dir, const SerialArgs& a, hipStream_t st);
+hipError_t launch_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t st, int* partials);
+hipError_t launch_grad(const Shape& s, const GradArgs& a, hipStream_t st);
+int grad_chunks(const Shape& s, int B, int N);  // batch chunks of the gradient's first pass
+int grad_nout(const Shape& s);            // weights + bias entries per layer
+bool shape_supported(const Shape& s);
+int min_tile(const Shape& s);             // fewest examples any sweep/residual workgroup covers
+
+// Dense VALU family (lp_dense_impl.h, instantiated per dtype in lp_dense_f32.hip / lp_dense_f64.hip)
+#define LP_DENSE_DECL(SFX)                                                                          \
+  hipError_t dense_sweep_##SFX(int q, int dir, const SweepArgs& a, hipStream_t st, int* partials);  \
+  hipError_t dense_serial_##SFX(int q, int dir, const SerialArgs& a, hipStream_t st);               \
+  hipError_t dense_resid_##SFX(int q, int dir, const ResidArgs& a, hipStream_t st, int* partials);  \
+  hipError_t dense_grad_##SFX(int q, const GradArgs& a, hipStream_t st);
+LP_DENSE_DECL(f32)
+LP_DENSE_DECL(f64)
+bool dense_width_supported(int q);
+int dense_grad_chunks(int B, int N);
+
+// Conv family (lp_conv.hip)
+hipError_t conv_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials);
+hipError_t conv_serial(const Shape& s, int dir, const SerialArgs& a, hipStream_t st);
+hipError_t conv_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t st, int* partials);
+hipError_t conv_grad(const Shape& s, const GradArgs& a, hipStream_t st);
+bool conv_supported(const Shape& s);
+int conv_grad_chunks(int B, int N);
+int conv_tile(const Shape& s);
+
+// Common kernels (lp_common.hip)
+hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_row0,
+                            long dst_step, long count, hipStream_t st);
+hipError_t launch_norm_reduce(const double* partial, int n, double* out, hipStream_t st);
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);
+hipError_t launch_open_forward(const Shape& s, int opening, int nf, int B, const void* y, const void* L,
+                               void* u0, hipStream_t st);
+hipError_t launch_open_grad(const Shape& s, int opening, int nf, int B, const void* y, const void* L,
+                            const void* lam0, void* dL, hipStream_t st);
+hipError_t launch_loss(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,
+                       const void* c, double* J, void* lamN, void* dW, void* dmu, hipStream_t st);
+hipError_t launch_sgd(int dtype, size_t n, double lr, const void* g, void* x, hipStream_t st);
+
+}  // namespace lp

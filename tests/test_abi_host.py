@@ -1,0 +1,126 @@
+"""The C-ABI library on the CPU host (no GPU): it loads, exports every symbol the
+header declares, and its host-side argument checks return the documented
+status codes before any device work is enqueued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1812_04352_amd import lp as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_symbols():
+    text = open(os.path.join(ROOT, "include", "lp.h")).read()
+    return sorted(set(re.findall(r"\b(lp_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = L.load()
+    declared = header_symbols()
+    assert declared, "no declarations found"
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(L.EXPORTS) == declared
+
+
+def test_version_and_status_strings():
+    lib = L.load()
+    assert lib.lp_abi_version() == L.LP_ABI_VERSION
+    for s in range(6):
+        assert lib.lp_status_string(s)
+    assert lib.lp_status_string(99) == b"unknown status"
+
+
+def _p(**kw):
+    base = dict(dtype="f32", layer="dense", act="tanh", N=64, B=100, C=32, h=0.1)
+    base.update(kw)
+    return L.problem(**base)
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every case fails host validation first
+
+
+def test_problem_validation_codes():
+    lib = L.load()
+    null = ctypes.c_void_p(0)
+    assert lib.lp_serial_forward(None, FAKE, FAKE, FAKE, null) == L.LP_EINVAL
+    p = _p()
+    p.abi_version = 7
+    assert lib.lp_serial_forward(ctypes.byref(p), FAKE, FAKE, FAKE, null) == L.LP_EINVAL
+    assert b"abi_version" in lib.lp_last_error()
+    for bad in (dict(N=0), dict(B=-1), dict(h=0.0), dict(h=float("nan")), dict(C=0)):
+        assert lib.lp_serial_forward(ctypes.byref(_p(**bad)), FAKE, FAKE, FAKE, null) == L.LP_EINVAL, bad
+    p = _p()
+    p.act = 9
+    assert lib.lp_serial_forward(ctypes.byref(p), FAKE, FAKE, FAKE, null) == L.LP_EINVAL
+    # a width with no kernel is a valid but unsupported problem
+    assert lib.lp_serial_forward(ctypes.byref(_p(C=48)), FAKE, FAKE, FAKE, null) == L.LP_EUNSUPPORTED
+    # NULL arrays
+    assert lib.lp_serial_forward(ctypes.byref(_p()), None, FAKE, FAKE, null) == L.LP_EINVAL
+
+
+def test_mgrit_validation_codes():
+    lib = L.load()
+    p = _p(N=48)
+    hist = (ctypes.c_double * 4)()
+    it = ctypes.c_int32(-1)
+
+    def call(mg, ws=FAKE, nbytes=1 << 40):
+        return lib.lp_mgrit_forward(ctypes.byref(p), ctypes.byref(mg), FAKE, FAKE, FAKE, ws, nbytes, hist,
+                                    ctypes.byref(it), None)
+
+    assert call(L.mgrit(cf=1)) == L.LP_EINVAL
+    assert call(L.mgrit(max_iter=0)) == L.LP_EINVAL
+    assert call(L.mgrit(max_levels=0)) == L.LP_EINVAL
+    # 48 -> 12 -> 3 is fine with cf = 4, but 12 is not divisible by 5 and 48 % 5 != 0
+    assert call(L.mgrit(cf=5, max_levels=2)) == L.LP_EINVAL
+    assert b"divisible" in lib.lp_last_error()
+    assert call(L.mgrit(cf=4, max_levels=4)) == L.LP_EINVAL  # 48 -> 12 -> 3 -> (3 % 4 != 0)
+    # workspace checks happen before any launch
+    mg = L.mgrit(cf=4, max_levels=3)
+    need = L.lp_workspace_bytes(p, mg)
+    assert call(mg, ws=None) == L.LP_EWORKSPACE
+    assert call(mg, ws=ctypes.c_void_p(0x1001)) == L.LP_EWORKSPACE  # misaligned
+    assert call(mg, nbytes=need - 1) == L.LP_EWORKSPACE
+    # adjoint: U and Lam must not alias
+    assert lib.lp_mgrit_adjoint(ctypes.byref(p), ctypes.byref(mg), FAKE, FAKE, FAKE, FAKE, FAKE, need, hist,
+                                ctypes.byref(it), None) == L.LP_EINVAL
+
+
+def test_workspace_sizes():
+    # config-3 shaped problem: 2048 -> 512 -> 128 -> 32 -> 8 with FCF staging
+    p = L.problem("f32", "dense", "tanh", 2048, 16384, 64, h=1 / 256)
+    mg = L.mgrit(cf=4, max_levels=16, min_coarse=8, max_iter=20)
+    slice_bytes = 16384 * 64 * 4
+    coarse = sum(n + 1 for n in (512, 128, 32, 8)) * 2 * slice_bytes
+    staging = sum(n + 1 for n in (512, 128, 32, 8)) * slice_bytes
+    got = L.lp_workspace_bytes(p, mg)
+    assert coarse + staging <= got <= coarse + staging + 64 << 20
+    # F-relaxation needs no staging
+    assert L.lp_workspace_bytes(p, L.mgrit(cf=4, max_levels=16, min_coarse=8, relax="F", max_iter=20)) < got
+    with pytest.raises(L.LpError):
+        L.lp_workspace_bytes(L.problem("f32", "dense", "tanh", 2048, 16384, 48, h=0.1))
+
+
+def test_helper_validation_codes():
+    lib = L.load()
+    p = _p()
+    J = ctypes.c_void_p(0x2000)
+    assert lib.lp_loss_terminal(ctypes.byref(p), 0, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, None) == L.LP_EINVAL
+    assert lib.lp_loss_terminal(ctypes.byref(p), 33, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, None) == L.LP_EINVAL
+    assert lib.lp_open_forward(ctypes.byref(p), 5, 3, FAKE, FAKE, FAKE, None) == L.LP_EINVAL
+    assert lib.lp_open_grad(ctypes.byref(p), L.LP_OPEN_IDENTITY, 3, FAKE, FAKE, FAKE, FAKE, None) == L.LP_EINVAL
+    assert lib.lp_sgd_update(7, 10, 0.1, FAKE, FAKE, None) == L.LP_EINVAL
+    assert lib.lp_residual_norm(ctypes.byref(p), 5, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30,
+                                ctypes.byref(ctypes.c_double()), None) == L.LP_EINVAL
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    p = _p(N=4, B=3, C=8)
+    K = torch.zeros(4, 8, 8)
+    with pytest.raises(ValueError):
+        L.lp_serial_forward(p, K, torch.zeros(4, 8), torch.zeros(5, 3, 8))

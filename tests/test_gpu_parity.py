@@ -1,0 +1,209 @@
+"""GPU parity: the HIP library (called through its C ABI) against the fp64 oracle
+on the same seeded inputs. Sizes here are ones the oracle finishes in seconds and
+still span several workgroup tiles and a ragged batch tail; the full workload
+sizes are checked on sampled examples in test_gpu_fullsize.py."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_1812_04352_amd import lp as L
+from workloads import WORKLOADS, random_state
+from lp_testutil import Case, assert_close, sched, tdt
+
+pytestmark = pytest.mark.gpu
+
+# (name, workload) at parity-test sizes
+DENSE = [
+    ("tiny_f64", WORKLOADS[1]),
+    ("relu32", WORKLOADS[2].with_overrides(N=64, B=300)),
+    ("tanh64", WORKLOADS[3].with_overrides(N=128, B=300)),
+    ("tanh32", WORKLOADS[5].with_overrides(N=64, B=513, n_features=40)),
+    ("srelu16_f64", WORKLOADS[1].with_overrides(C=16, act="smoothrelu", N=48, B=257)),
+    ("relu8_f32", WORKLOADS[2].with_overrides(C=8, N=32, B=77, n_features=12, n_classes=5)),
+]
+IDS = [n for n, _ in DENSE]
+
+_cache = {}
+
+
+def case(wl):
+    key = repr(wl)
+    if key not in _cache:
+        _cache[key] = Case(wl)
+    return _cache[key]
+
+
+def _lamN(c, U_gpu):
+    """Terminal adjoint value on each side from its own network output."""
+    wl = c.wl
+    J = torch.zeros(1, device="cuda", dtype=torch.float64)
+    lamN = torch.empty_like(U_gpu[-1])
+    dW = torch.empty_like(c.W)
+    dmu = torch.empty_like(c.mu)
+    L.lp_loss_terminal(c.p, wl.n_classes, U_gpu[-1], c.W, c.mu, c.onehot, J, lamN, dW, dmu)
+    return lamN, J, dW, dmu
+
+
+@pytest.mark.parametrize("name,wl", DENSE, ids=IDS)
+def test_open_forward(name, wl):
+    c = case(wl)
+    assert_close(c.u0.cpu().numpy(), c.u0_ref, wl.dtype, "u0")
+
+
+@pytest.mark.parametrize("name,wl", DENSE, ids=IDS)
+def test_serial_forward_and_adjoint(name, wl):
+    c = case(wl)
+    U = c.new_traj()
+    L.lp_serial_forward(c.p, c.K, c.b, U)
+    Uref = O.serial_forward(c.u0_ref, c.d["K"], c.d["b"], wl.h, wl.act)
+    assert_close(U.cpu().numpy(), Uref, wl.dtype, "U")
+    lamN, J, dW, dmu = _lamN(c, U)
+    Jr, lamNr, dWr, dmur = O.loss_terminal(Uref[-1], c.d["W"], c.d["mu"], c.d["onehot"])
+    assert abs(J.item() - Jr) <= 10 * {"f32": 1e-6, "f64": 1e-14}[wl.dtype] * abs(Jr)
+    assert_close(lamN.cpu().numpy(), lamNr, wl.dtype, "lamN")
+    assert_close(dW.cpu().numpy(), dWr, wl.dtype, "dW")
+    assert_close(dmu.cpu().numpy(), dmur, wl.dtype, "dmu")
+    Lam = torch.zeros_like(U)
+    Lam[-1] = lamN
+    L.lp_serial_adjoint(c.p, c.K, c.b, U, Lam)
+    Lref = O.serial_adjoint(Uref, lamNr, c.d["K"], c.d["b"], wl.h, wl.act)
+    assert_close(Lam.cpu().numpy(), Lref, wl.dtype, "Lam")
+    # reduced gradient of the layer weights and of the opening layer
+    ws = L.alloc_workspace(c.p)
+    dK, db = torch.empty_like(c.K), torch.empty_like(c.b)
+    L.lp_gradient(c.p, c.K, c.b, U, Lam, dK, db, ws)
+    dKr, dbr = O.gradient(Uref, Lref, c.d["K"], c.d["b"], wl.h, wl.act)
+    assert_close(dK.cpu().numpy(), dKr, wl.dtype, "dK")
+    assert_close(db.cpu().numpy(), dbr, wl.dtype, "db")
+    if wl.opening != "identity":
+        dL = torch.empty_like(c.L_in)
+        L.lp_open_grad(c.p, L.OPENING[wl.opening], wl.n_features, c.y, c.L_in, Lam[0], dL)
+        dLr = O.open_grad(c.d["y"], c.d["L_in"], Lref[0], wl.act, wl.opening)
+        assert_close(dL.cpu().numpy(), dLr, wl.dtype, "dL_in")
+
+
+@pytest.mark.parametrize("relax", ["FCF", "F"])
+@pytest.mark.parametrize("name,wl", DENSE, ids=IDS)
+def test_mgrit_forward_iterates(name, wl, relax):
+    c = case(wl)
+    iters = max(wl.fwd_iters, 3)
+    mg = sched(wl, iters, relax=relax)
+    ws = L.alloc_workspace(c.p, mg)
+    U = c.new_traj()
+    it, hist = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws)
+    assert it == iters
+    Ur, hr, _ = O.mgrit_forward(c.ref_traj(), c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf,
+                                max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=relax, max_iter=iters)
+    assert_close(U.cpu().numpy(), Ur, wl.dtype, "U iterate")
+    # residual history: relative to rho_1 (late entries sit near the rounding floor in fp32)
+    floor = {"f32": 3e-5, "f64": 1e-11}[wl.dtype]
+    for m in range(iters):
+        assert abs(hist[m] - hr[m]) <= floor * hr[0] + 1e-5 * hr[m], (m, hist, hr)
+
+
+@pytest.mark.parametrize("relax", ["FCF", "F"])
+@pytest.mark.parametrize("name,wl", DENSE, ids=IDS)
+def test_mgrit_adjoint_iterates(name, wl, relax):
+    c = case(wl)
+    U = c.new_traj()
+    L.lp_serial_forward(c.p, c.K, c.b, U)
+    lamN, _, _, _ = _lamN(c, U)
+    Uref = O.serial_forward(c.u0_ref, c.d["K"], c.d["b"], wl.h, wl.act)
+    lamNr = O.loss_terminal(Uref[-1], c.d["W"], c.d["mu"], c.d["onehot"])[1]
+    iters = max(wl.adj_iters, 3)
+    mg = sched(wl, iters, relax=relax)
+    ws = L.alloc_workspace(c.p, mg)
+    Lam = torch.zeros_like(U)
+    Lam[-1] = lamN
+    it, hist = L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, Lam, ws)
+    L0 = np.zeros_like(Uref)
+    L0[-1] = lamNr
+    Lr, hr, _ = O.mgrit_adjoint(Uref, L0, c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=wl.max_levels,
+                                min_coarse=wl.min_coarse, relax=relax, max_iter=iters)
+    assert_close(Lam.cpu().numpy(), Lr, wl.dtype, "Lam iterate")
+    floor = {"f32": 3e-5, "f64": 1e-11}[wl.dtype]
+    for m in range(iters):
+        assert abs(hist[m] - hr[m]) <= floor * hr[0] + 1e-5 * hr[m], (m, hist, hr)
+
+
+@pytest.mark.parametrize("name,wl", DENSE, ids=IDS)
+def test_residual_norms(name, wl):
+    c = case(wl)
+    mg = sched(wl, 1)
+    ws = L.alloc_workspace(c.p, mg)
+    U = c.new_traj()
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws)
+    Ur, _, _ = O.mgrit_forward(c.ref_traj(), c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=wl.relax, max_iter=1)
+    r = L.lp_residual_norm(c.p, L.LP_STATE, c.K, c.b, U, None, ws)
+    rr = O.residual_norm_state(Ur, c.d["K"], c.d["b"], wl.h, wl.act)
+    assert abs(r - rr) <= {"f32": 1e-4, "f64": 1e-10}[wl.dtype] * rr
+    # adjoint: each side linearises at its own forward iterate; the terminal value is a
+    # seeded random state given to both
+    lamN = random_state(wl, 77)[0]
+    Lam = torch.zeros_like(U)
+    Lam[-1] = torch.from_numpy(lamN).to(U)
+    Lr = np.zeros_like(Ur)
+    Lr[-1] = lamN
+    L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, Lam, ws)
+    Lr, _, _ = O.mgrit_adjoint(Ur, Lr, c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf,
+                               max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=1)
+    r = L.lp_residual_norm(c.p, L.LP_ADJOINT, c.K, c.b, U, Lam, ws)
+    rr = O.residual_norm_adjoint(Ur, Lr, c.d["K"], c.d["b"], wl.h, wl.act)
+    assert abs(r - rr) <= {"f32": 1e-4, "f64": 1e-10}[wl.dtype] * rr
+
+
+@pytest.mark.parametrize("name,wl", DENSE[:4], ids=IDS[:4])
+def test_invariants_on_gpu(name, wl):
+    """Properties of MGRIT checked on the GPU alone: the serial solution has zero
+    residual and is a fixed point; two-level F-relaxation is exact after N/c
+    iterations (Parareal finite-step exactness)."""
+    c = case(wl)
+    S = c.new_traj()
+    L.lp_serial_forward(c.p, c.K, c.b, S)
+    need = max(L.lp_workspace_bytes(c.p, sched(wl, wl.N // wl.cf, relax="F", levels=2)),
+               L.lp_workspace_bytes(c.p, sched(wl, 1, warm=True)))
+    big = torch.empty(need, dtype=torch.uint8, device="cuda")
+    nrm = float(S.double().norm())
+    assert L.lp_residual_norm(c.p, L.LP_STATE, c.K, c.b, S, None, big) <= {"f32": 1e-6, "f64": 1e-14}[wl.dtype] * nrm
+    U = S.clone()
+    it, hist = L.lp_mgrit_forward(c.p, sched(wl, 1, warm=True), c.K, c.b, U, big)
+    assert float((U - S).abs().max()) <= {"f32": 1e-5, "f64": 1e-13}[wl.dtype] * float(S.abs().max())
+    assert hist[0] <= {"f32": 1e-5, "f64": 1e-13}[wl.dtype] * nrm
+    U = c.new_traj()
+    L.lp_mgrit_forward(c.p, sched(wl, wl.N // wl.cf, relax="F", levels=2), c.K, c.b, U, big)
+    assert_close(U.cpu().numpy(), S.cpu().numpy(), wl.dtype, "two-level F after N/c iterations")
+
+
+def test_stop_rules_and_errors():
+    wl = DENSE[2][1]
+    c = case(wl)
+    mg = sched(wl, 30, rtol=1e-4)
+    ws = L.alloc_workspace(c.p, mg)
+    U = c.new_traj()
+    it, hist = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws)
+    assert it < 30 and hist[-1] <= 1e-4 * hist[0] and all(h > 1e-4 * hist[0] for h in hist[:-1])
+    # workspace too small -> LP_EWORKSPACE before any work is enqueued
+    with pytest.raises(L.LpError) as e:
+        L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws[:128])
+    assert e.value.status == L.LP_EWORKSPACE
+    # non-finite input -> LP_ENONFINITE
+    U = c.new_traj()
+    U[0, 0, 0] = float("nan")
+    with pytest.raises(L.LpError) as e:
+        L.lp_mgrit_forward(c.p, sched(wl, 2), c.K, c.b, U, ws)
+    assert e.value.status == L.LP_ENONFINITE
+
+
+def test_empty_batch_is_a_no_op():
+    wl = DENSE[1][1]
+    p = L.problem(wl.dtype, wl.layer, wl.act, wl.N, 0, wl.C, h=wl.h)
+    K = torch.zeros((wl.N, wl.C, wl.C), device="cuda", dtype=tdt(wl))
+    b = torch.zeros((wl.N, wl.C), device="cuda", dtype=tdt(wl))
+    U = torch.zeros((wl.N + 1, 0, wl.C), device="cuda", dtype=tdt(wl))
+    ws = L.alloc_workspace(p, sched(wl, 2))
+    assert L.lp_mgrit_forward(p, sched(wl, 2), K, b, U, ws) == (0, [])
+    dK, db = torch.ones_like(K), torch.ones_like(b)
+    L.lp_gradient(p, K, b, U, U.clone(), dK, db, ws)
+    assert float(dK.abs().max()) == 0.0 and float(db.abs().max()) == 0.0
