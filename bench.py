@@ -1,0 +1,338 @@
+"""Benchmark of the layer-parallel ResNet hot path on one MI355X.
+
+One step = one gradient evaluation of the workload with MGRIT: the workload's
+number of forward MGRIT iterations (cold start), the loss and adjoint terminal
+value, the adjoint MGRIT iterations, and the reduced gradient, all through the
+C ABI on the current stream, with every input resident in HBM. The metric is
+layer-steps x examples per second per MGRIT forward+adjoint iteration:
+
+    value = N * B * (iterations per step) / (seconds per step)
+
+where "iterations per step" counts forward+adjoint iteration pairs; the
+gradient's cost is included in the step time. The dominant kernel (largest
+summed time in a traced warm-up step) is timed live with HIP events recorded by
+the library on the launch stream over the timed steps, and compared with its
+algorithmic bytes or flops (the model below) to give the roofline fraction.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PEAK_TFLOPS = {"f32": 157.3, "f64": 78.6}  # dense MFMA / fp32 vector (packed), fp64
+
+KIND_NAMES = ["fwd_fc", "fwd_fres", "fwd_corrf", "fwd_coarsest", "adj_fc", "adj_fres", "adj_corrf",
+              "adj_coarsest", "gradient", "residual", "serial"]
+
+
+def level_sizes(N, cf, max_levels, min_coarse):
+    sizes = [N]
+    while len(sizes) < max_levels and sizes[-1] > min_coarse:
+        sizes.append(sizes[-1] // cf)
+    return sizes
+
+
+def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int):
+    """Algorithmic HBM bytes and flops of every launch of one kernel kind in one
+    step (summed over MGRIT levels and iterations), and the launch count.
+
+    Per interval and example (q features, e bytes per value, c = cf), on level l
+    (G rows exist on coarse levels only):
+      fwd FC:    read C-point + c G rows, write 1 staged C-point;      c * 2q^2 flops
+      fwd FRES:  read 2 C-points + c G rows, write G' and X' (1/c);    c * 2q^2
+      fwd CORRF: read C-point + coarse value + (c-1) G rows, write c;  (c-1) * 2q^2
+      adjoint:   the same, plus one primal row per step, 4q^2 flops per step,
+                 and one extra transposed product (2q^2) in FRES for the coarse step
+      coarsest:  read 1 + N_L G rows (+ N_L primal rows), write N_L rows
+      gradient:  per layer read U[n] and Lam[n+1], write dK, db;      4q^2 per layer
+    Each launch also reads the weights of its level once: N_l (q^2 + q) values."""
+    q, B, c = wl.q, wl.B, wl.cf
+    e = 4 if wl.dtype == "f32" else 8
+    row = B * q * e
+    sizes = level_sizes(wl.N, c, wl.max_levels, wl.min_coarse)
+    L = len(sizes)
+    fcf = wl.relax == "FCF"
+    adj = kind.startswith("adj")
+    iters = adj_iters if adj else fwd_iters
+    fstep = (4 if adj else 2) * q * q
+    byts = flops = launches = 0
+    if kind == "gradient":
+        return 2 * wl.N * row + wl.N * (q * q + q) * e, 4.0 * q * q * B * wl.N, 1
+    for l, Nl in enumerate(sizes):
+        wbytes = Nl * (q * q + q) * e
+        g = 1 if l >= 1 else 0
+        if l == L - 1:
+            if kind.endswith("coarsest"):
+                byts += (1 + g * Nl + Nl + (Nl if adj else 0)) * row + wbytes
+                flops += Nl * fstep * B
+                launches += 1
+            continue
+        Nc = Nl // c
+        xn = (1.0 / c) if (l + 1 < L - 1) else 0.0
+        if kind.endswith("_fc") and fcf:
+            byts += Nc * (2 + g * c + (c if adj else 0)) * row + wbytes
+            flops += Nc * c * fstep * B
+            launches += 1
+        elif kind.endswith("_fres"):
+            byts += Nc * (3 + xn + g * c + (c if adj else 0)) * row + wbytes
+            flops += Nc * (c * fstep + (2 * q * q if adj else 0)) * B
+            launches += 1
+        elif kind.endswith("_corrf"):
+            byts += Nc * (2 + c + g * (c - 1) + ((c - 1) if adj else 0)) * row + wbytes
+            flops += Nc * (c - 1) * fstep * B
+            launches += 1
+    return byts * iters, flops * iters, launches * iters
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1812_04352_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was
+    taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(workload, {}).get(kernel)
+    if not ent or ent.get("source_hash") != source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, budget_s: float = 12.0):
+    """The oracle (fp64 NumPy) timed on the host: one MGRIT forward iteration and
+    one adjoint iteration on a bounded batch sample, repeated until about
+    budget_s seconds have passed."""
+    import numpy as np
+
+    import oracle as O
+    from workloads import generate
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_info = threadpool_limits = None
+    ncores = len(os.sched_getaffinity(0))
+    Bs = min(wl.B, 1024 if wl.layer == "dense" else 16)
+    d = generate(wl.with_overrides(B=Bs))
+    ctx = threadpool_limits(ncores) if threadpool_limits else None
+    try:
+        u0 = O.open_forward(d["y"], d["L_in"], wl.act, wl.opening)
+        U = np.zeros((wl.N + 1,) + u0.shape)
+        U[0] = u0
+        args = dict(cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=1)
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            Uo, _, _ = O.mgrit_forward(U, d["K"], d["b"], wl.h, wl.act, **args)
+            lamN = O.loss_terminal(Uo[-1], d["W"], d["mu"], d["onehot"])[1]
+            Lam = np.zeros_like(Uo)
+            Lam[-1] = lamN
+            O.mgrit_adjoint(Uo, Lam, d["K"], d["b"], wl.h, wl.act, **args)
+            reps += 1
+            if time.perf_counter() - t0 >= budget_s:
+                break
+        dt = time.perf_counter() - t0
+        threads = ncores
+        if threadpool_info:
+            th = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+            threads = max(th) if th else 1
+    finally:
+        if ctx is not None:
+            ctx.__exit__(None, None, None)
+    return {"value": wl.N * Bs * reps / dt, "unit": "layer-steps*examples/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {Bs} of {wl.B} examples, {reps} x (1 forward + 1 adjoint MGRIT iteration, "
+                      f"{wl.relax}, {len(level_sizes(wl.N, wl.cf, wl.max_levels, wl.min_coarse))} levels), "
+                      f"fp64 NumPy, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default: the second workload)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1812_04352_amd import lp as L
+    from workloads import WORKLOADS, generate
+
+    wl = WORKLOADS[args.config]
+
+    def note(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    if wl.layer != "dense":
+        print("conv workload: kernels not available in this build", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    dt = torch.float32 if wl.dtype == "f32" else torch.float64
+    d = generate(wl)
+
+    def g(x):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(device="cuda", dtype=dt)
+
+    K, b, W, mu, y, c = (g(d[k]) for k in ("K", "b", "W", "mu", "y", "onehot"))
+    Lin = g(d["L_in"]) if d["L_in"] is not None else None
+    p = L.problem(wl.dtype, wl.layer, wl.act, wl.N, wl.B, wl.C, wl.H, wl.W, wl.h)
+    U = torch.zeros((wl.N + 1, wl.B, wl.q), device="cuda", dtype=dt)
+    L.lp_open_forward(p, L.OPENING[wl.opening], wl.n_features, y, Lin, U[0])
+    Lam = torch.zeros_like(U)
+    J = torch.zeros(1, device="cuda", dtype=torch.float64)
+    dW, dmu = torch.empty_like(W), torch.empty_like(mu)
+    dK, db = torch.empty_like(K), torch.empty_like(b)
+
+    note(f"cfg{wl.cfg} inputs on the GPU")
+    # iteration counts: fixed by the workload, or found once with its stop rule
+    fwd_iters, adj_iters = wl.fwd_iters, wl.adj_iters
+    if wl.rtol > 0 or wl.stag > 0:
+        mg = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, wl.fwd_iters, False, wl.rtol, wl.stag)
+        ws = L.alloc_workspace(p, mg)
+        fwd_iters, _ = L.lp_mgrit_forward(p, mg, K, b, U, ws)
+        L.lp_loss_terminal(p, wl.n_classes, U[-1], W, mu, c, J, Lam[-1], dW, dmu)
+        adj_iters, _ = L.lp_mgrit_adjoint(p, L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax,
+                                                     wl.adj_iters, False, wl.rtol, wl.stag), K, b, U, Lam, ws)
+        del ws
+    mgF = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, fwd_iters)
+    mgA = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, adj_iters)
+    ws = L.alloc_workspace(p, mgF if fwd_iters >= adj_iters else mgA)
+    hist = {}
+
+    def step():
+        _, hist["fwd"] = L.lp_mgrit_forward(p, mgF, K, b, U, ws)
+        L.lp_loss_terminal(p, wl.n_classes, U[-1], W, mu, c, J, Lam[-1], dW, dmu)
+        _, hist["adj"] = L.lp_mgrit_adjoint(p, mgA, K, b, U, Lam, ws)
+        L.lp_gradient(p, K, b, U, Lam, dK, db, ws)
+
+    note(f"iterations fwd={fwd_iters} adj={adj_iters}; warm-up")
+    # warm-up; the first step is traced for every kind to find the dominant kernel
+    lib = L.load()
+    lib.lp_trace_enable((1 << 11) - 1)
+    step()
+    torch.cuda.synchronize()
+    per_kind = {}
+    for k, name in enumerate(KIND_NAMES):
+        n, ms = ctypes_read(lib, k)
+        if n:
+            per_kind[name] = ms
+    dominant = max(per_kind, key=per_kind.get)
+    lib.lp_trace_enable(0)
+    for _ in range(max(0, args.warmup - 1)):
+        step()
+    torch.cuda.synchronize()
+
+    note(f"timed region: {args.steps} steps, dominant kernel {dominant}")
+    # timed region: only the dominant kind is traced
+    lib.lp_trace_enable(1 << KIND_NAMES.index(dominant))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    nl, kms = ctypes_read(lib, KIND_NAMES.index(dominant))
+    lib.lp_trace_enable(0)
+    ms_step = (t1 - t0) * 1000.0 / args.steps
+    pairs = 0.5 * (fwd_iters + adj_iters)
+    value = wl.N * wl.B * pairs / (ms_step / 1000.0)
+
+    # roofline of the dominant kernel
+    byts, flops, launches = kernel_model(wl, dominant, fwd_iters, adj_iters)
+    assert nl == launches * args.steps, (dominant, nl, launches, args.steps)
+    avg_ms = kms / nl
+    intensity = flops / byts
+    ridge = PEAK_TFLOPS[wl.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if intensity < ridge:
+        achieved = byts / launches / (avg_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        achieved = flops / launches / (avg_ms / 1e3) / 1e12
+        roof = {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS[wl.dtype], "unit": "TFLOP/s"}
+    roof["frac"] = achieved / roof["peak"]
+    roof["traffic"] = measured_traffic(dominant, f"cfg{wl.cfg}")
+    roof["kernel"] = dominant
+    roof["launches_per_step"] = launches
+    roof["avg_launch_ms"] = avg_ms
+    roof["algorithmic_bytes_per_launch"] = byts / launches
+    roof["algorithmic_flops_per_launch"] = flops / launches
+
+    # single-GPU context: the layer-serial forward pass (the baseline method)
+    Us = U.clone()
+    L.lp_serial_forward(p, K, b, Us)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(5):
+        L.lp_serial_forward(p, K, b, Us)
+    torch.cuda.synchronize()
+    serial_ms = (time.perf_counter() - t0) * 200.0
+
+    out = {
+        "metric": "layer-steps*examples/s per MGRIT fwd+adjoint iteration",
+        "value": value,
+        "unit": "layer-steps*examples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"cfg{wl.cfg}: {wl.name}", "N": wl.N, "B": wl.B, "width": wl.q,
+                   "activation": wl.act, "mgrit": {"cf": wl.cf, "levels": len(level_sizes(
+                       wl.N, wl.cf, wl.max_levels, wl.min_coarse)), "relax": wl.relax,
+                       "fwd_iters": fwd_iters, "adj_iters": adj_iters},
+                   "step": "MGRIT forward iterations + loss + MGRIT adjoint iterations + gradient"},
+        "roofline": roof,
+        "kernel_ms_per_step": {k: v for k, v in sorted(per_kind.items(), key=lambda t: -t[1])},
+        "serial_forward_ms": serial_ms,
+        "residual_history": {"fwd": hist["fwd"], "adj": hist["adj"]},
+    }
+    if not args.no_cpu:
+        note("CPU oracle baseline")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+def ctypes_read(lib, kind):
+    import ctypes
+    n = ctypes.c_int32(0)
+    ms = ctypes.c_double(0.0)
+    rc = lib.lp_trace_read(kind, -1, ctypes.byref(n), ctypes.byref(ms))
+    if rc != 0:
+        raise RuntimeError(f"lp_trace_read failed: {rc}")
+    return n.value, ms.value
+
+
+if __name__ == "__main__":
+    main()

@@ -195,6 +195,24 @@ int32_t lp_loss_terminal(const lp_problem* prob, int32_t nc, const void* uN, con
  * design update of Algorithm 2 with a scaled-identity Hessian approximation). */
 int32_t lp_sgd_update(int32_t dtype, size_t n, double lr, const void* g, void* x, void* stream);
 
+/* ---- tracing (a profiling aid, not part of the method) ----
+ * When enabled for a kernel kind, every launch of that kind records a pair of
+ * HIP events on the launch's stream; lp_trace_read sums their elapsed times.
+ * Kinds: the three sweeps of a non-coarsest MGRIT level, the coarsest-level
+ * solve, for each direction; the gradient; the residual norm; layer-serial solves. */
+enum {
+  LP_TRACE_FWD_FC = 0, LP_TRACE_FWD_FRES = 1, LP_TRACE_FWD_CORRF = 2, LP_TRACE_FWD_COARSEST = 3,
+  LP_TRACE_ADJ_FC = 4, LP_TRACE_ADJ_FRES = 5, LP_TRACE_ADJ_CORRF = 6, LP_TRACE_ADJ_COARSEST = 7,
+  LP_TRACE_GRADIENT = 8, LP_TRACE_RESIDUAL = 9, LP_TRACE_SERIAL = 10, LP_TRACE_KINDS = 11
+};
+/* Start recording the kinds in `kind_mask` (bit k = kind k; 0 stops) and clear
+ * earlier records. At most 65536 launches are recorded; later ones are counted
+ * as dropped. Returns LP_OK or LP_EHIP. */
+int32_t lp_trace_enable(uint32_t kind_mask);
+/* Wait for the recorded events and report, for one kind and MGRIT level
+ * (level -1: all levels), the launch count (host) and summed milliseconds (host). */
+int32_t lp_trace_read(int32_t kind, int32_t level, int32_t* launches, double* total_ms);
+
 #ifdef __cplusplus
 }
 #endif

@@ -8,8 +8,9 @@
 // MGRIT sweeps follow Algorithm 1 (Section 3.1) with the F/C relaxations of
 // eqs. Frelax / Crelax and FAS restriction by injection.
 //
-// The activation and the sweep mode are uniform runtime values; only the
-// dtype T and the width Q are template parameters (the row lives in registers).
+// The activation is a uniform runtime value; the dtype T and the width Q are
+// template parameters (the row lives in registers), and each sweep mode is its
+// own kernel symbol so profiles attribute time per mode.
 // Included once per dtype by lp_dense_f32.hip / lp_dense_f64.hip.
 #pragma once
 
@@ -150,11 +151,11 @@ __device__ __forceinline__ void correct_row(T (&v)[Q], const T* __restrict__ cs,
 //          r = f - C_{k+1}; restriction: G'[k+1] = f - Phi_{l+1}(C_k), X'[k+1] = C_{k+1}.
 //   CORRF: correct C_k with the coarse solution, then c-1 F steps written to X;
 //          the last interval also corrects C-point N_l.
-template <typename T, int Q>
+template <typename T, int Q, int MODE>
 __global__ __launch_bounds__(NT) void k_fwd_sweep(SweepArgs a) {
   __shared__ T W[2][WStage<T, Q>::n];
   __shared__ double red[NT];
-  const int mode = a.mode;
+  constexpr int mode = MODE;  // one kernel symbol per sweep mode
   const int k = blockIdx.x;
   const int Nc = gridDim.x;
   const int e = blockIdx.y * NT + threadIdx.x;
@@ -254,11 +255,11 @@ __global__ __launch_bounds__(NT) void k_fwd_sweep(SweepArgs a) {
 //          G'[k] = f_k - Phibar_{l+1}(C_{k+1}), X'[k] = C_k.
 //   CORRF: correct C_{k+1}, then c-1 F steps written to X; interval 0 also
 //          corrects C-point 0.
-template <typename T, int Q>
+template <typename T, int Q, int MODE>
 __global__ __launch_bounds__(NT) void k_adj_sweep(SweepArgs a) {
   __shared__ T W[2][WStage<T, Q>::n];
   __shared__ double red[NT];
-  const int mode = a.mode;
+  constexpr int mode = MODE;  // one kernel symbol per sweep mode
   const int k = blockIdx.x;
   const int Nc = gridDim.x;
   const int e = blockIdx.y * NT + threadIdx.x;
@@ -621,8 +622,15 @@ template <typename T, int Q>
 hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   const dim3 grid(a.Nl / a.c, (a.B + NT - 1) / NT);
   if (partials) *partials = (int)(grid.x * grid.y);
-  if (dir == DIR_FWD) k_fwd_sweep<T, Q><<<grid, NT, 0, st>>>(a);
-  else k_adj_sweep<T, Q><<<grid, NT, 0, st>>>(a);
+  if (dir == DIR_FWD) {
+    if (a.mode == SWEEP_FC) k_fwd_sweep<T, Q, SWEEP_FC><<<grid, NT, 0, st>>>(a);
+    else if (a.mode == SWEEP_FRES) k_fwd_sweep<T, Q, SWEEP_FRES><<<grid, NT, 0, st>>>(a);
+    else k_fwd_sweep<T, Q, SWEEP_CORRF><<<grid, NT, 0, st>>>(a);
+  } else {
+    if (a.mode == SWEEP_FC) k_adj_sweep<T, Q, SWEEP_FC><<<grid, NT, 0, st>>>(a);
+    else if (a.mode == SWEEP_FRES) k_adj_sweep<T, Q, SWEEP_FRES><<<grid, NT, 0, st>>>(a);
+    else k_adj_sweep<T, Q, SWEEP_CORRF><<<grid, NT, 0, st>>>(a);
+  }
   return hipGetLastError();
 }
 
@@ -657,14 +665,14 @@ hipError_t grad(const GradArgs& a, hipStream_t st) {
 }  // namespace lp
 
 // Defines the per-dtype entry points dense_*_SFX over the supported widths.
-#define LP_DENSE_DEFINE(T, SFX)                                                                        \
+#define LP_DENSE_DEFINE(T, SFX, WIDE)                                                                        \
   namespace lp {                                                                                       \
   hipError_t dense_sweep_##SFX(int q, int dir, const SweepArgs& a, hipStream_t st, int* partials) {    \
     switch (q) {                                                                                       \
       case 8: return dense::sweep<T, 8>(dir, a, st, partials);                                         \
       case 16: return dense::sweep<T, 16>(dir, a, st, partials);                                       \
       case 32: return dense::sweep<T, 32>(dir, a, st, partials);                                       \
-      case 64: return dense::sweep<T, 64>(dir, a, st, partials);                                       \
+      case 64: if (WIDE) return dense::sweep<T, (WIDE ? 64 : 8)>(dir, a, st, partials); break;                                       \
     }                                                                                                  \
     return hipErrorNotSupported;                                                                       \
   }                                                                                                    \
@@ -673,7 +681,7 @@ hipError_t grad(const GradArgs& a, hipStream_t st) {
       case 8: return dense::serial<T, 8>(dir, a, st);                                                  \
       case 16: return dense::serial<T, 16>(dir, a, st);                                                \
       case 32: return dense::serial<T, 32>(dir, a, st);                                                \
-      case 64: return dense::serial<T, 64>(dir, a, st);                                                \
+      case 64: if (WIDE) return dense::serial<T, (WIDE ? 64 : 8)>(dir, a, st); break;                                                \
     }                                                                                                  \
     return hipErrorNotSupported;                                                                       \
   }                                                                                                    \
@@ -682,7 +690,7 @@ hipError_t grad(const GradArgs& a, hipStream_t st) {
       case 8: return dense::resid<T, 8>(dir, a, st, partials);                                         \
       case 16: return dense::resid<T, 16>(dir, a, st, partials);                                       \
       case 32: return dense::resid<T, 32>(dir, a, st, partials);                                       \
-      case 64: return dense::resid<T, 64>(dir, a, st, partials);                                       \
+      case 64: if (WIDE) return dense::resid<T, (WIDE ? 64 : 8)>(dir, a, st, partials); break;                                       \
     }                                                                                                  \
     return hipErrorNotSupported;                                                                       \
   }                                                                                                    \
@@ -691,7 +699,7 @@ hipError_t grad(const GradArgs& a, hipStream_t st) {
       case 8: return dense::grad<T, 8>(a, st);                                                         \
       case 16: return dense::grad<T, 16>(a, st);                                                       \
       case 32: return dense::grad<T, 32>(a, st);                                                       \
-      case 64: return dense::grad<T, 64>(a, st);                                                       \
+      case 64: if (WIDE) return dense::grad<T, (WIDE ? 64 : 8)>(a, st); break;                                                       \
     }                                                                                                  \
     return hipErrorNotSupported;                                                                       \
   }                                                                                                    \

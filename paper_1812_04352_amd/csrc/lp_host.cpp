@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -39,6 +40,55 @@ int hip_fail(hipError_t e, const char* what) {
     hipError_t _e = (expr);                      \
     if (_e != hipSuccess) return hip_fail(_e, what); \
   } while (0)
+
+// ---------------------------------------------------------------- tracing
+// Event pairs around launches of the enabled kinds; summed on lp_trace_read.
+struct TraceRec {
+  int kind, level;
+  hipEvent_t a, b;
+};
+std::mutex g_trace_mu;
+uint32_t g_trace_mask = 0;
+std::vector<TraceRec> g_trace;
+std::vector<hipEvent_t> g_event_pool;
+size_t g_pool_used = 0;
+long g_trace_dropped = 0;
+constexpr size_t kTraceMax = 65536;
+
+hipEvent_t pool_event() {
+  if (g_pool_used == g_event_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    g_event_pool.push_back(e);
+  }
+  return g_event_pool[g_pool_used++];
+}
+
+// Records a start event on construction and a stop event on destruction when
+// the kind is being traced.
+struct TraceScope {
+  hipStream_t st;
+  hipEvent_t b = nullptr;
+  int idx = -1;
+  TraceScope(int kind, int level, hipStream_t s) : st(s) {
+    if (!(g_trace_mask & (1u << kind))) return;
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    if (g_trace.size() >= kTraceMax) {
+      ++g_trace_dropped;
+      return;
+    }
+    hipEvent_t a = pool_event();
+    b = pool_event();
+    if (!a || !b || hipEventRecord(a, st) != hipSuccess) {
+      b = nullptr;
+      return;
+    }
+    g_trace.push_back(TraceRec{kind, level, a, b});
+  }
+  ~TraceScope() {
+    if (b) hipEventRecord(b, st);
+  }
+};
 
 constexpr size_t kAlign = 256;
 size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -178,8 +228,10 @@ struct Solver {
   int cycle(int l) {
     const int L = (int)sizes.size();
     const double hl = p->h * (double)stride(l);
+    const int kb = dir == lp::DIR_FWD ? LP_TRACE_FWD_FC : LP_TRACE_ADJ_FC;  // first kind of this direction
     if (l == L - 1) {
       lp::SerialArgs a{p->act, K, b, Uf, p->B, sizes[l], stride(l), hl, X[l], G[l]};
+      TraceScope ts(kb + 3, l, st);
       LP_TRY(lp::launch_serial(sh, dir, a, st), "coarsest-level solve");
       return LP_OK;
     }
@@ -200,7 +252,10 @@ struct Solver {
     a.S = S[l];
     a.finest = l == 0;
     a.mode = lp::SWEEP_FC;
-    if (fcf) LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "FC-relaxation");
+    if (fcf) {
+      TraceScope ts(kb + 0, l, st);
+      LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "FC-relaxation");
+    }
     a.Cs = fcf ? S[l] : X[l];
     a.cs_stride = fcf ? 1 : m->cf;
     a.Xn = X[l + 1];
@@ -209,13 +264,17 @@ struct Solver {
     a.partial = l == 0 ? partial : nullptr;
     int np = 0;
     a.mode = lp::SWEEP_FRES;
-    LP_TRY(lp::launch_sweep(sh, dir, a, st, &np), "F-relaxation and restriction");
+    {
+      TraceScope ts(kb + 1, l, st);
+      LP_TRY(lp::launch_sweep(sh, dir, a, st, &np), "F-relaxation and restriction");
+    }
     if (l == 0) partials_used = np;
     int rc = cycle(l + 1);
     if (rc != LP_OK) return rc;
     a.V = X[l + 1];
     a.mode = lp::SWEEP_CORRF;
     a.partial = nullptr;
+    TraceScope ts(kb + 2, l, st);
     LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "correction and F-relaxation");
     return LP_OK;
   }
@@ -317,7 +376,7 @@ int dense_grad_chunks(int B, int N) {
 }
 
 bool shape_supported(const Shape& s) {
-  if (s.layer == 0) return s.H == 1 && s.W == 1 && dense_width_supported(s.C);
+  if (s.layer == 0) return s.H == 1 && s.W == 1 && dense_width_supported(s.C) && !(s.dtype == 1 && s.C > 32);
   return conv_supported(s);
 }
 
@@ -387,6 +446,7 @@ int32_t lp_serial_forward(const lp_problem* p, const void* K, const void* b, voi
   if (!K || !b || (p->B && !U)) return fail(LP_EINVAL, "NULL array argument");
   if (p->B == 0) return LP_OK;
   lp::SerialArgs a{p->act, K, b, nullptr, p->B, p->N, 1, p->h, U, nullptr};
+  TraceScope ts(LP_TRACE_SERIAL, 0, static_cast<hipStream_t>(stream));
   LP_TRY(lp::launch_serial(shape_of(p), lp::DIR_FWD, a, static_cast<hipStream_t>(stream)), "serial forward");
   return LP_OK;
 }
@@ -399,6 +459,7 @@ int32_t lp_serial_adjoint(const lp_problem* p, const void* K, const void* b, con
   if (p->B && U == Lam) return fail(LP_EINVAL, "U and Lam alias");
   if (p->B == 0) return LP_OK;
   lp::SerialArgs a{p->act, K, b, U, p->B, p->N, 1, p->h, Lam, nullptr};
+  TraceScope ts(LP_TRACE_SERIAL, 1, static_cast<hipStream_t>(stream));
   LP_TRY(lp::launch_serial(shape_of(p), lp::DIR_ADJ, a, static_cast<hipStream_t>(stream)), "serial adjoint");
   return LP_OK;
 }
@@ -430,6 +491,7 @@ int32_t lp_gradient(const lp_problem* p, const void* K, const void* b, const voi
   rc = check_ws(ws, ws_bytes, grad_bytes(p));
   if (rc) return rc;
   lp::GradArgs a{p->act, K, b, U, Lam, p->B, p->N, p->h, ws, lp::grad_chunks(s, p->B, p->N), dK, db};
+  TraceScope ts(LP_TRACE_GRADIENT, 0, st);
   LP_TRY(lp::launch_grad(s, a, st), "gradient");
   return LP_OK;
 }
@@ -452,7 +514,10 @@ int32_t lp_residual_norm(const lp_problem* p, int32_t which, const void* K, cons
   double* out = reinterpret_cast<double*>(static_cast<char*>(ws) + up((size_t)partial_capacity(p) * sizeof(double)));
   lp::ResidArgs a{p->act, K, b, U, Lam, p->B, p->N, p->h, partial};
   int np = 0;
-  LP_TRY(lp::launch_resid(shape_of(p), which == LP_STATE ? lp::DIR_FWD : lp::DIR_ADJ, a, st, &np), "residual");
+  {
+    TraceScope ts(LP_TRACE_RESIDUAL, which, st);
+    LP_TRY(lp::launch_resid(shape_of(p), which == LP_STATE ? lp::DIR_FWD : lp::DIR_ADJ, a, st, &np), "residual");
+  }
   LP_TRY(lp::launch_norm_reduce(partial, np, out, st), "residual norm");
   LP_TRY(hipMemcpyAsync(norm, out, sizeof(double), hipMemcpyDeviceToHost, st), "read residual norm");
   LP_TRY(hipStreamSynchronize(st), "stream sync");
@@ -512,6 +577,36 @@ int32_t lp_sgd_update(int32_t dtype, size_t n, double lr, const void* g, void* x
   if (dtype != LP_F32 && dtype != LP_F64) return fail(LP_EINVAL, "bad dtype %d", dtype);
   if (n && (!g || !x)) return fail(LP_EINVAL, "NULL array argument");
   LP_TRY(lp::launch_sgd(dtype, n, lr, g, x, static_cast<hipStream_t>(stream)), "sgd update");
+  return LP_OK;
+}
+
+int32_t lp_trace_enable(uint32_t kind_mask) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  // earlier records may still be pending on some stream: wait before reusing their events
+  for (const TraceRec& r : g_trace) hipEventSynchronize(r.b);
+  g_trace.clear();
+  g_pool_used = 0;
+  g_trace_dropped = 0;
+  g_trace_mask = kind_mask & ((1u << LP_TRACE_KINDS) - 1);
+  return LP_OK;
+}
+
+int32_t lp_trace_read(int32_t kind, int32_t level, int32_t* launches, double* total_ms) {
+  if (kind < 0 || kind >= LP_TRACE_KINDS) return fail(LP_EINVAL, "bad trace kind %d", kind);
+  if (!launches || !total_ms) return fail(LP_EINVAL, "NULL output");
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  int n = 0;
+  double ms = 0.0;
+  for (const TraceRec& r : g_trace) {
+    if (r.kind != kind || (level >= 0 && r.level != level)) continue;
+    LP_TRY(hipEventSynchronize(r.b), "trace event");
+    float t = 0.f;
+    LP_TRY(hipEventElapsedTime(&t, r.a, r.b), "trace event");
+    ms += t;
+    ++n;
+  }
+  *launches = n;
+  *total_ms = ms;
   return LP_OK;
 }
 

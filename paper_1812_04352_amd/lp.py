@@ -34,7 +34,7 @@ EXPORTS = (
     "lp_abi_version", "lp_status_string", "lp_last_error", "lp_workspace_bytes",
     "lp_serial_forward", "lp_serial_adjoint", "lp_mgrit_forward", "lp_mgrit_adjoint",
     "lp_gradient", "lp_residual_norm", "lp_open_forward", "lp_open_grad",
-    "lp_loss_terminal", "lp_sgd_update",
+    "lp_loss_terminal", "lp_sgd_update", "lp_trace_enable", "lp_trace_read",
 )
 
 
@@ -86,6 +86,8 @@ _SIGS = {
     "lp_open_grad": ([_P, _i32, _i32, _v, _v, _v, _v, _v], _i32),
     "lp_loss_terminal": ([_P, _i32, _v, _v, _v, _v, _v, _v, _v, _v, _v], _i32),
     "lp_sgd_update": ([_i32, _sz, ctypes.c_double, _v, _v, _v], _i32),
+    "lp_trace_enable": ([ctypes.c_uint32], _i32),
+    "lp_trace_read": ([_i32, _i32, _ip, _dp], _i32),
 }
 
 
@@ -266,6 +268,17 @@ def lp_loss_terminal(p: LpProblem, nc: int, uN, W, mu, c, J, lamN, dW, dmu) -> N
                                    _arr(J, 1, "J", torch.float64), _arr(lamN, p.B * p.q, "lamN", dt),
                                    _arr(dW, nc * p.q, "dW", dt), _arr(dmu, nc, "dmu", dt), _stream()),
            "lp_loss_terminal")
+
+
+def lp_trace_enable(kind_mask: int) -> None:
+    _check(load().lp_trace_enable(kind_mask), "lp_trace_enable")
+
+
+def lp_trace_read(kind: int, level: int = -1) -> Tuple[int, float]:
+    n = ctypes.c_int32(0)
+    ms = ctypes.c_double(0.0)
+    _check(load().lp_trace_read(kind, level, ctypes.byref(n), ctypes.byref(ms)), "lp_trace_read")
+    return n.value, ms.value
 
 
 def lp_sgd_update(x, g, lr: float) -> None:
