@@ -98,9 +98,9 @@ const char* lp_status_string(int32_t status);
 /* Message of the last failing call on this host thread ("" if none). */
 const char* lp_last_error(void);
 
-/* Workspace bytes that lp_mgrit_forward, lp_mgrit_adjoint, lp_gradient and
- * lp_residual_norm need for this problem and schedule (mg may be NULL: then only
- * the gradient and residual-norm needs are counted). Returns 0 for an invalid
+/* Workspace bytes that lp_mgrit_forward, lp_mgrit_adjoint, lp_gradient,
+ * lp_residual_norm and lp_loss_terminal need for this problem and schedule (mg
+ * may be NULL: then the MGRIT hierarchy is not counted). Returns 0 for an invalid
  * problem. The workspace holds the coarse levels (U_l and the FAS right-hand
  * side G_l for l >= 1), the relaxed C-points of every non-coarsest level,
  * per-workgroup residual partials (fp64) and per-chunk gradient partials. */
@@ -186,10 +186,11 @@ int32_t lp_open_grad(const lp_problem* prob, int32_t opening, int32_t nf, const 
  *   lamN   = (1/B) W^T (softmax(z_k) - c_k)   [B][q]      (the adjoint terminal value)
  *   dW     = (1/B) sum_k (softmax(z_k) - c_k) (u_k^N)^T   [nc][q]
  *   dmu    = (1/B) sum_k (softmax(z_k) - c_k)             [nc]
- * Requires 1 <= nc <= min(64, q) (lamN's rows hold the softmax residual between passes). */
+ * Requires 1 <= nc <= 64. The workspace holds the logits and fixed-order
+ * partial sums; lp_workspace_bytes(prob, ...) covers every nc <= 64. */
 int32_t lp_loss_terminal(const lp_problem* prob, int32_t nc, const void* uN, const void* W,
                          const void* mu, const void* c, double* J, void* lamN, void* dW,
-                         void* dmu, void* stream);
+                         void* dmu, void* ws, size_t ws_bytes, void* stream);
 
 /* Plain gradient step x <- x - lr * g on n elements of the given dtype (the
  * design update of Algorithm 2 with a scaled-identity Hessian approximation). */

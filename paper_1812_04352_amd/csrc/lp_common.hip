@@ -1,7 +1,7 @@
 // Kernels shared by every layer family: row copies (the MGRIT cold start), the
 // fixed-order residual-norm reduction, and the boundary helpers of the network
-// (opening layer, softmax cross-entropy and its adjoint terminal value, the
-// plain gradient step). The helpers sit outside the per-iteration hot path.
+// (opening layer and its gradient, the plain gradient step). The helpers sit
+// outside the per-iteration hot path. The loss helper lives in lp_loss.hip.
 #include <math.h>
 
 #include <type_traits>
@@ -147,73 +147,6 @@ __global__ __launch_bounds__(NT) void k_open_grad_conv(const T* y, const T* L, c
   }
 }
 
-// ---------------------------------------------------------------- loss and terminal value
-
-constexpr int MAXNC = 64;
-
-// Pass 1 (one workgroup): per example z = W u + mu, softmax, loss; the row
-// d_e = (softmax - c)/B is parked in the first nc entries of lamN's row e.
-template <typename T>
-__global__ __launch_bounds__(1024) void k_loss_pass1(const T* uN, const T* Wc, const T* mu, const T* c,
-                                                     double* J, T* lamN, int B, int q, int nc) {
-  __shared__ double sh[1024];
-  double lsum = 0.0;
-  for (int e = threadIdx.x; e < B; e += 1024) {
-    double z[MAXNC];
-    double zmax = -INFINITY;
-    for (int j = 0; j < nc; ++j) {
-      T acc = T(0);
-      for (int i = 0; i < q; ++i) acc = fma(Wc[(size_t)j * q + i], uN[(size_t)e * q + i], acc);
-      z[j] = (double)(acc + mu[j]);
-      zmax = z[j] > zmax ? z[j] : zmax;
-    }
-    double den = 0.0;
-    for (int j = 0; j < nc; ++j) den += exp(z[j] - zmax);
-    const double lden = log(den);
-    for (int j = 0; j < nc; ++j) {
-      const double cj = (double)c[(size_t)e * nc + j];
-      const double logp = (z[j] - zmax) - lden;
-      lsum -= cj * logp;
-      lamN[(size_t)e * q + j] = (T)((exp(logp) - cj) / (double)B);
-    }
-  }
-  lsum = block_sum<1024>(lsum, sh);
-  if (threadIdx.x == 0) J[0] = lsum / (double)B;
-}
-
-// Pass 2: dW[j][i] = sum_e d[e][j] u[e][i], dmu[j] = sum_e d[e][j] (examples in order).
-template <typename T>
-__global__ __launch_bounds__(NT) void k_loss_pass2(const T* uN, const T* lamN, T* dW, T* dmu, int B, int q,
-                                                   int nc) {
-  const size_t o = (size_t)blockIdx.x * NT + threadIdx.x;
-  const size_t nw = (size_t)nc * q;
-  if (o >= nw + nc) return;
-  T acc = T(0);
-  if (o < nw) {
-    const size_t j = o / q, i = o - j * q;
-    for (int e = 0; e < B; ++e) acc = fma(lamN[(size_t)e * q + j], uN[(size_t)e * q + i], acc);
-    dW[o] = acc;
-  } else {
-    const size_t j = o - nw;
-    for (int e = 0; e < B; ++e) acc += lamN[(size_t)e * q + j];
-    dmu[j] = acc;
-  }
-}
-
-// Pass 3: lamN[e] = W^T d_e (the row's first nc entries hold d_e on entry).
-template <typename T>
-__global__ __launch_bounds__(NT) void k_loss_pass3(const T* Wc, T* lamN, int B, int q, int nc) {
-  const int e = blockIdx.x * NT + threadIdx.x;
-  if (e >= B) return;
-  T d[MAXNC];
-  for (int j = 0; j < nc; ++j) d[j] = lamN[(size_t)e * q + j];
-  for (int i = 0; i < q; ++i) {
-    T acc = T(0);
-    for (int j = 0; j < nc; ++j) acc = fma(Wc[(size_t)j * q + i], d[j], acc);
-    lamN[(size_t)e * q + i] = acc;
-  }
-}
-
 template <typename T>
 __global__ __launch_bounds__(NT) void k_sgd(size_t n, T lr, const T* g, T* x) {
   for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < n; i += (size_t)gridDim.x * NT)
@@ -264,22 +197,6 @@ hipError_t open_grad_t(const Shape& s, int opening, int nf, int B, const void* y
   });
 }
 
-template <typename T>
-hipError_t loss_t(int B, int q, int nc, const void* uN, const void* Wc, const void* mu, const void* c,
-                  double* J, void* lamN, void* dW, void* dmu, hipStream_t st) {
-  k_loss_pass1<T><<<1, 1024, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu, (const T*)c, J, (T*)lamN, B,
-                                      q, nc);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  const size_t no = (size_t)nc * q + nc;
-  k_loss_pass2<T><<<(unsigned)((no + NT - 1) / NT), NT, 0, st>>>((const T*)uN, (const T*)lamN, (T*)dW,
-                                                                 (T*)dmu, B, q, nc);
-  err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  k_loss_pass3<T><<<(B + NT - 1) / NT, NT, 0, st>>>((const T*)Wc, (T*)lamN, B, q, nc);
-  return hipGetLastError();
-}
-
 }  // namespace
 
 hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_row0, long dst_step,
@@ -312,12 +229,6 @@ hipError_t launch_open_grad(const Shape& s, int opening, int nf, int B, const vo
                             const void* lam0, void* dL, hipStream_t st) {
   return s.dtype == 0 ? open_grad_t<float>(s, opening, nf, B, y, L, lam0, dL, st)
                       : open_grad_t<double>(s, opening, nf, B, y, L, lam0, dL, st);
-}
-
-hipError_t launch_loss(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,
-                       const void* c, double* J, void* lamN, void* dW, void* dmu, hipStream_t st) {
-  return dtype == 0 ? loss_t<float>(B, q, nc, uN, Wc, mu, c, J, lamN, dW, dmu, st)
-                    : loss_t<double>(B, q, nc, uN, Wc, mu, c, J, lamN, dW, dmu, st);
 }
 
 hipError_t launch_sgd(int dtype, size_t n, double lr, const void* g, void* x, hipStream_t st) {

@@ -1,0 +1,631 @@
+// Dense fp32 residual layers of width 32 or 64 on the matrix cores (gfx950
+// v_mfma_f32_32x32x2_f32).
+//
+// One wave owns 32 examples for all steps of an interval. The layer product
+// z = K_n v is a (q x q) x (q x 32) contraction: M = output feature, N = example,
+// K = input feature. Its accumulator layout holds, in register r of block mb,
+// feature 32mb + 8(r/4) + 4(l/32) + (r%4) of example l%32 (lane l). That is also a
+// valid B-operand layout for the next step once the contraction index is
+// permuted the same way in the A operand: k-slice (mb, r) pairs feature
+// f(mb, r, 0) (lanes 0-31) with f(mb, r, 1) (lanes 32-63), so the A operand of
+// lane l is K[row][f(mb, r, l/32)]. Chained steps therefore never move the
+// state between lanes. K_n and b_n are staged in LDS (row-major, padded rows,
+// double-buffered: the next layer is fetched into registers while the current
+// step runs); the bias initialises the accumulators.
+//
+// Forward step (Section 2.2):  v <- v + h_l sigma(K_n v + b_n) (+ g)
+// Adjoint step (Section 3.2):  v <- v + h_l K_n^T (sigma'(K_n u^n + b_n) * v) (+ g);
+//   the transposed product reads K_n column-wise from the same LDS copy.
+// Sweep modes follow Algorithm 1 exactly as the VALU kernels do (lp_dense_impl.h).
+#include "lp_device.h"
+#include "lp_internal.h"
+
+namespace lp {
+namespace mfma {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int MODE_SERIAL = 3;  // whole-level serial solve (coarsest level, layer-serial)
+
+// tanh(x) = sign(x) (1 - t) / (1 + t) with t = exp(-2|x|), on the hardware exp2
+// and reciprocal; absolute error a few ulp of 1.
+__device__ __forceinline__ float tanh_fast(float x) {
+  const float t = __builtin_amdgcn_exp2f(-2.885390081777927f * fabsf(x));  // 2 log2(e) |x|
+  return copysignf((1.f - t) * __builtin_amdgcn_rcpf(1.f + t), x);
+}
+
+__device__ __forceinline__ float act_v(float z, int act) {
+  if (act == ACT_TANH) return tanh_fast(z);
+  if (act == ACT_RELU) return z > 0.f ? z : 0.f;
+  if (act == ACT_SMOOTHRELU) return act_f<float, ACT_SMOOTHRELU>(z);
+  return z;
+}
+
+__device__ __forceinline__ float dact_v(float z, int act) {
+  if (act == ACT_TANH) {
+    const float t = tanh_fast(z);
+    return 1.f - t * t;
+  }
+  if (act == ACT_RELU) return z > 0.f ? 1.f : 0.f;
+  if (act == ACT_SMOOTHRELU) return dact_f<float, ACT_SMOOTHRELU>(z);
+  return 1.f;
+}
+
+template <int Q, int WAVES>
+struct Cfg {
+  static constexpr int NT = 64 * WAVES;
+  static constexpr int MB = Q / 32;               // 32-feature blocks
+  static constexpr int LD = Q + 4;                // padded LDS row (floats)
+  static constexpr int WSZ = (Q + 1) * LD;        // K rows, then the bias row
+  static constexpr int PK = Q * Q / 4 / NT;       // float4s of K_n per thread when staging
+  static_assert(Q * Q / 4 % NT == 0, "K_n must split evenly over the workgroup");
+};
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// One layer's weights in flight between global memory and LDS.
+template <int Q, int WAVES>
+struct WRegs {
+  f32x4 k[Cfg<Q, WAVES>::PK];
+  f32x4 b;  // threads < Q/4 carry four bias entries
+};
+
+template <int Q, int WAVES>
+__device__ __forceinline__ void w_fetch(WRegs<Q, WAVES>& r, const float* __restrict__ K,
+                                        const float* __restrict__ b, size_t n) {
+  using C = Cfg<Q, WAVES>;
+  const f32x4* Kn = reinterpret_cast<const f32x4*>(K + n * (size_t)(Q * Q));
+#pragma unroll
+  for (int p = 0; p < C::PK; ++p) r.k[p] = Kn[threadIdx.x + p * C::NT];
+  r.b = threadIdx.x < Q / 4 ? reinterpret_cast<const f32x4*>(b + n * (size_t)Q)[threadIdx.x] : f32x4{};
+}
+
+template <int Q, int WAVES>
+__device__ __forceinline__ void w_put(float* sh, const WRegs<Q, WAVES>& r) {
+  using C = Cfg<Q, WAVES>;
+#pragma unroll
+  for (int p = 0; p < C::PK; ++p) {
+    const int el = (threadIdx.x + p * C::NT) * 4, row = el / Q, col = el - row * Q;
+    *reinterpret_cast<f32x4*>(sh + row * C::LD + col) = r.k[p];
+  }
+  if (threadIdx.x < Q / 4) *reinterpret_cast<f32x4*>(sh + Q * C::LD + threadIdx.x * 4) = r.b;
+}
+
+// Row access in accumulator layout: p points at the example's row + 4*(lane/32).
+template <int Q>
+__device__ __forceinline__ void load_c(f32x16 (&v)[Q / 32], const float* __restrict__ p) {
+#pragma unroll
+  for (int mb = 0; mb < Q / 32; ++mb)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 x = *reinterpret_cast<const float4*>(p + 32 * mb + 8 * g);
+      v[mb][4 * g + 0] = x.x;
+      v[mb][4 * g + 1] = x.y;
+      v[mb][4 * g + 2] = x.z;
+      v[mb][4 * g + 3] = x.w;
+    }
+}
+
+template <int Q>
+__device__ __forceinline__ void store_c(float* __restrict__ p, const f32x16 (&v)[Q / 32]) {
+#pragma unroll
+  for (int mb = 0; mb < Q / 32; ++mb)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<float4*>(p + 32 * mb + 8 * g) =
+          make_float4(v[mb][4 * g + 0], v[mb][4 * g + 1], v[mb][4 * g + 2], v[mb][4 * g + 3]);
+}
+
+template <int Q>
+__device__ __forceinline__ void add_c(f32x16 (&v)[Q / 32], const float* __restrict__ p) {
+  f32x16 t[Q / 32];
+  load_c<Q>(t, p);
+#pragma unroll
+  for (int mb = 0; mb < Q / 32; ++mb) v[mb] += t[mb];
+}
+
+template <int Q>
+__device__ __forceinline__ void zero_c(f32x16 (&v)[Q / 32]) {
+#pragma unroll
+  for (int mb = 0; mb < Q / 32; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) v[mb][r] = 0.f;
+}
+
+// z = K_n v + b_n in accumulator layout (W: staged weights; lane = lane id).
+template <int Q, int LD>
+__device__ __forceinline__ void prod(f32x16 (&z)[Q / 32], const f32x16 (&v)[Q / 32], const float* W,
+                                     int lane) {
+  const int h = lane >> 5, i = lane & 31;
+#pragma unroll
+  for (int ob = 0; ob < Q / 32; ++ob) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 bb = *reinterpret_cast<const float4*>(W + Q * LD + 32 * ob + 8 * g + 4 * h);
+      z[ob][4 * g + 0] = bb.x;
+      z[ob][4 * g + 1] = bb.y;
+      z[ob][4 * g + 2] = bb.z;
+      z[ob][4 * g + 3] = bb.w;
+    }
+    const float* rowp = W + (32 * ob + i) * LD + 4 * h;
+#pragma unroll
+    for (int ib = 0; ib < Q / 32; ++ib)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 a4 = *reinterpret_cast<const float4*>(rowp + 32 * ib + 8 * g);
+        z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, v[ib][4 * g + 0], z[ob], 0, 0, 0);
+        z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, v[ib][4 * g + 1], z[ob], 0, 0, 0);
+        z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, v[ib][4 * g + 2], z[ob], 0, 0, 0);
+        z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, v[ib][4 * g + 3], z[ob], 0, 0, 0);
+      }
+  }
+}
+
+// w = K_n^T s in accumulator layout (column reads of the staged K_n).
+template <int Q, int LD>
+__device__ __forceinline__ void prod_t(f32x16 (&w)[Q / 32], const f32x16 (&s)[Q / 32], const float* W,
+                                       int lane) {
+  const int h = lane >> 5, i = lane & 31;
+#pragma unroll
+  for (int ob = 0; ob < Q / 32; ++ob) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) w[ob][r] = 0.f;
+    const float* colp = W + 32 * ob + i + 4 * h * LD;
+#pragma unroll
+    for (int ib = 0; ib < Q / 32; ++ib)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float a = colp[(32 * ib + 8 * (r >> 2) + (r & 3)) * LD];
+        w[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, s[ib][r], w[ob], 0, 0, 0);
+      }
+  }
+}
+
+template <int Q>
+__device__ __forceinline__ void apply(f32x16 (&z)[Q / 32], int act, bool deriv) {
+#pragma unroll
+  for (int mb = 0; mb < Q / 32; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z[mb][r] = deriv ? dact_v(z[mb][r], act) : act_v(z[mb][r], act);
+}
+
+template <int Q>
+__device__ __forceinline__ void correct_c(f32x16 (&v)[Q / 32], const float* cs, const float* vs) {
+  f32x16 cv[Q / 32], vv[Q / 32];
+  load_c<Q>(cv, cs);
+  load_c<Q>(vv, vs);
+#pragma unroll
+  for (int mb = 0; mb < Q / 32; ++mb) v[mb] = cv[mb] + (vv[mb] - cv[mb]);
+}
+
+// Sum of squares of (a - b) over the lane's values, in fp64.
+template <int Q>
+__device__ __forceinline__ double sq_diff(const f32x16 (&a)[Q / 32], const f32x16 (&b)[Q / 32]) {
+  double acc = 0.0;
+#pragma unroll
+  for (int mb = 0; mb < Q / 32; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float d = a[mb][r] - b[mb][r];
+      acc += (double)d * (double)d;
+    }
+  return acc;
+}
+
+// Fixed-order workgroup sum of one double per lane; result in thread 0.
+template <int WAVES>
+__device__ __forceinline__ double wg_sum(double v, double* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double s = 0.0;
+  if (threadIdx.x == 0)
+    for (int w = 0; w < WAVES; ++w) s += red[w];
+  return s;
+}
+
+// ------------------------------------------------------------------ forward
+// Interval k = blockIdx.x (serial: the whole level), examples of blockIdx.y.
+template <int Q, int MODE, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
+  using C = Cfg<Q, WAVES>;
+  constexpr int MB = C::MB;
+  __shared__ float W[2][C::WSZ];
+  __shared__ double red[WAVES];
+  const int lane = threadIdx.x & 63;
+  const int k = blockIdx.x;
+  const int Nc = gridDim.x;
+  const int e = (blockIdx.y * WAVES + (threadIdx.x >> 6)) * 32 + (lane & 31);
+  const bool on = e < a.B;
+  const size_t slice = (size_t)a.B * Q;
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane >> 5);
+  const float* K = static_cast<const float*>(a.K);
+  const float* bb = static_cast<const float*>(a.b);
+  float* X = static_cast<float*>(a.X);
+  const float* G = static_cast<const float*>(a.G);
+  const float* Cs = static_cast<const float*>(a.Cs);
+  const float* Vn = static_cast<const float*>(a.V);
+  const int c = a.c;
+  const int nsteps = MODE == MODE_SERIAL ? a.Nl : (MODE == SWEEP_CORRF ? c - 1 : c);
+  const float hl = (float)a.hl, hc = (float)a.hc;
+  const long kc = MODE == MODE_SERIAL ? 0 : (long)k * c;
+
+  WRegs<Q, WAVES> wr;
+  w_fetch<Q, WAVES>(wr, K, bb, (size_t)kc * a.stride);
+  w_put<Q, WAVES>(W[0], wr);
+  __syncthreads();
+
+  f32x16 v[MB];
+  zero_c<Q>(v);
+  if (on) {
+    if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
+      load_c<Q>(v, X + kc * slice + row);
+      if (MODE == SWEEP_FC && k == 0) store_c<Q>(static_cast<float*>(a.S) + row, v);
+    } else if (MODE == SWEEP_FRES) {
+      load_c<Q>(v, Cs + (size_t)k * a.cs_stride * slice + row);
+    } else {
+      correct_c<Q>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+      if (k > 0) store_c<Q>(X + kc * slice + row, v);
+    }
+  }
+  f32x16 coarse[MB];
+  for (int j = 0; j < nsteps; ++j) {
+    // prefetch the next layer (the last step re-fetches its own: keeps wr in registers)
+    w_fetch<Q, WAVES>(wr, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j)) * a.stride);
+    f32x16 s[MB];
+    prod<Q, C::LD>(s, v, W[j & 1], lane);
+    apply<Q>(s, a.act, false);
+    if (MODE == SWEEP_FRES && j == 0) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) coarse[mb] = v[mb] + hc * s[mb];
+    }
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) v[mb] = v[mb] + hl * s[mb];
+    if (on) {
+      if (G) add_c<Q>(v, G + (kc + j + 1) * slice + row);
+      if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) store_c<Q>(X + (kc + j + 1) * slice + row, v);
+    }
+    w_put<Q, WAVES>(W[(j + 1) & 1], wr);
+    __syncthreads();
+  }
+
+  if (MODE == SWEEP_FC) {
+    if (on) store_c<Q>(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
+  } else if (MODE == SWEEP_FRES) {
+    double acc = 0.0;
+    if (on) {
+      f32x16 cn[MB];
+      load_c<Q>(cn, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
+      acc = sq_diff<Q>(v, cn);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) coarse[mb] = v[mb] - coarse[mb];  // g_{l+1}^{k+1}
+      store_c<Q>(static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + row, coarse);
+      if (a.xn_every > 0 && (k + 1) % a.xn_every == 0)
+        store_c<Q>(static_cast<float*>(a.Xn) + (size_t)(k + 1) * slice + row, cn);
+      if (k == 0) {
+        load_c<Q>(cn, Cs + row);
+        store_c<Q>(static_cast<float*>(a.Xn) + row, cn);
+      }
+    }
+    if (a.partial) {
+      const double s = wg_sum<WAVES>(acc, red);
+      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
+    }
+  } else if (MODE == SWEEP_CORRF) {
+    if (on && k == Nc - 1) {
+      correct_c<Q>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
+      store_c<Q>(X + (size_t)a.Nl * slice + row, v);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ adjoint
+// Interval k runs from its upper C-point (k+1)c down to kc; step j produces level
+// point i = (k+1)c-1-j, linearised at the fine state of index i*stride.
+template <int Q, int MODE, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
+  using C = Cfg<Q, WAVES>;
+  constexpr int MB = C::MB;
+  __shared__ float W[2][C::WSZ];
+  __shared__ double red[WAVES];
+  const int lane = threadIdx.x & 63;
+  const int k = blockIdx.x;
+  const int Nc = gridDim.x;
+  const int e = (blockIdx.y * WAVES + (threadIdx.x >> 6)) * 32 + (lane & 31);
+  const bool on = e < a.B;
+  const size_t slice = (size_t)a.B * Q;
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane >> 5);
+  const float* K = static_cast<const float*>(a.K);
+  const float* bb = static_cast<const float*>(a.b);
+  const float* Uf = static_cast<const float*>(a.Uf);
+  float* X = static_cast<float*>(a.X);
+  const float* G = static_cast<const float*>(a.G);
+  const float* Cs = static_cast<const float*>(a.Cs);
+  const float* Vn = static_cast<const float*>(a.V);
+  const int c = a.c;
+  const int nsteps = MODE == MODE_SERIAL ? a.Nl : (MODE == SWEEP_CORRF ? c - 1 : c);
+  const float hl = (float)a.hl, hc = (float)a.hc;
+  const long top = MODE == MODE_SERIAL ? (long)a.Nl : (long)(k + 1) * c;
+
+  WRegs<Q, WAVES> wr;
+  w_fetch<Q, WAVES>(wr, K, bb, (size_t)(top - 1) * a.stride);
+  w_put<Q, WAVES>(W[0], wr);
+  __syncthreads();
+
+  f32x16 v[MB], cu[MB];
+  zero_c<Q>(v);
+  if (on) {
+    if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
+      load_c<Q>(v, X + top * slice + row);
+      if (MODE == SWEEP_FC && k == Nc - 1) store_c<Q>(static_cast<float*>(a.S) + (size_t)Nc * slice + row, v);
+    } else if (MODE == SWEEP_FRES) {
+      load_c<Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
+    } else {
+      correct_c<Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
+      if (k + 1 < Nc) store_c<Q>(X + top * slice + row, v);
+    }
+  }
+  if (MODE == SWEEP_FRES) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) cu[mb] = v[mb];
+  }
+  for (int j = 0; j < nsteps; ++j) {
+    const long i = top - 1 - j;
+    w_fetch<Q, WAVES>(wr, K, bb, (size_t)(j + 1 < nsteps ? i - 1 : i) * a.stride);
+    f32x16 d[MB], w[MB];
+    {
+      f32x16 u[MB];
+      zero_c<Q>(u);
+      if (on) load_c<Q>(u, Uf + (size_t)i * a.stride * slice + row);
+      prod<Q, C::LD>(d, u, W[j & 1], lane);
+    }
+    apply<Q>(d, a.act, true);
+    if (MODE == SWEEP_FRES && j == nsteps - 1) {
+      // coarse adjoint step from the upper C-point, linearised at the same fine state
+      f32x16 s2[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) s2[mb] = d[mb] * cu[mb];
+      prod_t<Q, C::LD>(w, s2, W[j & 1], lane);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) cu[mb] = cu[mb] + hc * w[mb];
+    }
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) d[mb] = d[mb] * v[mb];
+    prod_t<Q, C::LD>(w, d, W[j & 1], lane);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) v[mb] = v[mb] + hl * w[mb];
+    if (on) {
+      if (G) add_c<Q>(v, G + (size_t)i * slice + row);
+      if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) store_c<Q>(X + (size_t)i * slice + row, v);
+    }
+    w_put<Q, WAVES>(W[(j + 1) & 1], wr);
+    __syncthreads();
+  }
+
+  if (MODE == SWEEP_FC) {
+    if (on) store_c<Q>(static_cast<float*>(a.S) + (size_t)k * slice + row, v);
+  } else if (MODE == SWEEP_FRES) {
+    double acc = 0.0;
+    if (on) {
+      f32x16 ck[MB];
+      load_c<Q>(ck, Cs + (size_t)k * a.cs_stride * slice + row);
+      acc = sq_diff<Q>(v, ck);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) cu[mb] = v[mb] - cu[mb];  // g_{l+1}^k
+      store_c<Q>(static_cast<float*>(a.Gn) + (size_t)k * slice + row, cu);
+      if (a.xn_every > 0 && k % a.xn_every == 0)
+        store_c<Q>(static_cast<float*>(a.Xn) + (size_t)k * slice + row, ck);
+      if (k == Nc - 1) {
+        load_c<Q>(ck, Cs + (size_t)Nc * a.cs_stride * slice + row);
+        store_c<Q>(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, ck);
+      }
+    }
+    if (a.partial) {
+      const double s = wg_sum<WAVES>(acc, red);
+      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
+    }
+  } else if (MODE == SWEEP_CORRF) {
+    if (on && k == 0) {
+      correct_c<Q>(v, Cs + row, Vn + row);
+      store_c<Q>(X + row, v);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ gradient
+// Workgroup (layer n, batch chunk). Each wave takes 32 examples at a time:
+// s = sigma'(K_n u + b_n) * lam^{n+1} in accumulator layout (one matrix-core
+// product), then s and u go through LDS as [example][feature] tiles so that
+// dK[i][j] += sum_e s[e][i] u[e][j] runs as a second product with the examples
+// as the contraction index (k-slice t pairs examples 2t and 2t+1). db sums the s
+// tile's columns. The four waves' accumulators are combined in a fixed order and
+// written as the chunk's partial; a second pass sums the chunks in order and
+// scales by h (deterministic).
+constexpr int GRAD_WAVES = 4;
+
+template <int Q>
+__global__ __launch_bounds__(64 * GRAD_WAVES) void k_grad(GradArgs a) {
+  using C = Cfg<Q, GRAD_WAVES>;
+  constexpr int MB = C::MB;
+  constexpr int TL = Q + 1;  // tile row (floats)
+  __shared__ float W[C::WSZ];
+  __shared__ float tile[GRAD_WAVES][2][32 * TL];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 5, li = lane & 31;
+  const int n = blockIdx.x, chunk = blockIdx.y;
+  const int per = (((a.B + a.nchunks - 1) / a.nchunks) + 32 * GRAD_WAVES - 1) / (32 * GRAD_WAVES) *
+                  (32 * GRAD_WAVES);
+  const int e0 = chunk * per, e1 = min(a.B, e0 + per);
+  const size_t slice = (size_t)a.B * Q;
+  const float* U = static_cast<const float*>(a.U) + (size_t)n * slice;
+  const float* L = static_cast<const float*>(a.Lam) + (size_t)(n + 1) * slice;
+  {
+    WRegs<Q, GRAD_WAVES> wr;
+    w_fetch<Q, GRAD_WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), n);
+    w_put<Q, GRAD_WAVES>(W, wr);
+  }
+  __syncthreads();
+  f32x16 acc[MB][MB];
+#pragma unroll
+  for (int x = 0; x < MB; ++x)
+#pragma unroll
+    for (int y = 0; y < MB; ++y)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[x][y][r] = 0.f;
+  float dbacc = 0.f;  // lane < Q: column sum of s over this wave's examples
+  float* st = tile[wave][0];
+  float* ut = tile[wave][1];
+  for (int base = e0; base < e1; base += 32 * GRAD_WAVES) {
+    const int e = base + wave * 32 + li;
+    const bool on = e < e1;
+    const size_t row = (size_t)(on ? e : 0) * Q + 4 * h;
+    f32x16 u[MB], s[MB];
+    zero_c<Q>(u);
+    zero_c<Q>(s);
+    if (on) {
+      load_c<Q>(u, U + row);
+      load_c<Q>(s, L + row);
+    }
+    {
+      f32x16 z[MB];
+      prod<Q, C::LD>(z, u, W, lane);
+      apply<Q>(z, a.act, true);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) s[mb] = z[mb] * s[mb];
+    }
+    // accumulator layout -> [example][feature] tiles
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int f = 32 * mb + 8 * (r >> 2) + 4 * h + (r & 3);
+        st[li * TL + f] = s[mb][r];
+        ut[li * TL + f] = u[mb][r];
+      }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      const int er = (2 * t + h) * TL + li;
+#pragma unroll
+      for (int x = 0; x < MB; ++x) {
+        const float av = st[er + 32 * x];
+#pragma unroll
+        for (int y = 0; y < MB; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, ut[er + 32 * y], acc[x][y], 0, 0, 0);
+      }
+    }
+    if (lane < Q)
+      for (int t = 0; t < 32; ++t) dbacc += st[t * TL + lane];
+    __syncthreads();
+  }
+  // combine the waves in order: wave w adds its accumulators into a Q x Q buffer
+  float* red = &tile[0][0][0];  // Q*Q + Q floats fit in the tiles
+  for (int w = 0; w < GRAD_WAVES; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int x = 0; x < MB; ++x)
+#pragma unroll
+        for (int y = 0; y < MB; ++y)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int i = 32 * x + 8 * (r >> 2) + 4 * h + (r & 3), j = 32 * y + li;
+            red[i * Q + j] = (w == 0 ? 0.f : red[i * Q + j]) + acc[x][y][r];
+          }
+      if (lane < Q) red[Q * Q + lane] = (w == 0 ? 0.f : red[Q * Q + lane]) + dbacc;
+    }
+    __syncthreads();
+  }
+  float* out = static_cast<float*>(a.partial) + ((size_t)n * a.nchunks + chunk) * (Q * Q + Q);
+  for (int o = threadIdx.x; o < Q * Q + Q; o += 64 * GRAD_WAVES) out[o] = red[o];
+}
+
+// Sum the chunk partials in chunk order and scale by h.
+__global__ __launch_bounds__(256) void k_grad_final(GradArgs a, int nw, int nbias) {
+  const int nout = nw + nbias;
+  const size_t o = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (o >= (size_t)a.N * nout) return;
+  const size_t n = o / nout, r = o - n * nout;
+  const float* p = static_cast<const float*>(a.partial) + n * a.nchunks * nout + r;
+  float s = 0.f;
+  for (int ch = 0; ch < a.nchunks; ++ch) s += p[(size_t)ch * nout];
+  s *= (float)a.h;
+  if (r < (size_t)nw) static_cast<float*>(a.dK)[n * nw + r] = s;
+  else static_cast<float*>(a.db)[n * nbias + (r - nw)] = s;
+}
+
+template <int Q>
+hipError_t grad(const GradArgs& a, hipStream_t st) {
+  k_grad<Q><<<dim3(a.N, a.nchunks), 64 * GRAD_WAVES, 0, st>>>(a);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const size_t tot = (size_t)a.N * (Q * Q + Q);
+  k_grad_final<<<(unsigned)((tot + 255) / 256), 256, 0, st>>>(a, Q * Q, Q);
+  return hipGetLastError();
+}
+
+constexpr int SWEEP_WAVES = 4;   // 128 examples per interval workgroup
+constexpr int SERIAL_WAVES = 1;  // 32 examples per serial workgroup (more workgroups)
+
+template <int Q>
+hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
+  constexpr int W4 = SWEEP_WAVES;
+  const dim3 grid(a.Nl / a.c, (a.B + 32 * W4 - 1) / (32 * W4));
+  if (partials) *partials = (int)(grid.x * grid.y);
+  if (dir == DIR_FWD) {
+    if (a.mode == SWEEP_FC) k_fwd<Q, SWEEP_FC, W4><<<grid, 64 * W4, 0, st>>>(a);
+    else if (a.mode == SWEEP_FRES) k_fwd<Q, SWEEP_FRES, W4><<<grid, 64 * W4, 0, st>>>(a);
+    else k_fwd<Q, SWEEP_CORRF, W4><<<grid, 64 * W4, 0, st>>>(a);
+  } else {
+    if (a.mode == SWEEP_FC) k_adj<Q, SWEEP_FC, W4><<<grid, 64 * W4, 0, st>>>(a);
+    else if (a.mode == SWEEP_FRES) k_adj<Q, SWEEP_FRES, W4><<<grid, 64 * W4, 0, st>>>(a);
+    else k_adj<Q, SWEEP_CORRF, W4><<<grid, 64 * W4, 0, st>>>(a);
+  }
+  return hipGetLastError();
+}
+
+template <int Q>
+hipError_t serial(int dir, const SerialArgs& s, hipStream_t st) {
+  constexpr int W1 = SERIAL_WAVES;
+  SweepArgs a{};
+  a.act = s.act;
+  a.mode = MODE_SERIAL;
+  a.K = s.K;
+  a.b = s.b;
+  a.Uf = s.Uf;
+  a.B = s.B;
+  a.Nl = s.Nl;
+  a.c = 1;
+  a.stride = s.stride;
+  a.hl = s.hl;
+  a.X = s.X;
+  a.G = s.G;
+  const dim3 grid(1, (s.B + 32 * W1 - 1) / (32 * W1));
+  if (dir == DIR_FWD) k_fwd<Q, MODE_SERIAL, W1><<<grid, 64 * W1, 0, st>>>(a);
+  else k_adj<Q, MODE_SERIAL, W1><<<grid, 64 * W1, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace mfma
+
+bool mfma_width_supported(int q) { return q == 32 || q == 64; }
+
+hipError_t mfma_sweep(int q, int dir, const SweepArgs& a, hipStream_t st, int* partials) {
+  if (q == 32) return mfma::sweep<32>(dir, a, st, partials);
+  if (q == 64) return mfma::sweep<64>(dir, a, st, partials);
+  return hipErrorNotSupported;
+}
+
+hipError_t mfma_serial(int q, int dir, const SerialArgs& a, hipStream_t st) {
+  if (q == 32) return mfma::serial<32>(dir, a, st);
+  if (q == 64) return mfma::serial<64>(dir, a, st);
+  return hipErrorNotSupported;
+}
+
+hipError_t mfma_grad(int q, const GradArgs& a, hipStream_t st) {
+  if (q == 32) return mfma::grad<32>(a, st);
+  if (q == 64) return mfma::grad<64>(a, st);
+  return hipErrorNotSupported;
+}
+
+}  // namespace lp

@@ -388,13 +388,24 @@ int grad_chunks(const Shape& s, int B, int N) {
 
 int grad_nout(const Shape& s) { return s.layer == 0 ? s.C * s.C + s.C : s.C * s.C * 9 + s.C; }
 
+// fp32 dense layers of width 32 or 64 run on the matrix cores unless the
+// environment variable LP_DENSE_PATH=valu selects the vector-ALU kernels (kept
+// for cross-checking the two implementations against each other).
+bool use_mfma(const Shape& s) {
+  if (s.layer != 0 || s.dtype != 0 || !mfma_width_supported(s.C)) return false;
+  const char* e = getenv("LP_DENSE_PATH");
+  return !(e && strcmp(e, "valu") == 0);
+}
+
 hipError_t launch_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   if (s.layer != 0) return conv_sweep(s, dir, a, st, partials);
+  if (use_mfma(s)) return mfma_sweep(s.C, dir, a, st, partials);
   return s.dtype == 0 ? dense_sweep_f32(s.C, dir, a, st, partials) : dense_sweep_f64(s.C, dir, a, st, partials);
 }
 
 hipError_t launch_serial(const Shape& s, int dir, const SerialArgs& a, hipStream_t st) {
   if (s.layer != 0) return conv_serial(s, dir, a, st);
+  if (use_mfma(s)) return mfma_serial(s.C, dir, a, st);
   return s.dtype == 0 ? dense_serial_f32(s.C, dir, a, st) : dense_serial_f64(s.C, dir, a, st);
 }
 
@@ -405,6 +416,7 @@ hipError_t launch_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t
 
 hipError_t launch_grad(const Shape& s, const GradArgs& a, hipStream_t st) {
   if (s.layer != 0) return conv_grad(s, a, st);
+  if (use_mfma(s)) return mfma_grad(s.C, a, st);
   return s.dtype == 0 ? dense_grad_f32(s.C, a, st) : dense_grad_f64(s.C, a, st);
 }
 
@@ -430,7 +442,7 @@ const char* lp_last_error(void) { return g_err.c_str(); }
 
 size_t lp_workspace_bytes(const lp_problem* p, const lp_mgrit* m) {
   if (check_problem(p) != LP_OK) return 0;
-  size_t need = std::max(grad_bytes(p), resid_bytes(p));
+  size_t need = std::max({grad_bytes(p), resid_bytes(p), lp::loss_workspace_bytes(p->B, (int)qdim(p), 64)});
   if (m) {
     std::vector<int> sizes;
     if (check_mgrit(p, m, sizes) != LP_OK) return 0;
@@ -561,13 +573,16 @@ int32_t lp_open_grad(const lp_problem* p, int32_t opening, int32_t nf, const voi
 }
 
 int32_t lp_loss_terminal(const lp_problem* p, int32_t nc, const void* uN, const void* W, const void* mu,
-                         const void* c, double* J, void* lamN, void* dW, void* dmu, void* stream) {
+                         const void* c, double* J, void* lamN, void* dW, void* dmu, void* ws, size_t ws_bytes,
+                         void* stream) {
   int rc = check_problem(p);
   if (rc) return rc;
-  if (nc < 1 || nc > 64 || (size_t)nc > qdim(p)) return fail(LP_EINVAL, "need 1 <= nc <= min(64, q), nc = %d", nc);
+  if (nc < 1 || nc > 64) return fail(LP_EINVAL, "need 1 <= nc <= 64, nc = %d", nc);
   if (!uN || !W || !mu || !c || !J || !lamN || !dW || !dmu) return fail(LP_EINVAL, "NULL array argument");
   if (p->B == 0) return fail(LP_EINVAL, "the mean loss needs B >= 1");
-  LP_TRY(lp::launch_loss(p->dtype, p->B, (int)qdim(p), nc, uN, W, mu, c, J, lamN, dW, dmu,
+  rc = check_ws(ws, ws_bytes, lp::loss_workspace_bytes(p->B, (int)qdim(p), nc));
+  if (rc) return rc;
+  LP_TRY(lp::launch_loss(p->dtype, p->B, (int)qdim(p), nc, uN, W, mu, c, J, lamN, dW, dmu, ws,
                          static_cast<hipStream_t>(stream)),
          "loss");
   return LP_OK;

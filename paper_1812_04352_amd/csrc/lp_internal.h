@@ -110,6 +110,12 @@ int min_tile(const Shape& s);             // fewest examples any sweep/residual 
 LP_DENSE_DECL(f32)
 LP_DENSE_DECL(f64)
 bool dense_width_supported(int q);
+
+// Dense fp32 matrix-core family (lp_dense_mfma.hip), widths 32 and 64
+bool mfma_width_supported(int q);
+hipError_t mfma_sweep(int q, int dir, const SweepArgs& a, hipStream_t st, int* partials);
+hipError_t mfma_serial(int q, int dir, const SerialArgs& a, hipStream_t st);
+hipError_t mfma_grad(int q, const GradArgs& a, hipStream_t st);
 int dense_grad_chunks(int B, int N);
 
 // Conv family (lp_conv.hip)
@@ -131,7 +137,8 @@ hipError_t launch_open_forward(const Shape& s, int opening, int nf, int B, const
 hipError_t launch_open_grad(const Shape& s, int opening, int nf, int B, const void* y, const void* L,
                             const void* lam0, void* dL, hipStream_t st);
 hipError_t launch_loss(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,
-                       const void* c, double* J, void* lamN, void* dW, void* dmu, hipStream_t st);
+                       const void* c, double* J, void* lamN, void* dW, void* dmu, void* ws, hipStream_t st);
+size_t loss_workspace_bytes(int B, int q, int nc);  // lp_loss.hip
 hipError_t launch_sgd(int dtype, size_t n, double lr, const void* g, void* x, hipStream_t st);
 
 }  // namespace lp

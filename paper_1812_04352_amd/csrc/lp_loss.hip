@@ -1,0 +1,135 @@
+// Softmax hypothesis and cross-entropy loss at the network output, and the
+// adjoint terminal value (Section 2.1, the softmax and loss equations; the
+// terminal condition of the adjoint equations in Section 2.3):
+//   z_k = W u_k^N + mu,  S_k = softmax(z_k),  J = (1/B) sum_k -c_k^T log S_k,
+//   d_k = (S_k - c_k) / B,  lam_k^N = W^T d_k,  dW = sum_k d_k (u_k^N)^T,  dmu = sum_k d_k.
+// A boundary helper outside the per-iteration hot path; all reductions run in a
+// fixed order. Workspace: logits/residuals d [B][nc] (fp64), per-example losses
+// [B] (fp64), and per-chunk partials of dW and dmu [nchunks][nc][q+1] (fp64).
+#include <math.h>
+
+#include "lp_device.h"
+#include "lp_internal.h"
+
+namespace lp {
+namespace {
+
+constexpr int NT = 256;
+constexpr int CHUNK = 256;  // examples per partial of dW, dmu
+
+// One wave per example: z[e][j] = mu_j + sum_i W[j][i] u[e][i], lanes split i.
+template <typename T>
+__global__ __launch_bounds__(64) void k_logits(const T* uN, const T* Wc, const T* mu, double* z, int q, int nc) {
+  const int e = blockIdx.x;
+  const int lane = threadIdx.x;
+  const T* u = uN + (size_t)e * q;
+  for (int j = 0; j < nc; ++j) {
+    double acc = 0.0;
+    for (int i = lane; i < q; i += 64) acc += (double)Wc[(size_t)j * q + i] * (double)u[i];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (lane == 0) z[(size_t)e * nc + j] = acc + (double)mu[j];
+  }
+}
+
+// Thread per example: softmax, loss_e, and d_e = (S_e - c_e)/B written over z.
+template <typename T>
+__global__ __launch_bounds__(NT) void k_softmax(double* z, const T* c, double* loss, int B, int nc) {
+  const int e = blockIdx.x * NT + threadIdx.x;
+  if (e >= B) return;
+  double* ze = z + (size_t)e * nc;
+  double zmax = -INFINITY;
+  for (int j = 0; j < nc; ++j) zmax = ze[j] > zmax ? ze[j] : zmax;
+  double den = 0.0;
+  for (int j = 0; j < nc; ++j) den += exp(ze[j] - zmax);
+  const double lden = log(den);
+  double l = 0.0;
+  for (int j = 0; j < nc; ++j) {
+    const double cj = (double)c[(size_t)e * nc + j];
+    const double logp = (ze[j] - zmax) - lden;
+    l -= cj * logp;
+    ze[j] = (exp(logp) - cj) / (double)B;
+  }
+  loss[e] = l;
+}
+
+// J = (1/B) sum_e loss_e, summed in a fixed order by one workgroup.
+__global__ __launch_bounds__(NT) void k_mean(const double* loss, int B, double* J) {
+  __shared__ double sh[NT];
+  double s = 0.0;
+  for (int e = threadIdx.x; e < B; e += NT) s += loss[e];
+  s = block_sum<NT>(s, sh);
+  if (threadIdx.x == 0) J[0] = s / (double)B;
+}
+
+// partial[ch][j][i] = sum_{e in chunk ch} d[e][j] u[e][i]; column q holds sum_e d[e][j].
+template <typename T>
+__global__ __launch_bounds__(NT) void k_wpart(const T* uN, const double* d, double* part, int B, int q, int nc) {
+  const int ch = blockIdx.x;
+  const size_t o = (size_t)blockIdx.y * NT + threadIdx.x;
+  const size_t nw = (size_t)nc * (q + 1);
+  if (o >= nw) return;
+  const int j = (int)(o / (q + 1)), i = (int)(o - (size_t)j * (q + 1));
+  const int e0 = ch * CHUNK, e1 = min(B, e0 + CHUNK);
+  double acc = 0.0;
+  for (int e = e0; e < e1; ++e) acc += d[(size_t)e * nc + j] * (i < q ? (double)uN[(size_t)e * q + i] : 1.0);
+  part[(size_t)ch * nw + o] = acc;
+}
+
+template <typename T>
+__global__ __launch_bounds__(NT) void k_wfinal(const double* part, int nch, T* dW, T* dmu, int q, int nc) {
+  const size_t o = (size_t)blockIdx.x * NT + threadIdx.x;
+  const size_t nw = (size_t)nc * (q + 1);
+  if (o >= nw) return;
+  double s = 0.0;
+  for (int ch = 0; ch < nch; ++ch) s += part[(size_t)ch * nw + o];
+  const int j = (int)(o / (q + 1)), i = (int)(o - (size_t)j * (q + 1));
+  if (i < q) dW[(size_t)j * q + i] = (T)s;
+  else dmu[j] = (T)s;
+}
+
+// lamN[e][i] = sum_j W[j][i] d[e][j]
+template <typename T>
+__global__ __launch_bounds__(NT) void k_lam(const T* Wc, const double* d, T* lamN, int B, int q, int nc) {
+  const size_t o = (size_t)blockIdx.x * NT + threadIdx.x;
+  if (o >= (size_t)B * q) return;
+  const size_t e = o / q, i = o - e * q;
+  double acc = 0.0;
+  for (int j = 0; j < nc; ++j) acc += (double)Wc[(size_t)j * q + i] * d[e * nc + j];
+  lamN[o] = (T)acc;
+}
+
+size_t up(size_t x) { return (x + 255) / 256 * 256; }
+
+template <typename T>
+hipError_t loss_t(int B, int q, int nc, const void* uN, const void* Wc, const void* mu, const void* c, double* J,
+                  void* lamN, void* dW, void* dmu, void* ws, hipStream_t st) {
+  char* w = static_cast<char*>(ws);
+  double* z = reinterpret_cast<double*>(w);
+  double* loss = reinterpret_cast<double*>(w + up((size_t)B * nc * 8));
+  double* part = reinterpret_cast<double*>(w + up((size_t)B * nc * 8) + up((size_t)B * 8));
+  const int nch = (B + CHUNK - 1) / CHUNK;
+  const size_t nw = (size_t)nc * (q + 1);
+  k_logits<T><<<B, 64, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu, z, q, nc);
+  k_softmax<T><<<(B + NT - 1) / NT, NT, 0, st>>>(z, (const T*)c, loss, B, nc);
+  k_mean<<<1, NT, 0, st>>>(loss, B, J);
+  k_wpart<T><<<dim3(nch, (unsigned)((nw + NT - 1) / NT)), NT, 0, st>>>((const T*)uN, z, part, B, q, nc);
+  k_wfinal<T><<<(unsigned)((nw + NT - 1) / NT), NT, 0, st>>>(part, nch, (T*)dW, (T*)dmu, q, nc);
+  k_lam<T><<<(unsigned)(((size_t)B * q + NT - 1) / NT), NT, 0, st>>>((const T*)Wc, z, (T*)lamN, B, q, nc);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t loss_workspace_bytes(int B, int q, int nc) {
+  const size_t nch = (size_t)(B + CHUNK - 1) / CHUNK;
+  return up((size_t)B * nc * 8) + up((size_t)B * 8) + up(nch * nc * (size_t)(q + 1) * 8);
+}
+
+hipError_t launch_loss(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,
+                       const void* c, double* J, void* lamN, void* dW, void* dmu, void* ws, hipStream_t st) {
+  return dtype == 0 ? loss_t<float>(B, q, nc, uN, Wc, mu, c, J, lamN, dW, dmu, ws, st)
+                    : loss_t<double>(B, q, nc, uN, Wc, mu, c, J, lamN, dW, dmu, ws, st);
+}
+
+}  // namespace lp

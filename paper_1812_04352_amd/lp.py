@@ -84,7 +84,7 @@ _SIGS = {
     "lp_residual_norm": ([_P, _i32, _v, _v, _v, _v, _v, _sz, _dp, _v], _i32),
     "lp_open_forward": ([_P, _i32, _i32, _v, _v, _v, _v], _i32),
     "lp_open_grad": ([_P, _i32, _i32, _v, _v, _v, _v, _v], _i32),
-    "lp_loss_terminal": ([_P, _i32, _v, _v, _v, _v, _v, _v, _v, _v, _v], _i32),
+    "lp_loss_terminal": ([_P, _i32, _v, _v, _v, _v, _v, _v, _v, _v, _v, _sz, _v], _i32),
     "lp_sgd_update": ([_i32, _sz, ctypes.c_double, _v, _v, _v], _i32),
     "lp_trace_enable": ([ctypes.c_uint32], _i32),
     "lp_trace_read": ([_i32, _i32, _ip, _dp], _i32),
@@ -260,13 +260,14 @@ def lp_open_grad(p: LpProblem, opening: int, nf: int, y, L_in, lam0, dL_in) -> N
            "lp_open_grad")
 
 
-def lp_loss_terminal(p: LpProblem, nc: int, uN, W, mu, c, J, lamN, dW, dmu) -> None:
+def lp_loss_terminal(p: LpProblem, nc: int, uN, W, mu, c, J, lamN, dW, dmu, ws) -> None:
     import torch
     dt = _elem_dtype(p)
+    wp, wn = _ws(ws, 1)
     _check(load().lp_loss_terminal(ctypes.byref(p), nc, _arr(uN, p.B * p.q, "uN", dt), _arr(W, nc * p.q, "W", dt),
                                    _arr(mu, nc, "mu", dt), _arr(c, p.B * nc, "c", dt),
                                    _arr(J, 1, "J", torch.float64), _arr(lamN, p.B * p.q, "lamN", dt),
-                                   _arr(dW, nc * p.q, "dW", dt), _arr(dmu, nc, "dmu", dt), _stream()),
+                                   _arr(dW, nc * p.q, "dW", dt), _arr(dmu, nc, "dmu", dt), wp, wn, _stream()),
            "lp_loss_terminal")
 
 

@@ -109,8 +109,14 @@ def test_helper_validation_codes():
     lib = L.load()
     p = _p()
     J = ctypes.c_void_p(0x2000)
-    assert lib.lp_loss_terminal(ctypes.byref(p), 0, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, None) == L.LP_EINVAL
-    assert lib.lp_loss_terminal(ctypes.byref(p), 33, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, None) == L.LP_EINVAL
+    big = 1 << 40
+    for nc in (0, 65):
+        assert lib.lp_loss_terminal(ctypes.byref(p), nc, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, FAKE, big,
+                                    None) == L.LP_EINVAL
+    assert lib.lp_loss_terminal(ctypes.byref(p), 10, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, FAKE, 1024,
+                                None) == L.LP_EWORKSPACE
+    assert lib.lp_loss_terminal(ctypes.byref(p), 10, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, None, big,
+                                None) == L.LP_EWORKSPACE
     assert lib.lp_open_forward(ctypes.byref(p), 5, 3, FAKE, FAKE, FAKE, None) == L.LP_EINVAL
     assert lib.lp_open_grad(ctypes.byref(p), L.LP_OPEN_IDENTITY, 3, FAKE, FAKE, FAKE, FAKE, None) == L.LP_EINVAL
     assert lib.lp_sgd_update(7, 10, 0.1, FAKE, FAKE, None) == L.LP_EINVAL

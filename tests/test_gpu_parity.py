@@ -41,7 +41,7 @@ def _lamN(c, U_gpu):
     lamN = torch.empty_like(U_gpu[-1])
     dW = torch.empty_like(c.W)
     dmu = torch.empty_like(c.mu)
-    L.lp_loss_terminal(c.p, wl.n_classes, U_gpu[-1], c.W, c.mu, c.onehot, J, lamN, dW, dmu)
+    L.lp_loss_terminal(c.p, wl.n_classes, U_gpu[-1], c.W, c.mu, c.onehot, J, lamN, dW, dmu, L.alloc_workspace(c.p))
     return lamN, J, dW, dmu
 
 
