@@ -189,7 +189,7 @@ Layout mgrit_layout(const lp_problem* p, const lp_mgrit* m, const std::vector<in
 size_t grad_bytes(const lp_problem* p) {
   const lp::Shape s = shape_of(p);
   const size_t nch = (size_t)lp::grad_chunks(s, p->B, p->N);
-  return up((size_t)p->N * nch * lp::grad_nout(s) * esize(p));
+  return up((size_t)p->N * nch * lp::grad_partial_floats(s) * esize(p));
 }
 
 size_t resid_bytes(const lp_problem* p) {
@@ -387,6 +387,10 @@ int grad_chunks(const Shape& s, int B, int N) {
 }
 
 int grad_nout(const Shape& s) { return s.layer == 0 ? s.C * s.C + s.C : s.C * s.C * 9 + s.C; }
+
+// Values one gradient workgroup writes as its chunk partial: dense dK and db;
+// conv the expanded 16 x 96 weight block plus db (see lp_conv.hip).
+int grad_partial_floats(const Shape& s) { return s.layer == 0 ? s.C * s.C + s.C : 16 * 96 + s.C; }
 
 // fp32 dense layers of width 32 or 64 run on the matrix cores unless the
 // environment variable LP_DENSE_PATH=valu selects the vector-ALU kernels (kept

@@ -98,6 +98,7 @@ hipError_t launch_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t
 hipError_t launch_grad(const Shape& s, const GradArgs& a, hipStream_t st);
 int grad_chunks(const Shape& s, int B, int N);  // batch chunks of the gradient's first pass
 int grad_nout(const Shape& s);            // weights + bias entries per layer
+int grad_partial_floats(const Shape& s);  // values per (layer, chunk) gradient partial
 bool shape_supported(const Shape& s);
 int min_tile(const Shape& s);             // fewest examples any sweep/residual workgroup covers
 

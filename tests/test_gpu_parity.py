@@ -21,6 +21,8 @@ DENSE = [
     ("tanh32", WORKLOADS[5].with_overrides(N=64, B=513, n_features=40)),
     ("srelu16_f64", WORKLOADS[1].with_overrides(C=16, act="smoothrelu", N=48, B=257)),
     ("relu8_f32", WORKLOADS[2].with_overrides(C=8, N=32, B=77, n_features=12, n_classes=5)),
+    ("conv_relu12", WORKLOADS[4].with_overrides(N=16, B=5, H=12, W=12, n_features=144, max_levels=3)),
+    ("conv_tanh28", WORKLOADS[4].with_overrides(N=16, B=3, act="tanh", max_levels=3)),
 ]
 IDS = [n for n, _ in DENSE]
 

@@ -147,7 +147,8 @@ def generate(wl: Workload, data_seed: Optional[int] = None,
         labels = rd.integers(0, nc, size=B)
     elif wl.cfg == 4:
         patterns = rd.uniform(0.0, 1.0, size=(nc, 5, 5))
-        offsets = rd.integers(0, 24, size=(nc, 2))
+        offsets = np.stack([rd.integers(0, wl.H - 4, size=nc), rd.integers(0, wl.W - 4, size=nc)], axis=1) \
+            if (wl.H, wl.W) != (28, 28) else rd.integers(0, 24, size=(nc, 2))
         labels = rd.integers(0, nc, size=B)
         y = rd.uniform(0.0, 1.0, size=(B, 1, wl.H, wl.W))
         for k in range(nc):
