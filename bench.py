@@ -177,7 +177,20 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default: the second workload)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 5 times (to scale HBM byte counters)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = 1 << 28  # fp32 values = 1 GiB
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read_per_launch": 4 * n, "copy_bytes_written_per_launch": 4 * n,
+                          "launches": 5}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
               file=sys.stderr)
@@ -279,7 +292,10 @@ def main():
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     else:
         achieved = flops / launches / (avg_ms / 1e3) / 1e12
-        roof = {"bound": "alu", "achieved": achieved, "peak": PEAK_TFLOPS[wl.dtype], "unit": "TFLOP/s"}
+        on_mfma = wl.dtype == "f32" and (wl.layer == "conv3x3" or wl.q in (32, 64)) and \
+            os.environ.get("LP_DENSE_PATH") != "valu"
+        roof = {"bound": "mfma" if on_mfma else "alu", "achieved": achieved, "peak": PEAK_TFLOPS[wl.dtype],
+                "unit": "TFLOP/s"}
     roof["frac"] = achieved / roof["peak"]
     roof["traffic"] = measured_traffic(dominant, f"cfg{wl.cfg}")
     roof["kernel"] = dominant

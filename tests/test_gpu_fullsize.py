@@ -1,0 +1,130 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark uses. Examples are independent in the forward and adjoint MGRIT
+solves, so the oracle runs on a sample of examples (the first ones, the last
+ones of the ragged final workgroup, and seeded random ones) and is compared
+element by element with the same examples of the full GPU solve. The reduced
+gradient couples the batch: it is compared with the oracle in full where that
+is cheap, and otherwise checked for additivity over the batch on the GPU."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_1812_04352_amd import lp as L
+from workloads import WORKLOADS
+from lp_testutil import Case, assert_close, sched
+
+pytestmark = pytest.mark.gpu
+
+
+def sample_of(B, n_rand, seed=0):
+    r = np.random.default_rng(seed)
+    idx = set(range(min(4, B))) | set(range(max(0, B - 4), B))
+    idx |= set(r.choice(B, size=min(n_rand, B), replace=False).tolist())
+    return np.array(sorted(idx))
+
+
+@pytest.fixture(scope="module", params=[1, 2, 3, 4, 5], ids=lambda c: f"cfg{c}")
+def full(request):
+    wl = WORKLOADS[request.param]
+    print(f"[fullsize] cfg{wl.cfg} {wl.name}", flush=True)
+    c = Case(wl)
+    yield c
+    del c
+    torch.cuda.empty_cache()
+
+
+def _stop_rule(wl, iters):
+    return sched(wl, iters, rtol=wl.rtol, stag=wl.stag)
+
+
+def _check_relu_gradient(dK, db, dKr, dbr, U, Lam, d, wl, rel_tau=1e-5):
+    """ReLU gradient check. sigma'(z) = 1[z > 0] is a decision; the fp32 GPU run and
+    the fp64 oracle reach the trajectory with rounding-level differences, so
+    pre-activations within tau of 0 may be decided either way. The difference must
+    be within the parity bar plus the largest change those ambiguous sites can make,
+    |h sum_{|z| < tau} lam u^T| elementwise (tau = rel_tau * max|z| per layer)."""
+    tol = 1e-5
+    A = np.zeros_like(dKr)
+    Ab = np.zeros_like(dbr)
+    for n in range(wl.N):
+        z = O.preact(d["K"][n].astype(np.float64), d["b"][n].astype(np.float64), U[n])
+        amb = np.abs(z) < rel_tau * np.abs(z).max()
+        lam = np.where(amb, np.abs(Lam[n + 1]), 0.0)
+        A[n] = wl.h * lam.T @ np.abs(U[n])
+        Ab[n] = wl.h * lam.sum(axis=0)
+    eK, eb = np.abs(dK - dKr), np.abs(db - dbr)
+    assert np.linalg.norm(eK) <= tol * np.linalg.norm(dKr) + np.linalg.norm(A), (np.linalg.norm(eK), np.linalg.norm(A))
+    assert np.all(eK <= 10 * tol * np.abs(dKr).max() + A)
+    assert np.linalg.norm(eb) <= tol * np.linalg.norm(dbr) + np.linalg.norm(Ab)
+    assert np.all(eb <= 10 * tol * np.abs(dbr).max() + Ab)
+
+
+def test_mgrit_forward_and_adjoint_full_size(full):
+    c = full
+    wl = c.wl
+    S = sample_of(wl.B, 8 if wl.layer == "conv3x3" else 12)
+    mg = _stop_rule(wl, wl.fwd_iters)
+    ws = L.alloc_workspace(c.p, mg)
+    U = c.new_traj()
+    itF, histF = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws)
+    assert all(np.isfinite(histF))
+    if wl.rtol > 0:
+        assert histF[-1] <= wl.rtol * histF[0] or itF == wl.fwd_iters or histF[-1] > wl.stag * histF[-2]
+    Ur = np.zeros((wl.N + 1, len(S)) + c.u0_ref.shape[1:])
+    Ur[0] = c.u0_ref[S]
+    Ur, _, _ = O.mgrit_forward(Ur, c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=wl.relax, max_iter=itF)
+    Ug = U[:, torch.from_numpy(S).cuda()].cpu().numpy()
+    assert_close(Ug, Ur, wl.dtype, f"cfg{wl.cfg} U sample after {itF} iterations")
+
+    # adjoint from each side's own terminal value; the oracle's terminal value on the
+    # sample carries 1/|sample| and is rescaled to the batch mean's 1/B
+    J = torch.zeros(1, device="cuda", dtype=torch.float64)
+    Lam = torch.zeros_like(U)
+    dW, dmu = torch.empty_like(c.W), torch.empty_like(c.mu)
+    L.lp_loss_terminal(c.p, wl.n_classes, U[-1], c.W, c.mu, c.onehot, J, Lam[-1], dW, dmu, ws)
+    mgA = _stop_rule(wl, wl.adj_iters)
+    itA, histA = L.lp_mgrit_adjoint(c.p, mgA, c.K, c.b, U, Lam, ws)
+    assert all(np.isfinite(histA))
+    lamN = O.loss_terminal(Ur[-1], c.d["W"], c.d["mu"], c.d["onehot"][S])[1] * (len(S) / wl.B)
+    Lr = np.zeros_like(Ur)
+    Lr[-1] = lamN
+    Lr, _, _ = O.mgrit_adjoint(Ur, Lr, c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=wl.relax, max_iter=itA)
+    Lg = Lam[:, torch.from_numpy(S).cuda()].cpu().numpy()
+    assert_close(Lg, Lr, wl.dtype, f"cfg{wl.cfg} Lam sample after {itA} iterations")
+
+    # gradient: full oracle comparison where cheap, else additivity over the batch
+    dK, db = torch.empty_like(c.K), torch.empty_like(c.b)
+    L.lp_gradient(c.p, c.K, c.b, U, Lam, dK, db, ws)
+    if wl.cfg in (1, 2):
+        Uf, _, _ = O.mgrit_forward(
+            np.concatenate([c.u0_ref[None], np.zeros((wl.N,) + c.u0_ref.shape)]), c.d["K"], c.d["b"], wl.h,
+            wl.act, cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=itF)
+        lamNf = O.loss_terminal(Uf[-1], c.d["W"], c.d["mu"], c.d["onehot"])[1]
+        Lf = np.zeros_like(Uf)
+        Lf[-1] = lamNf
+        Lf, _, _ = O.mgrit_adjoint(Uf, Lf, c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=wl.max_levels,
+                                   min_coarse=wl.min_coarse, relax=wl.relax, max_iter=itA)
+        dKr, dbr = O.gradient(Uf, Lf, c.d["K"], c.d["b"], wl.h, wl.act)
+        if wl.act == "relu":
+            _check_relu_gradient(dK.cpu().numpy(), db.cpu().numpy(), dKr, dbr, Uf, Lf, c.d, wl)
+        else:
+            assert_close(dK.cpu().numpy(), dKr, wl.dtype, "dK full size")
+            assert_close(db.cpu().numpy(), dbr, wl.dtype, "db full size")
+    else:
+        half = wl.B // 2
+        parts = []
+        for lo, hi in ((0, half), (half, wl.B)):
+            p2 = L.problem(wl.dtype, wl.layer, wl.act, wl.N, hi - lo, wl.C, wl.H, wl.W, wl.h)
+            Uh, Lh = U[:, lo:hi].contiguous(), Lam[:, lo:hi].contiguous()
+            dKh, dbh = torch.empty_like(c.K), torch.empty_like(c.b)
+            L.lp_gradient(p2, c.K, c.b, Uh, Lh, dKh, dbh, L.alloc_workspace(p2))
+            parts.append((dKh.double(), dbh.double()))
+            del Uh, Lh
+        sK = (parts[0][0] + parts[1][0]).cpu().numpy()
+        sb = (parts[0][1] + parts[1][1]).cpu().numpy()
+        assert_close(dK.cpu().numpy(), sK, wl.dtype, "dK additivity", scale=10)
+        assert_close(db.cpu().numpy(), sb, wl.dtype, "db additivity", scale=10)
+    del U, Lam, ws

@@ -209,3 +209,55 @@ def test_empty_batch_is_a_no_op():
     dK, db = torch.ones_like(K), torch.ones_like(b)
     L.lp_gradient(p, K, b, U, U.clone(), dK, db, ws)
     assert float(dK.abs().max()) == 0.0 and float(db.abs().max()) == 0.0
+
+
+@pytest.mark.parametrize("name,wl", [DENSE[1], DENSE[2]], ids=[DENSE[1][0], DENSE[2][0]])
+def test_valu_kernels_match_oracle(name, wl, monkeypatch):
+    """The vector-ALU kernels for fp32 widths that normally run on the matrix cores
+    (selected with LP_DENSE_PATH=valu) also meet the parity bar."""
+    monkeypatch.setenv("LP_DENSE_PATH", "valu")
+    c = case(wl)
+    mg = sched(wl, 3)
+    ws = L.alloc_workspace(c.p, mg)
+    U = c.new_traj()
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws)
+    Ur, _, _ = O.mgrit_forward(c.ref_traj(), c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=wl.relax, max_iter=3)
+    assert_close(U.cpu().numpy(), Ur, wl.dtype, "U (VALU)")
+    lamN = random_state(wl, 5)[0]
+    Lam = torch.zeros_like(U)
+    Lam[-1] = torch.from_numpy(lamN).to(U)
+    L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, Lam, ws)
+    L0 = np.zeros_like(Ur)
+    L0[-1] = lamN
+    Lr, _, _ = O.mgrit_adjoint(Ur, L0, c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=wl.relax, max_iter=3)
+    assert_close(Lam.cpu().numpy(), Lr, wl.dtype, "Lam (VALU)")
+    dK, db = torch.empty_like(c.K), torch.empty_like(c.b)
+    L.lp_gradient(c.p, c.K, c.b, U, Lam, dK, db, ws)
+    dKr, dbr = O.gradient(Ur, Lr, c.d["K"], c.d["b"], wl.h, wl.act)
+    assert_close(dK.cpu().numpy(), dKr, wl.dtype, "dK (VALU)")
+    assert_close(db.cpu().numpy(), dbr, wl.dtype, "db (VALU)")
+
+
+def test_one_shot_training_matches_oracle():
+    """Algorithm 2 with one forward and one adjoint MGRIT iteration per update and a
+    plain gradient step: per-update losses and final weights against the oracle's
+    one-shot run (reduced size, larger step so that the weights move)."""
+    from paper_1812_04352_amd.one_shot import OneShotTrainer
+    wl = WORKLOADS[5].with_overrides(N=64, B=300, n_features=40)
+    c = case(wl)
+    updates, lr = 12, 0.5
+    params = {k: getattr(c, k).clone() for k in ("K", "b", "W", "mu", "L_in")}
+    tr = OneShotTrainer(c.p, sched(wl, wl.fwd_iters), sched(wl, wl.adj_iters), params, c.y, c.onehot,
+                        wl.n_classes, L.OPENING[wl.opening], wl.n_features)
+    losses = tr.run(updates, lr)
+    d = c.d
+    lo, wo = O.one_shot(d["y"], d["onehot"], d["L_in"], d["K"], d["b"], d["W"], d["mu"], wl.h, wl.act, wl.opening,
+                        cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax,
+                        updates=updates, lr=lr, m1=wl.fwd_iters, m2=wl.adj_iters)
+    for i, (a, b) in enumerate(zip(losses, lo)):
+        assert abs(a - b) <= 1e-4 * abs(b), (i, a, b)
+    assert losses[-1] < losses[0]
+    for k in params:
+        assert_close(params[k].cpu().numpy(), wo[k], wl.dtype, f"{k} after {updates} updates", scale=10)
