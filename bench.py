@@ -72,30 +72,35 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int):
     byts = flops = launches = 0
     if kind == "gradient":
         return 2 * wl.N * row + wl.N * nweights * e, 4.0 * mac * B * wl.N, 1
-    for l, Nl in enumerate(sizes):
-        wbytes = Nl * nweights * e
-        g = 1 if l >= 1 else 0
-        if l == L - 1:
-            if kind.endswith("coarsest"):
-                byts += (1 + g * Nl + Nl + (Nl if adj else 0)) * row + wbytes
-                flops += Nl * fstep * B
+    # With FCF the finest level's correction is applied inside the next cycle's FC
+    # sweep (one more row read per interval from the second cycle on) and its
+    # correction + F-relaxation sweep runs once per solve.
+    for m in range(iters):
+        for l, Nl in enumerate(sizes):
+            wbytes = Nl * nweights * e
+            g = 1 if l >= 1 else 0
+            if l == L - 1:
+                if kind.endswith("coarsest"):
+                    byts += (1 + g * Nl + Nl + (Nl if adj else 0)) * row + wbytes
+                    flops += Nl * fstep * B
+                    launches += 1
+                continue
+            Nc = Nl // c
+            xn = (1.0 / c) if (l + 1 < L - 1) else 0.0
+            deferred = l == 0 and fcf
+            if kind.endswith("_fc") and fcf:
+                byts += Nc * (2 + g * c + (c if adj else 0) + (1 if deferred and m > 0 else 0)) * row + wbytes
+                flops += Nc * c * fstep * B
                 launches += 1
-            continue
-        Nc = Nl // c
-        xn = (1.0 / c) if (l + 1 < L - 1) else 0.0
-        if kind.endswith("_fc") and fcf:
-            byts += Nc * (2 + g * c + (c if adj else 0)) * row + wbytes
-            flops += Nc * c * fstep * B
-            launches += 1
-        elif kind.endswith("_fres"):
-            byts += Nc * (3 + xn + g * c + (c if adj else 0)) * row + wbytes
-            flops += Nc * (c * fstep + (2 * mac if adj else 0)) * B
-            launches += 1
-        elif kind.endswith("_corrf"):
-            byts += Nc * (2 + c + g * (c - 1) + ((c - 1) if adj else 0)) * row + wbytes
-            flops += Nc * (c - 1) * fstep * B
-            launches += 1
-    return byts * iters, flops * iters, launches * iters
+            elif kind.endswith("_fres"):
+                byts += Nc * (3 + xn + g * c + (c if adj else 0)) * row + wbytes
+                flops += Nc * (c * fstep + (2 * mac if adj else 0)) * B
+                launches += 1
+            elif kind.endswith("_corrf") and (not deferred or m == iters - 1):
+                byts += Nc * (2 + c + g * (c - 1) + ((c - 1) if adj else 0)) * row + wbytes
+                flops += Nc * (c - 1) * fstep * B
+                launches += 1
+    return byts, flops, launches
 
 
 def source_hash() -> str:

@@ -187,7 +187,9 @@ __global__ __launch_bounds__(NT) void k_fwd(SweepArgs a, int H, int W) {
   stage_w(sw[0], K, bb, (size_t)kc * a.stride);
   __syncthreads();
   if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
-    row_in(buf[0], X + kc * slice + eo, nullptr, g);
+    // a pending coarse-grid correction of the previous cycle is applied on the fly
+    if (MODE == SWEEP_FC && Vn) row_in(buf[0], Cs + (size_t)k * a.cs_stride * slice + eo, Vn + (size_t)k * slice + eo, g);
+    else row_in(buf[0], X + kc * slice + eo, nullptr, g);
     if (MODE == SWEEP_FC && k == 0) row_copy(static_cast<float*>(a.S) + eo, X + eo, g.q);
   } else if (MODE == SWEEP_FRES) {
     row_in(buf[0], Cs + (size_t)k * a.cs_stride * slice + eo, nullptr, g);
@@ -303,7 +305,9 @@ __global__ __launch_bounds__(NT) void k_adj(SweepArgs a, int H, int W) {
   stage_w(sw[0], K, bb, (size_t)(top - 1) * a.stride);
   __syncthreads();
   if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
-    row_in(buf[0], X + top * slice + eo, nullptr, g);
+    if (MODE == SWEEP_FC && Vn)
+      row_in(buf[0], Cs + (size_t)(k + 1) * a.cs_stride * slice + eo, Vn + (size_t)(k + 1) * slice + eo, g);
+    else row_in(buf[0], X + top * slice + eo, nullptr, g);
     if (MODE == SWEEP_FC && k == Nc - 1) row_copy(static_cast<float*>(a.S) + (size_t)Nc * slice + eo, X + top * slice + eo, g.q);
   } else if (MODE == SWEEP_FRES) {
     row_in(buf[0], Cs + (size_t)(k + 1) * a.cs_stride * slice + eo, nullptr, g);

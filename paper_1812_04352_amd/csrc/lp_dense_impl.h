@@ -182,7 +182,9 @@ __global__ __launch_bounds__(NT) void k_fwd_sweep(SweepArgs a) {
   T v[Q];
   if (on) {
     if (mode == SWEEP_FC) {
-      load_row<T, Q>(v, X + kc * slice + row);
+      // a pending coarse-grid correction of the previous cycle is applied on the fly
+      if (Vn) correct_row<T, Q>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+      else load_row<T, Q>(v, X + kc * slice + row);
       if (k == 0) store_row<T, Q>(static_cast<T*>(a.S) + row, v);
     } else if (mode == SWEEP_FRES) {
       load_row<T, Q>(v, Cs + (size_t)k * a.cs_stride * slice + row);
@@ -288,7 +290,9 @@ __global__ __launch_bounds__(NT) void k_adj_sweep(SweepArgs a) {
   T coarse[Q];  // FRES: holds C_{k+1} until the last step, then the coarse step
   if (on) {
     if (mode == SWEEP_FC) {
-      load_row<T, Q>(v, X + top * slice + row);
+      if (Vn)
+        correct_row<T, Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
+      else load_row<T, Q>(v, X + top * slice + row);
       if (k == Nc - 1) store_row<T, Q>(static_cast<T*>(a.S) + (size_t)Nc * slice + row, v);
     } else if (mode == SWEEP_FRES) {
       load_row<T, Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);

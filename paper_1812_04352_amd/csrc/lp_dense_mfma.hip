@@ -260,7 +260,10 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
   zero_c<Q>(v);
   if (on) {
     if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
-      load_c<Q>(v, X + kc * slice + row);
+      // a pending coarse-grid correction of the previous cycle is applied on the fly
+      if (MODE == SWEEP_FC && Vn)
+        correct_c<Q>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+      else load_c<Q>(v, X + kc * slice + row);
       if (MODE == SWEEP_FC && k == 0) store_c<Q>(static_cast<float*>(a.S) + row, v);
     } else if (MODE == SWEEP_FRES) {
       load_c<Q>(v, Cs + (size_t)k * a.cs_stride * slice + row);
@@ -357,7 +360,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
   zero_c<Q>(v);
   if (on) {
     if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
-      load_c<Q>(v, X + top * slice + row);
+      if (MODE == SWEEP_FC && Vn)
+        correct_c<Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
+      else load_c<Q>(v, X + top * slice + row);
       if (MODE == SWEEP_FC && k == Nc - 1) store_c<Q>(static_cast<float*>(a.S) + (size_t)Nc * slice + row, v);
     } else if (MODE == SWEEP_FRES) {
       load_c<Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);

@@ -147,6 +147,7 @@ int check_mgrit(const lp_problem* p, const lp_mgrit* m, std::vector<int>& sizes)
 // Workspace layout for one MGRIT solve.
 struct Layout {
   std::vector<size_t> X, G, S;  // byte offsets per level (X[0], G[0] unused)
+  size_t S0b = 0;               // second finest-level staging buffer
   size_t partial = 0, rho = 0, total = 0;
   int partial_cap = 0;
 };
@@ -175,6 +176,10 @@ Layout mgrit_layout(const lp_problem* p, const lp_mgrit* m, const std::vector<in
     for (int l = 0; l + 1 < nl; ++l) {
       L.S[l] = off;
       off = up(off + (size_t)(sizes[l + 1] + 1) * sl);
+    }
+    if (nl > 1) {  // second finest-level staging buffer
+      L.S0b = off;
+      off = up(off + (size_t)(sizes[1] + 1) * sl);
     }
   }
   L.partial_cap = partial_capacity(p);
@@ -215,6 +220,9 @@ struct Solver {
   const void* Uf;  // fine primal trajectory (adjoint)
   std::vector<int> sizes;
   std::vector<void*> X, G, S;
+  void* S0[2] = {nullptr, nullptr};  // finest-level staging buffers (FCF), used alternately
+  int cur0 = 0;
+  bool pending = false;              // finest-level correction not yet written back
   double* partial;
   hipStream_t st;
   int partials_used = 0;
@@ -249,14 +257,27 @@ struct Solver {
     a.hc = hl * (double)m->cf;
     a.X = X[l];
     a.G = G[l];
-    a.S = S[l];
+    // On the finest level with FCF the coarse-grid correction of a cycle is not
+    // written back: the next cycle's FC sweep starts from C + (V - C) (the same
+    // correction, applied on the fly), and the F-points, which no later sweep
+    // reads, are written once by finish() after the last cycle. The relaxed
+    // C-points then alternate between two staging buffers.
+    const bool defer = l == 0 && fcf;
+    void* Sl = defer ? S0[cur0] : S[l];
+    a.S = Sl;
     a.finest = l == 0;
     a.mode = lp::SWEEP_FC;
+    if (defer && pending) {
+      a.Cs = S0[cur0 ^ 1];
+      a.cs_stride = 1;
+      a.V = X[1];
+    }
     if (fcf) {
       TraceScope ts(kb + 0, l, st);
       LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "FC-relaxation");
     }
-    a.Cs = fcf ? S[l] : X[l];
+    a.V = nullptr;
+    a.Cs = fcf ? Sl : X[l];
     a.cs_stride = fcf ? 1 : m->cf;
     a.Xn = X[l + 1];
     a.Gn = G[l + 1];
@@ -271,11 +292,44 @@ struct Solver {
     if (l == 0) partials_used = np;
     int rc = cycle(l + 1);
     if (rc != LP_OK) return rc;
+    if (defer) {
+      pending = true;
+      cur0 ^= 1;
+      return LP_OK;
+    }
     a.V = X[l + 1];
     a.mode = lp::SWEEP_CORRF;
     a.partial = nullptr;
     TraceScope ts(kb + 2, l, st);
     LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "correction and F-relaxation");
+    return LP_OK;
+  }
+
+  // Apply the finest level's pending correction and F-relaxation (Algorithm 1,
+  // steps 4-5 of the last cycle), writing every row of the solution.
+  int finish() {
+    if (!pending) return LP_OK;
+    lp::SweepArgs a{};
+    a.act = p->act;
+    a.mode = lp::SWEEP_CORRF;
+    a.K = K;
+    a.b = b;
+    a.Uf = Uf;
+    a.B = p->B;
+    a.Nl = sizes[0];
+    a.c = m->cf;
+    a.stride = 1;
+    a.hl = p->h;
+    a.hc = p->h * (double)m->cf;
+    a.X = X[0];
+    a.Cs = S0[cur0 ^ 1];
+    a.cs_stride = 1;
+    a.V = X[1];
+    a.finest = 1;
+    const int kb = dir == lp::DIR_FWD ? LP_TRACE_FWD_FC : LP_TRACE_ADJ_FC;
+    TraceScope ts(kb + 2, 0, st);
+    LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "correction and F-relaxation");
+    pending = false;
     return LP_OK;
   }
 };
@@ -316,8 +370,11 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
     s.X[l] = w + lay.X[l];
     s.G[l] = w + lay.G[l];
   }
-  if (m->relax == LP_RELAX_FCF)
+  if (m->relax == LP_RELAX_FCF && L > 1) {
     for (int l = 0; l + 1 < L; ++l) s.S[l] = w + lay.S[l];
+    s.S0[0] = s.S[0];
+    s.S0[1] = w + lay.S0b;
+  }
   s.partial = reinterpret_cast<double*>(w + lay.partial);
   s.st = st;
   double* rho = reinterpret_cast<double*>(w + lay.rho);
@@ -349,6 +406,8 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
       if (m->stag > 0.0 && mi > 0 && r > m->stag * hist[mi - 1]) break;
     }
   }
+  rc = s.finish();
+  if (rc) return rc;
   if (!early) {
     hist.assign(it, 0.0);
     LP_TRY(hipMemcpyAsync(hist.data(), rho, it * sizeof(double), hipMemcpyDeviceToHost, st), "read residuals");

@@ -15,7 +15,7 @@ namespace lp {
 namespace {
 
 constexpr int NT = 256;
-constexpr int CHUNK = 256;  // examples per partial of dW, dmu
+constexpr int CHUNK = 32;  // examples per partial of dW, dmu (short chains, many workgroups)
 
 // One wave per example: z[e][j] = mu_j + sum_i W[j][i] u[e][i], lanes split i.
 template <typename T>
@@ -72,6 +72,7 @@ __global__ __launch_bounds__(NT) void k_wpart(const T* uN, const double* d, doub
   const int j = (int)(o / (q + 1)), i = (int)(o - (size_t)j * (q + 1));
   const int e0 = ch * CHUNK, e1 = min(B, e0 + CHUNK);
   double acc = 0.0;
+#pragma unroll 8
   for (int e = e0; e < e1; ++e) acc += d[(size_t)e * nc + j] * (i < q ? (double)uN[(size_t)e * q + i] : 1.0);
   part[(size_t)ch * nw + o] = acc;
 }
