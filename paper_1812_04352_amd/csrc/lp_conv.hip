@@ -68,12 +68,12 @@ __device__ __forceinline__ float dact_v(float z, int act) {
 }
 
 __device__ __forceinline__ void stage_w(float* sw, const float* __restrict__ K, const float* __restrict__ b,
-                                        size_t n) {
-  for (int i = threadIdx.x; i < WV; i += NT) sw[i] = i < KW ? K[n * KW + i] : b[n * CH + (i - KW)];
+                                        size_t n, int nt = NT) {
+  for (int i = threadIdx.x; i < WV; i += nt) sw[i] = i < KW ? K[n * KW + i] : b[n * CH + (i - KW)];
 }
 
-__device__ __forceinline__ void zero_buf(float* buf, int n) {
-  for (int i = threadIdx.x; i < n; i += NT) buf[i] = 0.f;
+__device__ __forceinline__ void zero_buf(float* buf, int n, int nt = NT) {
+  for (int i = threadIdx.x; i < n; i += nt) buf[i] = 0.f;
 }
 
 // global example row [C][H][W] -> padded LDS interior, optionally corrected:
@@ -95,8 +95,8 @@ __device__ __forceinline__ void row_out(float* __restrict__ dst, const float* bu
   }
 }
 
-__device__ __forceinline__ void row_copy(float* __restrict__ dst, const float* __restrict__ src, int q) {
-  for (int i = threadIdx.x; i < q; i += NT) dst[i] = src[i];
+__device__ __forceinline__ void row_copy(float* __restrict__ dst, const float* __restrict__ src, int q, int nt = NT) {
+  for (int i = threadIdx.x; i < q; i += nt) dst[i] = src[i];
 }
 
 // Expanded weights of one lane for the 24 k-slices: A-row (co, dy) = (n/2, n%2)
@@ -135,11 +135,11 @@ __device__ __forceinline__ TileLane tile_lane(int t, int lane, const Geo& g) {
 }
 
 // acc += Wbig^T-slices x patches of the buffer for one tile
-__device__ __forceinline__ f32x4 conv_tile(const float (&wr)[24], const float* buf, int base, const Geo& g,
+__device__ __forceinline__ f32x4 conv_tile(const float (&wr)[24], const float* buf, int base, int cs, int pw,
                                            f32x4 acc) {
 #pragma unroll
   for (int s = 0; s < 24; ++s) {
-    const int off = (s / 12) * 4 * g.PHW + ((s % 12) / 3) * g.PW + (s % 3);
+    const int off = (s / 12) * 4 * cs + ((s % 12) / 3) * pw + (s % 3);
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wr[s], buf[base + off], acc, 0, 0, 0);
   }
   return acc;
@@ -160,18 +160,158 @@ __device__ __forceinline__ double wg_sum(double v, double* red) {
   return s;
 }
 
-// ------------------------------------------------------------------ forward
-template <int MODE>
-__global__ __launch_bounds__(NT) void k_fwd(SweepArgs a, int H, int W) {
-  __shared__ float buf[2][BUF];
-  __shared__ float sw[2][WV];
-  __shared__ double red[WAVES];
-  const Geo g(H, W);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// ------------------------------------------------------------------ sweeps
+// One workgroup runs one example through one interval (or, serially, through a
+// whole level). The state being evolved lives in registers at the lane's own
+// output pixels; the one LDS image buffer holds whatever the next product reads
+// (the forward state, the adjoint's primal state and then s = d * lam), with a
+// zero halo. Wave w owns tiles w*TPW .. w*TPW+TPW-1, so a 28 x 28 image (25
+// tiles) runs on 5 waves with no idle tile slots. Each product runs for all of
+// the wave's tiles before the elementwise work, so the matrix-core chains of
+// the tiles interleave; the adjoint loads the next step's primal state before
+// the step's products.
+
+// Sweep geometry, computed on the host.
+struct SGeo {
+  int H, W;
+  int PW;    // padded row length W + 2
+  int CS;    // LDS channel stride: >= (H+2)(W+2) and = 16 (mod 64), so the four
+             // 16-lane groups of a patch read (channels g, g+1, g+2, g+3) hit
+             // disjoint banks
+  int HW, q;
+  int NPP;   // pair-pixels (H/2) W
+  int NT16;  // tiles of 16 pair-pixels
+  int NW;    // waves per workgroup: ceil(NT16 / TPW)
+};
+
+constexpr int TPW = 5;   // tiles per wave (each costs 4 registers per per-pixel array)
+constexpr int MAXW = 8;  // waves per workgroup at most
+
+constexpr __host__ __device__ SGeo make_geo(int H, int W) {
+  const int phw = (H + 2) * (W + 2);
+  const int npp = H / 2 * W, nt16 = (H / 2 * W + 15) / 16;
+  return SGeo{H, W, W + 2, phw + (((16 - phw) % 64) + 64) % 64, H * W, CH * H * W, npp, nt16, (nt16 + TPW - 1) / TPW};
+}
+
+// Geometry of a kernel instance: compile-time for the specialised image sizes
+// (the patch reads then use immediate LDS offsets), else the launch argument.
+template <int GH, int GW>
+__device__ __forceinline__ SGeo geo_of(const SGeo& ga) {
+  if constexpr (GH == 0) return ga;
+  else return make_geo(GH, GW);
+}
+
+// The lane's pair-pixel in tile t: patch origin, own output offsets (register 0:
+// channel 2*(lane/16), row 2Y, column x) and whether it lies in the image; lanes
+// past the last pair-pixel repeat it and never write.
+struct Px {
+  int base, lds, gl;
+  bool ok;
+};
+
+__device__ __forceinline__ Px px_of(const SGeo& g, int t, int lane) {
+  Px p;
+  int P = 16 * t + (lane & 15);
+  p.ok = P < g.NPP;
+  if (!p.ok) P = g.NPP - 1;
+  const int Y = P / g.W, x = P - Y * g.W, grp = lane >> 4;
+  p.base = grp * g.CS + 2 * Y * g.PW + x;
+  p.lds = 2 * grp * g.CS + (2 * Y + 1) * g.PW + x + 1;
+  p.gl = 2 * grp * g.HW + 2 * Y * g.W + x;
+  return p;
+}
+
+// accumulator register r: channel 2*(lane/16) + r/2, row 2Y + r%2
+__device__ __forceinline__ int lds_r(const SGeo& g, const Px& p, int r) { return p.lds + (r >> 1) * g.CS + (r & 1) * g.PW; }
+__device__ __forceinline__ int gl_r(const SGeo& g, const Px& p, int r) { return p.gl + (r >> 1) * g.HW + (r & 1) * g.W; }
+
+__device__ __forceinline__ f32x4 ld_px(const float* __restrict__ src, const SGeo& g, const Px& p) {
+  f32x4 v;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) v[r] = src[gl_r(g, p, r)];
+  return v;
+}
+
+__device__ __forceinline__ void st_px(float* __restrict__ dst, f32x4 v, const SGeo& g, const Px& p) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) dst[gl_r(g, p, r)] = v[r];
+}
+
+__device__ __forceinline__ void put_px(float* buf, f32x4 v, const SGeo& g, const Px& p) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) buf[lds_r(g, p, r)] = v[r];
+}
+
+__device__ __forceinline__ f32x4 bias_px(const float* sw, int lane) {
+  const int co = 2 * (lane >> 4);
+  return f32x4{sw[KW + co], sw[KW + co], sw[KW + co + 1], sw[KW + co + 1]};
+}
+
+// sigma (D = false) or sigma' (D = true) of the first n tiles, one branch on the
+// activation for all of them
+template <bool D>
+__device__ __forceinline__ void act_tiles(f32x4 (&z)[TPW], int n, int act) {
+  switch (act) {
+    case ACT_TANH:
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        if (tt >= n) break;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float t = tanh_fast(z[tt][r]);
+          z[tt][r] = D ? 1.f - t * t : t;
+        }
+      }
+      break;
+    case ACT_RELU:
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        if (tt >= n) break;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) z[tt][r] = D ? (z[tt][r] > 0.f ? 1.f : 0.f) : (z[tt][r] > 0.f ? z[tt][r] : 0.f);
+      }
+      break;
+    case ACT_SMOOTHRELU:
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        if (tt >= n) break;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          z[tt][r] = D ? dact_f<float, ACT_SMOOTHRELU>(z[tt][r]) : act_f<float, ACT_SMOOTHRELU>(z[tt][r]);
+      }
+      break;
+    default:
+      if (D) {
+#pragma unroll
+        for (int tt = 0; tt < TPW; ++tt) z[tt] = f32x4{1.f, 1.f, 1.f, 1.f};
+      }
+      break;
+  }
+}
+
+__device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double s = 0.0;
+  if (threadIdx.x == 0)
+    for (int w = 0; w < nw; ++w) s += red[w];
+  return s;
+}
+
+template <int MODE, int GH, int GW>
+__global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
+  const SGeo g = geo_of<GH, GW>(ga);
+  extern __shared__ float lds[];
+  float* buf = lds;               // CH * CS
+  float* sw = lds + CH * g.CS;    // two layers
+  __shared__ double red[MAXW];
+  const int lane = threadIdx.x & 63, t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
+  // the wave's tiles (all TPW of them when the tiles fill the waves exactly)
+  const int ntl = (GH > 0 && g.NT16 % TPW == 0) ? TPW : min(TPW, g.NT16 - t0);
   const int k = blockIdx.x, Nc = gridDim.x;
-  const int e = blockIdx.y;
-  const size_t slice = (size_t)a.B * g.q;
-  const size_t eo = (size_t)e * g.q;
+  const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
   const float* K = static_cast<const float*>(a.K);
   const float* bb = static_cast<const float*>(a.b);
   float* X = static_cast<float*>(a.X);
@@ -183,86 +323,110 @@ __global__ __launch_bounds__(NT) void k_fwd(SweepArgs a, int H, int W) {
   const float hl = (float)a.hl, hc = (float)a.hc;
   const long kc = MODE == MODE_SERIAL ? 0 : (long)k * c;
 
-  zero_buf(&buf[0][0], 2 * BUF);
-  stage_w(sw[0], K, bb, (size_t)kc * a.stride);
-  __syncthreads();
+  zero_buf(buf, CH * g.CS, nt);
+  stage_w(sw, K, bb, (size_t)kc * a.stride, nt);
+  // starting state: C-point k, corrected when a coarse solution is given
+  const float* src;
+  const float* vsrc = nullptr;
   if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
     // a pending coarse-grid correction of the previous cycle is applied on the fly
-    if (MODE == SWEEP_FC && Vn) row_in(buf[0], Cs + (size_t)k * a.cs_stride * slice + eo, Vn + (size_t)k * slice + eo, g);
-    else row_in(buf[0], X + kc * slice + eo, nullptr, g);
-    if (MODE == SWEEP_FC && k == 0) row_copy(static_cast<float*>(a.S) + eo, X + eo, g.q);
-  } else if (MODE == SWEEP_FRES) {
-    row_in(buf[0], Cs + (size_t)k * a.cs_stride * slice + eo, nullptr, g);
+    if (MODE == SWEEP_FC && Vn) {
+      src = Cs + (size_t)k * a.cs_stride * slice + eo;
+      vsrc = Vn + (size_t)k * slice + eo;
+    } else {
+      src = X + kc * slice + eo;
+    }
   } else {
-    row_in(buf[0], Cs + (size_t)k * a.cs_stride * slice + eo, Vn + (size_t)k * slice + eo, g);
+    src = Cs + (size_t)k * a.cs_stride * slice + eo;
+    if (MODE == SWEEP_CORRF) vsrc = Vn + (size_t)k * slice + eo;
   }
+  f32x4 v[TPW];
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) {
+    if (tt >= ntl) break;
+    const Px p = px_of(g, t0 + tt, lane);
+    v[tt] = ld_px(src, g, p);
+    if (vsrc) v[tt] = v[tt] + (ld_px(vsrc, g, p) - v[tt]);
+  }
+  __syncthreads();  // halo zeroed
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) {
+    if (tt >= ntl) break;
+    const Px p = px_of(g, t0 + tt, lane);
+    if (p.ok) {
+      put_px(buf, v[tt], g, p);
+      if (MODE == SWEEP_CORRF && k > 0) st_px(X + kc * slice + eo, v[tt], g, p);
+    }
+  }
+  if (MODE == SWEEP_FC && k == 0) row_copy(static_cast<float*>(a.S) + eo, X + eo, g.q, nt);
   __syncthreads();
-  if (MODE == SWEEP_CORRF && k > 0) row_out(X + kc * slice + eo, buf[0], g);
 
-  float coarse[MAXT][4];
+  f32x4 coarse[TPW];
   for (int j = 0; j < nsteps; ++j) {
-    const int cur = j & 1;
-    float wr[24];
-    gather_w<false>(wr, sw[cur], lane);
-    stage_w(sw[cur ^ 1], K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j)) * a.stride);
+    const float* swc = sw + (j & 1) * WV;
+    stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j)) * a.stride, nt);
+    f32x4 z[TPW];
+    {
+      float wr[24];
+      gather_w<false>(wr, swc, lane);
+      const f32x4 bias = bias_px(swc, lane);
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        if (tt >= ntl) break;
+        z[tt] = conv_tile(wr, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, bias);
+      }
+    }
+    act_tiles<false>(z, ntl, a.act);
     const float* gi = G ? G + (kc + j + 1) * slice + eo : nullptr;
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      if (MODE == SWEEP_FRES && j == 0) coarse[tt] = v[tt] + hc * z[tt];
+      v[tt] = v[tt] + hl * z[tt];
+      if (gi) v[tt] += ld_px(gi, g, px_of(g, t0 + tt, lane));
+    }
+    __syncthreads();  // every read of the step's input is done
     float* xo = (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) ? X + (kc + j + 1) * slice + eo : nullptr;
 #pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      f32x4 acc;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] = sw[cur][KW + out_ch(lane, r)];
-      acc = conv_tile(wr, buf[cur], L.base, g, acc);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        const int pos = co * g.PHW + (y + 1) * g.PW + L.x + 1;
-        const int go = co * g.HW + y * g.W + L.x;
-        const float old = buf[cur][pos];
-        const float sg = act_v(acc[r], a.act);
-        if (MODE == SWEEP_FRES && j == 0) coarse[tt][r] = old + hc * sg;
-        float nv = old + hl * sg;
-        if (L.valid) {
-          if (gi) nv += gi[go];
-          buf[cur ^ 1][pos] = nv;
-          if (xo) xo[go] = nv;
-        }
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) {
+        put_px(buf, v[tt], g, p);
+        if (xo) st_px(xo, v[tt], g, p);
       }
     }
     __syncthreads();
   }
-  const float* fin = buf[nsteps & 1];
+
   if (MODE == SWEEP_FC) {
-    row_out(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + eo, fin, g);
+    float* so = static_cast<float*>(a.S) + (size_t)(k + 1) * slice + eo;
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) st_px(so, v[tt], g, p);
+    }
   } else if (MODE == SWEEP_FRES) {
     const float* cn = Cs + (size_t)(k + 1) * a.cs_stride * slice + eo;
     float* gn = static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + eo;
     double acc = 0.0;
 #pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      if (!L.valid) continue;
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) {
+        const f32x4 rr = v[tt] - ld_px(cn, g, p);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        const int pos = co * g.PHW + (y + 1) * g.PW + L.x + 1;
-        const int go = co * g.HW + y * g.W + L.x;
-        const float f = fin[pos];
-        const float rr = f - cn[go];
-        acc += (double)rr * (double)rr;
-        gn[go] = f - coarse[tt][r];  // g_{l+1}^{k+1} = f_{k+1} - Phi_{l+1}(C_k)
+        for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
+        st_px(gn, v[tt] - coarse[tt], g, p);  // g_{l+1}^{k+1} = f_{k+1} - Phi_{l+1}(C_k)
       }
     }
     if (a.xn_every > 0 && (k + 1) % a.xn_every == 0)
-      row_copy(static_cast<float*>(a.Xn) + (size_t)(k + 1) * slice + eo, cn, g.q);
-    if (k == 0) row_copy(static_cast<float*>(a.Xn) + eo, Cs + eo, g.q);
+      row_copy(static_cast<float*>(a.Xn) + (size_t)(k + 1) * slice + eo, cn, g.q, nt);
+    if (k == 0) row_copy(static_cast<float*>(a.Xn) + eo, Cs + eo, g.q, nt);
     if (a.partial) {
-      const double s = wg_sum(acc, red);
+      const double s = wg_sum_n(acc, red, g.NW);
       if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
     }
   } else if (MODE == SWEEP_CORRF) {
@@ -270,24 +434,25 @@ __global__ __launch_bounds__(NT) void k_fwd(SweepArgs a, int H, int W) {
       const float* cs = Cs + (size_t)Nc * a.cs_stride * slice + eo;
       const float* vs = Vn + (size_t)Nc * slice + eo;
       float* xo = X + (size_t)a.Nl * slice + eo;
-      for (int i = threadIdx.x; i < g.q; i += NT) xo[i] = cs[i] + (vs[i] - cs[i]);
+      for (int i = threadIdx.x; i < g.q; i += nt) xo[i] = cs[i] + (vs[i] - cs[i]);
     }
   }
 }
 
-// ------------------------------------------------------------------ adjoint
-// Step: u^n -> LDS, d = sigma'(K u + b), s = d * lam -> LDS, lam' = lam + h K^T s (+ g).
-template <int MODE>
-__global__ __launch_bounds__(NT) void k_adj(SweepArgs a, int H, int W) {
-  __shared__ float buf[3][BUF];  // lam (ping-pong) and the primal state / s
-  __shared__ float sw[2][WV];
-  __shared__ double red[WAVES];
-  const Geo g(H, W);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// Adjoint step at level point i: d = sigma'(K u + b) with u the fine primal state
+// of point i, s = d * lam, lam' = lam + h K^T s (+ g).
+template <int MODE, int GH, int GW>
+__global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
+  const SGeo g = geo_of<GH, GW>(ga);
+  extern __shared__ float lds[];
+  float* buf = lds;               // CH * CS: u, then s
+  float* sw = lds + CH * g.CS;    // two layers
+  __shared__ double red[MAXW];
+  const int lane = threadIdx.x & 63, t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
+  // the wave's tiles (all TPW of them when the tiles fill the waves exactly)
+  const int ntl = (GH > 0 && g.NT16 % TPW == 0) ? TPW : min(TPW, g.NT16 - t0);
   const int k = blockIdx.x, Nc = gridDim.x;
-  const int e = blockIdx.y;
-  const size_t slice = (size_t)a.B * g.q;
-  const size_t eo = (size_t)e * g.q;
+  const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
   const float* K = static_cast<const float*>(a.K);
   const float* bb = static_cast<const float*>(a.b);
   const float* Uf = static_cast<const float*>(a.Uf);
@@ -299,163 +464,160 @@ __global__ __launch_bounds__(NT) void k_adj(SweepArgs a, int H, int W) {
   const int nsteps = MODE == MODE_SERIAL ? a.Nl : (MODE == SWEEP_CORRF ? c - 1 : c);
   const float hl = (float)a.hl, hc = (float)a.hc;
   const long top = MODE == MODE_SERIAL ? (long)a.Nl : (long)(k + 1) * c;
-  float* bu = buf[2];
+  const size_t ustep = (size_t)a.stride * slice;
 
-  zero_buf(&buf[0][0], 3 * BUF);
-  stage_w(sw[0], K, bb, (size_t)(top - 1) * a.stride);
-  __syncthreads();
+  zero_buf(buf, CH * g.CS, nt);
+  stage_w(sw, K, bb, (size_t)(top - 1) * a.stride, nt);
+  const float* src;
+  const float* vsrc = nullptr;
   if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
-    if (MODE == SWEEP_FC && Vn)
-      row_in(buf[0], Cs + (size_t)(k + 1) * a.cs_stride * slice + eo, Vn + (size_t)(k + 1) * slice + eo, g);
-    else row_in(buf[0], X + top * slice + eo, nullptr, g);
-    if (MODE == SWEEP_FC && k == Nc - 1) row_copy(static_cast<float*>(a.S) + (size_t)Nc * slice + eo, X + top * slice + eo, g.q);
-  } else if (MODE == SWEEP_FRES) {
-    row_in(buf[0], Cs + (size_t)(k + 1) * a.cs_stride * slice + eo, nullptr, g);
+    if (MODE == SWEEP_FC && Vn) {
+      src = Cs + (size_t)(k + 1) * a.cs_stride * slice + eo;
+      vsrc = Vn + (size_t)(k + 1) * slice + eo;
+    } else {
+      src = X + top * slice + eo;
+    }
   } else {
-    row_in(buf[0], Cs + (size_t)(k + 1) * a.cs_stride * slice + eo, Vn + (size_t)(k + 1) * slice + eo, g);
+    src = Cs + (size_t)(k + 1) * a.cs_stride * slice + eo;
+    if (MODE == SWEEP_CORRF) vsrc = Vn + (size_t)(k + 1) * slice + eo;
   }
+  f32x4 lam[TPW], un[TPW];
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) {
+    if (tt >= ntl) break;
+    const Px p = px_of(g, t0 + tt, lane);
+    lam[tt] = ld_px(src, g, p);
+    if (vsrc) lam[tt] = lam[tt] + (ld_px(vsrc, g, p) - lam[tt]);
+    un[tt] = ld_px(Uf + (size_t)(top - 1) * ustep + eo, g, p);
+  }
+  __syncthreads();  // halo zeroed
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) {
+    if (tt >= ntl) break;
+    const Px p = px_of(g, t0 + tt, lane);
+    if (p.ok) {
+      put_px(buf, un[tt], g, p);
+      if (MODE == SWEEP_CORRF && k + 1 < Nc) st_px(X + top * slice + eo, lam[tt], g, p);
+    }
+  }
+  if (MODE == SWEEP_FC && k == Nc - 1) row_copy(static_cast<float*>(a.S) + (size_t)Nc * slice + eo, X + top * slice + eo, g.q, nt);
   __syncthreads();
-  if (MODE == SWEEP_CORRF && k + 1 < Nc) row_out(X + top * slice + eo, buf[0], g);
 
-  float dd[MAXT][4];
-  float cu[MAXT][4];  // FRES: the upper C-point, then the coarse step
-  if (MODE == SWEEP_FRES) {
-#pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        cu[tt][r] = buf[0][co * g.PHW + (y + 1) * g.PW + L.x + 1];
-      }
-    }
-  }
+  f32x4 dd[TPW];  // sigma'(z) of the step (after the loop: of the last one)
   for (int j = 0; j < nsteps; ++j) {
-    const int cur = j & 1;
     const long i = top - 1 - j;
-    float wf[24], wt[24];
-    gather_w<false>(wf, sw[cur], lane);
-    gather_w<true>(wt, sw[cur], lane);
-    row_in(bu, Uf + (size_t)i * a.stride * slice + eo, nullptr, g);
-    __syncthreads();
-    // d = sigma'(K u + b)
+    const bool more = j + 1 < nsteps;
+    const float* swc = sw + (j & 1) * WV;
+    if (more) {
 #pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      f32x4 acc;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] = sw[cur][KW + out_ch(lane, r)];
-      acc = conv_tile(wf, bu, L.base, g, acc);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) dd[tt][r] = dact_v(acc[r], a.act);
-    }
-    __syncthreads();
-    // s = d * lam into the primal buffer (its halo stays zero)
-#pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      if (!L.valid) continue;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        const int pos = co * g.PHW + (y + 1) * g.PW + L.x + 1;
-        bu[pos] = dd[tt][r] * buf[cur][pos];
+      for (int tt = 0; tt < TPW; ++tt) {
+        if (tt >= ntl) break;
+        un[tt] = ld_px(Uf + (size_t)(i - 1) * ustep + eo, g, px_of(g, t0 + tt, lane));
       }
     }
-    stage_w(sw[cur ^ 1], K, bb, (size_t)(j + 1 < nsteps ? i - 1 : i) * a.stride);
+    stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(more ? i - 1 : i) * a.stride, nt);
+    // d = sigma'(K u + b)
+    {
+      float wr[24];
+      gather_w<false>(wr, swc, lane);
+      const f32x4 bias = bias_px(swc, lane);
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        if (tt >= ntl) break;
+        dd[tt] = conv_tile(wr, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, bias);
+      }
+    }
+    act_tiles<true>(dd, ntl, a.act);
+    float wt[24];
+    gather_w<true>(wt, swc, lane);
+    __syncthreads();  // every read of u is done
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) put_px(buf, dd[tt] * lam[tt], g, p);
+    }
     __syncthreads();
+    f32x4 w[TPW];
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      w[tt] = conv_tile(wt, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
     const float* gi = G ? G + (size_t)i * slice + eo : nullptr;
     float* xo = (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) ? X + (size_t)i * slice + eo : nullptr;
 #pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      acc = conv_tile(wt, bu, L.base, g, acc);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        const int pos = co * g.PHW + (y + 1) * g.PW + L.x + 1;
-        const int go = co * g.HW + y * g.W + L.x;
-        float nv = buf[cur][pos] + hl * acc[r];
-        if (L.valid) {
-          if (gi) nv += gi[go];
-          buf[cur ^ 1][pos] = nv;
-          if (xo) xo[go] = nv;
-        }
-      }
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      lam[tt] = lam[tt] + hl * w[tt];
+      if (gi) lam[tt] += ld_px(gi, g, p);
+      if (xo && p.ok) st_px(xo, lam[tt], g, p);
     }
-    if (MODE == SWEEP_FRES && j == nsteps - 1) {
-      // coarse adjoint step from the upper C-point, linearised at the same fine state
-      __syncthreads();
+    __syncthreads();  // every read of s is done
+    if (more) {
 #pragma unroll
-      for (int tt = 0; tt < MAXT; ++tt) {
-        const int t = wave + tt * WAVES;
-        if (t >= g.NT16) break;
-        const TileLane L = tile_lane(t, lane, g);
-        if (!L.valid) continue;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-          bu[co * g.PHW + (y + 1) * g.PW + L.x + 1] = dd[tt][r] * cu[tt][r];
-        }
-      }
-      __syncthreads();
-#pragma unroll
-      for (int tt = 0; tt < MAXT; ++tt) {
-        const int t = wave + tt * WAVES;
-        if (t >= g.NT16) break;
-        const TileLane L = tile_lane(t, lane, g);
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        acc = conv_tile(wt, bu, L.base, g, acc);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) cu[tt][r] = cu[tt][r] + hc * acc[r];
+      for (int tt = 0; tt < TPW; ++tt) {
+        if (tt >= ntl) break;
+        const Px p = px_of(g, t0 + tt, lane);
+        if (p.ok) put_px(buf, un[tt], g, p);
       }
     }
     __syncthreads();
   }
-  const float* fin = buf[nsteps & 1];
+
   if (MODE == SWEEP_FC) {
-    row_out(static_cast<float*>(a.S) + (size_t)k * slice + eo, fin, g);
+    float* so = static_cast<float*>(a.S) + (size_t)k * slice + eo;
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) st_px(so, lam[tt], g, p);
+    }
   } else if (MODE == SWEEP_FRES) {
+    // coarse adjoint step from the upper C-point, linearised at the fine state of
+    // the interval's last step (its weights are in both layer slots)
+    f32x4 cu[TPW];
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      cu[tt] = ld_px(src, g, p);
+      if (p.ok) put_px(buf, dd[tt] * cu[tt], g, p);
+    }
+    float wt[24];
+    gather_w<true>(wt, sw, lane);
+    __syncthreads();
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      cu[tt] += hc * conv_tile(wt, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
     const float* ck = Cs + (size_t)k * a.cs_stride * slice + eo;
     float* gn = static_cast<float*>(a.Gn) + (size_t)k * slice + eo;
     double acc = 0.0;
 #pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      if (!L.valid) continue;
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) {
+        const f32x4 rr = lam[tt] - ld_px(ck, g, p);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        const int pos = co * g.PHW + (y + 1) * g.PW + L.x + 1;
-        const int go = co * g.HW + y * g.W + L.x;
-        const float f = fin[pos];
-        const float rr = f - ck[go];
-        acc += (double)rr * (double)rr;
-        gn[go] = f - cu[tt][r];  // g_{l+1}^k = f_k - Phibar_{l+1}(C_{k+1})
+        for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
+        st_px(gn, lam[tt] - cu[tt], g, p);  // g_{l+1}^k = f_k - Phibar_{l+1}(C_{k+1})
       }
     }
-    if (a.xn_every > 0 && k % a.xn_every == 0) row_copy(static_cast<float*>(a.Xn) + (size_t)k * slice + eo, ck, g.q);
+    if (a.xn_every > 0 && k % a.xn_every == 0) row_copy(static_cast<float*>(a.Xn) + (size_t)k * slice + eo, ck, g.q, nt);
     if (k == Nc - 1)
-      row_copy(static_cast<float*>(a.Xn) + (size_t)Nc * slice + eo, Cs + (size_t)Nc * a.cs_stride * slice + eo, g.q);
+      row_copy(static_cast<float*>(a.Xn) + (size_t)Nc * slice + eo, Cs + (size_t)Nc * a.cs_stride * slice + eo, g.q, nt);
     if (a.partial) {
-      const double s = wg_sum(acc, red);
+      const double s = wg_sum_n(acc, red, g.NW);
       if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
     }
   } else if (MODE == SWEEP_CORRF) {
     if (k == 0) {
       float* xo = X + eo;
-      for (int i = threadIdx.x; i < g.q; i += NT) xo[i] = Cs[eo + i] + (Vn[eo + i] - Cs[eo + i]);
+      for (int i = threadIdx.x; i < g.q; i += nt) xo[i] = Cs[eo + i] + (Vn[eo + i] - Cs[eo + i]);
     }
   }
 }
@@ -494,7 +656,7 @@ __global__ __launch_bounds__(NT) void k_resid(ResidArgs a, int H, int W) {
     f32x4 acc;
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[r] = sw[KW + out_ch(lane, r)];
-    acc = conv_tile(wf, buf[0], L.base, g, acc);
+    acc = conv_tile(wf, buf[0], L.base, g.PHW, g.PW, acc);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
@@ -531,7 +693,7 @@ __global__ __launch_bounds__(NT) void k_resid(ResidArgs a, int H, int W) {
       if (t >= g.NT16) break;
       const TileLane L = tile_lane(t, lane, g);
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      acc = conv_tile(wt, buf[0], L.base, g, acc);
+      acc = conv_tile(wt, buf[0], L.base, g.PHW, g.PW, acc);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
@@ -597,7 +759,7 @@ __global__ __launch_bounds__(NT) void k_grad(GradArgs a, int H, int W) {
       f32x4 z;
 #pragma unroll
       for (int r = 0; r < 4; ++r) z[r] = sw[KW + out_ch(lane, r)];
-      z = conv_tile(wf, buf[0], L.base, g, z);
+      z = conv_tile(wf, buf[0], L.base, g.PHW, g.PW, z);
       if (!L.valid) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -682,10 +844,45 @@ __global__ __launch_bounds__(NT) void k_grad_final(GradArgs a) {
 
 }  // namespace conv
 
+namespace {
+
+conv::SGeo sweep_geo(const Shape& s) { return conv::make_geo(s.H, s.W); }
+
+size_t sweep_lds(const conv::SGeo& g) { return (size_t)(conv::CH * g.CS + 2 * conv::WV) * sizeof(float); }
+
+// Sweep kernels with the geometry as template arguments (0, 0: runtime).
+template <int GH, int GW>
+void sweep_kernels(int dir, int mode, void (*&f)(SweepArgs, conv::SGeo)) {
+  using namespace conv;
+  if (dir == DIR_FWD) {
+    if (mode == SWEEP_FC) f = k_fwd<SWEEP_FC, GH, GW>;
+    else if (mode == SWEEP_FRES) f = k_fwd<SWEEP_FRES, GH, GW>;
+    else if (mode == SWEEP_CORRF) f = k_fwd<SWEEP_CORRF, GH, GW>;
+    else f = k_fwd<MODE_SERIAL, GH, GW>;
+  } else {
+    if (mode == SWEEP_FC) f = k_adj<SWEEP_FC, GH, GW>;
+    else if (mode == SWEEP_FRES) f = k_adj<SWEEP_FRES, GH, GW>;
+    else if (mode == SWEEP_CORRF) f = k_adj<SWEEP_CORRF, GH, GW>;
+    else f = k_adj<MODE_SERIAL, GH, GW>;
+  }
+}
+
+hipError_t launch_conv_sweep(const Shape& s, int dir, const SweepArgs& a, dim3 grid, hipStream_t st) {
+  const conv::SGeo g = sweep_geo(s);
+  void (*f)(SweepArgs, conv::SGeo) = nullptr;
+  if (s.H == 28 && s.W == 28) sweep_kernels<28, 28>(dir, a.mode, f);  // MNIST-sized images
+  else sweep_kernels<0, 0>(dir, a.mode, f);
+  hipLaunchKernelGGL(f, grid, dim3(64 * g.NW), sweep_lds(g), st, a, g);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 bool conv_supported(const Shape& s) {
   return s.layer == 1 && s.dtype == 0 && s.C == conv::CH && s.H % 2 == 0 && s.H >= 2 && s.W >= 4 &&
          s.H + 2 <= conv::MAXPD && s.W + 2 <= conv::MAXPD &&
-         (s.H / 2 * s.W + 15) / 16 <= conv::WAVES * conv::MAXT;
+         (s.H / 2 * s.W + 15) / 16 <= conv::WAVES * conv::MAXT &&
+         (s.H / 2 * s.W + 15) / 16 <= conv::MAXW * conv::TPW;
 }
 
 int conv_tile(const Shape&) { return 1; }
@@ -699,17 +896,7 @@ int conv_grad_chunks(int B, int N) {
 hipError_t conv_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   const dim3 grid(a.Nl / a.c, a.B);
   if (partials) *partials = (int)(grid.x * grid.y);
-  using namespace conv;
-  if (dir == DIR_FWD) {
-    if (a.mode == SWEEP_FC) k_fwd<SWEEP_FC><<<grid, NT, 0, st>>>(a, s.H, s.W);
-    else if (a.mode == SWEEP_FRES) k_fwd<SWEEP_FRES><<<grid, NT, 0, st>>>(a, s.H, s.W);
-    else k_fwd<SWEEP_CORRF><<<grid, NT, 0, st>>>(a, s.H, s.W);
-  } else {
-    if (a.mode == SWEEP_FC) k_adj<SWEEP_FC><<<grid, NT, 0, st>>>(a, s.H, s.W);
-    else if (a.mode == SWEEP_FRES) k_adj<SWEEP_FRES><<<grid, NT, 0, st>>>(a, s.H, s.W);
-    else k_adj<SWEEP_CORRF><<<grid, NT, 0, st>>>(a, s.H, s.W);
-  }
-  return hipGetLastError();
+  return launch_conv_sweep(s, dir, a, grid, st);
 }
 
 hipError_t conv_serial(const Shape& s, int dir, const SerialArgs& sa, hipStream_t st) {
@@ -726,10 +913,7 @@ hipError_t conv_serial(const Shape& s, int dir, const SerialArgs& sa, hipStream_
   a.hl = sa.hl;
   a.X = sa.X;
   a.G = sa.G;
-  const dim3 grid(1, sa.B);
-  if (dir == DIR_FWD) conv::k_fwd<conv::MODE_SERIAL><<<grid, conv::NT, 0, st>>>(a, s.H, s.W);
-  else conv::k_adj<conv::MODE_SERIAL><<<grid, conv::NT, 0, st>>>(a, s.H, s.W);
-  return hipGetLastError();
+  return launch_conv_sweep(s, dir, a, dim3(1, sa.B), st);
 }
 
 hipError_t conv_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t st, int* partials) {
