@@ -709,92 +709,125 @@ __global__ __launch_bounds__(NT) void k_resid(ResidArgs a, int H, int W) {
 }
 
 // ------------------------------------------------------------------ gradient
-// Workgroup (layer n, batch chunk). Per example: s = sigma'(K u + b) * lam^{n+1}
-// (the forward product), written to LDS; then dWbig[(co,dy)][k] += s[co][2Y+dy][x] *
-// patch[P][k] with the pair-pixels as contraction index (k-slice = 4 pair-pixels,
-// lane group = one of them): A = s (rows (co,dy)), B = patches (96 columns in 6
-// blocks of 16). db sums s. Waves split the pair-pixel slices; the workgroup's
-// partial is combined in a fixed order.
+// Workgroup (layer n, batch chunk), with the sweeps' wave and tile layout. Per
+// example: s = sigma'(K u + b) * lam^{n+1} at the lane's own pixels (the
+// forward product over the wave's tiles), written to LDS; then
+// dWbig[(co,dy)][k] += s[co][2Y+dy][x] * patch[P][k] with the pair-pixels as
+// contraction index (k-slice = 4 pair-pixels, lane group = one of them): A = s
+// (rows (co,dy)), B = patches of u (96 columns in 6 blocks of 16). db sums s
+// from registers. The next example's u is loaded before the products. Waves and
+// lanes are combined in a fixed order.
 constexpr int GOUT = 16 * 96 + CH;  // dWbig then db per chunk
 
-__global__ __launch_bounds__(NT) void k_grad(GradArgs a, int H, int W) {
-  __shared__ float buf[2][BUF];  // u (padded), s (padded)
-  __shared__ float sw[WV];
-  __shared__ float red[GOUT];
-  const Geo g(H, W);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+template <int GH, int GW>
+__global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
+  const SGeo g = geo_of<GH, GW>(ga);
+  extern __shared__ float lds[];
+  float* bu = lds;                   // CH * CS: u
+  float* bs = lds + CH * g.CS;       // CH * CS: s
+  float* sw = lds + 2 * CH * g.CS;   // the layer's weights
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, t0 = wave * TPW, nt = blockDim.x;
+  const int ntl = (GH > 0 && g.NT16 % TPW == 0) ? TPW : min(TPW, g.NT16 - t0);
   const int n = blockIdx.x, chunk = blockIdx.y;
   const int per = (a.B + a.nchunks - 1) / a.nchunks;
   const int e0 = chunk * per, e1 = min(a.B, e0 + per);
   const size_t slice = (size_t)a.B * g.q;
   const float* U = static_cast<const float*>(a.U) + (size_t)n * slice;
   const float* Lm = static_cast<const float*>(a.Lam) + (size_t)(n + 1) * slice;
-  zero_buf(&buf[0][0], 2 * BUF);
-  stage_w(sw, static_cast<const float*>(a.K), static_cast<const float*>(a.b), n);
-  __syncthreads();
-  float wf[24];
-  gather_w<false>(wf, sw, lane);
+
+  zero_buf(lds, 2 * CH * g.CS, nt);
+  stage_w(sw, static_cast<const float*>(a.K), static_cast<const float*>(a.b), n, nt);
   // B-operand offsets: column k = 16 nb + lane%16 -> (ci, r, tx), relative to the
   // pair-pixel's (row 2Y, col x) origin in padded coordinates
   int koff[6];
 #pragma unroll
   for (int nb = 0; nb < 6; ++nb) {
     const int kk = 16 * nb + (lane & 15);
-    const int ci = kk / 12, r = (kk % 12) / 3, tx = kk % 3;
-    koff[nb] = ci * g.PHW + r * g.PW + tx;
+    koff[nb] = (kk / 12) * g.CS + ((kk % 12) / 3) * g.PW + kk % 3;
   }
   f32x4 acc[6];
 #pragma unroll
   for (int nb = 0; nb < 6; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float dbacc = 0.f;
+  float db0 = 0.f, db1 = 0.f;  // channels 2*(lane/16) and 2*(lane/16)+1
   const int nsl = (g.NPP + 3) / 4;  // pair-pixel slices of 4
+  f32x4 un[TPW];
+  if (e0 < e1) {
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      un[tt] = ld_px(U + (size_t)e0 * g.q, g, px_of(g, t0 + tt, lane));
+    }
+  }
+  __syncthreads();  // buffers zeroed, weights staged
+  float wf[24];
+  gather_w<false>(wf, sw, lane);
+  const f32x4 bias = bias_px(sw, lane);
+  if (e0 < e1) {
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) put_px(bu, un[tt], g, p);
+    }
+  }
+  __syncthreads();
   for (int e = e0; e < e1; ++e) {
-    row_in(buf[0], U + (size_t)e * g.q, nullptr, g);
-    __syncthreads();
+    const bool more = e + 1 < e1;
+    f32x4 z[TPW], lam[TPW];
 #pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      f32x4 z;
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      lam[tt] = ld_px(Lm + (size_t)e * g.q, g, p);
+      if (more) un[tt] = ld_px(U + (size_t)(e + 1) * g.q, g, p);
+    }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) z[r] = sw[KW + out_ch(lane, r)];
-      z = conv_tile(wf, buf[0], L.base, g.PHW, g.PW, z);
-      if (!L.valid) continue;
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      z[tt] = conv_tile(wf, bu, px_of(g, t0 + tt, lane).base, g.CS, g.PW, bias);
+    }
+    act_tiles<true>(z, ntl, a.act);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        const int go = co * g.HW + y * g.W + L.x;
-        const float s = dact_v(z[r], a.act) * Lm[(size_t)e * g.q + go];
-        buf[1][co * g.PHW + (y + 1) * g.PW + L.x + 1] = s;
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (tt >= ntl) break;
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) {
+        const f32x4 s = z[tt] * lam[tt];
+        put_px(bs, s, g, p);
+        db0 += s[0] + s[1];
+        db1 += s[2] + s[3];
       }
     }
     __syncthreads();
     // contraction over pair-pixels
-    for (int sl = wave; sl < nsl; sl += WAVES) {
+    for (int sl = wave; sl < nsl; sl += g.NW) {
       const int P = 4 * sl + (lane >> 4);
       const bool ok = P < g.NPP;
       const int Pc = ok ? P : g.NPP - 1;
       const int Y = Pc / g.W, x = Pc - Y * g.W;
       const int nA = lane & 15, co = nA >> 1, dy = nA & 1;
-      const float av = ok ? buf[1][co * g.PHW + (2 * Y + dy + 1) * g.PW + x + 1] : 0.f;
+      const float av = ok ? bs[co * g.CS + (2 * Y + dy + 1) * g.PW + x + 1] : 0.f;
       const int pb = 2 * Y * g.PW + x;  // (row 2Y-1+r, col x-1+tx) padded = (2Y+r, x+tx)
 #pragma unroll
       for (int nb = 0; nb < 6; ++nb)
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, buf[0][pb + koff[nb]], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bu[pb + koff[nb]], acc[nb], 0, 0, 0);
     }
-    // db: thread t sums channel t % 8 over pixels t/8, t/8 + 32, ...
-    {
-      const int ch = threadIdx.x & (CH - 1);
-      for (int p = threadIdx.x >> 3; p < g.HW; p += NT / CH) {
-        const int y = p / g.W, x = p - y * g.W;
-        dbacc += buf[1][ch * g.PHW + (y + 1) * g.PW + x + 1];
+    __syncthreads();
+    if (more) {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        if (tt >= ntl) break;
+        const Px p = px_of(g, t0 + tt, lane);
+        if (p.ok) put_px(bu, un[tt], g, p);
       }
     }
     __syncthreads();
   }
-  // combine waves in order: D[(co,dy) = 4(lane/16)+r][k = 16 nb + lane%16]
-  for (int w = 0; w < WAVES; ++w) {
+  // combine waves in order (the image buffers are free now):
+  // D[(co,dy) = 4(lane/16)+r][k = 16 nb + lane%16]
+  float* red = lds;               // GOUT
+  float* dbp = lds + GOUT;        // two per thread
+  for (int w = 0; w < g.NW; ++w) {
     if (wave == w) {
 #pragma unroll
       for (int nb = 0; nb < 6; ++nb)
@@ -806,18 +839,20 @@ __global__ __launch_bounds__(NT) void k_grad(GradArgs a, int H, int W) {
     }
     __syncthreads();
   }
-  // db: per channel, the 32 thread partials in thread order
-  __shared__ float dbp[NT];
-  dbp[threadIdx.x] = dbacc;
+  dbp[2 * threadIdx.x] = db0;
+  dbp[2 * threadIdx.x + 1] = db1;
   __syncthreads();
+  // db per channel: its 16 lanes of every wave, in thread order
   if (threadIdx.x < CH) {
+    const int ch = threadIdx.x, grp = ch >> 1;
     float s = 0.f;
-    for (int t = threadIdx.x; t < NT; t += CH) s += dbp[t];
-    red[16 * 96 + threadIdx.x] = s;
+    for (int w = 0; w < g.NW; ++w)
+      for (int l = 0; l < 16; ++l) s += dbp[2 * (64 * w + 16 * grp + l) + (ch & 1)];
+    red[16 * 96 + ch] = s;
   }
   __syncthreads();
   float* out = static_cast<float*>(a.partial) + ((size_t)n * a.nchunks + chunk) * GOUT;
-  for (int o = threadIdx.x; o < GOUT; o += NT) out[o] = red[o];
+  for (int o = threadIdx.x; o < GOUT; o += nt) out[o] = red[o];
 }
 
 // dK[n][co][ci][ty][tx] = h sum_chunks sum_dy dWbig[(co,dy)][(ci, ty+dy, tx)], db[n][co] = h sum db.
@@ -925,7 +960,14 @@ hipError_t conv_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t s
 }
 
 hipError_t conv_grad(const Shape& s, const GradArgs& a, hipStream_t st) {
-  conv::k_grad<<<dim3(a.N, a.nchunks), conv::NT, 0, st>>>(a, s.H, s.W);
+  const conv::SGeo g = sweep_geo(s);
+  // image buffers and weights, reused at the end for the partial and the db terms
+  const int fl = 2 * conv::CH * g.CS + conv::WV, red = conv::GOUT + 2 * 64 * g.NW;
+  const size_t sh = (size_t)(fl > red ? fl : red) * sizeof(float);
+  if (s.H == 28 && s.W == 28)
+    conv::k_grad<28, 28><<<dim3(a.N, a.nchunks), 64 * g.NW, sh, st>>>(a, g);
+  else
+    conv::k_grad<0, 0><<<dim3(a.N, a.nchunks), 64 * g.NW, sh, st>>>(a, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t tot = (size_t)a.N * (conv::KW + conv::CH);
