@@ -165,11 +165,12 @@ __device__ __forceinline__ double wg_sum(double v, double* red) {
 // whole level). The state being evolved lives in registers at the lane's own
 // output pixels; the one LDS image buffer holds whatever the next product reads
 // (the forward state, the adjoint's primal state and then s = d * lam), with a
-// zero halo. Wave w owns tiles w*TPW .. w*TPW+TPW-1, so a 28 x 28 image (25
-// tiles) runs on 5 waves with no idle tile slots. Each product runs for all of
-// the wave's tiles before the elementwise work, so the matrix-core chains of
-// the tiles interleave; the adjoint loads the next step's primal state before
-// the step's products.
+// zero halo. Wave w owns tiles w*TPW .. w*TPW+TPW-1; a 28 x 28 image (25 tiles)
+// runs on 4 waves, one per SIMD, the last one carrying three ghost tiles (lanes
+// past the image repeat its last pair-pixel and write nothing), so every wave
+// does the same work and no loop over tiles branches. Each product runs for all
+// of the wave's tiles before the elementwise work. The adjoint issues the loads
+// of the next step's primal state before its second product.
 
 // Sweep geometry, computed on the host.
 struct SGeo {
@@ -184,7 +185,7 @@ struct SGeo {
   int NW;    // waves per workgroup: ceil(NT16 / TPW)
 };
 
-constexpr int TPW = 5;   // tiles per wave (each costs 4 registers per per-pixel array)
+constexpr int TPW = 7;   // tiles per wave (each costs 4 registers per per-pixel array)
 constexpr int MAXW = 8;  // waves per workgroup at most
 
 constexpr __host__ __device__ SGeo make_geo(int H, int W) {
@@ -242,20 +243,26 @@ __device__ __forceinline__ void put_px(float* buf, f32x4 v, const SGeo& g, const
   for (int r = 0; r < 4; ++r) buf[lds_r(g, p, r)] = v[r];
 }
 
+// Products of the wave's tiles, z[tt] = init + Wbig^T x patches.
+__device__ __forceinline__ void conv_tiles(f32x4 (&z)[TPW], const float (&wr)[24], const float* buf, const SGeo& g,
+                                           int t0, int lane, f32x4 init) {
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) z[tt] = conv_tile(wr, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, init);
+}
+
 __device__ __forceinline__ f32x4 bias_px(const float* sw, int lane) {
   const int co = 2 * (lane >> 4);
   return f32x4{sw[KW + co], sw[KW + co], sw[KW + co + 1], sw[KW + co + 1]};
 }
 
-// sigma (D = false) or sigma' (D = true) of the first n tiles, one branch on the
+// sigma (D = false) or sigma' (D = true) of the wave's tiles, one branch on the
 // activation for all of them
 template <bool D>
-__device__ __forceinline__ void act_tiles(f32x4 (&z)[TPW], int n, int act) {
+__device__ __forceinline__ void act_tiles(f32x4 (&z)[TPW], int act) {
   switch (act) {
     case ACT_TANH:
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) {
-        if (tt >= n) break;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float t = tanh_fast(z[tt][r]);
@@ -266,7 +273,6 @@ __device__ __forceinline__ void act_tiles(f32x4 (&z)[TPW], int n, int act) {
     case ACT_RELU:
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) {
-        if (tt >= n) break;
 #pragma unroll
         for (int r = 0; r < 4; ++r) z[tt][r] = D ? (z[tt][r] > 0.f ? 1.f : 0.f) : (z[tt][r] > 0.f ? z[tt][r] : 0.f);
       }
@@ -274,7 +280,6 @@ __device__ __forceinline__ void act_tiles(f32x4 (&z)[TPW], int n, int act) {
     case ACT_SMOOTHRELU:
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) {
-        if (tt >= n) break;
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           z[tt][r] = D ? dact_f<float, ACT_SMOOTHRELU>(z[tt][r]) : act_f<float, ACT_SMOOTHRELU>(z[tt][r]);
@@ -308,8 +313,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
   float* sw = lds + CH * g.CS;    // two layers
   __shared__ double red[MAXW];
   const int lane = threadIdx.x & 63, t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
-  // the wave's tiles (all TPW of them when the tiles fill the waves exactly)
-  const int ntl = (GH > 0 && g.NT16 % TPW == 0) ? TPW : min(TPW, g.NT16 - t0);
   const int k = blockIdx.x, Nc = gridDim.x;
   const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
   const float* K = static_cast<const float*>(a.K);
@@ -343,7 +346,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
   f32x4 v[TPW];
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt) {
-    if (tt >= ntl) break;
     const Px p = px_of(g, t0 + tt, lane);
     v[tt] = ld_px(src, g, p);
     if (vsrc) v[tt] = v[tt] + (ld_px(vsrc, g, p) - v[tt]);
@@ -351,7 +353,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
   __syncthreads();  // halo zeroed
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt) {
-    if (tt >= ntl) break;
     const Px p = px_of(g, t0 + tt, lane);
     if (p.ok) {
       put_px(buf, v[tt], g, p);
@@ -370,17 +371,12 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
       float wr[24];
       gather_w<false>(wr, swc, lane);
       const f32x4 bias = bias_px(swc, lane);
-#pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) {
-        if (tt >= ntl) break;
-        z[tt] = conv_tile(wr, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, bias);
-      }
+      conv_tiles(z, wr, buf, g, t0, lane, bias);
     }
-    act_tiles<false>(z, ntl, a.act);
+    act_tiles<false>(z, a.act);
     const float* gi = G ? G + (kc + j + 1) * slice + eo : nullptr;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       if (MODE == SWEEP_FRES && j == 0) coarse[tt] = v[tt] + hc * z[tt];
       v[tt] = v[tt] + hl * z[tt];
       if (gi) v[tt] += ld_px(gi, g, px_of(g, t0 + tt, lane));
@@ -389,7 +385,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
     float* xo = (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) ? X + (kc + j + 1) * slice + eo : nullptr;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) {
         put_px(buf, v[tt], g, p);
@@ -403,7 +398,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
     float* so = static_cast<float*>(a.S) + (size_t)(k + 1) * slice + eo;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) st_px(so, v[tt], g, p);
     }
@@ -413,7 +407,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
     double acc = 0.0;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) {
         const f32x4 rr = v[tt] - ld_px(cn, g, p);
@@ -449,8 +442,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
   float* sw = lds + CH * g.CS;    // two layers
   __shared__ double red[MAXW];
   const int lane = threadIdx.x & 63, t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
-  // the wave's tiles (all TPW of them when the tiles fill the waves exactly)
-  const int ntl = (GH > 0 && g.NT16 % TPW == 0) ? TPW : min(TPW, g.NT16 - t0);
   const int k = blockIdx.x, Nc = gridDim.x;
   const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
   const float* K = static_cast<const float*>(a.K);
@@ -484,7 +475,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
   f32x4 lam[TPW], un[TPW];
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt) {
-    if (tt >= ntl) break;
     const Px p = px_of(g, t0 + tt, lane);
     lam[tt] = ld_px(src, g, p);
     if (vsrc) lam[tt] = lam[tt] + (ld_px(vsrc, g, p) - lam[tt]);
@@ -493,7 +483,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
   __syncthreads();  // halo zeroed
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt) {
-    if (tt >= ntl) break;
     const Px p = px_of(g, t0 + tt, lane);
     if (p.ok) {
       put_px(buf, un[tt], g, p);
@@ -508,47 +497,35 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     const long i = top - 1 - j;
     const bool more = j + 1 < nsteps;
     const float* swc = sw + (j & 1) * WV;
-    if (more) {
-#pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) {
-        if (tt >= ntl) break;
-        un[tt] = ld_px(Uf + (size_t)(i - 1) * ustep + eo, g, px_of(g, t0 + tt, lane));
-      }
-    }
     stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(more ? i - 1 : i) * a.stride, nt);
     // d = sigma'(K u + b)
     {
       float wr[24];
       gather_w<false>(wr, swc, lane);
       const f32x4 bias = bias_px(swc, lane);
-#pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) {
-        if (tt >= ntl) break;
-        dd[tt] = conv_tile(wr, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, bias);
-      }
+      conv_tiles(dd, wr, buf, g, t0, lane, bias);
     }
-    act_tiles<true>(dd, ntl, a.act);
+    act_tiles<true>(dd, a.act);
     float wt[24];
     gather_w<true>(wt, swc, lane);
     __syncthreads();  // every read of u is done
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) put_px(buf, dd[tt] * lam[tt], g, p);
     }
     __syncthreads();
-    f32x4 w[TPW];
+    // the next step's primal state arrives while the transposed product runs
+    if (more) {
 #pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
-      w[tt] = conv_tile(wt, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, f32x4{0.f, 0.f, 0.f, 0.f});
+      for (int tt = 0; tt < TPW; ++tt) un[tt] = ld_px(Uf + (size_t)(i - 1) * ustep + eo, g, px_of(g, t0 + tt, lane));
     }
+    f32x4 w[TPW];
+    conv_tiles(w, wt, buf, g, t0, lane, f32x4{0.f, 0.f, 0.f, 0.f});
     const float* gi = G ? G + (size_t)i * slice + eo : nullptr;
     float* xo = (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) ? X + (size_t)i * slice + eo : nullptr;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       lam[tt] = lam[tt] + hl * w[tt];
       if (gi) lam[tt] += ld_px(gi, g, p);
@@ -558,7 +535,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     if (more) {
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) {
-        if (tt >= ntl) break;
         const Px p = px_of(g, t0 + tt, lane);
         if (p.ok) put_px(buf, un[tt], g, p);
       }
@@ -570,7 +546,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     float* so = static_cast<float*>(a.S) + (size_t)k * slice + eo;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) st_px(so, lam[tt], g, p);
     }
@@ -580,7 +555,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     f32x4 cu[TPW];
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       cu[tt] = ld_px(src, g, p);
       if (p.ok) put_px(buf, dd[tt] * cu[tt], g, p);
@@ -588,17 +562,15 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     float wt[24];
     gather_w<true>(wt, sw, lane);
     __syncthreads();
+    f32x4 w[TPW];
+    conv_tiles(w, wt, buf, g, t0, lane, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
-      cu[tt] += hc * conv_tile(wt, buf, px_of(g, t0 + tt, lane).base, g.CS, g.PW, f32x4{0.f, 0.f, 0.f, 0.f});
-    }
+    for (int tt = 0; tt < TPW; ++tt) cu[tt] += hc * w[tt];
     const float* ck = Cs + (size_t)k * a.cs_stride * slice + eo;
     float* gn = static_cast<float*>(a.Gn) + (size_t)k * slice + eo;
     double acc = 0.0;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) {
         const f32x4 rr = lam[tt] - ld_px(ck, g, p);
@@ -715,8 +687,8 @@ __global__ __launch_bounds__(NT) void k_resid(ResidArgs a, int H, int W) {
 // dWbig[(co,dy)][k] += s[co][2Y+dy][x] * patch[P][k] with the pair-pixels as
 // contraction index (k-slice = 4 pair-pixels, lane group = one of them): A = s
 // (rows (co,dy)), B = patches of u (96 columns in 6 blocks of 16). db sums s
-// from registers. The next example's u is loaded before the products. Waves and
-// lanes are combined in a fixed order.
+// from registers. The next example's u is loaded during the contraction. Waves
+// and lanes are combined in a fixed order.
 constexpr int GOUT = 16 * 96 + CH;  // dWbig then db per chunk
 
 template <int GH, int GW>
@@ -727,7 +699,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   float* bs = lds + CH * g.CS;       // CH * CS: s
   float* sw = lds + 2 * CH * g.CS;   // the layer's weights
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, t0 = wave * TPW, nt = blockDim.x;
-  const int ntl = (GH > 0 && g.NT16 % TPW == 0) ? TPW : min(TPW, g.NT16 - t0);
   const int n = blockIdx.x, chunk = blockIdx.y;
   const int per = (a.B + a.nchunks - 1) / a.nchunks;
   const int e0 = chunk * per, e1 = min(a.B, e0 + per);
@@ -754,7 +725,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   if (e0 < e1) {
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       un[tt] = ld_px(U + (size_t)e0 * g.q, g, px_of(g, t0 + tt, lane));
     }
   }
@@ -765,7 +735,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   if (e0 < e1) {
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) put_px(bu, un[tt], g, p);
     }
@@ -776,20 +745,13 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
     f32x4 z[TPW], lam[TPW];
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       lam[tt] = ld_px(Lm + (size_t)e * g.q, g, p);
-      if (more) un[tt] = ld_px(U + (size_t)(e + 1) * g.q, g, p);
     }
+    conv_tiles(z, wf, bu, g, t0, lane, bias);
+    act_tiles<true>(z, a.act);
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
-      z[tt] = conv_tile(wf, bu, px_of(g, t0 + tt, lane).base, g.CS, g.PW, bias);
-    }
-    act_tiles<true>(z, ntl, a.act);
-#pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) {
-      if (tt >= ntl) break;
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) {
         const f32x4 s = z[tt] * lam[tt];
@@ -799,6 +761,11 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
       }
     }
     __syncthreads();
+    // the next example's primal state arrives while the contraction runs
+    if (more) {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) un[tt] = ld_px(U + (size_t)(e + 1) * g.q, g, px_of(g, t0 + tt, lane));
+    }
     // contraction over pair-pixels
     for (int sl = wave; sl < nsl; sl += g.NW) {
       const int P = 4 * sl + (lane >> 4);
@@ -816,7 +783,6 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
     if (more) {
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) {
-        if (tt >= ntl) break;
         const Px p = px_of(g, t0 + tt, lane);
         if (p.ok) put_px(bu, un[tt], g, p);
       }
