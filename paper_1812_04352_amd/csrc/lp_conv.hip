@@ -312,7 +312,8 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
   float* buf = lds;               // CH * CS
   float* sw = lds + CH * g.CS;    // two layers
   __shared__ double red[MAXW];
-  const int lane = threadIdx.x & 63, t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
+  int lane = threadIdx.x & 63;
+  const int t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
   const int k = blockIdx.x, Nc = gridDim.x;
   const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
   const float* K = static_cast<const float*>(a.K);
@@ -364,6 +365,10 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
 
   f32x4 coarse[TPW];
   for (int j = 0; j < nsteps; ++j) {
+    // an empty asm statement makes the lane index opaque to the optimiser, so the
+    // tile offsets derived from it are recomputed each step instead of being kept
+    // live in registers through the loop (fewer registers, more resident waves)
+    asm volatile("" : "+v"(lane));
     const float* swc = sw + (j & 1) * WV;
     stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j)) * a.stride, nt);
     f32x4 z[TPW];
