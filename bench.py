@@ -245,17 +245,20 @@ def main():
     ws = L.alloc_workspace(p, mgF if fwd_iters >= adj_iters else mgA)
     hist = {}
 
-    def step():
-        _, hist["fwd"] = L.lp_mgrit_forward(p, mgF, K, b, U, ws)
+    def step(history=False):
+        # the residual histories are read back (a host round trip) only when asked
+        _, hf = L.lp_mgrit_forward(p, mgF, K, b, U, ws, history=history)
         L.lp_loss_terminal(p, wl.n_classes, U[-1], W, mu, c, J, Lam[-1], dW, dmu, ws)
-        _, hist["adj"] = L.lp_mgrit_adjoint(p, mgA, K, b, U, Lam, ws)
+        _, ha = L.lp_mgrit_adjoint(p, mgA, K, b, U, Lam, ws, history=history)
         L.lp_gradient(p, K, b, U, Lam, dK, db, ws)
+        if history:
+            hist["fwd"], hist["adj"] = hf, ha
 
     note(f"iterations fwd={fwd_iters} adj={adj_iters}; warm-up")
     # warm-up; the second step is traced for every kind to find the dominant kernel
     # (the first one also pays for loading the code objects)
     lib = L.load()
-    step()
+    step(history=True)
     torch.cuda.synchronize()
     lib.lp_trace_enable((1 << 11) - 1)
     step()

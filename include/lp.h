@@ -20,8 +20,9 @@
  *     `ws_bytes` bytes (see lp_workspace_bytes) and return LP_EWORKSPACE if it is
  *     too small or not 256-byte aligned.
  *   - All device work is enqueued on `stream` (a hipStream_t; NULL is the default
- *     stream). A call that returns a host value (res_hist, iters, norm) waits for
- *     `stream` before returning; other calls return without waiting.
+ *     stream). A call that returns a value computed on the device (res_hist,
+ *     norm, or an iteration count decided by a stopping rule) waits for `stream`
+ *     before returning; other calls return without waiting.
  *   - All floating-point arrays of one call have the problem's dtype
  *     (LP_F32: float, LP_F64: double). Layouts are row-major, contiguous:
  *       trajectory U, Lam  [N+1][B][q]     (conv: [N+1][B][C][H][W]); q = C*H*W
@@ -130,7 +131,11 @@ int32_t lp_serial_adjoint(const lp_problem* prob, const void* K, const void* b, 
  * norm ||G - A(U)|| over all examples and features, taken at the finest level's
  * C-points after the relaxation of iteration m (Algorithm 1, step 2).
  * iters (host, nullable): V-cycles run. Not converging within max_iter is not
- * an error. */
+ * an error.
+ * With rtol = stag = 0 the call runs max_iter V-cycles; if res_hist is then
+ * NULL it reads nothing back and returns without waiting for the stream (and
+ * without checking the norms for non-finite values). A stopping rule makes the
+ * call read rho_m after every V-cycle. */
 int32_t lp_mgrit_forward(const lp_problem* prob, const lp_mgrit* mg, const void* K,
                          const void* b, void* U, void* ws, size_t ws_bytes, double* res_hist,
                          int32_t* iters, void* stream);

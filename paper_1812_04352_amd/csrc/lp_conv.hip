@@ -878,7 +878,7 @@ hipError_t launch_conv_sweep(const Shape& s, int dir, const SweepArgs& a, dim3 g
   void (*f)(SweepArgs, conv::SGeo) = nullptr;
   if (s.H == 28 && s.W == 28) sweep_kernels<28, 28>(dir, a.mode, f);  // MNIST-sized images
   else sweep_kernels<0, 0>(dir, a.mode, f);
-  hipLaunchKernelGGL(f, grid, dim3(64 * g.NW), sweep_lds(g), st, a, g);
+  launch(f, grid, dim3(64 * g.NW), sweep_lds(g), st, a, g);
   return hipGetLastError();
 }
 
@@ -925,8 +925,8 @@ hipError_t conv_serial(const Shape& s, int dir, const SerialArgs& sa, hipStream_
 hipError_t conv_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t st, int* partials) {
   const dim3 grid(a.N, a.B);
   if (partials) *partials = (int)(grid.x * grid.y);
-  if (dir == DIR_FWD) conv::k_resid<DIR_FWD><<<grid, conv::NT, 0, st>>>(a, s.H, s.W);
-  else conv::k_resid<DIR_ADJ><<<grid, conv::NT, 0, st>>>(a, s.H, s.W);
+  if (dir == DIR_FWD) launch(conv::k_resid<DIR_FWD>, grid, conv::NT, 0, st, a, s.H, s.W);
+  else launch(conv::k_resid<DIR_ADJ>, grid, conv::NT, 0, st, a, s.H, s.W);
   return hipGetLastError();
 }
 
@@ -936,13 +936,13 @@ hipError_t conv_grad(const Shape& s, const GradArgs& a, hipStream_t st) {
   const int fl = 2 * conv::CH * g.CS + conv::WV, red = conv::GOUT + 2 * 64 * g.NW;
   const size_t sh = (size_t)(fl > red ? fl : red) * sizeof(float);
   if (s.H == 28 && s.W == 28)
-    conv::k_grad<28, 28><<<dim3(a.N, a.nchunks), 64 * g.NW, sh, st>>>(a, g);
+    launch(conv::k_grad<28, 28>, dim3(a.N, a.nchunks), 64 * g.NW, sh, st, a, g);
   else
-    conv::k_grad<0, 0><<<dim3(a.N, a.nchunks), 64 * g.NW, sh, st>>>(a, g);
+    launch(conv::k_grad<0, 0>, dim3(a.N, a.nchunks), 64 * g.NW, sh, st, a, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t tot = (size_t)a.N * (conv::KW + conv::CH);
-  conv::k_grad_final<<<(unsigned)((tot + conv::NT - 1) / conv::NT), conv::NT, 0, st>>>(a);
+  launch(conv::k_grad_final, (unsigned)((tot + conv::NT - 1) / conv::NT), conv::NT, 0, st, a);
   return hipGetLastError();
 }
 

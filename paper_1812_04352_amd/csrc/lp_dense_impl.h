@@ -627,13 +627,13 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   const dim3 grid(a.Nl / a.c, (a.B + NT - 1) / NT);
   if (partials) *partials = (int)(grid.x * grid.y);
   if (dir == DIR_FWD) {
-    if (a.mode == SWEEP_FC) k_fwd_sweep<T, Q, SWEEP_FC><<<grid, NT, 0, st>>>(a);
-    else if (a.mode == SWEEP_FRES) k_fwd_sweep<T, Q, SWEEP_FRES><<<grid, NT, 0, st>>>(a);
-    else k_fwd_sweep<T, Q, SWEEP_CORRF><<<grid, NT, 0, st>>>(a);
+    if (a.mode == SWEEP_FC) launch(k_fwd_sweep<T, Q, SWEEP_FC>, grid, NT, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_fwd_sweep<T, Q, SWEEP_FRES>, grid, NT, 0, st, a);
+    else launch(k_fwd_sweep<T, Q, SWEEP_CORRF>, grid, NT, 0, st, a);
   } else {
-    if (a.mode == SWEEP_FC) k_adj_sweep<T, Q, SWEEP_FC><<<grid, NT, 0, st>>>(a);
-    else if (a.mode == SWEEP_FRES) k_adj_sweep<T, Q, SWEEP_FRES><<<grid, NT, 0, st>>>(a);
-    else k_adj_sweep<T, Q, SWEEP_CORRF><<<grid, NT, 0, st>>>(a);
+    if (a.mode == SWEEP_FC) launch(k_adj_sweep<T, Q, SWEEP_FC>, grid, NT, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_adj_sweep<T, Q, SWEEP_FRES>, grid, NT, 0, st, a);
+    else launch(k_adj_sweep<T, Q, SWEEP_CORRF>, grid, NT, 0, st, a);
   }
   return hipGetLastError();
 }
@@ -641,8 +641,8 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
 template <typename T, int Q>
 hipError_t serial(int dir, const SerialArgs& a, hipStream_t st) {
   const dim3 grid((a.B + NT - 1) / NT);
-  if (dir == DIR_FWD) k_fwd_serial<T, Q><<<grid, NT, 0, st>>>(a);
-  else k_adj_serial<T, Q><<<grid, NT, 0, st>>>(a);
+  if (dir == DIR_FWD) launch(k_fwd_serial<T, Q>, grid, NT, 0, st, a);
+  else launch(k_adj_serial<T, Q>, grid, NT, 0, st, a);
   return hipGetLastError();
 }
 
@@ -650,18 +650,18 @@ template <typename T, int Q>
 hipError_t resid(int dir, const ResidArgs& a, hipStream_t st, int* partials) {
   const dim3 grid(a.N, (a.B + NT - 1) / NT);
   if (partials) *partials = (int)(grid.x * grid.y);
-  if (dir == DIR_FWD) k_resid<T, Q, DIR_FWD><<<grid, NT, 0, st>>>(a);
-  else k_resid<T, Q, DIR_ADJ><<<grid, NT, 0, st>>>(a);
+  if (dir == DIR_FWD) launch(k_resid<T, Q, DIR_FWD>, grid, NT, 0, st, a);
+  else launch(k_resid<T, Q, DIR_ADJ>, grid, NT, 0, st, a);
   return hipGetLastError();
 }
 
 template <typename T, int Q>
 hipError_t grad(const GradArgs& a, hipStream_t st) {
-  k_grad_partial<T, Q><<<dim3(a.N, a.nchunks), NT, 0, st>>>(a);
+  launch(k_grad_partial<T, Q>, dim3(a.N, a.nchunks), NT, 0, st, a);
   const hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t tot = (size_t)a.N * (Q * Q + Q);
-  k_grad_final<T><<<(unsigned)((tot + NT - 1) / NT), NT, 0, st>>>(a, Q * Q, Q);
+  launch(k_grad_final<T>, (unsigned)((tot + NT - 1) / NT), NT, 0, st, a, Q * Q, Q);
   return hipGetLastError();
 }
 

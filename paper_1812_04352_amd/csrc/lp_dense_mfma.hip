@@ -273,9 +273,22 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     }
   }
   f32x16 coarse[MB];
+  // The serial solve (one wave per workgroup, few workgroups) is latency-bound:
+  // it loads the G row of the next step one step ahead (every lane loads a valid
+  // row; columns of lanes past the batch are never stored). The sweeps keep the
+  // registers for occupancy instead.
+  constexpr bool PF = MODE == MODE_SERIAL;
+  f32x16 gn[MB];
+  if (PF && G) load_c<Q>(gn, G + (kc + 1) * slice + row);
   for (int j = 0; j < nsteps; ++j) {
     // prefetch the next layer (the last step re-fetches its own: keeps wr in registers)
     w_fetch<Q, WAVES>(wr, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j)) * a.stride);
+    f32x16 gc[MB];
+    if (PF && G) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) gc[mb] = gn[mb];
+      if (j + 1 < nsteps) load_c<Q>(gn, G + (kc + j + 2) * slice + row);
+    }
     f32x16 s[MB];
     prod<Q, C::LD>(s, v, W[j & 1], lane);
     apply<Q>(s, a.act, false);
@@ -285,8 +298,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     }
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) v[mb] = v[mb] + hl * s[mb];
+    if (PF && G) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) v[mb] += gc[mb];
+    }
     if (on) {
-      if (G) add_c<Q>(v, G + (kc + j + 1) * slice + row);
+      if (!PF && G) add_c<Q>(v, G + (kc + j + 1) * slice + row);
       if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) store_c<Q>(X + (kc + j + 1) * slice + row, v);
     }
     w_put<Q, WAVES>(W[(j + 1) & 1], wr);
@@ -375,14 +392,36 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) cu[mb] = v[mb];
   }
+  // The serial solve loads the next step's primal and G rows one step ahead
+  // (every lane loads a valid row; columns of lanes past the batch are never
+  // stored); the sweeps keep the registers for occupancy instead.
+  constexpr bool PF = MODE == MODE_SERIAL;
+  f32x16 un[MB], gn[MB];
+  if (PF) {
+    load_c<Q>(un, Uf + (size_t)(top - 1) * a.stride * slice + row);
+    if (G) load_c<Q>(gn, G + (size_t)(top - 1) * slice + row);
+  }
   for (int j = 0; j < nsteps; ++j) {
     const long i = top - 1 - j;
     w_fetch<Q, WAVES>(wr, K, bb, (size_t)(j + 1 < nsteps ? i - 1 : i) * a.stride);
-    f32x16 d[MB], w[MB];
+    f32x16 d[MB], w[MB], gc[MB];
     {
       f32x16 u[MB];
-      zero_c<Q>(u);
-      if (on) load_c<Q>(u, Uf + (size_t)i * a.stride * slice + row);
+      if (PF) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) u[mb] = un[mb];
+        if (G) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) gc[mb] = gn[mb];
+        }
+        if (j + 1 < nsteps) {
+          load_c<Q>(un, Uf + (size_t)(i - 1) * a.stride * slice + row);
+          if (G) load_c<Q>(gn, G + (size_t)(i - 1) * slice + row);
+        }
+      } else {
+        zero_c<Q>(u);
+        if (on) load_c<Q>(u, Uf + (size_t)i * a.stride * slice + row);
+      }
       prod<Q, C::LD>(d, u, W[j & 1], lane);
     }
     apply<Q>(d, a.act, true);
@@ -400,8 +439,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
     prod_t<Q, C::LD>(w, d, W[j & 1], lane);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) v[mb] = v[mb] + hl * w[mb];
+    if (PF && G) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) v[mb] += gc[mb];
+    }
     if (on) {
-      if (G) add_c<Q>(v, G + (size_t)i * slice + row);
+      if (!PF && G) add_c<Q>(v, G + (size_t)i * slice + row);
       if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) store_c<Q>(X + (size_t)i * slice + row, v);
     }
     w_put<Q, WAVES>(W[(j + 1) & 1], wr);
@@ -561,11 +604,11 @@ __global__ __launch_bounds__(256) void k_grad_final(GradArgs a, int nw, int nbia
 
 template <int Q>
 hipError_t grad(const GradArgs& a, hipStream_t st) {
-  k_grad<Q><<<dim3(a.N, a.nchunks), 64 * GRAD_WAVES, 0, st>>>(a);
+  launch(k_grad<Q>, dim3(a.N, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t tot = (size_t)a.N * (Q * Q + Q);
-  k_grad_final<<<(unsigned)((tot + 255) / 256), 256, 0, st>>>(a, Q * Q, Q);
+  launch(k_grad_final, (unsigned)((tot + 255) / 256), 256, 0, st, a, Q * Q, Q);
   return hipGetLastError();
 }
 
@@ -578,13 +621,13 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   const dim3 grid(a.Nl / a.c, (a.B + 32 * W4 - 1) / (32 * W4));
   if (partials) *partials = (int)(grid.x * grid.y);
   if (dir == DIR_FWD) {
-    if (a.mode == SWEEP_FC) k_fwd<Q, SWEEP_FC, W4><<<grid, 64 * W4, 0, st>>>(a);
-    else if (a.mode == SWEEP_FRES) k_fwd<Q, SWEEP_FRES, W4><<<grid, 64 * W4, 0, st>>>(a);
-    else k_fwd<Q, SWEEP_CORRF, W4><<<grid, 64 * W4, 0, st>>>(a);
+    if (a.mode == SWEEP_FC) launch(k_fwd<Q, SWEEP_FC, W4>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_fwd<Q, SWEEP_FRES, W4>, grid, 64 * W4, 0, st, a);
+    else launch(k_fwd<Q, SWEEP_CORRF, W4>, grid, 64 * W4, 0, st, a);
   } else {
-    if (a.mode == SWEEP_FC) k_adj<Q, SWEEP_FC, W4><<<grid, 64 * W4, 0, st>>>(a);
-    else if (a.mode == SWEEP_FRES) k_adj<Q, SWEEP_FRES, W4><<<grid, 64 * W4, 0, st>>>(a);
-    else k_adj<Q, SWEEP_CORRF, W4><<<grid, 64 * W4, 0, st>>>(a);
+    if (a.mode == SWEEP_FC) launch(k_adj<Q, SWEEP_FC, W4>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_adj<Q, SWEEP_FRES, W4>, grid, 64 * W4, 0, st, a);
+    else launch(k_adj<Q, SWEEP_CORRF, W4>, grid, 64 * W4, 0, st, a);
   }
   return hipGetLastError();
 }
@@ -606,8 +649,8 @@ hipError_t serial(int dir, const SerialArgs& s, hipStream_t st) {
   a.X = s.X;
   a.G = s.G;
   const dim3 grid(1, (s.B + 32 * W1 - 1) / (32 * W1));
-  if (dir == DIR_FWD) k_fwd<Q, MODE_SERIAL, W1><<<grid, 64 * W1, 0, st>>>(a);
-  else k_adj<Q, MODE_SERIAL, W1><<<grid, 64 * W1, 0, st>>>(a);
+  if (dir == DIR_FWD) launch(k_fwd<Q, MODE_SERIAL, W1>, grid, 64 * W1, 0, st, a);
+  else launch(k_adj<Q, MODE_SERIAL, W1>, grid, 64 * W1, 0, st, a);
   return hipGetLastError();
 }
 

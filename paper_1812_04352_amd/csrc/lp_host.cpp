@@ -55,6 +55,15 @@ size_t g_pool_used = 0;
 long g_trace_dropped = 0;
 constexpr size_t kTraceMax = 65536;
 
+}  // namespace
+
+lp::LaunchEvents& lp::launch_events() {
+  static thread_local LaunchEvents e;
+  return e;
+}
+
+namespace {
+
 hipEvent_t pool_event() {
   if (g_pool_used == g_event_pool.size()) {
     hipEvent_t e;
@@ -64,29 +73,32 @@ hipEvent_t pool_event() {
   return g_event_pool[g_pool_used++];
 }
 
-// Records a start event on construction and a stop event on destruction when
-// the kind is being traced.
+// When the kind is being traced, hands an event pair to the kernel launches
+// inside the scope (they record the first kernel's start and the last one's end
+// on their own dispatches) and keeps the record if any kernel was launched.
 struct TraceScope {
-  hipStream_t st;
-  hipEvent_t b = nullptr;
-  int idx = -1;
-  TraceScope(int kind, int level, hipStream_t s) : st(s) {
+  long idx = -1;
+  TraceScope(int kind, int level, hipStream_t) {
     if (!(g_trace_mask & (1u << kind))) return;
     std::lock_guard<std::mutex> lk(g_trace_mu);
     if (g_trace.size() >= kTraceMax) {
       ++g_trace_dropped;
       return;
     }
-    hipEvent_t a = pool_event();
-    b = pool_event();
-    if (!a || !b || hipEventRecord(a, st) != hipSuccess) {
-      b = nullptr;
-      return;
-    }
+    hipEvent_t a = pool_event(), b = pool_event();
+    if (!a || !b) return;
+    idx = (long)g_trace.size();
     g_trace.push_back(TraceRec{kind, level, a, b});
+    lp::launch_events() = lp::LaunchEvents{a, b, 0};
   }
   ~TraceScope() {
-    if (b) hipEventRecord(b, st);
+    if (idx < 0) return;
+    lp::LaunchEvents& e = lp::launch_events();
+    if (e.launched == 0) {  // nothing ran: void the record (its events hold no times)
+      std::lock_guard<std::mutex> lk(g_trace_mu);
+      g_trace[idx].kind = -1;
+    }
+    e = lp::LaunchEvents{};
   }
 };
 
@@ -408,7 +420,9 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
   }
   rc = s.finish();
   if (rc) return rc;
-  if (!early) {
+  // With neither a stopping rule nor a history to return, nothing is read back:
+  // the call returns with the work enqueued (and the norms are not checked).
+  if (!early && res_hist) {
     hist.assign(it, 0.0);
     LP_TRY(hipMemcpyAsync(hist.data(), rho, it * sizeof(double), hipMemcpyDeviceToHost, st), "read residuals");
     LP_TRY(hipStreamSynchronize(st), "stream sync");

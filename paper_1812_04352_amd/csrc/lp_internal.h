@@ -2,11 +2,34 @@
 // launchers. Not part of the public ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace lp {
+
+// Tracing hook. While a traced call runs, the kernels it launches record their
+// own start (the first launch) and end (every launch; the last one stands) into
+// these events on the dispatch itself, so tracing puts no marker packets into
+// the stream between kernels. Thread-local; set and cleared by the host.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+  int launched = 0;
+};
+LaunchEvents& launch_events();
+
+template <typename... P, typename... A>
+inline void launch(void (*k)(P...), dim3 grid, dim3 block, size_t shmem, hipStream_t st, A... args) {
+  LaunchEvents& e = launch_events();
+  if (e.stop) {
+    hipExtLaunchKernelGGL(k, grid, block, (uint32_t)shmem, st, e.launched ? nullptr : e.start, e.stop, 0u,
+                          static_cast<P>(args)...);
+    ++e.launched;
+  } else {
+    k<<<grid, block, shmem, st>>>(static_cast<P>(args)...);
+  }
+}
 
 enum Dir { DIR_FWD = 0, DIR_ADJ = 1 };
 

@@ -54,11 +54,12 @@ __global__ __launch_bounds__(NT) void k_softmax(double* z, const T* c, double* l
 }
 
 // J = (1/B) sum_e loss_e, summed in a fixed order by one workgroup.
-__global__ __launch_bounds__(NT) void k_mean(const double* loss, int B, double* J) {
-  __shared__ double sh[NT];
+constexpr int NT_MEAN = 1024;
+__global__ __launch_bounds__(NT_MEAN) void k_mean(const double* loss, int B, double* J) {
+  __shared__ double sh[NT_MEAN];
   double s = 0.0;
-  for (int e = threadIdx.x; e < B; e += NT) s += loss[e];
-  s = block_sum<NT>(s, sh);
+  for (int e = threadIdx.x; e < B; e += NT_MEAN) s += loss[e];
+  s = block_sum<NT_MEAN>(s, sh);
   if (threadIdx.x == 0) J[0] = s / (double)B;
 }
 
@@ -77,16 +78,25 @@ __global__ __launch_bounds__(NT) void k_wpart(const T* uN, const double* d, doub
   part[(size_t)ch * nw + o] = acc;
 }
 
+// Sum of the chunk partials: a workgroup takes FO outputs, thread group g sums
+// chunks g, g + NT/FO, ... of one output, and the groups are added in order.
+constexpr int FO = 8;
 template <typename T>
 __global__ __launch_bounds__(NT) void k_wfinal(const double* part, int nch, T* dW, T* dmu, int q, int nc) {
-  const size_t o = (size_t)blockIdx.x * NT + threadIdx.x;
+  __shared__ double sh[NT];
   const size_t nw = (size_t)nc * (q + 1);
-  if (o >= nw) return;
+  const size_t o = (size_t)blockIdx.x * FO + (threadIdx.x % FO);
   double s = 0.0;
-  for (int ch = 0; ch < nch; ++ch) s += part[(size_t)ch * nw + o];
+  if (o < nw)
+    for (int ch = threadIdx.x / FO; ch < nch; ch += NT / FO) s += part[(size_t)ch * nw + o];
+  sh[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x >= FO || o >= nw) return;
+  double t = 0.0;
+  for (int g = 0; g < NT / FO; ++g) t += sh[g * FO + threadIdx.x];
   const int j = (int)(o / (q + 1)), i = (int)(o - (size_t)j * (q + 1));
-  if (i < q) dW[(size_t)j * q + i] = (T)s;
-  else dmu[j] = (T)s;
+  if (i < q) dW[(size_t)j * q + i] = (T)t;
+  else dmu[j] = (T)t;
 }
 
 // lamN[e][i] = sum_j W[j][i] d[e][j]
@@ -113,9 +123,9 @@ hipError_t loss_t(int B, int q, int nc, const void* uN, const void* Wc, const vo
   const size_t nw = (size_t)nc * (q + 1);
   k_logits<T><<<B, 64, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu, z, q, nc);
   k_softmax<T><<<(B + NT - 1) / NT, NT, 0, st>>>(z, (const T*)c, loss, B, nc);
-  k_mean<<<1, NT, 0, st>>>(loss, B, J);
+  k_mean<<<1, NT_MEAN, 0, st>>>(loss, B, J);
   k_wpart<T><<<dim3(nch, (unsigned)((nw + NT - 1) / NT)), NT, 0, st>>>((const T*)uN, z, part, B, q, nc);
-  k_wfinal<T><<<(unsigned)((nw + NT - 1) / NT), NT, 0, st>>>(part, nch, (T*)dW, (T*)dmu, q, nc);
+  k_wfinal<T><<<(unsigned)((nw + FO - 1) / FO), NT, 0, st>>>(part, nch, (T*)dW, (T*)dmu, q, nc);
   k_lam<T><<<(unsigned)(((size_t)B * q + NT - 1) / NT), NT, 0, st>>>((const T*)Wc, z, (T*)lamN, B, q, nc);
   return hipGetLastError();
 }

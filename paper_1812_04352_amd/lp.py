@@ -194,27 +194,30 @@ def lp_serial_adjoint(p: LpProblem, K, b, U, Lam) -> None:
                                     _arr(Lam, n, "Lam", _elem_dtype(p)), _stream()), "lp_serial_adjoint")
 
 
-def lp_mgrit_forward(p: LpProblem, mg: LpMgrit, K, b, U, ws) -> Tuple[int, list]:
+def lp_mgrit_forward(p: LpProblem, mg: LpMgrit, K, b, U, ws, history: bool = True) -> Tuple[int, list]:
+    """history=False passes no residual history: without a stopping rule the
+    call then returns without waiting for the stream (the list is empty)."""
     Kp, bp = _weights(p, K, b)
-    hist = (ctypes.c_double * max(1, mg.max_iter))()
+    hist = (ctypes.c_double * max(1, mg.max_iter))() if history else None
     it = ctypes.c_int32(0)
     wp, wn = _ws(ws, 1)
     _check(load().lp_mgrit_forward(ctypes.byref(p), ctypes.byref(mg), Kp, bp,
                                    _arr(U, (p.N + 1) * p.B * p.q, "U", _elem_dtype(p)), wp, wn, hist,
                                    ctypes.byref(it), _stream()), "lp_mgrit_forward")
-    return it.value, list(hist[:it.value])
+    return it.value, list(hist[:it.value]) if history else []
 
 
-def lp_mgrit_adjoint(p: LpProblem, mg: LpMgrit, K, b, U, Lam, ws) -> Tuple[int, list]:
+def lp_mgrit_adjoint(p: LpProblem, mg: LpMgrit, K, b, U, Lam, ws, history: bool = True) -> Tuple[int, list]:
+    """history as for lp_mgrit_forward."""
     Kp, bp = _weights(p, K, b)
     n = (p.N + 1) * p.B * p.q
-    hist = (ctypes.c_double * max(1, mg.max_iter))()
+    hist = (ctypes.c_double * max(1, mg.max_iter))() if history else None
     it = ctypes.c_int32(0)
     wp, wn = _ws(ws, 1)
     _check(load().lp_mgrit_adjoint(ctypes.byref(p), ctypes.byref(mg), Kp, bp, _arr(U, n, "U", _elem_dtype(p)),
                                    _arr(Lam, n, "Lam", _elem_dtype(p)), wp, wn, hist, ctypes.byref(it),
                                    _stream()), "lp_mgrit_adjoint")
-    return it.value, list(hist[:it.value])
+    return it.value, list(hist[:it.value]) if history else []
 
 
 def lp_gradient(p: LpProblem, K, b, U, Lam, dK, db, ws) -> None:

@@ -43,10 +43,10 @@ class OneShotTrainer:
         self.mgF.warm_start = int(warm)
         self.mgA.warm_start = int(warm)
         L.lp_open_forward(p, self.opening, self.nf, self.y, P.get("L_in"), self.U[0])
-        L.lp_mgrit_forward(p, self.mgF, P["K"], P["b"], self.U, self.ws)
+        L.lp_mgrit_forward(p, self.mgF, P["K"], P["b"], self.U, self.ws, history=False)
         L.lp_loss_terminal(p, self.nc, self.U[-1], P["W"], P["mu"], self.c, self.J, self.Lam[-1], G["W"], G["mu"],
                            self.ws)
-        L.lp_mgrit_adjoint(p, self.mgA, P["K"], P["b"], self.U, self.Lam, self.ws)
+        L.lp_mgrit_adjoint(p, self.mgA, P["K"], P["b"], self.U, self.Lam, self.ws, history=False)
         L.lp_gradient(p, P["K"], P["b"], self.U, self.Lam, G["K"], G["b"], self.ws)
         if "L_in" in P:
             L.lp_open_grad(p, self.opening, self.nf, self.y, P["L_in"], self.Lam[0], G["L_in"])

@@ -198,6 +198,54 @@ def test_stop_rules_and_errors():
     assert e.value.status == L.LP_ENONFINITE
 
 
+@pytest.mark.parametrize("name,wl", [DENSE[1], DENSE[2], DENSE[7]], ids=[DENSE[1][0], DENSE[2][0], DENSE[7][0]])
+def test_solves_without_history_match(name, wl):
+    """With no residual history and no stopping rule the solves return without
+    waiting for the stream; the iterates must equal those of the reading call."""
+    c = case(wl)
+    mg = sched(wl, 3)
+    ws = L.alloc_workspace(c.p, mg)
+    U1, U2 = c.new_traj(), c.new_traj()
+    assert L.lp_mgrit_forward(c.p, mg, c.K, c.b, U1, ws)[0] == 3
+    assert L.lp_mgrit_forward(c.p, mg, c.K, c.b, U2, ws, history=False) == (3, [])
+    torch.cuda.synchronize()
+    assert torch.equal(U1, U2)
+    L1 = torch.zeros_like(U1)
+    L1[-1] = _lamN(c, U1)[0]
+    L2 = L1.clone()
+    L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U1, L1, ws)
+    assert L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U1, L2, ws, history=False) == (3, [])
+    torch.cuda.synchronize()
+    assert torch.equal(L1, L2)
+
+
+def test_tracing_counts_launches():
+    """The trace records one timed entry per traced launch site: with FCF on L
+    levels and m V-cycles the forward solve runs m FC and m FRES sweeps per
+    non-coarsest level, m coarsest solves, and (with the finest correction
+    deferred) m CORRF sweeps per middle level plus one final finest CORRF."""
+    wl = DENSE[1][1]
+    c = case(wl)
+    m = 3
+    mg = sched(wl, m)
+    ws = L.alloc_workspace(c.p, mg)
+    U = c.new_traj()
+    L.lp_trace_enable((1 << 11) - 1)
+    try:
+        L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, history=False)
+        torch.cuda.synchronize()
+        levels = len(O.level_sizes(wl.N, wl.cf, wl.max_levels, wl.min_coarse))
+        got = {k: L.lp_trace_read(k) for k in range(4)}
+    finally:
+        L.lp_trace_enable(0)
+    assert got[0][0] == m * (levels - 1) and got[1][0] == m * (levels - 1)
+    assert got[3][0] == m
+    assert got[2][0] == m * (levels - 2) + 1
+    assert all(ms > 0.0 for n, ms in got.values() if n)
+    for k in range(4, 11):
+        assert L.lp_trace_read(k) == (0, 0.0)
+
+
 def test_empty_batch_is_a_no_op():
     wl = DENSE[1][1]
     p = L.problem(wl.dtype, wl.layer, wl.act, wl.N, 0, wl.C, h=wl.h)
