@@ -128,6 +128,76 @@ def measured_traffic(kernel: str, workload: str):
     return ent.get("bytes_per_launch")
 
 
+def kernel_kind(name: str):
+    """Trace kind of a library kernel from its (demangled) name, or None."""
+    import re
+    if "k_grad<" in name or "k_grad_partial<" in name:
+        return "gradient"
+    m = re.search(r"lp::(mfma|conv|dense)::k_(fwd|adj)(_sweep|_serial)?<([^>]*)>", name)
+    if not m:
+        return None
+    fam, d, suffix, targs = m.groups()
+    args = [t.strip() for t in targs.split(",")]
+    if suffix == "_serial":
+        mode = 3
+    else:
+        mode = int(args[{"mfma": 1, "conv": 0, "dense": 2}[fam]])
+    return f"{d}_" + ["fc", "fres", "corrf", "coarsest"][mode]
+
+
+def summarize_traffic(workload: str, fetch_dir: str, write_dir: str, copy_fetch_dir: str, copy_write_dir: str):
+    """HBM bytes per launch of every traced kernel kind from two rocprofv3 --pmc
+    runs of the benchmark (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
+    scaled by what the same counter reads for a plain copy of known size (two
+    more runs with --copy-calibration). Writes the entries of `workload` into
+    profiles/traffic.json with the current kernel source hash and prints the
+    table as markdown."""
+    import collections
+    import csv
+
+    def load(d):
+        per = collections.defaultdict(list)
+        for r in csv.DictReader(open(os.path.join(d, "run_counter_collection.csv"))):
+            per[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return per
+
+    f, w, cf, cw = load(fetch_dir), load(write_dir), load(copy_fetch_dir), load(copy_write_dir)
+    copy = [k for k in cf if "copyBuffer" in k or "copy" in k.lower()]
+    if not copy:
+        raise SystemExit("no copy kernel in the calibration runs")
+    ck = max(copy, key=lambda k: sum(cf[k]))
+    true_bytes = float(1 << 30)
+    f_scale = true_bytes / (sum(cf[ck]) / len(cf[ck]) * 1024.0)
+    w_scale = true_bytes / (sum(cw[ck]) / len(cw[ck]) * 1024.0)
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    rec = json.load(open(path)) if os.path.exists(path) else {}
+    ent = {}
+    print(f"Calibration: a plain copy of 1 GiB (`{ck}`, {len(cf[ck])} launches) reads FETCH_SIZE = "
+          f"{sum(cf[ck]) / len(cf[ck]):.0f} KiB and WRITE_SIZE = {sum(cw[ck]) / len(cw[ck]):.0f} KiB per launch, "
+          f"so true bytes = FETCH_SIZE x {f_scale:.3f} KiB and WRITE_SIZE x {w_scale:.3f} KiB.\n")
+    print("| kind | kernel | launches | FETCH_SIZE KiB/launch | WRITE_SIZE KiB/launch | HBM MB/launch |")
+    print("|---|---|---:|---:|---:|---:|")
+    by_kind = collections.defaultdict(lambda: [0, 0.0, 0.0, []])
+    for k in f:
+        kind = kernel_kind(k)
+        if kind is None or k not in w:
+            continue
+        b = by_kind[kind]
+        b[0] += len(f[k])
+        b[1] += sum(f[k])
+        b[2] += sum(w[k])
+        b[3].append(k)
+    for kind, (n, fs, ws, names) in sorted(by_kind.items(), key=lambda t: -(t[1][1] + t[1][2])):
+        fk, wk = fs / n, ws / n
+        byts = (fk * f_scale + wk * w_scale) * 1024.0
+        ent[kind] = {"bytes_per_launch": byts, "source_hash": source_hash(), "kernel": " / ".join(names)}
+        print(f"| {kind} | `{' / '.join(names)}` | {n} | {fk:.0f} | {wk:.0f} | {byts / 1e6:.1f} |")
+    rec[workload] = ent
+    with open(path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+
+
 def cpu_baseline(wl, budget_s: float = 12.0):
     """The oracle (fp64 NumPy) timed on the host: one MGRIT forward iteration and
     one adjoint iteration on a bounded batch sample, repeated until about
@@ -184,7 +254,13 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (to scale HBM byte counters)")
+    ap.add_argument("--traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="summarise rocprofv3 FETCH_SIZE / WRITE_SIZE runs of --config into profiles/traffic.json "
+                         "(no GPU needed)")
     args = ap.parse_args()
+    if args.traffic:
+        summarize_traffic(f"cfg{args.config}", *args.traffic)
+        return
     if args.copy_calibration:
         import torch
         n = 1 << 28  # fp32 values = 1 GiB
