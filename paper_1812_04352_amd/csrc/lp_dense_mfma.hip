@@ -226,7 +226,12 @@ __device__ __forceinline__ double wg_sum(double v, double* red) {
 }
 
 // ------------------------------------------------------------------ forward
-// Interval k = blockIdx.x (serial: the whole level), examples of blockIdx.y.
+// Interval k = blockIdx.y (serial: the whole level), examples of blockIdx.x.
+// Consecutive workgroups share an interval, so the round-robin dispatch over the
+// 8 XCDs gives each XCD every interval's weights once, in order, and its L2 only
+// has to hold the few intervals in flight (with the interval as the fast index,
+// an XCD received all tiles of every 8th interval and its weights overflowed L2
+// at N = 2048, q = 64).
 template <int Q, int MODE, int WAVES>
 __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
   using C = Cfg<Q, WAVES>;
@@ -234,9 +239,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
   __shared__ float W[2][C::WSZ];
   __shared__ double red[WAVES];
   const int lane = threadIdx.x & 63;
-  const int k = blockIdx.x;
-  const int Nc = gridDim.x;
-  const int e = (blockIdx.y * WAVES + (threadIdx.x >> 6)) * 32 + (lane & 31);
+  const int k = blockIdx.y;
+  const int Nc = gridDim.y;
+  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * 32 + (lane & 31);
   const bool on = e < a.B;
   const size_t slice = (size_t)a.B * Q;
   const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane >> 5);
@@ -330,7 +335,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     }
     if (a.partial) {
       const double s = wg_sum<WAVES>(acc, red);
-      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
+      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
     }
   } else if (MODE == SWEEP_CORRF) {
     if (on && k == Nc - 1) {
@@ -350,9 +355,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
   __shared__ float W[2][C::WSZ];
   __shared__ double red[WAVES];
   const int lane = threadIdx.x & 63;
-  const int k = blockIdx.x;
-  const int Nc = gridDim.x;
-  const int e = (blockIdx.y * WAVES + (threadIdx.x >> 6)) * 32 + (lane & 31);
+  const int k = blockIdx.y;
+  const int Nc = gridDim.y;
+  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * 32 + (lane & 31);
   const bool on = e < a.B;
   const size_t slice = (size_t)a.B * Q;
   const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane >> 5);
@@ -471,7 +476,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
     }
     if (a.partial) {
       const double s = wg_sum<WAVES>(acc, red);
-      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
+      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
     }
   } else if (MODE == SWEEP_CORRF) {
     if (on && k == 0) {
@@ -618,7 +623,8 @@ constexpr int SERIAL_WAVES = 1;  // 32 examples per serial workgroup (more workg
 template <int Q>
 hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   constexpr int W4 = SWEEP_WAVES;
-  const dim3 grid(a.Nl / a.c, (a.B + 32 * W4 - 1) / (32 * W4));
+  if (a.Nl / a.c > 65535) return hipErrorNotSupported;  // intervals index the grid's y dimension
+  const dim3 grid((a.B + 32 * W4 - 1) / (32 * W4), a.Nl / a.c);
   if (partials) *partials = (int)(grid.x * grid.y);
   if (dir == DIR_FWD) {
     if (a.mode == SWEEP_FC) launch(k_fwd<Q, SWEEP_FC, W4>, grid, 64 * W4, 0, st, a);
@@ -648,7 +654,7 @@ hipError_t serial(int dir, const SerialArgs& s, hipStream_t st) {
   a.hl = s.hl;
   a.X = s.X;
   a.G = s.G;
-  const dim3 grid(1, (s.B + 32 * W1 - 1) / (32 * W1));
+  const dim3 grid((s.B + 32 * W1 - 1) / (32 * W1), 1);
   if (dir == DIR_FWD) launch(k_fwd<Q, MODE_SERIAL, W1>, grid, 64 * W1, 0, st, a);
   else launch(k_adj<Q, MODE_SERIAL, W1>, grid, 64 * W1, 0, st, a);
   return hipGetLastError();
