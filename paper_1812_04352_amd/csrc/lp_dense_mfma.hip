@@ -34,23 +34,6 @@ __device__ __forceinline__ float tanh_fast(float x) {
   return copysignf((1.f - t) * __builtin_amdgcn_rcpf(1.f + t), x);
 }
 
-__device__ __forceinline__ float act_v(float z, int act) {
-  if (act == ACT_TANH) return tanh_fast(z);
-  if (act == ACT_RELU) return z > 0.f ? z : 0.f;
-  if (act == ACT_SMOOTHRELU) return act_f<float, ACT_SMOOTHRELU>(z);
-  return z;
-}
-
-__device__ __forceinline__ float dact_v(float z, int act) {
-  if (act == ACT_TANH) {
-    const float t = tanh_fast(z);
-    return 1.f - t * t;
-  }
-  if (act == ACT_RELU) return z > 0.f ? 1.f : 0.f;
-  if (act == ACT_SMOOTHRELU) return dact_f<float, ACT_SMOOTHRELU>(z);
-  return 1.f;
-}
-
 template <int Q, int WAVES>
 struct Cfg {
   static constexpr int NT = 64 * WAVES;
@@ -172,21 +155,54 @@ __device__ __forceinline__ void prod_t(f32x16 (&w)[Q / 32], const f32x16 (&s)[Q 
     for (int r = 0; r < 16; ++r) w[ob][r] = 0.f;
     const float* colp = W + 32 * ob + i + 4 * h * LD;
 #pragma unroll
-    for (int ib = 0; ib < Q / 32; ++ib)
+    for (int ib = 0; ib < Q / 32; ++ib) {
+      // the block's 16 column values are read before its products start
+      float a[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float a = colp[(32 * ib + 8 * (r >> 2) + (r & 3)) * LD];
-        w[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, s[ib][r], w[ob], 0, 0, 0);
-      }
+      for (int r = 0; r < 16; ++r) a[r] = colp[(32 * ib + 8 * (r >> 2) + (r & 3)) * LD];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) w[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[r], s[ib][r], w[ob], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // then the products
+    }
   }
 }
 
+// sigma (deriv = false) or sigma' (deriv = true) of every value, one branch on the
+// activation for the whole array
 template <int Q>
 __device__ __forceinline__ void apply(f32x16 (&z)[Q / 32], int act, bool deriv) {
+  switch (act) {
+    case ACT_TANH:
 #pragma unroll
-  for (int mb = 0; mb < Q / 32; ++mb)
+      for (int mb = 0; mb < Q / 32; ++mb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) z[mb][r] = deriv ? dact_v(z[mb][r], act) : act_v(z[mb][r], act);
+        for (int r = 0; r < 16; ++r) {
+          const float t = tanh_fast(z[mb][r]);
+          z[mb][r] = deriv ? 1.f - t * t : t;
+        }
+      break;
+    case ACT_RELU:
+#pragma unroll
+      for (int mb = 0; mb < Q / 32; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          z[mb][r] = deriv ? (z[mb][r] > 0.f ? 1.f : 0.f) : (z[mb][r] > 0.f ? z[mb][r] : 0.f);
+      break;
+    case ACT_SMOOTHRELU:
+#pragma unroll
+      for (int mb = 0; mb < Q / 32; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          z[mb][r] = deriv ? dact_f<float, ACT_SMOOTHRELU>(z[mb][r]) : act_f<float, ACT_SMOOTHRELU>(z[mb][r]);
+      break;
+    default:
+      if (deriv) {
+#pragma unroll
+        for (int mb = 0; mb < Q / 32; ++mb) z[mb] = 1.f;
+      }
+      break;
+  }
 }
 
 template <int Q>
@@ -617,7 +633,7 @@ hipError_t grad(const GradArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-constexpr int SWEEP_WAVES = 4;   // 128 examples per interval workgroup
+constexpr int SWEEP_WAVES = 4;   // 128 examples per interval workgroup (1 and 2 measured slower at q = 32)
 constexpr int SERIAL_WAVES = 1;  // 32 examples per serial workgroup (more workgroups)
 
 template <int Q>
