@@ -4,9 +4,9 @@
 // Layer operator (Section 2.1, K(theta) a convolution): cross-correlation with
 // zero "same" padding, z[co][y][x] = sum_{ci,ty,tx} K[co][ci][ty][tx] u[ci][y+ty-1][x+tx-1] + b[co].
 //
-// One workgroup owns one example for all steps of an interval; the example's
-// state lives in LDS in zero-padded [C][H+2][W+2] buffers (ping-pong). The image
-// is split into "pair-pixels": pair-pixel P = (Y, x) stands for the two output
+// One workgroup owns one example for all steps of an interval (the sweeps below
+// describe the register and LDS layout). The image is split into
+// "pair-pixels": pair-pixel P = (Y, x) stands for the two output
 // pixels (2Y, x) and (2Y+1, x). A 16 x 16 x 96 product gives the outputs of 16
 // pair-pixels for all (co, dy) in {0..7} x {0,1} (the M = 16 rows), contracting
 // over a 4-row window: k = (ci, r, tx), r = 0..3 the rows 2Y-1 .. 2Y+2. Row dy of
@@ -29,42 +29,14 @@ namespace conv {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int CH = 8;                  // channels
-constexpr int MAXPD = 32;              // padded image side bound (H, W <= 30)
-constexpr int BUF = CH * MAXPD * MAXPD;  // floats per padded state buffer
 constexpr int KW = CH * CH * 9;        // weights per layer
 constexpr int WV = KW + CH;            // weights + bias staged per layer
-constexpr int WAVES = 4;
-constexpr int NT = 64 * WAVES;
-constexpr int MAXT = 8;                // tiles per wave held in registers (NT16 <= WAVES * MAXT)
+constexpr int NT = 256;                // threads of the elementwise kernels
 constexpr int MODE_SERIAL = 3;
-
-struct Geo {
-  int H, W, PW, PHW, HW, q, NPP, NT16;
-  __device__ Geo(int h, int w)
-      : H(h), W(w), PW(w + 2), PHW((h + 2) * (w + 2)), HW(h * w), q(CH * h * w), NPP(h / 2 * w),
-        NT16((h / 2 * w + 15) / 16) {}
-};
 
 __device__ __forceinline__ float tanh_fast(float x) {
   const float t = __builtin_amdgcn_exp2f(-2.885390081777927f * fabsf(x));  // exp(-2|x|)
   return copysignf((1.f - t) * __builtin_amdgcn_rcpf(1.f + t), x);
-}
-
-__device__ __forceinline__ float act_v(float z, int act) {
-  if (act == ACT_TANH) return tanh_fast(z);
-  if (act == ACT_RELU) return z > 0.f ? z : 0.f;
-  if (act == ACT_SMOOTHRELU) return act_f<float, ACT_SMOOTHRELU>(z);
-  return z;
-}
-
-__device__ __forceinline__ float dact_v(float z, int act) {
-  if (act == ACT_TANH) {
-    const float t = tanh_fast(z);
-    return 1.f - t * t;
-  }
-  if (act == ACT_RELU) return z > 0.f ? 1.f : 0.f;
-  if (act == ACT_SMOOTHRELU) return dact_f<float, ACT_SMOOTHRELU>(z);
-  return 1.f;
 }
 
 __device__ __forceinline__ void stage_w(float* sw, const float* __restrict__ K, const float* __restrict__ b,
@@ -74,25 +46,6 @@ __device__ __forceinline__ void stage_w(float* sw, const float* __restrict__ K, 
 
 __device__ __forceinline__ void zero_buf(float* buf, int n, int nt = NT) {
   for (int i = threadIdx.x; i < n; i += nt) buf[i] = 0.f;
-}
-
-// global example row [C][H][W] -> padded LDS interior, optionally corrected:
-// dst = c + (v - c) when v is given (Algorithm 1, steps 4-5).
-__device__ __forceinline__ void row_in(float* buf, const float* __restrict__ c, const float* __restrict__ v,
-                                       const Geo& g) {
-  for (int i = threadIdx.x; i < g.q; i += NT) {
-    const int ch = i / g.HW, rem = i - ch * g.HW, y = rem / g.W, x = rem - y * g.W;
-    float val = c[i];
-    if (v) val = val + (v[i] - val);
-    buf[ch * g.PHW + (y + 1) * g.PW + x + 1] = val;
-  }
-}
-
-__device__ __forceinline__ void row_out(float* __restrict__ dst, const float* buf, const Geo& g) {
-  for (int i = threadIdx.x; i < g.q; i += NT) {
-    const int ch = i / g.HW, rem = i - ch * g.HW, y = rem / g.W, x = rem - y * g.W;
-    dst[i] = buf[ch * g.PHW + (y + 1) * g.PW + x + 1];
-  }
 }
 
 __device__ __forceinline__ void row_copy(float* __restrict__ dst, const float* __restrict__ src, int q, int nt = NT) {
@@ -115,25 +68,6 @@ __device__ __forceinline__ void gather_w(float (&wr)[24], const float* sw, int l
   }
 }
 
-// Lane's pair-pixel in tile t and its LDS patch base.
-struct TileLane {
-  int P;      // pair-pixel (clamped into range)
-  bool valid;
-  int Y, x;
-  int base;   // LDS offset of (ci = lane/16, row 2Y, col x) in padded coordinates
-};
-
-__device__ __forceinline__ TileLane tile_lane(int t, int lane, const Geo& g) {
-  TileLane L;
-  const int P = 16 * t + (lane & 15);
-  L.valid = P < g.NPP;
-  L.P = L.valid ? P : g.NPP - 1;
-  L.Y = L.P / g.W;
-  L.x = L.P - L.Y * g.W;
-  L.base = (lane >> 4) * g.PHW + 2 * L.Y * g.PW + L.x;
-  return L;
-}
-
 // acc += Wbig^T-slices x patches of the buffer for one tile
 __device__ __forceinline__ f32x4 conv_tile(const float (&wr)[24], const float* buf, int base, int cs, int pw,
                                            f32x4 acc) {
@@ -143,21 +77,6 @@ __device__ __forceinline__ f32x4 conv_tile(const float (&wr)[24], const float* b
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wr[s], buf[base + off], acc, 0, 0, 0);
   }
   return acc;
-}
-
-// Output element of accumulator register r for the lane: channel and row.
-__device__ __forceinline__ int out_ch(int lane, int r) { return 2 * (lane >> 4) + (r >> 1); }
-
-__device__ __forceinline__ double wg_sum(double v, double* red) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  double s = 0.0;
-  if (threadIdx.x == 0)
-    for (int w = 0; w < WAVES; ++w) s += red[w];
-  __syncthreads();
-  return s;
 }
 
 // ------------------------------------------------------------------ sweeps
@@ -600,88 +519,76 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
 }
 
 // ------------------------------------------------------------------ residual
-// Workgroup (n, example): forward r = Phi_n(U[n]) - U[n+1]; adjoint
-// r = Phibar_n(Lam[n+1]) - Lam[n]; writes the example's sum of r^2.
+// Workgroup (n, example), with the sweeps' wave and tile layout: forward
+// r = Phi_n(U[n]) - U[n+1]; adjoint r = Phibar_n(Lam[n+1]) - Lam[n]; writes the
+// example's sum of r^2 (fp64, lanes and waves combined in a fixed order).
 template <int DIR>
-__global__ __launch_bounds__(NT) void k_resid(ResidArgs a, int H, int W) {
-  __shared__ float buf[2][BUF];
-  __shared__ float sw[WV];
-  __shared__ double red[WAVES];
-  const Geo g(H, W);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = blockIdx.x, e = blockIdx.y;
-  const size_t slice = (size_t)a.B * g.q;
-  const size_t eo = (size_t)e * g.q;
+__global__ __launch_bounds__(64 * MAXW) void k_resid(ResidArgs a, SGeo g) {
+  extern __shared__ float lds[];
+  float* buf = lds;              // CH * CS: U[n], then (adjoint) s
+  float* sw = lds + CH * g.CS;   // the layer's weights
+  __shared__ double red[MAXW];
+  const int lane = threadIdx.x & 63, t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
+  const int n = blockIdx.x;
+  const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
   const float* U = static_cast<const float*>(a.U);
   const float* Lm = static_cast<const float*>(a.Lam);
   const float h = (float)a.h;
-  zero_buf(&buf[0][0], 2 * BUF);
-  stage_w(sw, static_cast<const float*>(a.K), static_cast<const float*>(a.b), n);
-  __syncthreads();
-  row_in(buf[0], U + (size_t)n * slice + eo, nullptr, g);
-  if (DIR == DIR_ADJ) row_in(buf[1], Lm + (size_t)(n + 1) * slice + eo, nullptr, g);
-  __syncthreads();
-  float wf[24];
-  gather_w<false>(wf, sw, lane);
-  float dd[MAXT][4];
-  double acc2 = 0.0;
+  zero_buf(buf, CH * g.CS, nt);
+  stage_w(sw, static_cast<const float*>(a.K), static_cast<const float*>(a.b), n, nt);
+  f32x4 un[TPW];
 #pragma unroll
-  for (int tt = 0; tt < MAXT; ++tt) {
-    const int t = wave + tt * WAVES;
-    if (t >= g.NT16) break;
-    const TileLane L = tile_lane(t, lane, g);
-    f32x4 acc;
+  for (int tt = 0; tt < TPW; ++tt) un[tt] = ld_px(U + (size_t)n * slice + eo, g, px_of(g, t0 + tt, lane));
+  __syncthreads();  // halo zeroed, weights staged
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] = sw[KW + out_ch(lane, r)];
-    acc = conv_tile(wf, buf[0], L.base, g.PHW, g.PW, acc);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-      const int pos = co * g.PHW + (y + 1) * g.PW + L.x + 1;
-      const int go = co * g.HW + y * g.W + L.x;
-      if (DIR == DIR_FWD) {
-        const float rr = (buf[0][pos] + h * act_v(acc[r], a.act)) - U[(size_t)(n + 1) * slice + eo + go];
-        if (L.valid) acc2 += (double)rr * (double)rr;
-      } else {
-        dd[tt][r] = dact_v(acc[r], a.act) * buf[1][pos];
-      }
-    }
+  for (int tt = 0; tt < TPW; ++tt) {
+    const Px p = px_of(g, t0 + tt, lane);
+    if (p.ok) put_px(buf, un[tt], g, p);
   }
-  if (DIR == DIR_ADJ) {
-    __syncthreads();
+  __syncthreads();
+  f32x4 z[TPW];
+  {
+    float wr[24];
+    gather_w<false>(wr, sw, lane);
+    conv_tiles(z, wr, buf, g, t0, lane, bias_px(sw, lane));
+  }
+  double acc = 0.0;
+  if (DIR == DIR_FWD) {
+    act_tiles<false>(z, a.act);
 #pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      if (!L.valid) continue;
+    for (int tt = 0; tt < TPW; ++tt) {
+      const Px p = px_of(g, t0 + tt, lane);
+      if (!p.ok) continue;
+      const f32x4 rr = (un[tt] + h * z[tt]) - ld_px(U + (size_t)(n + 1) * slice + eo, g, p);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        buf[0][co * g.PHW + (y + 1) * g.PW + L.x + 1] = dd[tt][r];
-      }
+      for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
+    }
+  } else {
+    act_tiles<true>(z, a.act);
+    f32x4 lam[TPW];
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) lam[tt] = ld_px(Lm + (size_t)(n + 1) * slice + eo, g, px_of(g, t0 + tt, lane));
+    __syncthreads();  // every read of U[n] is done
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) put_px(buf, z[tt] * lam[tt], g, p);
     }
     __syncthreads();
     float wt[24];
     gather_w<true>(wt, sw, lane);
+    f32x4 w[TPW];
+    conv_tiles(w, wt, buf, g, t0, lane, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-    for (int tt = 0; tt < MAXT; ++tt) {
-      const int t = wave + tt * WAVES;
-      if (t >= g.NT16) break;
-      const TileLane L = tile_lane(t, lane, g);
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      acc = conv_tile(wt, buf[0], L.base, g.PHW, g.PW, acc);
+    for (int tt = 0; tt < TPW; ++tt) {
+      const Px p = px_of(g, t0 + tt, lane);
+      if (!p.ok) continue;
+      const f32x4 rr = (lam[tt] + h * w[tt]) - ld_px(Lm + (size_t)n * slice + eo, g, p);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int co = out_ch(lane, r), y = 2 * L.Y + (r & 1);
-        const int pos = co * g.PHW + (y + 1) * g.PW + L.x + 1;
-        const int go = co * g.HW + y * g.W + L.x;
-        const float rr = (buf[1][pos] + h * acc[r]) - Lm[(size_t)n * slice + eo + go];
-        if (L.valid) acc2 += (double)rr * (double)rr;
-      }
+      for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
     }
   }
-  const double s = wg_sum(acc2, red);
+  const double s = wg_sum_n(acc, red, g.NW);
   if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
 }
 
@@ -884,11 +791,13 @@ hipError_t launch_conv_sweep(const Shape& s, int dir, const SweepArgs& a, dim3 g
 
 }  // namespace
 
+// fp32, C = 8, even H; at most MAXW waves of TPW tiles, and the gradient's two
+// image buffers within 64 KB of LDS (H, W up to 30 x 30)
 bool conv_supported(const Shape& s) {
-  return s.layer == 1 && s.dtype == 0 && s.C == conv::CH && s.H % 2 == 0 && s.H >= 2 && s.W >= 4 &&
-         s.H + 2 <= conv::MAXPD && s.W + 2 <= conv::MAXPD &&
-         (s.H / 2 * s.W + 15) / 16 <= conv::WAVES * conv::MAXT &&
-         (s.H / 2 * s.W + 15) / 16 <= conv::MAXW * conv::TPW;
+  if (s.layer != 1 || s.dtype != 0 || s.C != conv::CH || s.H < 2 || s.H % 2 || s.W < 1 || s.H > 4096 || s.W > 4096)
+    return false;
+  const conv::SGeo g = sweep_geo(s);
+  return g.NT16 <= conv::MAXW * conv::TPW && (2 * conv::CH * g.CS + conv::WV) * sizeof(float) <= 65536;
 }
 
 int conv_tile(const Shape&) { return 1; }
@@ -925,8 +834,9 @@ hipError_t conv_serial(const Shape& s, int dir, const SerialArgs& sa, hipStream_
 hipError_t conv_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t st, int* partials) {
   const dim3 grid(a.N, a.B);
   if (partials) *partials = (int)(grid.x * grid.y);
-  if (dir == DIR_FWD) launch(conv::k_resid<DIR_FWD>, grid, conv::NT, 0, st, a, s.H, s.W);
-  else launch(conv::k_resid<DIR_ADJ>, grid, conv::NT, 0, st, a, s.H, s.W);
+  const conv::SGeo g = sweep_geo(s);
+  if (dir == DIR_FWD) launch(conv::k_resid<DIR_FWD>, grid, dim3(64 * g.NW), sweep_lds(g), st, a, g);
+  else launch(conv::k_resid<DIR_ADJ>, grid, dim3(64 * g.NW), sweep_lds(g), st, a, g);
   return hipGetLastError();
 }
 
