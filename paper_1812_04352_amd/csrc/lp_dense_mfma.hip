@@ -1,15 +1,13 @@
 // Dense fp32 residual layers of width 32 or 64 on the matrix cores (gfx950
-// v_mfma_f32_32x32x2_f32).
+// v_mfma_f32_16x16x4_f32 for the sweeps and serial solves,
+// v_mfma_f32_32x32x2_f32 for the gradient).
 //
-// One wave owns 32 examples for all steps of an interval. The layer product
-// z = K_n v is a (q x q) x (q x 32) contraction: M = output feature, N = example,
-// K = input feature. Its accumulator layout holds, in register r of block mb,
-// feature 32mb + 8(r/4) + 4(l/32) + (r%4) of example l%32 (lane l). That is also a
-// valid B-operand layout for the next step once the contraction index is
-// permuted the same way in the A operand: k-slice (mb, r) pairs feature
-// f(mb, r, 0) (lanes 0-31) with f(mb, r, 1) (lanes 32-63), so the A operand of
-// lane l is K[row][f(mb, r, l/32)]. Chained steps therefore never move the
-// state between lanes. K_n and b_n are staged in LDS (row-major, padded rows,
+// One wave owns EX examples (16 or 32) for all steps of an interval. The layer
+// product z = K_n v is a (q x q) x (q x EX) contraction: M = output feature,
+// N = example, K = input feature. Its accumulator layout (see Lay below) is also
+// a valid B-operand layout for the next step once the contraction index is
+// permuted the same way in the A operand, so chained steps never move the state
+// between lanes. K_n and b_n are staged in LDS (row-major, padded rows,
 // double-buffered: the next layer is fetched into registers while the current
 // step runs); the bias initialises the accumulators.
 //
@@ -74,154 +72,213 @@ __device__ __forceinline__ void w_put(float* sh, const WRegs<Q, WAVES>& r) {
   if (threadIdx.x < Q / 4) *reinterpret_cast<f32x4*>(sh + Q * C::LD + threadIdx.x * 4) = r.b;
 }
 
-// Row access in accumulator layout: p points at the example's row + 4*(lane/32).
-template <int Q>
-__device__ __forceinline__ void load_c(f32x16 (&v)[Q / 32], const float* __restrict__ p) {
-#pragma unroll
-  for (int mb = 0; mb < Q / 32; ++mb)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const float4 x = *reinterpret_cast<const float4*>(p + 32 * mb + 8 * g);
-      v[mb][4 * g + 0] = x.x;
-      v[mb][4 * g + 1] = x.y;
-      v[mb][4 * g + 2] = x.z;
-      v[mb][4 * g + 3] = x.w;
-    }
-}
+// ------------------------------------------------------------------ layouts
+// Per-lane layout of a wave's examples in the accumulators of the two fp32
+// matrix-core shapes (lane l):
+//   EX = 32, v_mfma_f32_32x32x2_f32: register r of block mb holds feature
+//            32mb + 8(r/4) + 4(l/32) + r%4 of example l%32;
+//   EX = 16, v_mfma_f32_16x16x4_f32: register r of block mb holds feature
+//            16mb + 4(l/16) + r of example l%16.
+// In both, the accumulators are the next product's B operand once the A
+// operand's contraction index is permuted the same way (k-slice (mb, r) takes
+// the feature that register r of block mb holds in each lane group), so chained
+// steps never move state between lanes. A wave of the 16-example shape does half
+// the work per step with half the latency and needs about two thirds of the
+// registers; the sweeps and the serial solve use it, the gradient the other.
+template <int Q, int EX>
+struct Lay;
 
 template <int Q>
-__device__ __forceinline__ void store_c(float* __restrict__ p, const f32x16 (&v)[Q / 32]) {
-#pragma unroll
-  for (int mb = 0; mb < Q / 32; ++mb)
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-      *reinterpret_cast<float4*>(p + 32 * mb + 8 * g) =
-          make_float4(v[mb][4 * g + 0], v[mb][4 * g + 1], v[mb][4 * g + 2], v[mb][4 * g + 3]);
-}
+struct Lay<Q, 32> {
+  using V = f32x16;
+  static constexpr int NB = Q / 32, NV = 16;
 
-template <int Q>
-__device__ __forceinline__ void add_c(f32x16 (&v)[Q / 32], const float* __restrict__ p) {
-  f32x16 t[Q / 32];
-  load_c<Q>(t, p);
+  // p points at the example's row + 4*(lane/32)
+  __device__ static void load(V (&v)[NB], const float* __restrict__ p) {
 #pragma unroll
-  for (int mb = 0; mb < Q / 32; ++mb) v[mb] += t[mb];
-}
-
-template <int Q>
-__device__ __forceinline__ void zero_c(f32x16 (&v)[Q / 32]) {
-#pragma unroll
-  for (int mb = 0; mb < Q / 32; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) v[mb][r] = 0.f;
-}
-
-// z = K_n v + b_n in accumulator layout (W: staged weights; lane = lane id).
-template <int Q, int LD>
-__device__ __forceinline__ void prod(f32x16 (&z)[Q / 32], const f32x16 (&v)[Q / 32], const float* W,
-                                     int lane) {
-  const int h = lane >> 5, i = lane & 31;
-#pragma unroll
-  for (int ob = 0; ob < Q / 32; ++ob) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const float4 bb = *reinterpret_cast<const float4*>(W + Q * LD + 32 * ob + 8 * g + 4 * h);
-      z[ob][4 * g + 0] = bb.x;
-      z[ob][4 * g + 1] = bb.y;
-      z[ob][4 * g + 2] = bb.z;
-      z[ob][4 * g + 3] = bb.w;
-    }
-    const float* rowp = W + (32 * ob + i) * LD + 4 * h;
-#pragma unroll
-    for (int ib = 0; ib < Q / 32; ++ib)
+    for (int mb = 0; mb < NB; ++mb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const float4 a4 = *reinterpret_cast<const float4*>(rowp + 32 * ib + 8 * g);
-        z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, v[ib][4 * g + 0], z[ob], 0, 0, 0);
-        z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, v[ib][4 * g + 1], z[ob], 0, 0, 0);
-        z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, v[ib][4 * g + 2], z[ob], 0, 0, 0);
-        z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, v[ib][4 * g + 3], z[ob], 0, 0, 0);
+        const f32x4 x = *reinterpret_cast<const f32x4*>(p + 32 * mb + 8 * g);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[mb][4 * g + t] = x[t];
       }
   }
-}
 
-// w = K_n^T s in accumulator layout (column reads of the staged K_n).
-template <int Q, int LD>
-__device__ __forceinline__ void prod_t(f32x16 (&w)[Q / 32], const f32x16 (&s)[Q / 32], const float* W,
-                                       int lane) {
-  const int h = lane >> 5, i = lane & 31;
+  __device__ static void store(float* __restrict__ p, const V (&v)[NB]) {
 #pragma unroll
-  for (int ob = 0; ob < Q / 32; ++ob) {
+    for (int mb = 0; mb < NB; ++mb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) w[ob][r] = 0.f;
-    const float* colp = W + 32 * ob + i + 4 * h * LD;
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4*>(p + 32 * mb + 8 * g) =
+            f32x4{v[mb][4 * g + 0], v[mb][4 * g + 1], v[mb][4 * g + 2], v[mb][4 * g + 3]};
+  }
+
+  // z = K_n v + b_n (W: staged weights, row-major with row pitch LD, bias row last)
+  template <int LD>
+  __device__ static void prod(V (&z)[NB], const V (&v)[NB], const float* W, int lane) {
+    const int h = lane >> 5, i = lane & 31;
 #pragma unroll
-    for (int ib = 0; ib < Q / 32; ++ib) {
-      // the block's 16 column values are read before its products start
-      float a[16];
+    for (int ob = 0; ob < NB; ++ob) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) a[r] = colp[(32 * ib + 8 * (r >> 2) + (r & 3)) * LD];
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 bb = *reinterpret_cast<const f32x4*>(W + Q * LD + 32 * ob + 8 * g + 4 * h);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) w[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[r], s[ib][r], w[ob], 0, 0, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // LDS reads
-      __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // then the products
+        for (int t = 0; t < 4; ++t) z[ob][4 * g + t] = bb[t];
+      }
+      const float* rowp = W + (32 * ob + i) * LD + 4 * h;
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 a4 = *reinterpret_cast<const f32x4*>(rowp + 32 * ib + 8 * g);
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            z[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[t], v[ib][4 * g + t], z[ob], 0, 0, 0);
+        }
     }
   }
+
+  // w = K_n^T s (column reads of the staged K_n)
+  template <int LD>
+  __device__ static void prod_t(V (&w)[NB], const V (&s)[NB], const float* W, int lane) {
+    const int h = lane >> 5, i = lane & 31;
+#pragma unroll
+    for (int ob = 0; ob < NB; ++ob) {
+      w[ob] = 0.f;
+      const float* colp = W + 32 * ob + i + 4 * h * LD;
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib) {
+        // the block's 16 column values are read before its products start
+        float a[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) a[r] = colp[(32 * ib + 8 * (r >> 2) + (r & 3)) * LD];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) w[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[r], s[ib][r], w[ob], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // LDS reads
+        __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // then the products
+      }
+    }
+  }
+};
+
+template <int Q>
+struct Lay<Q, 16> {
+  using V = f32x4;
+  static constexpr int NB = Q / 16, NV = 4;
+
+  // p points at the example's row + 4*(lane/16)
+  __device__ static void load(V (&v)[NB], const float* __restrict__ p) {
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) v[mb] = *reinterpret_cast<const f32x4*>(p + 16 * mb);
+  }
+
+  __device__ static void store(float* __restrict__ p, const V (&v)[NB]) {
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) *reinterpret_cast<f32x4*>(p + 16 * mb) = v[mb];
+  }
+
+  // z = K_n v + b_n: A operand of slice (ib, r) in lane l is K[16ob + l%16][16ib + 4(l/16) + r]
+  template <int LD>
+  __device__ static void prod(V (&z)[NB], const V (&v)[NB], const float* W, int lane) {
+    const int g = lane >> 4, i = lane & 15;
+#pragma unroll
+    for (int ob = 0; ob < NB; ++ob) {
+      z[ob] = *reinterpret_cast<const f32x4*>(W + Q * LD + 16 * ob + 4 * g);
+      const float* rowp = W + (16 * ob + i) * LD + 4 * g;
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib) {
+        const f32x4 a4 = *reinterpret_cast<const f32x4*>(rowp + 16 * ib);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) z[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[r], v[ib][r], z[ob], 0, 0, 0);
+      }
+    }
+  }
+
+  // w = K_n^T s: A operand of slice (ib, r) in lane l is K[16ib + 4(l/16) + r][16ob + l%16]
+  template <int LD>
+  __device__ static void prod_t(V (&w)[NB], const V (&s)[NB], const float* W, int lane) {
+    const int g = lane >> 4, i = lane & 15;
+#pragma unroll
+    for (int ob = 0; ob < NB; ++ob) {
+      w[ob] = 0.f;
+      const float* colp = W + 16 * ob + i + 4 * g * LD;
+      float a[NB][4];
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) a[ib][r] = colp[(16 * ib + r) * LD];
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) w[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ib][r], s[ib][r], w[ob], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 4 * NB, 0);  // LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);  // then the products
+    }
+  }
+};
+
+template <typename V, int NB>
+__device__ __forceinline__ void add_to(V (&v)[NB], const V (&t)[NB]) {
+#pragma unroll
+  for (int mb = 0; mb < NB; ++mb) v[mb] += t[mb];
 }
 
 // sigma (deriv = false) or sigma' (deriv = true) of every value, one branch on the
 // activation for the whole array
-template <int Q>
-__device__ __forceinline__ void apply(f32x16 (&z)[Q / 32], int act, bool deriv) {
+template <typename V, int NB, int NV>
+__device__ __forceinline__ void apply(V (&z)[NB], int act, bool deriv) {
   switch (act) {
     case ACT_TANH:
 #pragma unroll
-      for (int mb = 0; mb < Q / 32; ++mb)
+      for (int mb = 0; mb < NB; ++mb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < NV; ++r) {
           const float t = tanh_fast(z[mb][r]);
           z[mb][r] = deriv ? 1.f - t * t : t;
         }
       break;
     case ACT_RELU:
 #pragma unroll
-      for (int mb = 0; mb < Q / 32; ++mb)
+      for (int mb = 0; mb < NB; ++mb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
+        for (int r = 0; r < NV; ++r)
           z[mb][r] = deriv ? (z[mb][r] > 0.f ? 1.f : 0.f) : (z[mb][r] > 0.f ? z[mb][r] : 0.f);
       break;
     case ACT_SMOOTHRELU:
 #pragma unroll
-      for (int mb = 0; mb < Q / 32; ++mb)
+      for (int mb = 0; mb < NB; ++mb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
+        for (int r = 0; r < NV; ++r)
           z[mb][r] = deriv ? dact_f<float, ACT_SMOOTHRELU>(z[mb][r]) : act_f<float, ACT_SMOOTHRELU>(z[mb][r]);
       break;
     default:
       if (deriv) {
 #pragma unroll
-        for (int mb = 0; mb < Q / 32; ++mb) z[mb] = 1.f;
+        for (int mb = 0; mb < NB; ++mb) z[mb] = 1.f;
       }
       break;
   }
 }
 
-template <int Q>
-__device__ __forceinline__ void correct_c(f32x16 (&v)[Q / 32], const float* cs, const float* vs) {
-  f32x16 cv[Q / 32], vv[Q / 32];
-  load_c<Q>(cv, cs);
-  load_c<Q>(vv, vs);
+// v = c + (v' - c) (Algorithm 1, the coarse-grid correction of a C-point)
+template <typename Lt>
+__device__ __forceinline__ void correct(typename Lt::V (&v)[Lt::NB], const float* cs, const float* vs) {
+  typename Lt::V cv[Lt::NB], vv[Lt::NB];
+  Lt::load(cv, cs);
+  Lt::load(vv, vs);
 #pragma unroll
-  for (int mb = 0; mb < Q / 32; ++mb) v[mb] = cv[mb] + (vv[mb] - cv[mb]);
+  for (int mb = 0; mb < Lt::NB; ++mb) v[mb] = cv[mb] + (vv[mb] - cv[mb]);
 }
 
 // Sum of squares of (a - b) over the lane's values, in fp64.
-template <int Q>
-__device__ __forceinline__ double sq_diff(const f32x16 (&a)[Q / 32], const f32x16 (&b)[Q / 32]) {
+template <typename V, int NB, int NV>
+__device__ __forceinline__ double sq_diff(const V (&a)[NB], const V (&b)[NB]) {
   double acc = 0.0;
 #pragma unroll
-  for (int mb = 0; mb < Q / 32; ++mb)
+  for (int mb = 0; mb < NB; ++mb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
+    for (int r = 0; r < NV; ++r) {
       const float d = a[mb][r] - b[mb][r];
       acc += (double)d * (double)d;
     }
@@ -248,19 +305,21 @@ __device__ __forceinline__ double wg_sum(double v, double* red) {
 // has to hold the few intervals in flight (with the interval as the fast index,
 // an XCD received all tiles of every 8th interval and its weights overflowed L2
 // at N = 2048, q = 64).
-template <int Q, int MODE, int WAVES>
+template <int Q, int MODE, int WAVES, int EX>
 __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
   using C = Cfg<Q, WAVES>;
-  constexpr int MB = C::MB;
+  using Lt = Lay<Q, EX>;
+  using V = typename Lt::V;
+  constexpr int NB = Lt::NB, NV = Lt::NV;
   __shared__ float W[2][C::WSZ];
   __shared__ double red[WAVES];
   const int lane = threadIdx.x & 63;
   const int k = blockIdx.y;
   const int Nc = gridDim.y;
-  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * 32 + (lane & 31);
+  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * EX + (lane % EX);
   const bool on = e < a.B;
   const size_t slice = (size_t)a.B * Q;
-  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane >> 5);
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane / EX);
   const float* K = static_cast<const float*>(a.K);
   const float* bb = static_cast<const float*>(a.b);
   float* X = static_cast<float*>(a.X);
@@ -277,76 +336,78 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
   w_put<Q, WAVES>(W[0], wr);
   __syncthreads();
 
-  f32x16 v[MB];
-  zero_c<Q>(v);
+  V v[NB];
+#pragma unroll
+  for (int mb = 0; mb < NB; ++mb) v[mb] = 0.f;
   if (on) {
     if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
       // a pending coarse-grid correction of the previous cycle is applied on the fly
       if (MODE == SWEEP_FC && Vn)
-        correct_c<Q>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
-      else load_c<Q>(v, X + kc * slice + row);
-      if (MODE == SWEEP_FC && k == 0) store_c<Q>(static_cast<float*>(a.S) + row, v);
+        correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+      else Lt::load(v, X + kc * slice + row);
+      if (MODE == SWEEP_FC && k == 0) Lt::store(static_cast<float*>(a.S) + row, v);
     } else if (MODE == SWEEP_FRES) {
-      load_c<Q>(v, Cs + (size_t)k * a.cs_stride * slice + row);
+      Lt::load(v, Cs + (size_t)k * a.cs_stride * slice + row);
     } else {
-      correct_c<Q>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
-      if (k > 0) store_c<Q>(X + kc * slice + row, v);
+      correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+      if (k > 0) Lt::store(X + kc * slice + row, v);
     }
   }
-  f32x16 coarse[MB];
+  V coarse[NB];
   // The serial solve (one wave per workgroup, few workgroups) is latency-bound:
   // it loads the G row of the next step one step ahead (every lane loads a valid
   // row; columns of lanes past the batch are never stored). The sweeps keep the
   // registers for occupancy instead.
   constexpr bool PF = MODE == MODE_SERIAL;
-  f32x16 gn[MB];
-  if (PF && G) load_c<Q>(gn, G + (kc + 1) * slice + row);
+  V gn[NB];
+  if (PF && G) Lt::load(gn, G + (kc + 1) * slice + row);
   for (int j = 0; j < nsteps; ++j) {
     // prefetch the next layer (the last step re-fetches its own: keeps wr in registers)
     w_fetch<Q, WAVES>(wr, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j)) * a.stride);
-    f32x16 gc[MB];
+    V gc[NB];
     if (PF && G) {
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) gc[mb] = gn[mb];
-      if (j + 1 < nsteps) load_c<Q>(gn, G + (kc + j + 2) * slice + row);
+      for (int mb = 0; mb < NB; ++mb) gc[mb] = gn[mb];
+      if (j + 1 < nsteps) Lt::load(gn, G + (kc + j + 2) * slice + row);
     }
-    f32x16 s[MB];
-    prod<Q, C::LD>(s, v, W[j & 1], lane);
-    apply<Q>(s, a.act, false);
+    V s[NB];
+    Lt::template prod<C::LD>(s, v, W[j & 1], lane);
+    apply<V, NB, NV>(s, a.act, false);
     if (MODE == SWEEP_FRES && j == 0) {
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) coarse[mb] = v[mb] + hc * s[mb];
+      for (int mb = 0; mb < NB; ++mb) coarse[mb] = v[mb] + hc * s[mb];
     }
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) v[mb] = v[mb] + hl * s[mb];
-    if (PF && G) {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) v[mb] += gc[mb];
-    }
+    for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * s[mb];
+    if (PF && G) add_to<V, NB>(v, gc);
     if (on) {
-      if (!PF && G) add_c<Q>(v, G + (kc + j + 1) * slice + row);
-      if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) store_c<Q>(X + (kc + j + 1) * slice + row, v);
+      if (!PF && G) {
+        V t[NB];
+        Lt::load(t, G + (kc + j + 1) * slice + row);
+        add_to<V, NB>(v, t);
+      }
+      if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) Lt::store(X + (kc + j + 1) * slice + row, v);
     }
     w_put<Q, WAVES>(W[(j + 1) & 1], wr);
     __syncthreads();
   }
 
   if (MODE == SWEEP_FC) {
-    if (on) store_c<Q>(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
+    if (on) Lt::store(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
   } else if (MODE == SWEEP_FRES) {
     double acc = 0.0;
     if (on) {
-      f32x16 cn[MB];
-      load_c<Q>(cn, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
-      acc = sq_diff<Q>(v, cn);
+      V cn[NB];
+      Lt::load(cn, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
+      acc = sq_diff<V, NB, NV>(v, cn);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) coarse[mb] = v[mb] - coarse[mb];  // g_{l+1}^{k+1}
-      store_c<Q>(static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + row, coarse);
+      for (int mb = 0; mb < NB; ++mb) coarse[mb] = v[mb] - coarse[mb];  // g_{l+1}^{k+1}
+      Lt::store(static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + row, coarse);
       if (a.xn_every > 0 && (k + 1) % a.xn_every == 0)
-        store_c<Q>(static_cast<float*>(a.Xn) + (size_t)(k + 1) * slice + row, cn);
+        Lt::store(static_cast<float*>(a.Xn) + (size_t)(k + 1) * slice + row, cn);
       if (k == 0) {
-        load_c<Q>(cn, Cs + row);
-        store_c<Q>(static_cast<float*>(a.Xn) + row, cn);
+        Lt::load(cn, Cs + row);
+        Lt::store(static_cast<float*>(a.Xn) + row, cn);
       }
     }
     if (a.partial) {
@@ -355,8 +416,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     }
   } else if (MODE == SWEEP_CORRF) {
     if (on && k == Nc - 1) {
-      correct_c<Q>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
-      store_c<Q>(X + (size_t)a.Nl * slice + row, v);
+      correct<Lt>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
+      Lt::store(X + (size_t)a.Nl * slice + row, v);
     }
   }
 }
@@ -364,19 +425,21 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
 // ------------------------------------------------------------------ adjoint
 // Interval k runs from its upper C-point (k+1)c down to kc; step j produces level
 // point i = (k+1)c-1-j, linearised at the fine state of index i*stride.
-template <int Q, int MODE, int WAVES>
+template <int Q, int MODE, int WAVES, int EX>
 __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
   using C = Cfg<Q, WAVES>;
-  constexpr int MB = C::MB;
+  using Lt = Lay<Q, EX>;
+  using V = typename Lt::V;
+  constexpr int NB = Lt::NB, NV = Lt::NV;
   __shared__ float W[2][C::WSZ];
   __shared__ double red[WAVES];
   const int lane = threadIdx.x & 63;
   const int k = blockIdx.y;
   const int Nc = gridDim.y;
-  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * 32 + (lane & 31);
+  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * EX + (lane % EX);
   const bool on = e < a.B;
   const size_t slice = (size_t)a.B * Q;
-  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane >> 5);
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane / EX);
   const float* K = static_cast<const float*>(a.K);
   const float* bb = static_cast<const float*>(a.b);
   const float* Uf = static_cast<const float*>(a.Uf);
@@ -394,100 +457,103 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
   w_put<Q, WAVES>(W[0], wr);
   __syncthreads();
 
-  f32x16 v[MB], cu[MB];
-  zero_c<Q>(v);
+  V v[NB], cu[NB];
+#pragma unroll
+  for (int mb = 0; mb < NB; ++mb) v[mb] = 0.f;
   if (on) {
     if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
       if (MODE == SWEEP_FC && Vn)
-        correct_c<Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
-      else load_c<Q>(v, X + top * slice + row);
-      if (MODE == SWEEP_FC && k == Nc - 1) store_c<Q>(static_cast<float*>(a.S) + (size_t)Nc * slice + row, v);
+        correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
+      else Lt::load(v, X + top * slice + row);
+      if (MODE == SWEEP_FC && k == Nc - 1) Lt::store(static_cast<float*>(a.S) + (size_t)Nc * slice + row, v);
     } else if (MODE == SWEEP_FRES) {
-      load_c<Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
+      Lt::load(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
     } else {
-      correct_c<Q>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
-      if (k + 1 < Nc) store_c<Q>(X + top * slice + row, v);
+      correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
+      if (k + 1 < Nc) Lt::store(X + top * slice + row, v);
     }
   }
   if (MODE == SWEEP_FRES) {
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) cu[mb] = v[mb];
+    for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb];
   }
   // The serial solve loads the next step's primal and G rows one step ahead
   // (every lane loads a valid row; columns of lanes past the batch are never
   // stored); the sweeps keep the registers for occupancy instead.
   constexpr bool PF = MODE == MODE_SERIAL;
-  f32x16 un[MB], gn[MB];
+  V un[NB], gn[NB];
   if (PF) {
-    load_c<Q>(un, Uf + (size_t)(top - 1) * a.stride * slice + row);
-    if (G) load_c<Q>(gn, G + (size_t)(top - 1) * slice + row);
+    Lt::load(un, Uf + (size_t)(top - 1) * a.stride * slice + row);
+    if (G) Lt::load(gn, G + (size_t)(top - 1) * slice + row);
   }
   for (int j = 0; j < nsteps; ++j) {
     const long i = top - 1 - j;
     w_fetch<Q, WAVES>(wr, K, bb, (size_t)(j + 1 < nsteps ? i - 1 : i) * a.stride);
-    f32x16 d[MB], w[MB], gc[MB];
+    V d[NB], w[NB], gc[NB];
     {
-      f32x16 u[MB];
+      V u[NB];
       if (PF) {
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) u[mb] = un[mb];
+        for (int mb = 0; mb < NB; ++mb) u[mb] = un[mb];
         if (G) {
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) gc[mb] = gn[mb];
+          for (int mb = 0; mb < NB; ++mb) gc[mb] = gn[mb];
         }
         if (j + 1 < nsteps) {
-          load_c<Q>(un, Uf + (size_t)(i - 1) * a.stride * slice + row);
-          if (G) load_c<Q>(gn, G + (size_t)(i - 1) * slice + row);
+          Lt::load(un, Uf + (size_t)(i - 1) * a.stride * slice + row);
+          if (G) Lt::load(gn, G + (size_t)(i - 1) * slice + row);
         }
       } else {
-        zero_c<Q>(u);
-        if (on) load_c<Q>(u, Uf + (size_t)i * a.stride * slice + row);
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) u[mb] = 0.f;
+        if (on) Lt::load(u, Uf + (size_t)i * a.stride * slice + row);
       }
-      prod<Q, C::LD>(d, u, W[j & 1], lane);
+      Lt::template prod<C::LD>(d, u, W[j & 1], lane);
     }
-    apply<Q>(d, a.act, true);
+    apply<V, NB, NV>(d, a.act, true);
     if (MODE == SWEEP_FRES && j == nsteps - 1) {
       // coarse adjoint step from the upper C-point, linearised at the same fine state
-      f32x16 s2[MB];
+      V s2[NB];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) s2[mb] = d[mb] * cu[mb];
-      prod_t<Q, C::LD>(w, s2, W[j & 1], lane);
+      for (int mb = 0; mb < NB; ++mb) s2[mb] = d[mb] * cu[mb];
+      Lt::template prod_t<C::LD>(w, s2, W[j & 1], lane);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) cu[mb] = cu[mb] + hc * w[mb];
+      for (int mb = 0; mb < NB; ++mb) cu[mb] = cu[mb] + hc * w[mb];
     }
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) d[mb] = d[mb] * v[mb];
-    prod_t<Q, C::LD>(w, d, W[j & 1], lane);
+    for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * v[mb];
+    Lt::template prod_t<C::LD>(w, d, W[j & 1], lane);
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) v[mb] = v[mb] + hl * w[mb];
-    if (PF && G) {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) v[mb] += gc[mb];
-    }
+    for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * w[mb];
+    if (PF && G) add_to<V, NB>(v, gc);
     if (on) {
-      if (!PF && G) add_c<Q>(v, G + (size_t)i * slice + row);
-      if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) store_c<Q>(X + (size_t)i * slice + row, v);
+      if (!PF && G) {
+        V t[NB];
+        Lt::load(t, G + (size_t)i * slice + row);
+        add_to<V, NB>(v, t);
+      }
+      if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) Lt::store(X + (size_t)i * slice + row, v);
     }
     w_put<Q, WAVES>(W[(j + 1) & 1], wr);
     __syncthreads();
   }
 
   if (MODE == SWEEP_FC) {
-    if (on) store_c<Q>(static_cast<float*>(a.S) + (size_t)k * slice + row, v);
+    if (on) Lt::store(static_cast<float*>(a.S) + (size_t)k * slice + row, v);
   } else if (MODE == SWEEP_FRES) {
     double acc = 0.0;
     if (on) {
-      f32x16 ck[MB];
-      load_c<Q>(ck, Cs + (size_t)k * a.cs_stride * slice + row);
-      acc = sq_diff<Q>(v, ck);
+      V ck[NB];
+      Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
+      acc = sq_diff<V, NB, NV>(v, ck);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) cu[mb] = v[mb] - cu[mb];  // g_{l+1}^k
-      store_c<Q>(static_cast<float*>(a.Gn) + (size_t)k * slice + row, cu);
+      for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb] - cu[mb];  // g_{l+1}^k
+      Lt::store(static_cast<float*>(a.Gn) + (size_t)k * slice + row, cu);
       if (a.xn_every > 0 && k % a.xn_every == 0)
-        store_c<Q>(static_cast<float*>(a.Xn) + (size_t)k * slice + row, ck);
+        Lt::store(static_cast<float*>(a.Xn) + (size_t)k * slice + row, ck);
       if (k == Nc - 1) {
-        load_c<Q>(ck, Cs + (size_t)Nc * a.cs_stride * slice + row);
-        store_c<Q>(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, ck);
+        Lt::load(ck, Cs + (size_t)Nc * a.cs_stride * slice + row);
+        Lt::store(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, ck);
       }
     }
     if (a.partial) {
@@ -496,8 +562,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
     }
   } else if (MODE == SWEEP_CORRF) {
     if (on && k == 0) {
-      correct_c<Q>(v, Cs + row, Vn + row);
-      store_c<Q>(X + row, v);
+      correct<Lt>(v, Cs + row, Vn + row);
+      Lt::store(X + row, v);
     }
   }
 }
@@ -549,17 +615,18 @@ __global__ __launch_bounds__(64 * GRAD_WAVES) void k_grad(GradArgs a) {
     const int e = base + wave * 32 + li;
     const bool on = e < e1;
     const size_t row = (size_t)(on ? e : 0) * Q + 4 * h;
+    using Lt = Lay<Q, 32>;
     f32x16 u[MB], s[MB];
-    zero_c<Q>(u);
-    zero_c<Q>(s);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) u[mb] = s[mb] = 0.f;
     if (on) {
-      load_c<Q>(u, U + row);
-      load_c<Q>(s, L + row);
+      Lt::load(u, U + row);
+      Lt::load(s, L + row);
     }
     {
       f32x16 z[MB];
-      prod<Q, C::LD>(z, u, W, lane);
-      apply<Q>(z, a.act, true);
+      Lt::template prod<C::LD>(z, u, W, lane);
+      apply<f32x16, MB, 16>(z, a.act, true);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) s[mb] = z[mb] * s[mb];
     }
@@ -633,23 +700,29 @@ hipError_t grad(const GradArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-constexpr int SWEEP_WAVES = 4;   // 128 examples per interval workgroup (1 and 2 measured slower at q = 32)
-constexpr int SERIAL_WAVES = 1;  // 32 examples per serial workgroup (more workgroups)
+constexpr int SWEEP_WAVES = 4;   // waves per interval workgroup (1 and 2 measured slower at q = 32)
+constexpr int SERIAL_WAVES = 1;  // one wave per serial workgroup (more workgroups)
+
+// The sweeps run on the 16-example shape: measured faster than the 32-example
+// one on every workload (q = 32 and 64, level 0 included), with fewer registers
+// per wave and twice the waves.
+constexpr int SWEEP_EX = 16;
 
 template <int Q>
 hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
-  constexpr int W4 = SWEEP_WAVES;
-  if (a.Nl / a.c > 65535) return hipErrorNotSupported;  // intervals index the grid's y dimension
-  const dim3 grid((a.B + 32 * W4 - 1) / (32 * W4), a.Nl / a.c);
+  constexpr int W4 = SWEEP_WAVES, EX = SWEEP_EX;
+  const long Nc = a.Nl / a.c;
+  if (Nc > 65535) return hipErrorNotSupported;  // intervals index the grid's y dimension
+  const dim3 grid((a.B + EX * W4 - 1) / (EX * W4), (unsigned)Nc);
   if (partials) *partials = (int)(grid.x * grid.y);
   if (dir == DIR_FWD) {
-    if (a.mode == SWEEP_FC) launch(k_fwd<Q, SWEEP_FC, W4>, grid, 64 * W4, 0, st, a);
-    else if (a.mode == SWEEP_FRES) launch(k_fwd<Q, SWEEP_FRES, W4>, grid, 64 * W4, 0, st, a);
-    else launch(k_fwd<Q, SWEEP_CORRF, W4>, grid, 64 * W4, 0, st, a);
+    if (a.mode == SWEEP_FC) launch(k_fwd<Q, SWEEP_FC, W4, EX>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_fwd<Q, SWEEP_FRES, W4, EX>, grid, 64 * W4, 0, st, a);
+    else launch(k_fwd<Q, SWEEP_CORRF, W4, EX>, grid, 64 * W4, 0, st, a);
   } else {
-    if (a.mode == SWEEP_FC) launch(k_adj<Q, SWEEP_FC, W4>, grid, 64 * W4, 0, st, a);
-    else if (a.mode == SWEEP_FRES) launch(k_adj<Q, SWEEP_FRES, W4>, grid, 64 * W4, 0, st, a);
-    else launch(k_adj<Q, SWEEP_CORRF, W4>, grid, 64 * W4, 0, st, a);
+    if (a.mode == SWEEP_FC) launch(k_adj<Q, SWEEP_FC, W4, EX>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_adj<Q, SWEEP_FRES, W4, EX>, grid, 64 * W4, 0, st, a);
+    else launch(k_adj<Q, SWEEP_CORRF, W4, EX>, grid, 64 * W4, 0, st, a);
   }
   return hipGetLastError();
 }
@@ -670,9 +743,9 @@ hipError_t serial(int dir, const SerialArgs& s, hipStream_t st) {
   a.hl = s.hl;
   a.X = s.X;
   a.G = s.G;
-  const dim3 grid((s.B + 32 * W1 - 1) / (32 * W1), 1);
-  if (dir == DIR_FWD) launch(k_fwd<Q, MODE_SERIAL, W1>, grid, 64 * W1, 0, st, a);
-  else launch(k_adj<Q, MODE_SERIAL, W1>, grid, 64 * W1, 0, st, a);
+  const dim3 grid((s.B + SWEEP_EX * W1 - 1) / (SWEEP_EX * W1), 1);
+  if (dir == DIR_FWD) launch(k_fwd<Q, MODE_SERIAL, W1, SWEEP_EX>, grid, 64 * W1, 0, st, a);
+  else launch(k_adj<Q, MODE_SERIAL, W1, SWEEP_EX>, grid, 64 * W1, 0, st, a);
   return hipGetLastError();
 }
 

@@ -13,7 +13,9 @@ import ctypes
 import os
 from typing import Optional, Sequence, Tuple
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblp.so")
+# the in-tree build; LP_LIBRARY names another build of the same library (e.g. to
+# compare kernel variants under the same tests)
+LIB_PATH = os.environ.get("LP_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblp.so")
 
 LP_ABI_VERSION = 1
 LP_OK, LP_EINVAL, LP_EUNSUPPORTED, LP_EWORKSPACE, LP_EHIP, LP_ENONFINITE = range(6)
