@@ -38,8 +38,8 @@ struct Cfg {
   static constexpr int MB = Q / 32;               // 32-feature blocks
   static constexpr int LD = Q + 4;                // padded LDS row (floats)
   static constexpr int WSZ = (Q + 1) * LD;        // K rows, then the bias row
-  static constexpr int PK = Q * Q / 4 / NT;       // float4s of K_n per thread when staging
-  static_assert(Q * Q / 4 % NT == 0, "K_n must split evenly over the workgroup");
+  static constexpr int PK = (Q * Q / 4 + NT - 1) / NT;  // float4s of K_n per thread when staging
+  static constexpr bool PART = Q * Q / 4 % NT != 0;      // the last float4 slot is not every thread's
 };
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -57,7 +57,10 @@ __device__ __forceinline__ void w_fetch(WRegs<Q, WAVES>& r, const float* __restr
   using C = Cfg<Q, WAVES>;
   const f32x4* Kn = reinterpret_cast<const f32x4*>(K + n * (size_t)(Q * Q));
 #pragma unroll
-  for (int p = 0; p < C::PK; ++p) r.k[p] = Kn[threadIdx.x + p * C::NT];
+  for (int p = 0; p < C::PK; ++p) {
+    const int idx = threadIdx.x + p * C::NT;
+    r.k[p] = (!C::PART || idx < Q * Q / 4) ? Kn[idx] : f32x4{};
+  }
   r.b = threadIdx.x < Q / 4 ? reinterpret_cast<const f32x4*>(b + n * (size_t)Q)[threadIdx.x] : f32x4{};
 }
 
@@ -66,7 +69,9 @@ __device__ __forceinline__ void w_put(float* sh, const WRegs<Q, WAVES>& r) {
   using C = Cfg<Q, WAVES>;
 #pragma unroll
   for (int p = 0; p < C::PK; ++p) {
-    const int el = (threadIdx.x + p * C::NT) * 4, row = el / Q, col = el - row * Q;
+    const int idx = threadIdx.x + p * C::NT;
+    if (C::PART && idx >= Q * Q / 4) continue;
+    const int el = idx * 4, row = el / Q, col = el - row * Q;
     *reinterpret_cast<f32x4*>(sh + row * C::LD + col) = r.k[p];
   }
   if (threadIdx.x < Q / 4) *reinterpret_cast<f32x4*>(sh + Q * C::LD + threadIdx.x * 4) = r.b;
@@ -700,7 +705,7 @@ hipError_t grad(const GradArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-constexpr int SWEEP_WAVES = 4;   // waves per interval workgroup (1 and 2 measured slower at q = 32)
+constexpr int SWEEP_WAVES = 4;   // waves per interval workgroup (2 and 8 measured slower or equal)
 constexpr int SERIAL_WAVES = 1;  // one wave per serial workgroup (more workgroups)
 
 // The sweeps run on the 16-example shape: measured faster than the 32-example
