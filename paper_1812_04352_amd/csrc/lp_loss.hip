@@ -17,40 +17,50 @@ namespace {
 constexpr int NT = 256;
 constexpr int CHUNK = 32;  // examples per partial of dW, dmu (short chains, many workgroups)
 
-// One wave per example: z[e][j] = mu_j + sum_i W[j][i] u[e][i], lanes split i.
+// Head of the network, one segment of S lanes per example (S = the power of two
+// >= nc; lane j of the segment owns class j): the logits z_j = mu_j + W_j . u
+// (each lane sums the features i = j mod S, the segment adds the partials),
+// the softmax and loss_e with segment reductions, d_j = (S_j - c_j)/B, and
+// lam^N = W^T d (each lane takes features i = j mod S). All sums run in fp64 and
+// in a fixed order.
 template <typename T>
-__global__ __launch_bounds__(64) void k_logits(const T* uN, const T* Wc, const T* mu, double* z, int q, int nc) {
-  const int e = blockIdx.x;
-  const int lane = threadIdx.x;
-  const T* u = uN + (size_t)e * q;
-  for (int j = 0; j < nc; ++j) {
-    double acc = 0.0;
-    for (int i = lane; i < q; i += 64) acc += (double)Wc[(size_t)j * q + i] * (double)u[i];
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-    if (lane == 0) z[(size_t)e * nc + j] = acc + (double)mu[j];
+__global__ __launch_bounds__(NT) void k_head(const T* uN, const T* Wc, const T* mu, const T* c, double* d,
+                                             double* loss, T* lamN, int B, int q, int nc, int S) {
+  __shared__ double dsh[NT];
+  const int t = threadIdx.x, j = t & (S - 1), seg = t - j;
+  const int e = blockIdx.x * (NT / S) + t / S;
+  const bool on = e < B;  // uniform over a segment
+  const T* u = uN + (size_t)(on ? e : B - 1) * q;
+  double zj = -INFINITY;
+  for (int jj = 0; jj < nc; ++jj) {
+    double p = 0.0;
+    for (int i = j; i < q; i += S) p += (double)Wc[(size_t)jj * q + i] * (double)u[i];
+    for (int off = S / 2; off > 0; off >>= 1) p += __shfl_xor(p, off, 64);
+    if (j == jj) zj = p + (double)mu[jj];
   }
-}
-
-// Thread per example: softmax, loss_e, and d_e = (S_e - c_e)/B written over z.
-template <typename T>
-__global__ __launch_bounds__(NT) void k_softmax(double* z, const T* c, double* loss, int B, int nc) {
-  const int e = blockIdx.x * NT + threadIdx.x;
-  if (e >= B) return;
-  double* ze = z + (size_t)e * nc;
-  double zmax = -INFINITY;
-  for (int j = 0; j < nc; ++j) zmax = ze[j] > zmax ? ze[j] : zmax;
-  double den = 0.0;
-  for (int j = 0; j < nc; ++j) den += exp(ze[j] - zmax);
+  double m = zj;
+  for (int off = S / 2; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off, 64));
+  const bool cls = j < nc;
+  double den = cls ? exp(zj - m) : 0.0;
+  for (int off = S / 2; off > 0; off >>= 1) den += __shfl_xor(den, off, 64);
   const double lden = log(den);
-  double l = 0.0;
-  for (int j = 0; j < nc; ++j) {
-    const double cj = (double)c[(size_t)e * nc + j];
-    const double logp = (ze[j] - zmax) - lden;
-    l -= cj * logp;
-    ze[j] = (exp(logp) - cj) / (double)B;
+  const double cj = cls && on ? (double)c[(size_t)e * nc + j] : 0.0;
+  const double logp = cls ? (zj - m) - lden : 0.0;
+  double l = cls ? -cj * logp : 0.0;
+  for (int off = S / 2; off > 0; off >>= 1) l += __shfl_xor(l, off, 64);
+  const double dj = cls ? (exp(logp) - cj) / (double)B : 0.0;
+  if (on) {
+    if (cls) d[(size_t)e * nc + j] = dj;
+    if (j == 0) loss[e] = l;
   }
-  loss[e] = l;
+  dsh[t] = dj;
+  __syncthreads();
+  if (!on) return;
+  for (int i = j; i < q; i += S) {
+    double acc = 0.0;
+    for (int jj = 0; jj < nc; ++jj) acc += (double)Wc[(size_t)jj * q + i] * dsh[seg + jj];
+    lamN[(size_t)e * q + i] = (T)acc;
+  }
 }
 
 // J = (1/B) sum_e loss_e, summed in a fixed order by one workgroup.
@@ -99,17 +109,6 @@ __global__ __launch_bounds__(NT) void k_wfinal(const double* part, int nch, T* d
   else dmu[j] = (T)t;
 }
 
-// lamN[e][i] = sum_j W[j][i] d[e][j]
-template <typename T>
-__global__ __launch_bounds__(NT) void k_lam(const T* Wc, const double* d, T* lamN, int B, int q, int nc) {
-  const size_t o = (size_t)blockIdx.x * NT + threadIdx.x;
-  if (o >= (size_t)B * q) return;
-  const size_t e = o / q, i = o - e * q;
-  double acc = 0.0;
-  for (int j = 0; j < nc; ++j) acc += (double)Wc[(size_t)j * q + i] * d[e * nc + j];
-  lamN[o] = (T)acc;
-}
-
 size_t up(size_t x) { return (x + 255) / 256 * 256; }
 
 template <typename T>
@@ -121,12 +120,14 @@ hipError_t loss_t(int B, int q, int nc, const void* uN, const void* Wc, const vo
   double* part = reinterpret_cast<double*>(w + up((size_t)B * nc * 8) + up((size_t)B * 8));
   const int nch = (B + CHUNK - 1) / CHUNK;
   const size_t nw = (size_t)nc * (q + 1);
-  k_logits<T><<<B, 64, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu, z, q, nc);
-  k_softmax<T><<<(B + NT - 1) / NT, NT, 0, st>>>(z, (const T*)c, loss, B, nc);
+  int S = 1;
+  while (S < nc) S *= 2;
+  const int per = NT / S;  // examples per workgroup
+  k_head<T><<<(B + per - 1) / per, NT, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu, (const T*)c, z, loss,
+                                                (T*)lamN, B, q, nc, S);
   k_mean<<<1, NT_MEAN, 0, st>>>(loss, B, J);
   k_wpart<T><<<dim3(nch, (unsigned)((nw + NT - 1) / NT)), NT, 0, st>>>((const T*)uN, z, part, B, q, nc);
   k_wfinal<T><<<(unsigned)((nw + FO - 1) / FO), NT, 0, st>>>(part, nch, (T*)dW, (T*)dmu, q, nc);
-  k_lam<T><<<(unsigned)(((size_t)B * q + NT - 1) / NT), NT, 0, st>>>((const T*)Wc, z, (T*)lamN, B, q, nc);
   return hipGetLastError();
 }
 
