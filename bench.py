@@ -43,7 +43,14 @@ def level_sizes(N, cf, max_levels, min_coarse):
     return sizes
 
 
-def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int):
+def record_bytes(wl) -> int:
+    """Bytes per value of the sigma' record the step keeps (0: none is kept)."""
+    if wl.layer != "dense" or wl.dtype != "f32" or wl.act == "identity" or wl.q not in (32, 64):
+        return 0
+    return 1 if wl.act == "relu" else 4
+
+
+def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
     """Algorithmic HBM bytes and flops of every launch of one kernel kind in one
     step (summed over MGRIT levels and iterations), and the launch count.
 
@@ -55,8 +62,13 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int):
       adjoint:   the same, plus one primal row per step, 4q^2 flops per step,
                  and one extra transposed product (2q^2) in FRES for the coarse step
       coarsest:  read 1 + N_L G rows (+ N_L primal rows), write N_L rows
-      gradient:  per layer read U[n] and Lam[n+1], write dK, db;      4q^2 per layer
-    Each launch also reads the weights of its level once: N_l (q^2 + q) values."""
+      gradient:  per layer read U[n], Lam[n+1] and K_n, write dK, db;  4q^2 per layer
+    Each launch also reads the weights of its level once: N_l (q^2 + q) values.
+    With a sigma' record of rec bytes per value (rrow per example row), the
+    adjoint reads one record row per step instead of a primal row and skips the
+    forward product (2q^2 flops per step), the gradient (width 64) reads the
+    record instead of K_n and takes no forward product, and the final finest CORRF writes c
+    record rows per interval and takes one more product."""
     q, B, c = wl.q, wl.B, wl.cf
     e = 4 if wl.dtype == "f32" else 8
     row = B * q * e
@@ -68,10 +80,15 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int):
     # multiply-adds of one layer product K v per example: q^2 dense, 9 C^2 H W conv
     mac = q * q if wl.layer == "dense" else 9 * wl.C * wl.C * wl.H * wl.W
     nweights = (q * q + q) if wl.layer == "dense" else (9 * wl.C * wl.C + wl.C)
-    fstep = (4 if adj else 2) * mac
+    rrow = B * q * rec
+    # the adjoint's per-step traffic in primal rows, and its flops per step
+    arow = (rrow / row) if rec else 1.0
+    fstep = (2 if adj and rec else 4 if adj else 2) * mac
     byts = flops = launches = 0
     if kind == "gradient":
-        return 2 * wl.N * row + wl.N * nweights * e, 4.0 * mac * B * wl.N, 1
+        if rec and q >= 64:  # the width-32 kernel recomputes sigma'
+            return 2 * wl.N * row + wl.N * rrow + wl.N * nweights * e, 2.0 * mac * B * wl.N, 1
+        return 2 * wl.N * row + 2 * wl.N * nweights * e, 4.0 * mac * B * wl.N, 1
     # With FCF the finest level's correction is applied inside the next cycle's FC
     # sweep (one more row read per interval from the second cycle on) and its
     # correction + F-relaxation sweep runs once per solve.
@@ -81,7 +98,7 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int):
             g = 1 if l >= 1 else 0
             if l == L - 1:
                 if kind.endswith("coarsest"):
-                    byts += (1 + g * Nl + Nl + (Nl if adj else 0)) * row + wbytes
+                    byts += (1 + g * Nl + Nl + (Nl * arow if adj else 0)) * row + wbytes
                     flops += Nl * fstep * B
                     launches += 1
                 continue
@@ -89,16 +106,20 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int):
             xn = (1.0 / c) if (l + 1 < L - 1) else 0.0
             deferred = l == 0 and fcf
             if kind.endswith("_fc") and fcf:
-                byts += Nc * (2 + g * c + (c if adj else 0) + (1 if deferred and m > 0 else 0)) * row + wbytes
+                byts += Nc * (2 + g * c + (c * arow if adj else 0) + (1 if deferred and m > 0 else 0)) * row + wbytes
                 flops += Nc * c * fstep * B
                 launches += 1
             elif kind.endswith("_fres"):
-                byts += Nc * (3 + xn + g * c + (c if adj else 0)) * row + wbytes
+                byts += Nc * (3 + xn + g * c + (c * arow if adj else 0)) * row + wbytes
                 flops += Nc * (c * fstep + (2 * mac if adj else 0)) * B
                 launches += 1
             elif kind.endswith("_corrf") and (not deferred or m == iters - 1):
-                byts += Nc * (2 + c + g * (c - 1) + ((c - 1) if adj else 0)) * row + wbytes
+                byts += Nc * (2 + c + g * (c - 1) + ((c - 1) * arow if adj else 0)) * row + wbytes
                 flops += Nc * (c - 1) * fstep * B
+                if rec and not adj and l == 0:
+                    # the final finest sweep keeps the record of all c layers
+                    byts += Nc * c * rrow
+                    flops += Nc * 2 * mac * B
                 launches += 1
     return byts, flops, launches
 
@@ -251,6 +272,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default: the second workload)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-record", action="store_true",
+                    help="let the adjoint and the gradient recompute sigma' instead of reading the record")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (to scale HBM byte counters)")
@@ -320,13 +343,16 @@ def main():
     mgA = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, adj_iters)
     ws = L.alloc_workspace(p, mgF if fwd_iters >= adj_iters else mgA)
     hist = {}
+    # the forward's final sweep keeps sigma'(z) for the adjoint and the gradient
+    rec_e = 0 if args.no_record else record_bytes(wl)
+    rec = L.alloc_dsig(p) if rec_e else None
 
     def step(history=False):
         # the residual histories are read back (a host round trip) only when asked
-        _, hf = L.lp_mgrit_forward(p, mgF, K, b, U, ws, history=history)
+        _, hf = L.lp_mgrit_forward(p, mgF, K, b, U, ws, history=history, dsig=rec)
         L.lp_loss_terminal(p, wl.n_classes, U[-1], W, mu, c, J, Lam[-1], dW, dmu, ws)
-        _, ha = L.lp_mgrit_adjoint(p, mgA, K, b, U, Lam, ws, history=history)
-        L.lp_gradient(p, K, b, U, Lam, dK, db, ws)
+        _, ha = L.lp_mgrit_adjoint(p, mgA, K, b, U, Lam, ws, history=history, dsig=rec)
+        L.lp_gradient(p, K, b, U, Lam, dK, db, ws, dsig=rec)
         if history:
             hist["fwd"], hist["adj"] = hf, ha
 
@@ -366,7 +392,7 @@ def main():
     value = wl.N * wl.B * pairs / (ms_step / 1000.0)
 
     # roofline of the dominant kernel
-    byts, flops, launches = kernel_model(wl, dominant, fwd_iters, adj_iters)
+    byts, flops, launches = kernel_model(wl, dominant, fwd_iters, adj_iters, rec_e)
     assert nl == launches * args.steps, (dominant, nl, launches, args.steps)
     avg_ms = kms / nl
     intensity = flops / byts
@@ -415,6 +441,7 @@ def main():
                    "activation": wl.act, "mgrit": {"cf": wl.cf, "levels": len(level_sizes(
                        wl.N, wl.cf, wl.max_levels, wl.min_coarse)), "relax": wl.relax,
                        "fwd_iters": fwd_iters, "adj_iters": adj_iters},
+                   "sigma_record": {0: None, 1: "u8", 4: "f32"}[rec_e],
                    "step": "MGRIT forward iterations + loss + MGRIT adjoint iterations + gradient"},
         "roofline": roof,
         "kernel_ms_per_step": {k: v for k, v in sorted(per_kind.items(), key=lambda t: -t[1])},

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LP_ABI_VERSION 1
+#define LP_ABI_VERSION 2
 
 typedef enum {
   LP_OK = 0,
@@ -107,19 +107,36 @@ const char* lp_last_error(void);
  * per-workgroup residual partials (fp64) and per-chunk gradient partials. */
 size_t lp_workspace_bytes(const lp_problem* prob, const lp_mgrit* mg);
 
+/* Record of the activation derivative along a forward trajectory (optional in
+ * every call that takes `dsig`): sigma'(K_n U[n] + b_n) for n = 0..N-1, the
+ * factor the adjoint steps and the gradient apply (Section 3.2, Section 2.3).
+ * Layout [N][B][q] in the problem's element order, one value per element: a
+ * byte 0 or 1 for LP_RELU, the problem dtype for LP_TANH and LP_SMOOTHRELU; no
+ * storage for LP_IDENTITY (sigma' = 1). A forward call given `dsig` writes the
+ * record of the trajectory it returns; an adjoint or gradient call given `dsig`
+ * uses it instead of recomputing K_n U[n] + b_n from U (saving one layer
+ * product per step), so it must hold the record of the U and the weights that
+ * call receives. NULL: not written / recomputed from U.
+ * Returns the record's size in bytes, or 0 where the kernels for this problem
+ * keep none: an invalid problem, LP_IDENTITY, and every problem outside the
+ * fp32 dense matrix-core widths (32 and 64), including fp64 and 3x3
+ * convolutions. Where it returns 0 every call ignores `dsig`. */
+size_t lp_dsig_bytes(const lp_problem* prob);
+
 /* Layer-serial forward propagation (Section 2.3, state equations; the baseline
  * method): U[n+1] = Phi(U[n], theta^n) for n = 0..N-1.
- * U [N+1][B][q]: row 0 is read (u^0 = L_in y), rows 1..N are written. */
+ * U [N+1][B][q]: row 0 is read (u^0 = L_in y), rows 1..N are written.
+ * dsig (nullable): the trajectory's sigma' record is written. */
 int32_t lp_serial_forward(const lp_problem* prob, const void* K, const void* b, void* U,
-                          void* stream);
+                          void* dsig, void* stream);
 
 /* Layer-serial adjoint propagation (Section 2.3, adjoint equations; this is
  * backpropagation): Lam[n] = (d_u Phi(U[n], theta^n))^T Lam[n+1]
  *                          = Lam[n+1] + h K_n^T (sigma'(K_n U[n] + b_n) * Lam[n+1]),
  * n = N-1..0. Lam row N is read (terminal value), rows 0..N-1 are written.
- * U is read only. */
+ * U is read only. dsig (nullable): the sigma' record of U. */
 int32_t lp_serial_adjoint(const lp_problem* prob, const void* K, const void* b, const void* U,
-                          void* Lam, void* stream);
+                          const void* dsig, void* Lam, void* stream);
 
 /* MGRIT solve of the state equations A(U, theta) = G (Section 3.1, the
  * space-time system and Algorithm 1 with FAS).
@@ -135,10 +152,13 @@ int32_t lp_serial_adjoint(const lp_problem* prob, const void* K, const void* b, 
  * With rtol = stag = 0 the call runs max_iter V-cycles; if res_hist is then
  * NULL it reads nothing back and returns without waiting for the stream (and
  * without checking the norms for non-finite values). A stopping rule makes the
- * call read rho_m after every V-cycle. */
+ * call read rho_m after every V-cycle.
+ * dsig (nullable): the sigma' record of the returned iterate is written (by the
+ * final F-relaxation, which then also takes the product of the layer before each
+ * C-point). */
 int32_t lp_mgrit_forward(const lp_problem* prob, const lp_mgrit* mg, const void* K,
-                         const void* b, void* U, void* ws, size_t ws_bytes, double* res_hist,
-                         int32_t* iters, void* stream);
+                         const void* b, void* U, void* dsig, void* ws, size_t ws_bytes,
+                         double* res_hist, int32_t* iters, void* stream);
 
 /* MGRIT solve of the adjoint equations (Section 3.2, the adjoint space-time
  * system), linearised at the trajectory U (read only).
@@ -146,10 +166,12 @@ int32_t lp_mgrit_forward(const lp_problem* prob, const lp_mgrit* mg, const void*
  * warm_start the other rows are the initial guess (rows at multiples of cf are
  * read), else ignored; on return they hold the iterate. Coarse levels take the
  * adjoint step of size cf^l h linearised at the injected fine state U[i cf^l].
- * res_hist, iters as for lp_mgrit_forward, on the adjoint residual. */
+ * res_hist, iters as for lp_mgrit_forward, on the adjoint residual.
+ * dsig (nullable): the sigma' record of U; every level then reads sigma' of the
+ * injected fine state from it. */
 int32_t lp_mgrit_adjoint(const lp_problem* prob, const lp_mgrit* mg, const void* K,
-                         const void* b, const void* U, void* Lam, void* ws, size_t ws_bytes,
-                         double* res_hist, int32_t* iters, void* stream);
+                         const void* b, const void* U, const void* dsig, void* Lam, void* ws,
+                         size_t ws_bytes, double* res_hist, int32_t* iters, void* stream);
 
 /* Reduced gradient with respect to the layer weights (Section 2.3, design
  * equations, without regularisation):
@@ -158,9 +180,13 @@ int32_t lp_mgrit_adjoint(const lp_problem* prob, const lp_mgrit* mg, const void*
  *   db[n] = h sum_k s_k^n             (conv: summed over pixels per channel)
  * summed over the batch in a fixed order (bitwise reproducible).
  * dK like K, db like b; both written. The 1/B factor of the mean loss is
- * expected inside Lam (it is part of the terminal value). */
+ * expected inside Lam (it is part of the terminal value). dsig (nullable): the
+ * sigma' record of U; the width-32 kernel recomputes sigma' even when given one
+ * (there the extra record read costs more HBM time than the product it saves),
+ * with results equal to rounding. */
 int32_t lp_gradient(const lp_problem* prob, const void* K, const void* b, const void* U,
-                    const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes, void* stream);
+                    const void* dsig, const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes,
+                    void* stream);
 
 /* Full-grid residual norm (fp64, host result; the stopping quantity ||G - A(U)||):
  *   which = LP_STATE:   (sum_{n=1..N} ||Phi(U[n-1], theta^{n-1}) - U[n]||^2)^{1/2}

@@ -119,6 +119,18 @@ struct Lay<Q, 32> {
             f32x4{v[mb][4 * g + 0], v[mb][4 * g + 1], v[mb][4 * g + 2], v[mb][4 * g + 3]};
   }
 
+  // sigma' record of ReLU (one byte per element, 0 or 1), p at the element offset
+  __device__ static void load_mask(V (&v)[NB], const uint8_t* __restrict__ p) {
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(p + 32 * mb + 8 * g);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[mb][4 * g + t] = (w >> (8 * t)) & 0xffu ? 1.f : 0.f;
+      }
+  }
+
   // z = K_n v + b_n (W: staged weights, row-major with row pitch LD, bias row last)
   template <int LD>
   __device__ static void prod(V (&z)[NB], const V (&v)[NB], const float* W, int lane) {
@@ -181,6 +193,26 @@ struct Lay<Q, 16> {
   __device__ static void store(float* __restrict__ p, const V (&v)[NB]) {
 #pragma unroll
     for (int mb = 0; mb < NB; ++mb) *reinterpret_cast<f32x4*>(p + 16 * mb) = v[mb];
+  }
+
+  // sigma' record of ReLU (one byte per element, 0 or 1), p at the element offset
+  __device__ static void load_mask(V (&v)[NB], const uint8_t* __restrict__ p) {
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) {
+      const uint32_t w = *reinterpret_cast<const uint32_t*>(p + 16 * mb);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[mb][r] = (w >> (8 * r)) & 0xffu ? 1.f : 0.f;
+    }
+  }
+
+  __device__ static void store_mask(uint8_t* __restrict__ p, const V (&v)[NB]) {
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) {
+      uint32_t w = 0;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) w |= (v[mb][r] != 0.f ? 1u : 0u) << (8 * r);
+      *reinterpret_cast<uint32_t*>(p + 16 * mb) = w;
+    }
   }
 
   // z = K_n v + b_n: A operand of slice (ib, r) in lane l is K[16ob + l%16][16ib + 4(l/16) + r]
@@ -290,6 +322,19 @@ __device__ __forceinline__ double sq_diff(const V (&a)[NB], const V (&b)[NB]) {
   return acc;
 }
 
+// The sigma' record at element offset off: bytes for ReLU, fp32 otherwise.
+template <typename Lt>
+__device__ __forceinline__ void load_dsig(typename Lt::V (&d)[Lt::NB], const void* rec, size_t off, int act) {
+  if (act == ACT_RELU) Lt::load_mask(d, static_cast<const uint8_t*>(rec) + off);
+  else Lt::load(d, static_cast<const float*>(rec) + off);
+}
+
+template <typename Lt>
+__device__ __forceinline__ void store_dsig(void* rec, size_t off, int act, const typename Lt::V (&d)[Lt::NB]) {
+  if (act == ACT_RELU) Lt::store_mask(static_cast<uint8_t*>(rec) + off, d);
+  else Lt::store(static_cast<float*>(rec) + off, d);
+}
+
 // Fixed-order workgroup sum of one double per lane; result in thread 0.
 template <int WAVES>
 __device__ __forceinline__ double wg_sum(double v, double* red) {
@@ -310,7 +355,7 @@ __device__ __forceinline__ double wg_sum(double v, double* red) {
 // has to hold the few intervals in flight (with the interval as the fast index,
 // an XCD received all tiles of every 8th interval and its weights overflowed L2
 // at N = 2048, q = 64).
-template <int Q, int MODE, int WAVES, int EX>
+template <int Q, int MODE, int WAVES, int EX, bool REC>
 __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
   using C = Cfg<Q, WAVES>;
   using Lt = Lay<Q, EX>;
@@ -364,11 +409,15 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
   // row; columns of lanes past the batch are never stored). The sweeps keep the
   // registers for occupancy instead.
   constexpr bool PF = MODE == MODE_SERIAL;
+  // the final F-relaxation (and a level-0 serial solve) records sigma'(z) of every
+  // layer; CORRF then also takes the product of the layer before the next C-point
+  constexpr bool rec = REC && (MODE == SWEEP_CORRF || MODE == MODE_SERIAL);
+  constexpr int extra = MODE == SWEEP_CORRF && rec ? 1 : 0;
   V gn[NB];
   if (PF && G) Lt::load(gn, G + (kc + 1) * slice + row);
   for (int j = 0; j < nsteps; ++j) {
-    // prefetch the next layer (the last step re-fetches its own: keeps wr in registers)
-    w_fetch<Q, WAVES>(wr, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j)) * a.stride);
+    // prefetch the next layer (the last step re-fetches its own, or the extra one)
+    w_fetch<Q, WAVES>(wr, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j + extra)) * a.stride);
     V gc[NB];
     if (PF && G) {
 #pragma unroll
@@ -377,6 +426,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     }
     V s[NB];
     Lt::template prod<C::LD>(s, v, W[j & 1], lane);
+    if constexpr (rec) {
+      V dz[NB];
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) dz[mb] = s[mb];
+      apply<V, NB, NV>(dz, a.act, true);
+      if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + j) * a.stride * slice + row, a.act, dz);
+    }
     apply<V, NB, NV>(s, a.act, false);
     if (MODE == SWEEP_FRES && j == 0) {
 #pragma unroll
@@ -397,6 +453,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     __syncthreads();
   }
 
+  if constexpr (extra != 0) {
+    // sigma' of the layer before the next C-point, from the last F-point
+    V z[NB];
+    Lt::template prod<C::LD>(z, v, W[nsteps & 1], lane);
+    apply<V, NB, NV>(z, a.act, true);
+    if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + nsteps) * a.stride * slice + row, a.act, z);
+  }
   if (MODE == SWEEP_FC) {
     if (on) Lt::store(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
   } else if (MODE == SWEEP_FRES) {
@@ -430,7 +493,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
 // ------------------------------------------------------------------ adjoint
 // Interval k runs from its upper C-point (k+1)c down to kc; step j produces level
 // point i = (k+1)c-1-j, linearised at the fine state of index i*stride.
-template <int Q, int MODE, int WAVES, int EX>
+template <int Q, int MODE, int WAVES, int EX, bool REC>
 __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
   using C = Cfg<Q, WAVES>;
   using Lt = Lay<Q, EX>;
@@ -486,36 +549,38 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
   // (every lane loads a valid row; columns of lanes past the batch are never
   // stored); the sweeps keep the registers for occupancy instead.
   constexpr bool PF = MODE == MODE_SERIAL;
+  constexpr bool rec = REC;  // sigma' from the record instead of K u + b
   V un[NB], gn[NB];
   if (PF) {
-    Lt::load(un, Uf + (size_t)(top - 1) * a.stride * slice + row);
+    if (!rec) Lt::load(un, Uf + (size_t)(top - 1) * a.stride * slice + row);
     if (G) Lt::load(gn, G + (size_t)(top - 1) * slice + row);
   }
   for (int j = 0; j < nsteps; ++j) {
     const long i = top - 1 - j;
     w_fetch<Q, WAVES>(wr, K, bb, (size_t)(j + 1 < nsteps ? i - 1 : i) * a.stride);
     V d[NB], w[NB], gc[NB];
-    {
+    if (PF && G) {
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) gc[mb] = gn[mb];
+      if (j + 1 < nsteps) Lt::load(gn, G + (size_t)(i - 1) * slice + row);
+    }
+    if constexpr (rec) {
+      // every lane reads a valid row; columns of lanes past the batch are never stored
+      load_dsig<Lt>(d, a.dsig, (size_t)i * a.stride * slice + row, a.act);
+    } else {
       V u[NB];
       if (PF) {
 #pragma unroll
         for (int mb = 0; mb < NB; ++mb) u[mb] = un[mb];
-        if (G) {
-#pragma unroll
-          for (int mb = 0; mb < NB; ++mb) gc[mb] = gn[mb];
-        }
-        if (j + 1 < nsteps) {
-          Lt::load(un, Uf + (size_t)(i - 1) * a.stride * slice + row);
-          if (G) Lt::load(gn, G + (size_t)(i - 1) * slice + row);
-        }
+        if (j + 1 < nsteps) Lt::load(un, Uf + (size_t)(i - 1) * a.stride * slice + row);
       } else {
 #pragma unroll
         for (int mb = 0; mb < NB; ++mb) u[mb] = 0.f;
         if (on) Lt::load(u, Uf + (size_t)i * a.stride * slice + row);
       }
       Lt::template prod<C::LD>(d, u, W[j & 1], lane);
+      apply<V, NB, NV>(d, a.act, true);
     }
-    apply<V, NB, NV>(d, a.act, true);
     if (MODE == SWEEP_FRES && j == nsteps - 1) {
       // coarse adjoint step from the upper C-point, linearised at the same fine state
       V s2[NB];
@@ -584,7 +649,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
 // scales by h (deterministic).
 constexpr int GRAD_WAVES = 4;
 
-template <int Q>
+template <int Q, bool REC>
 __global__ __launch_bounds__(64 * GRAD_WAVES) void k_grad(GradArgs a) {
   using C = Cfg<Q, GRAD_WAVES>;
   constexpr int MB = C::MB;
@@ -630,8 +695,12 @@ __global__ __launch_bounds__(64 * GRAD_WAVES) void k_grad(GradArgs a) {
     }
     {
       f32x16 z[MB];
-      Lt::template prod<C::LD>(z, u, W, lane);
-      apply<f32x16, MB, 16>(z, a.act, true);
+      if constexpr (REC) {
+        load_dsig<Lt>(z, a.dsig, (size_t)n * slice + row, a.act);
+      } else {
+        Lt::template prod<C::LD>(z, u, W, lane);
+        apply<f32x16, MB, 16>(z, a.act, true);
+      }
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) s[mb] = z[mb] * s[mb];
     }
@@ -697,7 +766,11 @@ __global__ __launch_bounds__(256) void k_grad_final(GradArgs a, int nw, int nbia
 
 template <int Q>
 hipError_t grad(const GradArgs& a, hipStream_t st) {
-  launch(k_grad<Q>, dim3(a.N, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
+  // at width 32 the kernel is HBM-bound and a third row read per layer costs more
+  // than the forward product it replaces
+  constexpr bool REC_OK = Q >= 64;
+  if (REC_OK && a.dsig) launch(k_grad<Q, REC_OK>, dim3(a.N, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
+  else launch(k_grad<Q, false>, dim3(a.N, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t tot = (size_t)a.N * (Q * Q + Q);
@@ -720,14 +793,21 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   if (Nc > 65535) return hipErrorNotSupported;  // intervals index the grid's y dimension
   const dim3 grid((a.B + EX * W4 - 1) / (EX * W4), (unsigned)Nc);
   if (partials) *partials = (int)(grid.x * grid.y);
+  const bool rec = a.dsig != nullptr;
   if (dir == DIR_FWD) {
-    if (a.mode == SWEEP_FC) launch(k_fwd<Q, SWEEP_FC, W4, EX>, grid, 64 * W4, 0, st, a);
-    else if (a.mode == SWEEP_FRES) launch(k_fwd<Q, SWEEP_FRES, W4, EX>, grid, 64 * W4, 0, st, a);
-    else launch(k_fwd<Q, SWEEP_CORRF, W4, EX>, grid, 64 * W4, 0, st, a);
+    // only the final F-relaxation writes the sigma' record
+    if (a.mode == SWEEP_FC) launch(k_fwd<Q, SWEEP_FC, W4, EX, false>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_fwd<Q, SWEEP_FRES, W4, EX, false>, grid, 64 * W4, 0, st, a);
+    else if (rec) launch(k_fwd<Q, SWEEP_CORRF, W4, EX, true>, grid, 64 * W4, 0, st, a);
+    else launch(k_fwd<Q, SWEEP_CORRF, W4, EX, false>, grid, 64 * W4, 0, st, a);
+  } else if (rec) {
+    if (a.mode == SWEEP_FC) launch(k_adj<Q, SWEEP_FC, W4, EX, true>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_adj<Q, SWEEP_FRES, W4, EX, true>, grid, 64 * W4, 0, st, a);
+    else launch(k_adj<Q, SWEEP_CORRF, W4, EX, true>, grid, 64 * W4, 0, st, a);
   } else {
-    if (a.mode == SWEEP_FC) launch(k_adj<Q, SWEEP_FC, W4, EX>, grid, 64 * W4, 0, st, a);
-    else if (a.mode == SWEEP_FRES) launch(k_adj<Q, SWEEP_FRES, W4, EX>, grid, 64 * W4, 0, st, a);
-    else launch(k_adj<Q, SWEEP_CORRF, W4, EX>, grid, 64 * W4, 0, st, a);
+    if (a.mode == SWEEP_FC) launch(k_adj<Q, SWEEP_FC, W4, EX, false>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_adj<Q, SWEEP_FRES, W4, EX, false>, grid, 64 * W4, 0, st, a);
+    else launch(k_adj<Q, SWEEP_CORRF, W4, EX, false>, grid, 64 * W4, 0, st, a);
   }
   return hipGetLastError();
 }
@@ -748,9 +828,16 @@ hipError_t serial(int dir, const SerialArgs& s, hipStream_t st) {
   a.hl = s.hl;
   a.X = s.X;
   a.G = s.G;
+  a.dsig = s.dsig;
   const dim3 grid((s.B + SWEEP_EX * W1 - 1) / (SWEEP_EX * W1), 1);
-  if (dir == DIR_FWD) launch(k_fwd<Q, MODE_SERIAL, W1, SWEEP_EX>, grid, 64 * W1, 0, st, a);
-  else launch(k_adj<Q, MODE_SERIAL, W1, SWEEP_EX>, grid, 64 * W1, 0, st, a);
+  constexpr int EX = SWEEP_EX;
+  if (dir == DIR_FWD) {
+    if (s.dsig) launch(k_fwd<Q, MODE_SERIAL, W1, EX, true>, grid, 64 * W1, 0, st, a);
+    else launch(k_fwd<Q, MODE_SERIAL, W1, EX, false>, grid, 64 * W1, 0, st, a);
+  } else {
+    if (s.dsig) launch(k_adj<Q, MODE_SERIAL, W1, EX, true>, grid, 64 * W1, 0, st, a);
+    else launch(k_adj<Q, MODE_SERIAL, W1, EX, false>, grid, 64 * W1, 0, st, a);
+  }
   return hipGetLastError();
 }
 

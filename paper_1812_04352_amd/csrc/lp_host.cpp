@@ -230,6 +230,7 @@ struct Solver {
   const void* K;
   const void* b;
   const void* Uf;  // fine primal trajectory (adjoint)
+  void* dsig = nullptr;  // sigma' record (written by the forward's final level-0 F-relaxation, read by the adjoint)
   std::vector<int> sizes;
   std::vector<void*> X, G, S;
   void* S0[2] = {nullptr, nullptr};  // finest-level staging buffers (FCF), used alternately
@@ -250,7 +251,8 @@ struct Solver {
     const double hl = p->h * (double)stride(l);
     const int kb = dir == lp::DIR_FWD ? LP_TRACE_FWD_FC : LP_TRACE_ADJ_FC;  // first kind of this direction
     if (l == L - 1) {
-      lp::SerialArgs a{p->act, K, b, Uf, p->B, sizes[l], stride(l), hl, X[l], G[l]};
+      lp::SerialArgs a{p->act, K, b, Uf, p->B, sizes[l], stride(l), hl, X[l], G[l],
+                       dir == lp::DIR_ADJ || l == 0 ? dsig : nullptr};
       TraceScope ts(kb + 3, l, st);
       LP_TRY(lp::launch_serial(sh, dir, a, st), "coarsest-level solve");
       return LP_OK;
@@ -269,6 +271,7 @@ struct Solver {
     a.hc = hl * (double)m->cf;
     a.X = X[l];
     a.G = G[l];
+    a.dsig = dir == lp::DIR_ADJ ? dsig : nullptr;  // the forward writes it in its final F-relaxation only
     // On the finest level with FCF the coarse-grid correction of a cycle is not
     // written back: the next cycle's FC sweep starts from C + (V - C) (the same
     // correction, applied on the fly), and the F-points, which no later sweep
@@ -312,6 +315,7 @@ struct Solver {
     a.V = X[l + 1];
     a.mode = lp::SWEEP_CORRF;
     a.partial = nullptr;
+    if (dir == lp::DIR_FWD && l == 0) a.dsig = dsig;
     TraceScope ts(kb + 2, l, st);
     LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "correction and F-relaxation");
     return LP_OK;
@@ -338,6 +342,7 @@ struct Solver {
     a.cs_stride = 1;
     a.V = X[1];
     a.finest = 1;
+    a.dsig = dsig;
     const int kb = dir == lp::DIR_FWD ? LP_TRACE_FWD_FC : LP_TRACE_ADJ_FC;
     TraceScope ts(kb + 2, 0, st);
     LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "correction and F-relaxation");
@@ -347,8 +352,8 @@ struct Solver {
 };
 
 int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, const void* b,
-                const void* U, void* Xuser, void* ws, size_t ws_bytes, double* res_hist, int32_t* iters,
-                void* stream) {
+                const void* U, void* Xuser, void* dsig, void* ws, size_t ws_bytes, double* res_hist,
+                int32_t* iters, void* stream) {
   int rc = check_problem(p);
   if (rc) return rc;
   std::vector<int> sizes;
@@ -373,6 +378,7 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
   s.K = K;
   s.b = b;
   s.Uf = U;
+  s.dsig = lp::dsig_supported(shape_of(p)) ? dsig : nullptr;
   s.sizes = sizes;
   s.X.assign(L, nullptr);
   s.G.assign(L, nullptr);
@@ -474,6 +480,10 @@ bool use_mfma(const Shape& s) {
   return !(e && strcmp(e, "valu") == 0);
 }
 
+// the sigma' record is written and read by the dense matrix-core kernels (no
+// record exists for the identity activation)
+bool dsig_supported(const Shape& s) { return s.act != LP_IDENTITY && use_mfma(s); }
+
 hipError_t launch_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   if (s.layer != 0) return conv_sweep(s, dir, a, st, partials);
   if (use_mfma(s)) return mfma_sweep(s.C, dir, a, st, partials);
@@ -529,43 +539,58 @@ size_t lp_workspace_bytes(const lp_problem* p, const lp_mgrit* m) {
   return need;
 }
 
-int32_t lp_serial_forward(const lp_problem* p, const void* K, const void* b, void* U, void* stream) {
+size_t lp_dsig_bytes(const lp_problem* p) {
+  if (check_problem(p) != LP_OK) return 0;
+  g_err.clear();
+  if (!lp::dsig_supported(shape_of(p))) return 0;
+  const size_t per = p->act == LP_RELU ? 1 : esize(p);
+  return (size_t)p->N * p->B * qdim(p) * per;
+}
+
+// The record is only written and read where the kernels support it, so a
+// forward and an adjoint call on the same problem always agree.
+void* dsig_for(const lp_problem* p, const void* dsig) {
+  return lp::dsig_supported(shape_of(p)) ? const_cast<void*>(dsig) : nullptr;
+}
+
+int32_t lp_serial_forward(const lp_problem* p, const void* K, const void* b, void* U, void* dsig, void* stream) {
   int rc = check_problem(p);
   if (rc) return rc;
   if (!K || !b || (p->B && !U)) return fail(LP_EINVAL, "NULL array argument");
   if (p->B == 0) return LP_OK;
-  lp::SerialArgs a{p->act, K, b, nullptr, p->B, p->N, 1, p->h, U, nullptr};
+  lp::SerialArgs a{p->act, K, b, nullptr, p->B, p->N, 1, p->h, U, nullptr, dsig_for(p, dsig)};
   TraceScope ts(LP_TRACE_SERIAL, 0, static_cast<hipStream_t>(stream));
   LP_TRY(lp::launch_serial(shape_of(p), lp::DIR_FWD, a, static_cast<hipStream_t>(stream)), "serial forward");
   return LP_OK;
 }
 
-int32_t lp_serial_adjoint(const lp_problem* p, const void* K, const void* b, const void* U, void* Lam,
-                          void* stream) {
+int32_t lp_serial_adjoint(const lp_problem* p, const void* K, const void* b, const void* U, const void* dsig,
+                          void* Lam, void* stream) {
   int rc = check_problem(p);
   if (rc) return rc;
   if (!K || !b || (p->B && (!U || !Lam))) return fail(LP_EINVAL, "NULL array argument");
   if (p->B && U == Lam) return fail(LP_EINVAL, "U and Lam alias");
   if (p->B == 0) return LP_OK;
-  lp::SerialArgs a{p->act, K, b, U, p->B, p->N, 1, p->h, Lam, nullptr};
+  lp::SerialArgs a{p->act, K, b, U, p->B, p->N, 1, p->h, Lam, nullptr, dsig_for(p, dsig)};
   TraceScope ts(LP_TRACE_SERIAL, 1, static_cast<hipStream_t>(stream));
   LP_TRY(lp::launch_serial(shape_of(p), lp::DIR_ADJ, a, static_cast<hipStream_t>(stream)), "serial adjoint");
   return LP_OK;
 }
 
 int32_t lp_mgrit_forward(const lp_problem* p, const lp_mgrit* m, const void* K, const void* b, void* U,
-                         void* ws, size_t ws_bytes, double* res_hist, int32_t* iters, void* stream) {
-  return mgrit_solve(p, m, lp::DIR_FWD, K, b, nullptr, U, ws, ws_bytes, res_hist, iters, stream);
+                         void* dsig, void* ws, size_t ws_bytes, double* res_hist, int32_t* iters, void* stream) {
+  return mgrit_solve(p, m, lp::DIR_FWD, K, b, nullptr, U, dsig, ws, ws_bytes, res_hist, iters, stream);
 }
 
 int32_t lp_mgrit_adjoint(const lp_problem* p, const lp_mgrit* m, const void* K, const void* b, const void* U,
-                         void* Lam, void* ws, size_t ws_bytes, double* res_hist, int32_t* iters,
-                         void* stream) {
-  return mgrit_solve(p, m, lp::DIR_ADJ, K, b, U, Lam, ws, ws_bytes, res_hist, iters, stream);
+                         const void* dsig, void* Lam, void* ws, size_t ws_bytes, double* res_hist,
+                         int32_t* iters, void* stream) {
+  return mgrit_solve(p, m, lp::DIR_ADJ, K, b, U, Lam, const_cast<void*>(dsig), ws, ws_bytes, res_hist, iters,
+                     stream);
 }
 
-int32_t lp_gradient(const lp_problem* p, const void* K, const void* b, const void* U, const void* Lam,
-                    void* dK, void* db, void* ws, size_t ws_bytes, void* stream) {
+int32_t lp_gradient(const lp_problem* p, const void* K, const void* b, const void* U, const void* dsig,
+                    const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_problem(p);
   if (rc) return rc;
   if (!K || !b || !dK || !db || (p->B && (!U || !Lam))) return fail(LP_EINVAL, "NULL array argument");
@@ -579,7 +604,8 @@ int32_t lp_gradient(const lp_problem* p, const void* K, const void* b, const voi
   }
   rc = check_ws(ws, ws_bytes, grad_bytes(p));
   if (rc) return rc;
-  lp::GradArgs a{p->act, K, b, U, Lam, p->B, p->N, p->h, ws, lp::grad_chunks(s, p->B, p->N), dK, db};
+  lp::GradArgs a{p->act, K, b, U, Lam, p->B, p->N, p->h, ws, lp::grad_chunks(s, p->B, p->N), dK, db,
+                 dsig_for(p, dsig)};
   TraceScope ts(LP_TRACE_GRADIENT, 0, st);
   LP_TRY(lp::launch_grad(s, a, st), "gradient");
   return LP_OK;

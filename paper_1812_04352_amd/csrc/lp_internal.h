@@ -62,6 +62,8 @@ struct SweepArgs {
   const void* V;       // CORRF: next level solution
   double* partial;     // FRES: per-workgroup sum of squared residuals (nullable)
   int finest;          // 1 on level 0: the fixed boundary row (u^0 or lam^N) is never written
+  void* dsig;          // sigma' record [N][B][q] (nullable): forward level-0 CORRF writes it
+                       // (every layer of its intervals), the adjoint reads it at i*stride
 };
 
 // Serial (coarsest level or layer-serial) solve of X over Nl steps.
@@ -76,6 +78,7 @@ struct SerialArgs {
   double hl;
   void* X;
   const void* G;       // nullable
+  void* dsig;          // sigma' record (nullable): written by a level-0 forward solve, read by the adjoint
 };
 
 struct ResidArgs {
@@ -103,6 +106,7 @@ struct GradArgs {
   int nchunks;
   void* dK;
   void* db;
+  const void* dsig;    // sigma' record of U (nullable)
 };
 
 struct Shape {
@@ -120,6 +124,7 @@ hipError_t launch_serial(const Shape& s, int dir, const SerialArgs& a, hipStream
 hipError_t launch_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t st, int* partials);
 hipError_t launch_grad(const Shape& s, const GradArgs& a, hipStream_t st);
 int grad_chunks(const Shape& s, int B, int N);  // batch chunks of the gradient's first pass
+bool dsig_supported(const Shape& s);            // kernels that write and read the sigma' record
 int grad_nout(const Shape& s);            // weights + bias entries per layer
 int grad_partial_floats(const Shape& s);  // values per (layer, chunk) gradient partial
 bool shape_supported(const Shape& s);

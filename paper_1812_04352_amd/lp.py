@@ -17,7 +17,7 @@ from typing import Optional, Sequence, Tuple
 # compare kernel variants under the same tests)
 LIB_PATH = os.environ.get("LP_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblp.so")
 
-LP_ABI_VERSION = 1
+LP_ABI_VERSION = 2
 LP_OK, LP_EINVAL, LP_EUNSUPPORTED, LP_EWORKSPACE, LP_EHIP, LP_ENONFINITE = range(6)
 LP_F32, LP_F64 = 0, 1
 LP_DENSE, LP_CONV3X3 = 0, 1
@@ -34,7 +34,7 @@ OPENING = {"identity": LP_OPEN_IDENTITY, "dense_act": LP_OPEN_DENSE_ACT, "conv_a
 # Every symbol the header declares (checked by the CPU test suite).
 EXPORTS = (
     "lp_abi_version", "lp_status_string", "lp_last_error", "lp_workspace_bytes",
-    "lp_serial_forward", "lp_serial_adjoint", "lp_mgrit_forward", "lp_mgrit_adjoint",
+    "lp_dsig_bytes", "lp_serial_forward", "lp_serial_adjoint", "lp_mgrit_forward", "lp_mgrit_adjoint",
     "lp_gradient", "lp_residual_norm", "lp_open_forward", "lp_open_grad",
     "lp_loss_terminal", "lp_sgd_update", "lp_trace_enable", "lp_trace_read",
 )
@@ -78,11 +78,12 @@ _SIGS = {
     "lp_status_string": ([_i32], ctypes.c_char_p),
     "lp_last_error": ([], ctypes.c_char_p),
     "lp_workspace_bytes": ([_P, _M], _sz),
-    "lp_serial_forward": ([_P, _v, _v, _v, _v], _i32),
-    "lp_serial_adjoint": ([_P, _v, _v, _v, _v, _v], _i32),
-    "lp_mgrit_forward": ([_P, _M, _v, _v, _v, _v, _sz, _dp, _ip, _v], _i32),
-    "lp_mgrit_adjoint": ([_P, _M, _v, _v, _v, _v, _v, _sz, _dp, _ip, _v], _i32),
-    "lp_gradient": ([_P, _v, _v, _v, _v, _v, _v, _v, _sz, _v], _i32),
+    "lp_dsig_bytes": ([_P], _sz),
+    "lp_serial_forward": ([_P, _v, _v, _v, _v, _v], _i32),
+    "lp_serial_adjoint": ([_P, _v, _v, _v, _v, _v, _v], _i32),
+    "lp_mgrit_forward": ([_P, _M, _v, _v, _v, _v, _v, _sz, _dp, _ip, _v], _i32),
+    "lp_mgrit_adjoint": ([_P, _M, _v, _v, _v, _v, _v, _v, _sz, _dp, _ip, _v], _i32),
+    "lp_gradient": ([_P, _v, _v, _v, _v, _v, _v, _v, _v, _sz, _v], _i32),
     "lp_residual_norm": ([_P, _i32, _v, _v, _v, _v, _v, _sz, _dp, _v], _i32),
     "lp_open_forward": ([_P, _i32, _i32, _v, _v, _v, _v], _i32),
     "lp_open_grad": ([_P, _i32, _i32, _v, _v, _v, _v, _v], _i32),
@@ -183,51 +184,76 @@ def alloc_workspace(p: LpProblem, mg: Optional[LpMgrit] = None, device="cuda"):
     return torch.empty(lp_workspace_bytes(p, mg), dtype=torch.uint8, device=device)
 
 
-def lp_serial_forward(p: LpProblem, K, b, U) -> None:
+def lp_dsig_bytes(p: LpProblem) -> int:
+    return int(load().lp_dsig_bytes(ctypes.byref(p)))
+
+
+def alloc_dsig(p: LpProblem, device="cuda"):
+    """A buffer for the sigma' record of p (may be empty: the identity has none)."""
+    import torch
+    return torch.empty(max(1, lp_dsig_bytes(p)), dtype=torch.uint8, device=device)
+
+
+def _dsig(p: LpProblem, dsig):
+    """Device pointer of a sigma' record buffer (any dtype, counted in bytes), or NULL."""
+    if dsig is None:
+        return None
+    if not dsig.is_cuda or not dsig.is_contiguous():
+        raise ValueError("dsig must be a contiguous GPU tensor")
+    need = lp_dsig_bytes(p)
+    if dsig.numel() * dsig.element_size() < need:
+        raise ValueError(f"dsig holds {dsig.numel() * dsig.element_size()} bytes, needs {need}")
+    return ctypes.c_void_p(dsig.data_ptr())
+
+
+def lp_serial_forward(p: LpProblem, K, b, U, dsig=None) -> None:
     Kp, bp = _weights(p, K, b)
     _check(load().lp_serial_forward(ctypes.byref(p), Kp, bp, _arr(U, (p.N + 1) * p.B * p.q, "U", _elem_dtype(p)),
-                                    _stream()), "lp_serial_forward")
+                                    _dsig(p, dsig), _stream()), "lp_serial_forward")
 
 
-def lp_serial_adjoint(p: LpProblem, K, b, U, Lam) -> None:
+def lp_serial_adjoint(p: LpProblem, K, b, U, Lam, dsig=None) -> None:
     Kp, bp = _weights(p, K, b)
     n = (p.N + 1) * p.B * p.q
-    _check(load().lp_serial_adjoint(ctypes.byref(p), Kp, bp, _arr(U, n, "U", _elem_dtype(p)),
+    _check(load().lp_serial_adjoint(ctypes.byref(p), Kp, bp, _arr(U, n, "U", _elem_dtype(p)), _dsig(p, dsig),
                                     _arr(Lam, n, "Lam", _elem_dtype(p)), _stream()), "lp_serial_adjoint")
 
 
-def lp_mgrit_forward(p: LpProblem, mg: LpMgrit, K, b, U, ws, history: bool = True) -> Tuple[int, list]:
+def lp_mgrit_forward(p: LpProblem, mg: LpMgrit, K, b, U, ws, history: bool = True,
+                     dsig=None) -> Tuple[int, list]:
     """history=False passes no residual history: without a stopping rule the
-    call then returns without waiting for the stream (the list is empty)."""
+    call then returns without waiting for the stream (the list is empty).
+    dsig: a buffer (alloc_dsig) that receives the iterate's sigma' record."""
     Kp, bp = _weights(p, K, b)
     hist = (ctypes.c_double * max(1, mg.max_iter))() if history else None
     it = ctypes.c_int32(0)
     wp, wn = _ws(ws, 1)
     _check(load().lp_mgrit_forward(ctypes.byref(p), ctypes.byref(mg), Kp, bp,
-                                   _arr(U, (p.N + 1) * p.B * p.q, "U", _elem_dtype(p)), wp, wn, hist,
-                                   ctypes.byref(it), _stream()), "lp_mgrit_forward")
+                                   _arr(U, (p.N + 1) * p.B * p.q, "U", _elem_dtype(p)), _dsig(p, dsig), wp, wn,
+                                   hist, ctypes.byref(it), _stream()), "lp_mgrit_forward")
     return it.value, list(hist[:it.value]) if history else []
 
 
-def lp_mgrit_adjoint(p: LpProblem, mg: LpMgrit, K, b, U, Lam, ws, history: bool = True) -> Tuple[int, list]:
-    """history as for lp_mgrit_forward."""
+def lp_mgrit_adjoint(p: LpProblem, mg: LpMgrit, K, b, U, Lam, ws, history: bool = True,
+                     dsig=None) -> Tuple[int, list]:
+    """history as for lp_mgrit_forward; dsig: the sigma' record of U (or None)."""
     Kp, bp = _weights(p, K, b)
     n = (p.N + 1) * p.B * p.q
     hist = (ctypes.c_double * max(1, mg.max_iter))() if history else None
     it = ctypes.c_int32(0)
     wp, wn = _ws(ws, 1)
     _check(load().lp_mgrit_adjoint(ctypes.byref(p), ctypes.byref(mg), Kp, bp, _arr(U, n, "U", _elem_dtype(p)),
-                                   _arr(Lam, n, "Lam", _elem_dtype(p)), wp, wn, hist, ctypes.byref(it),
-                                   _stream()), "lp_mgrit_adjoint")
+                                   _dsig(p, dsig), _arr(Lam, n, "Lam", _elem_dtype(p)), wp, wn, hist,
+                                   ctypes.byref(it), _stream()), "lp_mgrit_adjoint")
     return it.value, list(hist[:it.value]) if history else []
 
 
-def lp_gradient(p: LpProblem, K, b, U, Lam, dK, db, ws) -> None:
+def lp_gradient(p: LpProblem, K, b, U, Lam, dK, db, ws, dsig=None) -> None:
     Kp, bp = _weights(p, K, b)
     dKp, dbp = _weights(p, dK, db)
     n = (p.N + 1) * p.B * p.q
     wp, wn = _ws(ws, 1)
-    _check(load().lp_gradient(ctypes.byref(p), Kp, bp, _arr(U, n, "U", _elem_dtype(p)),
+    _check(load().lp_gradient(ctypes.byref(p), Kp, bp, _arr(U, n, "U", _elem_dtype(p)), _dsig(p, dsig),
                               _arr(Lam, n, "Lam", _elem_dtype(p)), dKp, dbp, wp, wn, _stream()), "lp_gradient")
 
 

@@ -34,6 +34,8 @@ class OneShotTrainer:
         self.ws = torch.empty(need, dtype=torch.uint8, device="cuda")
         self.J = torch.zeros(1, device="cuda", dtype=torch.float64)
         self.G = {k: torch.empty_like(v) for k, v in params.items()}
+        # sigma' along the forward iterate, kept for the adjoint and the gradient
+        self.rec = L.alloc_dsig(prob) if L.lp_dsig_bytes(prob) else None
         self.updates = 0
 
     def step(self, lr: float) -> None:
@@ -43,11 +45,11 @@ class OneShotTrainer:
         self.mgF.warm_start = int(warm)
         self.mgA.warm_start = int(warm)
         L.lp_open_forward(p, self.opening, self.nf, self.y, P.get("L_in"), self.U[0])
-        L.lp_mgrit_forward(p, self.mgF, P["K"], P["b"], self.U, self.ws, history=False)
+        L.lp_mgrit_forward(p, self.mgF, P["K"], P["b"], self.U, self.ws, history=False, dsig=self.rec)
         L.lp_loss_terminal(p, self.nc, self.U[-1], P["W"], P["mu"], self.c, self.J, self.Lam[-1], G["W"], G["mu"],
                            self.ws)
-        L.lp_mgrit_adjoint(p, self.mgA, P["K"], P["b"], self.U, self.Lam, self.ws, history=False)
-        L.lp_gradient(p, P["K"], P["b"], self.U, self.Lam, G["K"], G["b"], self.ws)
+        L.lp_mgrit_adjoint(p, self.mgA, P["K"], P["b"], self.U, self.Lam, self.ws, history=False, dsig=self.rec)
+        L.lp_gradient(p, P["K"], P["b"], self.U, self.Lam, G["K"], G["b"], self.ws, dsig=self.rec)
         if "L_in" in P:
             L.lp_open_grad(p, self.opening, self.nf, self.y, P["L_in"], self.Lam[0], G["L_in"])
         for k in P:

@@ -46,20 +46,20 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every case fails host vali
 def test_problem_validation_codes():
     lib = L.load()
     null = ctypes.c_void_p(0)
-    assert lib.lp_serial_forward(None, FAKE, FAKE, FAKE, null) == L.LP_EINVAL
+    assert lib.lp_serial_forward(None, FAKE, FAKE, FAKE, None, null) == L.LP_EINVAL
     p = _p()
     p.abi_version = 7
-    assert lib.lp_serial_forward(ctypes.byref(p), FAKE, FAKE, FAKE, null) == L.LP_EINVAL
+    assert lib.lp_serial_forward(ctypes.byref(p), FAKE, FAKE, FAKE, None, null) == L.LP_EINVAL
     assert b"abi_version" in lib.lp_last_error()
     for bad in (dict(N=0), dict(B=-1), dict(h=0.0), dict(h=float("nan")), dict(C=0)):
-        assert lib.lp_serial_forward(ctypes.byref(_p(**bad)), FAKE, FAKE, FAKE, null) == L.LP_EINVAL, bad
+        assert lib.lp_serial_forward(ctypes.byref(_p(**bad)), FAKE, FAKE, FAKE, None, null) == L.LP_EINVAL, bad
     p = _p()
     p.act = 9
-    assert lib.lp_serial_forward(ctypes.byref(p), FAKE, FAKE, FAKE, null) == L.LP_EINVAL
+    assert lib.lp_serial_forward(ctypes.byref(p), FAKE, FAKE, FAKE, None, null) == L.LP_EINVAL
     # a width with no kernel is a valid but unsupported problem
-    assert lib.lp_serial_forward(ctypes.byref(_p(C=48)), FAKE, FAKE, FAKE, null) == L.LP_EUNSUPPORTED
+    assert lib.lp_serial_forward(ctypes.byref(_p(C=48)), FAKE, FAKE, FAKE, None, null) == L.LP_EUNSUPPORTED
     # NULL arrays
-    assert lib.lp_serial_forward(ctypes.byref(_p()), None, FAKE, FAKE, null) == L.LP_EINVAL
+    assert lib.lp_serial_forward(ctypes.byref(_p()), None, FAKE, FAKE, None, null) == L.LP_EINVAL
 
 
 def test_mgrit_validation_codes():
@@ -69,7 +69,7 @@ def test_mgrit_validation_codes():
     it = ctypes.c_int32(-1)
 
     def call(mg, ws=FAKE, nbytes=1 << 40):
-        return lib.lp_mgrit_forward(ctypes.byref(p), ctypes.byref(mg), FAKE, FAKE, FAKE, ws, nbytes, hist,
+        return lib.lp_mgrit_forward(ctypes.byref(p), ctypes.byref(mg), FAKE, FAKE, FAKE, None, ws, nbytes, hist,
                                     ctypes.byref(it), None)
 
     assert call(L.mgrit(cf=1)) == L.LP_EINVAL
@@ -86,7 +86,7 @@ def test_mgrit_validation_codes():
     assert call(mg, ws=ctypes.c_void_p(0x1001)) == L.LP_EWORKSPACE  # misaligned
     assert call(mg, nbytes=need - 1) == L.LP_EWORKSPACE
     # adjoint: U and Lam must not alias
-    assert lib.lp_mgrit_adjoint(ctypes.byref(p), ctypes.byref(mg), FAKE, FAKE, FAKE, FAKE, FAKE, need, hist,
+    assert lib.lp_mgrit_adjoint(ctypes.byref(p), ctypes.byref(mg), FAKE, FAKE, FAKE, None, FAKE, FAKE, need, hist,
                                 ctypes.byref(it), None) == L.LP_EINVAL
 
 
@@ -104,6 +104,24 @@ def test_workspace_sizes():
     assert L.lp_workspace_bytes(p, L.mgrit(cf=4, max_levels=16, min_coarse=8, relax="F", max_iter=20)) < got
     with pytest.raises(L.LpError):
         L.lp_workspace_bytes(L.problem("f32", "dense", "tanh", 2048, 16384, 48, h=0.1))
+
+
+def test_dsig_record_sizes(monkeypatch):
+    # one byte per value for ReLU, fp32 for smooth activations, none for the identity
+    assert L.lp_dsig_bytes(_p(act="relu")) == 64 * 100 * 32
+    assert L.lp_dsig_bytes(_p(act="tanh")) == 64 * 100 * 32 * 4
+    assert L.lp_dsig_bytes(_p(act="smoothrelu", C=64)) == 64 * 100 * 64 * 4
+    assert L.lp_dsig_bytes(_p(act="identity")) == 0
+    # kernels that keep no record
+    assert L.lp_dsig_bytes(_p(act="smoothrelu", dtype="f64")) == 0
+    assert L.lp_dsig_bytes(_p(C=8)) == 0
+    assert L.lp_dsig_bytes(L.problem("f32", "conv3x3", "relu", 16, 5, 8, H=12, W=12, h=0.1)) == 0
+    monkeypatch.setenv("LP_DENSE_PATH", "valu")
+    assert L.lp_dsig_bytes(_p()) == 0
+    monkeypatch.delenv("LP_DENSE_PATH")
+    bad = _p()
+    bad.abi_version = 1
+    assert L.lp_dsig_bytes(bad) == 0
 
 
 def test_helper_validation_codes():

@@ -309,3 +309,111 @@ def test_one_shot_training_matches_oracle():
     assert losses[-1] < losses[0]
     for k in params:
         assert_close(params[k].cpu().numpy(), wo[k], wl.dtype, f"{k} after {updates} updates", scale=10)
+
+
+# fp32 widths on the matrix cores with a non-identity activation: the ones that keep a sigma' record
+RECORDED = [DENSE[1], DENSE[2], DENSE[3],
+            ("srelu32", WORKLOADS[2].with_overrides(act="smoothrelu", N=32, B=77, max_levels=2))]
+
+
+def _check_record(c, U, rec):
+    """The record against sigma'(K_n u_n + b_n) evaluated by the oracle in fp64 at
+    the trajectory the GPU returned. ReLU's 0/1 bytes may differ from the fp64
+    decision only where the pre-activation is within fp32 rounding of zero."""
+    wl = c.wl
+    Uh = U.double().cpu().numpy()
+    z = np.stack([O.preact(c.d["K"][n], c.d["b"][n], Uh[n]) for n in range(wl.N)])
+    want = O.dact(z, wl.act)
+    if wl.act == "relu":
+        got = rec[: z.size].cpu().numpy().reshape(z.shape)
+        assert set(np.unique(got)) <= {0, 1}
+        bad = got != want
+        scale = np.abs(z).max()
+        assert np.all(np.abs(z[bad]) <= 1e-5 * scale), f"{bad.sum()} wrong record bytes"
+    else:
+        got = rec.view(torch.float32)[: z.size].cpu().numpy().reshape(z.shape)
+        np.testing.assert_allclose(got, want, rtol=0, atol=2e-5)
+
+
+@pytest.mark.parametrize("relax", ["FCF", "F"])
+@pytest.mark.parametrize("name,wl", RECORDED, ids=[n for n, _ in RECORDED])
+def test_sigma_record_in_mgrit(name, wl, relax):
+    """An MGRIT forward solve that keeps the sigma' record returns the same
+    trajectory, and its record holds sigma' at that trajectory; an adjoint that
+    reads the record returns what the recomputing adjoint returns bit for bit,
+    and the gradient that reads it meets the parity bar."""
+    wl = wl.with_overrides(relax=relax)
+    c = case(wl)
+    mg = sched(wl, 2)
+    ws = L.alloc_workspace(c.p, mg)
+    U1, U2 = c.new_traj(), c.new_traj()
+    rec = L.alloc_dsig(c.p)
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U1, ws, history=False)
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U2, ws, history=False, dsig=rec)
+    torch.cuda.synchronize()
+    assert torch.equal(U1, U2)
+    _check_record(c, U1, rec)
+    L1 = torch.zeros_like(U1)
+    L1[-1] = _lamN(c, U1)[0]
+    L2 = L1.clone()
+    L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U1, L1, ws, history=False)
+    L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U1, L2, ws, history=False, dsig=rec)
+    torch.cuda.synchronize()
+    assert torch.equal(L1, L2)
+    dK1, db1 = torch.empty_like(c.K), torch.empty_like(c.b)
+    dK2, db2 = torch.empty_like(c.K), torch.empty_like(c.b)
+    L.lp_gradient(c.p, c.K, c.b, U1, L1, dK1, db1, ws)
+    L.lp_gradient(c.p, c.K, c.b, U1, L1, dK2, db2, ws, dsig=rec)
+    dKr, dbr = O.gradient(U1.double().cpu().numpy(), L1.double().cpu().numpy(), c.d["K"], c.d["b"], wl.h, wl.act)
+    assert_close(dK2.cpu().numpy(), dKr, wl.dtype, "dK (record)")
+    assert_close(db2.cpu().numpy(), dbr, wl.dtype, "db (record)")
+    assert_close(dK2.cpu().numpy(), dK1.double().cpu().numpy(), wl.dtype, "dK record vs recompute")
+
+
+@pytest.mark.parametrize("name,wl", RECORDED[:2], ids=[n for n, _ in RECORDED[:2]])
+def test_sigma_record_in_serial_solves(name, wl):
+    """The serial forward writes the record for every layer; the serial adjoint
+    that reads it matches the recomputing one bit for bit. A one-level MGRIT
+    solve (a serial solve on the finest level) writes it too."""
+    c = case(wl)
+    U = c.new_traj()
+    rec = L.alloc_dsig(c.p)
+    L.lp_serial_forward(c.p, c.K, c.b, U, dsig=rec)
+    torch.cuda.synchronize()
+    _check_record(c, U, rec)
+    L1 = torch.zeros_like(U)
+    L1[-1] = _lamN(c, U)[0]
+    L2 = L1.clone()
+    L.lp_serial_adjoint(c.p, c.K, c.b, U, L1)
+    L.lp_serial_adjoint(c.p, c.K, c.b, U, L2, dsig=rec)
+    torch.cuda.synchronize()
+    assert torch.equal(L1, L2)
+    mg = sched(wl, 1, levels=1)
+    ws = L.alloc_workspace(c.p, mg)
+    rec2 = torch.full_like(rec, 7)
+    U2 = c.new_traj()
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U2, ws, history=False, dsig=rec2)
+    torch.cuda.synchronize()
+    assert torch.equal(U, U2) and torch.equal(rec, rec2)
+
+
+def test_sigma_record_is_ignored_where_unsupported():
+    """Kernels that keep no record (fp64, the identity) report a size of 0, leave
+    a buffer passed anyway untouched and give the same results."""
+    wl = DENSE[0][1]
+    c = case(wl)
+    mg = sched(wl, 2)
+    ws = L.alloc_workspace(c.p, mg)
+    assert L.lp_dsig_bytes(c.p) == 0
+    rec = torch.full((4096,), 3, dtype=torch.uint8, device="cuda")
+    U1, U2 = c.new_traj(), c.new_traj()
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U1, ws, history=False)
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U2, ws, history=False, dsig=rec)
+    torch.cuda.synchronize()
+    assert torch.equal(U1, U2)
+    assert int(rec.min()) == 3 and int(rec.max()) == 3
+    p = L.problem("f32", "dense", "identity", 8, 5, 32, h=0.1)
+    assert L.lp_dsig_bytes(p) == 0
+    K = torch.zeros(8, 32, 32, device="cuda")
+    U = torch.zeros(9, 5, 32, device="cuda")
+    L.lp_serial_forward(p, K, torch.zeros(8, 32, device="cuda"), U, dsig=L.alloc_dsig(p))
