@@ -45,7 +45,7 @@ def level_sizes(N, cf, max_levels, min_coarse):
 
 def record_bytes(wl) -> int:
     """Bytes per value of the sigma' record the step keeps (0: none is kept)."""
-    if wl.layer != "dense" or wl.dtype != "f32" or wl.act == "identity" or wl.q not in (32, 64):
+    if wl.dtype != "f32" or wl.act == "identity" or (wl.layer == "dense" and wl.q not in (32, 64)):
         return 0
     return 1 if wl.act == "relu" else 4
 
@@ -86,7 +86,7 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
     fstep = (2 if adj and rec else 4 if adj else 2) * mac
     byts = flops = launches = 0
     if kind == "gradient":
-        if rec and q >= 64:  # the width-32 kernel recomputes sigma'
+        if rec and (wl.layer != "dense" or q >= 64):  # the dense width-32 kernel recomputes sigma'
             return 2 * wl.N * row + wl.N * rrow + wl.N * nweights * e, 2.0 * mac * B * wl.N, 1
         return 2 * wl.N * row + 2 * wl.N * nweights * e, 4.0 * mac * B * wl.N, 1
     # With FCF the finest level's correction is applied inside the next cycle's FC

@@ -118,9 +118,9 @@ size_t lp_workspace_bytes(const lp_problem* prob, const lp_mgrit* mg);
  * product per step), so it must hold the record of the U and the weights that
  * call receives. NULL: not written / recomputed from U.
  * Returns the record's size in bytes, or 0 where the kernels for this problem
- * keep none: an invalid problem, LP_IDENTITY, and every problem outside the
- * fp32 dense matrix-core widths (32 and 64), including fp64 and 3x3
- * convolutions. Where it returns 0 every call ignores `dsig`. */
+ * keep none: an invalid problem, LP_IDENTITY, fp64, and dense widths other than
+ * 32 and 64 (the fp32 matrix-core kernels). Where it returns 0 every call
+ * ignores `dsig`. */
 size_t lp_dsig_bytes(const lp_problem* prob);
 
 /* Layer-serial forward propagation (Section 2.3, state equations; the baseline

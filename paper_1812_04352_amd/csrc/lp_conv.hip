@@ -213,6 +213,45 @@ __device__ __forceinline__ void act_tiles(f32x4 (&z)[TPW], int act) {
   }
 }
 
+// sigma'(z) of one value, the arithmetic of act_tiles<true>
+__device__ __forceinline__ float dact_one(float z, int act) {
+  switch (act) {
+    case ACT_TANH: {
+      const float t = tanh_fast(z);
+      return 1.f - t * t;
+    }
+    case ACT_RELU: return z > 0.f ? 1.f : 0.f;
+    case ACT_SMOOTHRELU: return dact_f<float, ACT_SMOOTHRELU>(z);
+    default: return 1.f;
+  }
+}
+
+// The sigma' record at the lane's own output pixels (same layout as the state):
+// a byte 0/1 for ReLU, fp32 otherwise. rec_put takes the pre-activation.
+__device__ __forceinline__ void rec_put(void* rec, size_t off, f32x4 z, const SGeo& g, const Px& p, int act) {
+  if (act == ACT_RELU) {
+    uint8_t* r8 = static_cast<uint8_t*>(rec) + off;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) r8[gl_r(g, p, r)] = z[r] > 0.f ? 1 : 0;
+  } else {
+    float* rf = static_cast<float*>(rec) + off;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) rf[gl_r(g, p, r)] = dact_one(z[r], act);
+  }
+}
+
+__device__ __forceinline__ f32x4 rec_get(const void* rec, size_t off, const SGeo& g, const Px& p, int act) {
+  f32x4 d;
+  if (act == ACT_RELU) {
+    const uint8_t* r8 = static_cast<const uint8_t*>(rec) + off;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) d[r] = r8[gl_r(g, p, r)] ? 1.f : 0.f;
+  } else {
+    d = ld_px(static_cast<const float*>(rec) + off, g, p);
+  }
+  return d;
+}
+
 __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
@@ -224,7 +263,7 @@ __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
   return s;
 }
 
-template <int MODE, int GH, int GW>
+template <int MODE, int GH, int GW, bool REC>
 __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
@@ -282,6 +321,10 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
   if (MODE == SWEEP_FC && k == 0) row_copy(static_cast<float*>(a.S) + eo, X + eo, g.q, nt);
   __syncthreads();
 
+  // the final F-relaxation (and a level-0 serial solve) records sigma'(z) of every
+  // layer; CORRF then also takes the product of the layer before the next C-point
+  constexpr bool rec = REC && (MODE == SWEEP_CORRF || MODE == MODE_SERIAL);
+  constexpr int extra = MODE == SWEEP_CORRF && rec ? 1 : 0;
   f32x4 coarse[TPW];
   for (int j = 0; j < nsteps; ++j) {
     // an empty asm statement makes the lane index opaque to the optimiser, so the
@@ -289,13 +332,20 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
     // live in registers through the loop (fewer registers, more resident waves)
     asm volatile("" : "+v"(lane));
     const float* swc = sw + (j & 1) * WV;
-    stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j)) * a.stride, nt);
+    stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j + extra)) * a.stride, nt);
     f32x4 z[TPW];
     {
       float wr[24];
       gather_w<false>(wr, swc, lane);
       const f32x4 bias = bias_px(swc, lane);
       conv_tiles(z, wr, buf, g, t0, lane, bias);
+    }
+    if constexpr (rec) {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        const Px p = px_of(g, t0 + tt, lane);
+        if (p.ok) rec_put(a.dsig, (size_t)(kc + j) * a.stride * slice + eo, z[tt], g, p, a.act);
+      }
     }
     act_tiles<false>(z, a.act);
     const float* gi = G ? G + (kc + j + 1) * slice + eo : nullptr;
@@ -318,6 +368,20 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
     __syncthreads();
   }
 
+  if constexpr (extra != 0) {
+    // sigma' of the layer before the next C-point, from the last F-point (in the
+    // buffer) and that layer's weights (staged by the last step)
+    const float* swc = sw + (nsteps & 1) * WV;
+    f32x4 z[TPW];
+    float wr[24];
+    gather_w<false>(wr, swc, lane);
+    conv_tiles(z, wr, buf, g, t0, lane, bias_px(swc, lane));
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) rec_put(a.dsig, (size_t)(kc + nsteps) * a.stride * slice + eo, z[tt], g, p, a.act);
+    }
+  }
   if (MODE == SWEEP_FC) {
     float* so = static_cast<float*>(a.S) + (size_t)(k + 1) * slice + eo;
 #pragma unroll
@@ -357,15 +421,17 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
 }
 
 // Adjoint step at level point i: d = sigma'(K u + b) with u the fine primal state
-// of point i, s = d * lam, lam' = lam + h K^T s (+ g).
-template <int MODE, int GH, int GW>
+// of point i (or d read from the sigma' record: REC), s = d * lam,
+// lam' = lam + h K^T s (+ g).
+template <int MODE, int GH, int GW, bool REC>
 __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
   float* buf = lds;               // CH * CS: u, then s
   float* sw = lds + CH * g.CS;    // two layers
   __shared__ double red[MAXW];
-  const int lane = threadIdx.x & 63, t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
+  int lane = threadIdx.x & 63;
+  const int t0 = (threadIdx.x >> 6) * TPW, nt = blockDim.x;
   const int k = blockIdx.x, Nc = gridDim.x;
   const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
   const float* K = static_cast<const float*>(a.K);
@@ -402,14 +468,14 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     const Px p = px_of(g, t0 + tt, lane);
     lam[tt] = ld_px(src, g, p);
     if (vsrc) lam[tt] = lam[tt] + (ld_px(vsrc, g, p) - lam[tt]);
-    un[tt] = ld_px(Uf + (size_t)(top - 1) * ustep + eo, g, p);
+    if (!REC) un[tt] = ld_px(Uf + (size_t)(top - 1) * ustep + eo, g, p);
   }
   __syncthreads();  // halo zeroed
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt) {
     const Px p = px_of(g, t0 + tt, lane);
     if (p.ok) {
-      put_px(buf, un[tt], g, p);
+      if (!REC) put_px(buf, un[tt], g, p);
       if (MODE == SWEEP_CORRF && k + 1 < Nc) st_px(X + top * slice + eo, lam[tt], g, p);
     }
   }
@@ -418,21 +484,30 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
 
   f32x4 dd[TPW];  // sigma'(z) of the step (after the loop: of the last one)
   for (int j = 0; j < nsteps; ++j) {
+    // tile offsets recomputed each step (see k_fwd) where that lowers the
+    // register count (compiler-measured per variant)
+    constexpr bool OPAQUE = REC ? (MODE == SWEEP_FC || MODE == SWEEP_FRES) : MODE != SWEEP_FRES;
+    if constexpr (OPAQUE) asm volatile("" : "+v"(lane));
     const long i = top - 1 - j;
     const bool more = j + 1 < nsteps;
     const float* swc = sw + (j & 1) * WV;
     stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(more ? i - 1 : i) * a.stride, nt);
     // d = sigma'(K u + b)
-    {
+    if constexpr (REC) {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) dd[tt] = rec_get(a.dsig, (size_t)i * ustep + eo, g, px_of(g, t0 + tt, lane), a.act);
+    } else {
       float wr[24];
       gather_w<false>(wr, swc, lane);
       const f32x4 bias = bias_px(swc, lane);
       conv_tiles(dd, wr, buf, g, t0, lane, bias);
+      act_tiles<true>(dd, a.act);
     }
-    act_tiles<true>(dd, a.act);
     float wt[24];
     gather_w<true>(wt, swc, lane);
-    __syncthreads();  // every read of u is done
+    // every read of u is done (with the record, the buffer was last read by the
+    // previous step's transposed product, which ended with a barrier)
+    if (!REC) __syncthreads();
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
       const Px p = px_of(g, t0 + tt, lane);
@@ -440,7 +515,7 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     }
     __syncthreads();
     // the next step's primal state arrives while the transposed product runs
-    if (more) {
+    if (!REC && more) {
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) un[tt] = ld_px(Uf + (size_t)(i - 1) * ustep + eo, g, px_of(g, t0 + tt, lane));
     }
@@ -456,14 +531,16 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
       if (xo && p.ok) st_px(xo, lam[tt], g, p);
     }
     __syncthreads();  // every read of s is done
-    if (more) {
+    if (!REC) {
+      if (more) {
 #pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) {
-        const Px p = px_of(g, t0 + tt, lane);
-        if (p.ok) put_px(buf, un[tt], g, p);
+        for (int tt = 0; tt < TPW; ++tt) {
+          const Px p = px_of(g, t0 + tt, lane);
+          if (p.ok) put_px(buf, un[tt], g, p);
+        }
       }
+      __syncthreads();
     }
-    __syncthreads();
   }
 
   if (MODE == SWEEP_FC) {
@@ -481,7 +558,10 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     for (int tt = 0; tt < TPW; ++tt) {
       const Px p = px_of(g, t0 + tt, lane);
       cu[tt] = ld_px(src, g, p);
-      if (p.ok) put_px(buf, dd[tt] * cu[tt], g, p);
+      // with the record, sigma' of the last step is read again rather than kept
+      // live in registers through the loop
+      const f32x4 d = REC ? rec_get(a.dsig, (size_t)(top - nsteps) * ustep + eo, g, p, a.act) : dd[tt];
+      if (p.ok) put_px(buf, d * cu[tt], g, p);
     }
     float wt[24];
     gather_w<true>(wt, sw, lane);
@@ -603,7 +683,7 @@ __global__ __launch_bounds__(64 * MAXW) void k_resid(ResidArgs a, SGeo g) {
 // and lanes are combined in a fixed order.
 constexpr int GOUT = 16 * 96 + CH;  // dWbig then db per chunk
 
-template <int GH, int GW>
+template <int GH, int GW, bool REC>
 __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
@@ -660,8 +740,14 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
       const Px p = px_of(g, t0 + tt, lane);
       lam[tt] = ld_px(Lm + (size_t)e * g.q, g, p);
     }
-    conv_tiles(z, wf, bu, g, t0, lane, bias);
-    act_tiles<true>(z, a.act);
+    if constexpr (REC) {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt)
+        z[tt] = rec_get(a.dsig, (size_t)n * slice + (size_t)e * g.q, g, px_of(g, t0 + tt, lane), a.act);
+    } else {
+      conv_tiles(z, wf, bu, g, t0, lane, bias);
+      act_tiles<true>(z, a.act);
+    }
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
       const Px p = px_of(g, t0 + tt, lane);
@@ -764,27 +850,35 @@ conv::SGeo sweep_geo(const Shape& s) { return conv::make_geo(s.H, s.W); }
 size_t sweep_lds(const conv::SGeo& g) { return (size_t)(conv::CH * g.CS + 2 * conv::WV) * sizeof(float); }
 
 // Sweep kernels with the geometry as template arguments (0, 0: runtime).
-template <int GH, int GW>
+// Only the forward CORRF and serial kernels write the record; every adjoint
+// kernel can read it.
+template <int GH, int GW, bool REC>
 void sweep_kernels(int dir, int mode, void (*&f)(SweepArgs, conv::SGeo)) {
   using namespace conv;
   if (dir == DIR_FWD) {
-    if (mode == SWEEP_FC) f = k_fwd<SWEEP_FC, GH, GW>;
-    else if (mode == SWEEP_FRES) f = k_fwd<SWEEP_FRES, GH, GW>;
-    else if (mode == SWEEP_CORRF) f = k_fwd<SWEEP_CORRF, GH, GW>;
-    else f = k_fwd<MODE_SERIAL, GH, GW>;
+    if (mode == SWEEP_FC) f = k_fwd<SWEEP_FC, GH, GW, false>;
+    else if (mode == SWEEP_FRES) f = k_fwd<SWEEP_FRES, GH, GW, false>;
+    else if (mode == SWEEP_CORRF) f = k_fwd<SWEEP_CORRF, GH, GW, REC>;
+    else f = k_fwd<MODE_SERIAL, GH, GW, REC>;
   } else {
-    if (mode == SWEEP_FC) f = k_adj<SWEEP_FC, GH, GW>;
-    else if (mode == SWEEP_FRES) f = k_adj<SWEEP_FRES, GH, GW>;
-    else if (mode == SWEEP_CORRF) f = k_adj<SWEEP_CORRF, GH, GW>;
-    else f = k_adj<MODE_SERIAL, GH, GW>;
+    if (mode == SWEEP_FC) f = k_adj<SWEEP_FC, GH, GW, REC>;
+    else if (mode == SWEEP_FRES) f = k_adj<SWEEP_FRES, GH, GW, REC>;
+    else if (mode == SWEEP_CORRF) f = k_adj<SWEEP_CORRF, GH, GW, REC>;
+    else f = k_adj<MODE_SERIAL, GH, GW, REC>;
   }
 }
 
 hipError_t launch_conv_sweep(const Shape& s, int dir, const SweepArgs& a, dim3 grid, hipStream_t st) {
   const conv::SGeo g = sweep_geo(s);
   void (*f)(SweepArgs, conv::SGeo) = nullptr;
-  if (s.H == 28 && s.W == 28) sweep_kernels<28, 28>(dir, a.mode, f);  // MNIST-sized images
-  else sweep_kernels<0, 0>(dir, a.mode, f);
+  const bool rec = a.dsig != nullptr;
+  if (s.H == 28 && s.W == 28) {  // MNIST-sized images
+    if (rec) sweep_kernels<28, 28, true>(dir, a.mode, f);
+    else sweep_kernels<28, 28, false>(dir, a.mode, f);
+  } else {
+    if (rec) sweep_kernels<0, 0, true>(dir, a.mode, f);
+    else sweep_kernels<0, 0, false>(dir, a.mode, f);
+  }
   launch(f, grid, dim3(64 * g.NW), sweep_lds(g), st, a, g);
   return hipGetLastError();
 }
@@ -828,6 +922,7 @@ hipError_t conv_serial(const Shape& s, int dir, const SerialArgs& sa, hipStream_
   a.hl = sa.hl;
   a.X = sa.X;
   a.G = sa.G;
+  a.dsig = sa.dsig;
   return launch_conv_sweep(s, dir, a, dim3(1, sa.B), st);
 }
 
@@ -845,10 +940,10 @@ hipError_t conv_grad(const Shape& s, const GradArgs& a, hipStream_t st) {
   // image buffers and weights, reused at the end for the partial and the db terms
   const int fl = 2 * conv::CH * g.CS + conv::WV, red = conv::GOUT + 2 * 64 * g.NW;
   const size_t sh = (size_t)(fl > red ? fl : red) * sizeof(float);
-  if (s.H == 28 && s.W == 28)
-    launch(conv::k_grad<28, 28>, dim3(a.N, a.nchunks), 64 * g.NW, sh, st, a, g);
-  else
-    launch(conv::k_grad<0, 0>, dim3(a.N, a.nchunks), 64 * g.NW, sh, st, a, g);
+  void (*f)(GradArgs, conv::SGeo);
+  if (s.H == 28 && s.W == 28) f = a.dsig ? conv::k_grad<28, 28, true> : conv::k_grad<28, 28, false>;
+  else f = a.dsig ? conv::k_grad<0, 0, true> : conv::k_grad<0, 0, false>;
+  launch(f, dim3(a.N, a.nchunks), 64 * g.NW, sh, st, a, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t tot = (size_t)a.N * (conv::KW + conv::CH);

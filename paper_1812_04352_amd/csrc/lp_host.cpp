@@ -480,9 +480,11 @@ bool use_mfma(const Shape& s) {
   return !(e && strcmp(e, "valu") == 0);
 }
 
-// the sigma' record is written and read by the dense matrix-core kernels (no
-// record exists for the identity activation)
-bool dsig_supported(const Shape& s) { return s.act != LP_IDENTITY && use_mfma(s); }
+// the sigma' record is written and read by the dense matrix-core kernels and
+// the convolution kernels (no record exists for the identity activation)
+bool dsig_supported(const Shape& s) {
+  return s.act != LP_IDENTITY && (use_mfma(s) || (s.layer == 1 && conv_supported(s)));
+}
 
 hipError_t launch_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   if (s.layer != 0) return conv_sweep(s, dir, a, st, partials);

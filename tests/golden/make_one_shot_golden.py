@@ -1,6 +1,6 @@
 """Write the per-update losses of simultaneous (one-shot) layer-parallel training
-on the one-shot workload (dense width 32, N = 1024, B = 16384, 100 updates,
-3-level MGRIT with one forward and one adjoint iteration per update, plain
+on the one-shot workload (dense width 32, N = 1024, B = 16384, 3-level MGRIT
+with one forward and one adjoint iteration per update, plain
 gradient step lr = 1e-2; Algorithm 2 with m1 = m2 = 1 and a scaled-identity
 Hessian approximation), next to layer-serial gradient descent from the same
 seed, both computed by the fp64 oracle.

@@ -115,7 +115,9 @@ def test_dsig_record_sizes(monkeypatch):
     # kernels that keep no record
     assert L.lp_dsig_bytes(_p(act="smoothrelu", dtype="f64")) == 0
     assert L.lp_dsig_bytes(_p(C=8)) == 0
-    assert L.lp_dsig_bytes(L.problem("f32", "conv3x3", "relu", 16, 5, 8, H=12, W=12, h=0.1)) == 0
+    assert L.lp_dsig_bytes(L.problem("f32", "conv3x3", "relu", 16, 5, 8, H=12, W=12, h=0.1)) == 16 * 5 * 8 * 144
+    assert L.lp_dsig_bytes(L.problem("f32", "conv3x3", "tanh", 16, 5, 8, H=28, W=28, h=0.1)) == 16 * 5 * 8 * 784 * 4
+    assert L.lp_dsig_bytes(L.problem("f64", "conv3x3", "tanh", 16, 5, 8, H=28, W=28, h=0.1)) == 0
     monkeypatch.setenv("LP_DENSE_PATH", "valu")
     assert L.lp_dsig_bytes(_p()) == 0
     monkeypatch.delenv("LP_DENSE_PATH")

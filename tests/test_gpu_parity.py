@@ -313,7 +313,8 @@ def test_one_shot_training_matches_oracle():
 
 # fp32 widths on the matrix cores with a non-identity activation: the ones that keep a sigma' record
 RECORDED = [DENSE[1], DENSE[2], DENSE[3],
-            ("srelu32", WORKLOADS[2].with_overrides(act="smoothrelu", N=32, B=77, max_levels=2))]
+            ("srelu32", WORKLOADS[2].with_overrides(act="smoothrelu", N=32, B=77, max_levels=2)),
+            DENSE[6], DENSE[7]]
 
 
 def _check_record(c, U, rec):
@@ -370,7 +371,7 @@ def test_sigma_record_in_mgrit(name, wl, relax):
     assert_close(dK2.cpu().numpy(), dK1.double().cpu().numpy(), wl.dtype, "dK record vs recompute")
 
 
-@pytest.mark.parametrize("name,wl", RECORDED[:2], ids=[n for n, _ in RECORDED[:2]])
+@pytest.mark.parametrize("name,wl", RECORDED[:2] + RECORDED[4:], ids=[n for n, _ in RECORDED[:2] + RECORDED[4:]])
 def test_sigma_record_in_serial_solves(name, wl):
     """The serial forward writes the record for every layer; the serial adjoint
     that reads it matches the recomputing one bit for bit. A one-level MGRIT
