@@ -329,23 +329,24 @@ def main():
     dK, db = torch.empty_like(K), torch.empty_like(b)
 
     note(f"cfg{wl.cfg} inputs on the GPU")
+    # the forward's final sweep keeps sigma'(z) for the adjoint and the gradient
+    rec_e = 0 if args.no_record else record_bytes(wl)
+    rec = L.alloc_dsig(p) if rec_e else None
     # iteration counts: fixed by the workload, or found once with its stop rule
     fwd_iters, adj_iters = wl.fwd_iters, wl.adj_iters
     if wl.rtol > 0 or wl.stag > 0:
         mg = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, wl.fwd_iters, False, wl.rtol, wl.stag)
         ws = L.alloc_workspace(p, mg)
-        fwd_iters, _ = L.lp_mgrit_forward(p, mg, K, b, U, ws)
+        fwd_iters, _ = L.lp_mgrit_forward(p, mg, K, b, U, ws, dsig=rec)
         L.lp_loss_terminal(p, wl.n_classes, U[-1], W, mu, c, J, Lam[-1], dW, dmu, ws)
         adj_iters, _ = L.lp_mgrit_adjoint(p, L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax,
-                                                     wl.adj_iters, False, wl.rtol, wl.stag), K, b, U, Lam, ws)
+                                                     wl.adj_iters, False, wl.rtol, wl.stag), K, b, U, Lam, ws,
+                                          dsig=rec)
         del ws
     mgF = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, fwd_iters)
     mgA = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, adj_iters)
     ws = L.alloc_workspace(p, mgF if fwd_iters >= adj_iters else mgA)
     hist = {}
-    # the forward's final sweep keeps sigma'(z) for the adjoint and the gradient
-    rec_e = 0 if args.no_record else record_bytes(wl)
-    rec = L.alloc_dsig(p) if rec_e else None
 
     def step(history=False):
         # the residual histories are read back (a host round trip) only when asked
