@@ -15,6 +15,9 @@
 // Adjoint step (Section 3.2):  v <- v + h_l K_n^T (sigma'(K_n u^n + b_n) * v) (+ g);
 //   the transposed product reads K_n column-wise from the same LDS copy.
 // Sweep modes follow Algorithm 1 exactly as the VALU kernels do (lp_dense_impl.h).
+#include <stdlib.h>
+#include <string.h>
+
 #include "lp_device.h"
 #include "lp_internal.h"
 
@@ -638,6 +641,337 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
   }
 }
 
+// ------------------------------------------------------------------ interval-resident sweeps
+// With c = 4 the sweeps of the width-32 layers are latency-bound when every step
+// waits on its own rows behind a barrier. These variants stage the weights of all
+// the interval's layers in LDS at once and request every row the interval reads
+// (right-hand-side rows, sigma' record or primal rows, the second C-point) before
+// the first step, so a workgroup waits on memory about once, and the step loop
+// has no barrier. Arithmetic and operand order are those of k_fwd / k_adj, step
+// by step. Lanes past the batch read example 0's rows (valid memory) and store
+// nothing; in the matrix-core products every example is its own column, so those
+// lanes do not touch the others' results.
+constexpr int IV_CF = 4;
+
+// Weights and biases of NL consecutive layers in flight between global memory and LDS.
+template <int Q, int NL, int WAVES>
+struct WAll {
+  static constexpr int NT = 64 * WAVES;
+  static constexpr int KV = Q * Q / 4;  // float4 slots of one K_n
+  static constexpr int BV = Q / 4;      // float4 slots of one b_n
+  static constexpr int PK = (NL * KV + NT - 1) / NT;
+  static constexpr int PB = (NL * BV + NT - 1) / NT;
+  f32x4 k[PK];
+  f32x4 b[PB];
+};
+
+// Slot j holds fine layer (n0 + dn j) * stride.
+template <int Q, int NL, int WAVES>
+__device__ __forceinline__ void wall_fetch(WAll<Q, NL, WAVES>& r, const float* __restrict__ K,
+                                           const float* __restrict__ b, long n0, long dn, long stride) {
+  using A = WAll<Q, NL, WAVES>;
+#pragma unroll
+  for (int p = 0; p < A::PK; ++p) {
+    const int idx = threadIdx.x + p * A::NT;
+    if (idx < NL * A::KV) {
+      const int j = idx / A::KV, w = idx - j * A::KV;
+      r.k[p] = reinterpret_cast<const f32x4*>(K + (size_t)((n0 + dn * j) * stride) * (Q * Q))[w];
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < A::PB; ++p) {
+    const int idx = threadIdx.x + p * A::NT;
+    if (idx < NL * A::BV) {
+      const int j = idx / A::BV, w = idx - j * A::BV;
+      r.b[p] = reinterpret_cast<const f32x4*>(b + (size_t)((n0 + dn * j) * stride) * Q)[w];
+    }
+  }
+}
+
+template <int Q, int NL, int WAVES>
+__device__ __forceinline__ void wall_put(float* sh, const WAll<Q, NL, WAVES>& r) {
+  using A = WAll<Q, NL, WAVES>;
+  using C = Cfg<Q, WAVES>;
+#pragma unroll
+  for (int p = 0; p < A::PK; ++p) {
+    const int idx = threadIdx.x + p * A::NT;
+    if (idx < NL * A::KV) {
+      const int j = idx / A::KV, w = idx - j * A::KV;
+      const int el = w * 4, row = el / Q, col = el - row * Q;
+      *reinterpret_cast<f32x4*>(sh + j * C::WSZ + row * C::LD + col) = r.k[p];
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < A::PB; ++p) {
+    const int idx = threadIdx.x + p * A::NT;
+    if (idx < NL * A::BV) {
+      const int j = idx / A::BV, w = idx - j * A::BV;
+      *reinterpret_cast<f32x4*>(sh + j * C::WSZ + Q * C::LD + w * 4) = r.b[p];
+    }
+  }
+}
+
+// A sigma' record row as loaded: the raw bytes of ReLU's 0/1 record (one word per
+// block) or the fp32 values of the smooth activations.
+template <typename Lt, bool BYTES>
+struct RecRow;
+template <typename Lt>
+struct RecRow<Lt, true> {
+  uint32_t w[Lt::NB];
+  __device__ void load(const void* rec, size_t off) {
+    const uint8_t* p = static_cast<const uint8_t*>(rec) + off;
+#pragma unroll
+    for (int mb = 0; mb < Lt::NB; ++mb) w[mb] = *reinterpret_cast<const uint32_t*>(p + 16 * mb);
+  }
+  __device__ void get(typename Lt::V (&d)[Lt::NB]) const {
+#pragma unroll
+    for (int mb = 0; mb < Lt::NB; ++mb)
+#pragma unroll
+      for (int r = 0; r < Lt::NV; ++r) d[mb][r] = (w[mb] >> (8 * r)) & 0xffu ? 1.f : 0.f;
+  }
+};
+template <typename Lt>
+struct RecRow<Lt, false> {
+  typename Lt::V v[Lt::NB];
+  __device__ void load(const void* rec, size_t off) { Lt::load(v, static_cast<const float*>(rec) + off); }
+  __device__ void get(typename Lt::V (&d)[Lt::NB]) const {
+#pragma unroll
+    for (int mb = 0; mb < Lt::NB; ++mb) d[mb] = v[mb];
+  }
+};
+
+// REC: the final F-relaxation writes the sigma' record (CORRF only).
+// HASG: the level has right-hand-side rows (every level but the finest).
+template <int Q, int MODE, int WAVES, bool REC, bool HASG>
+__global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
+  constexpr int EX = 16;
+  using C = Cfg<Q, WAVES>;
+  using Lt = Lay<Q, EX>;
+  using V = typename Lt::V;
+  constexpr int NB = Lt::NB, NV = Lt::NV;
+  constexpr bool rec = REC && MODE == SWEEP_CORRF;
+  constexpr int NS = MODE == SWEEP_CORRF ? IV_CF - 1 : IV_CF;
+  constexpr int NL = NS + (rec ? 1 : 0);
+  __shared__ float W[NL * C::WSZ];
+  __shared__ double red[WAVES];
+  const int lane = threadIdx.x & 63;
+  const int k = blockIdx.y;
+  const int Nc = gridDim.y;
+  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * EX + (lane % EX);
+  const bool on = e < a.B;
+  const size_t slice = (size_t)a.B * Q;
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane / EX);
+  float* X = static_cast<float*>(a.X);
+  const float* G = static_cast<const float*>(a.G);
+  const float* Cs = static_cast<const float*>(a.Cs);
+  const float* Vn = static_cast<const float*>(a.V);
+  const float hl = (float)a.hl, hc = (float)a.hc;
+  const long kc = (long)k * IV_CF;
+
+  WAll<Q, NL, WAVES> wr;
+  wall_fetch<Q, NL, WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), kc, 1, a.stride);
+  V v[NB], cn[NB], g[HASG ? NS : 1][NB];
+  if (MODE == SWEEP_FC) {
+    // a pending coarse-grid correction of the previous cycle is applied on the fly
+    if (Vn) correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+    else Lt::load(v, X + kc * slice + row);
+  } else if (MODE == SWEEP_FRES) {
+    Lt::load(v, Cs + (size_t)k * a.cs_stride * slice + row);
+    Lt::load(cn, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
+  } else {
+    correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+  }
+  if constexpr (HASG) {
+#pragma unroll
+    for (int j = 0; j < NS; ++j) Lt::load(g[j], G + (kc + j + 1) * slice + row);
+  }
+  wall_put<Q, NL, WAVES>(W, wr);
+  __syncthreads();
+  if (on) {
+    if (MODE == SWEEP_FC && k == 0) Lt::store(static_cast<float*>(a.S) + row, v);
+    if (MODE == SWEEP_CORRF && k > 0) Lt::store(X + kc * slice + row, v);
+  }
+
+  V coarse[NB];
+#pragma unroll
+  for (int j = 0; j < NS; ++j) {
+    V s[NB];
+    Lt::template prod<C::LD>(s, v, W + j * C::WSZ, lane);
+    if constexpr (rec) {
+      V dz[NB];
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) dz[mb] = s[mb];
+      apply<V, NB, NV>(dz, a.act, true);
+      if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + j) * a.stride * slice + row, a.act, dz);
+    }
+    apply<V, NB, NV>(s, a.act, false);
+    if (MODE == SWEEP_FRES && j == 0) {
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) coarse[mb] = v[mb] + hc * s[mb];
+    }
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * s[mb];
+    if constexpr (HASG) add_to<V, NB>(v, g[j]);
+    if (MODE == SWEEP_CORRF && on) Lt::store(X + (kc + j + 1) * slice + row, v);
+  }
+
+  if constexpr (rec) {
+    // sigma' of the layer before the next C-point, from the last F-point
+    V z[NB];
+    Lt::template prod<C::LD>(z, v, W + NS * C::WSZ, lane);
+    apply<V, NB, NV>(z, a.act, true);
+    if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + NS) * a.stride * slice + row, a.act, z);
+  }
+  if (MODE == SWEEP_FC) {
+    if (on) Lt::store(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
+  } else if (MODE == SWEEP_FRES) {
+    double acc = 0.0;
+    if (on) {
+      acc = sq_diff<V, NB, NV>(v, cn);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) coarse[mb] = v[mb] - coarse[mb];  // g_{l+1}^{k+1}
+      Lt::store(static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + row, coarse);
+      if (a.xn_every > 0 && (k + 1) % a.xn_every == 0)
+        Lt::store(static_cast<float*>(a.Xn) + (size_t)(k + 1) * slice + row, cn);
+      if (k == 0) {
+        Lt::load(cn, Cs + row);
+        Lt::store(static_cast<float*>(a.Xn) + row, cn);
+      }
+    }
+    if (a.partial) {
+      const double s = wg_sum<WAVES>(acc, red);
+      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
+    }
+  } else if (MODE == SWEEP_CORRF) {
+    if (on && k == Nc - 1) {
+      correct<Lt>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
+      Lt::store(X + (size_t)a.Nl * slice + row, v);
+    }
+  }
+}
+
+// REC: sigma' comes from the record (ReLU: RBYTES, one byte per value) instead of
+// the layer product at the primal state.
+template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG>
+__global__ __launch_bounds__(64 * WAVES) void k_adj_iv(SweepArgs a) {
+  constexpr int EX = 16;
+  using C = Cfg<Q, WAVES>;
+  using Lt = Lay<Q, EX>;
+  using V = typename Lt::V;
+  constexpr int NB = Lt::NB, NV = Lt::NV;
+  constexpr int NS = MODE == SWEEP_CORRF ? IV_CF - 1 : IV_CF;
+  __shared__ float W[NS * C::WSZ];
+  __shared__ double red[WAVES];
+  const int lane = threadIdx.x & 63;
+  const int k = blockIdx.y;
+  const int Nc = gridDim.y;
+  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * EX + (lane % EX);
+  const bool on = e < a.B;
+  const size_t slice = (size_t)a.B * Q;
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane / EX);
+  const float* Uf = static_cast<const float*>(a.Uf);
+  float* X = static_cast<float*>(a.X);
+  const float* G = static_cast<const float*>(a.G);
+  const float* Cs = static_cast<const float*>(a.Cs);
+  const float* Vn = static_cast<const float*>(a.V);
+  const float hl = (float)a.hl, hc = (float)a.hc;
+  const long top = (long)(k + 1) * IV_CF;
+
+  WAll<Q, NS, WAVES> wr;
+  wall_fetch<Q, NS, WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), top - 1, -1,
+                           a.stride);
+  V v[NB], cu[NB], ck[NB];
+  if (MODE == SWEEP_FC) {
+    if (Vn) correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
+    else Lt::load(v, X + top * slice + row);
+  } else if (MODE == SWEEP_FRES) {
+    Lt::load(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
+    Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
+  } else {
+    correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
+  }
+  // step j is linearised at fine index (top - 1 - j) * stride
+  RecRow<Lt, RBYTES> rr[REC ? NS : 1];
+  V u[REC ? 1 : NS][NB];
+  if constexpr (REC) {
+#pragma unroll
+    for (int j = 0; j < NS; ++j) rr[j].load(a.dsig, (size_t)(top - 1 - j) * a.stride * slice + row);
+  } else {
+#pragma unroll
+    for (int j = 0; j < NS; ++j) Lt::load(u[j], Uf + (size_t)(top - 1 - j) * a.stride * slice + row);
+  }
+  V g[HASG ? NS : 1][NB];
+  if constexpr (HASG) {
+#pragma unroll
+    for (int j = 0; j < NS; ++j) Lt::load(g[j], G + (size_t)(top - 1 - j) * slice + row);
+  }
+  wall_put<Q, NS, WAVES>(W, wr);
+  __syncthreads();
+  if (MODE == SWEEP_FRES) {
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb];
+  }
+  if (on) {
+    if (MODE == SWEEP_FC && k == Nc - 1) Lt::store(static_cast<float*>(a.S) + (size_t)Nc * slice + row, v);
+    if (MODE == SWEEP_CORRF && k + 1 < Nc) Lt::store(X + top * slice + row, v);
+  }
+
+#pragma unroll
+  for (int j = 0; j < NS; ++j) {
+    const float* Wj = W + j * C::WSZ;
+    V d[NB], w[NB];
+    if constexpr (REC) {
+      rr[j].get(d);
+    } else {
+      Lt::template prod<C::LD>(d, u[j], Wj, lane);
+      apply<V, NB, NV>(d, a.act, true);
+    }
+    if (MODE == SWEEP_FRES && j == NS - 1) {
+      // coarse adjoint step from the upper C-point, linearised at the same fine state
+      V s2[NB];
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) s2[mb] = d[mb] * cu[mb];
+      Lt::template prod_t<C::LD>(w, s2, Wj, lane);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) cu[mb] = cu[mb] + hc * w[mb];
+    }
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * v[mb];
+    Lt::template prod_t<C::LD>(w, d, Wj, lane);
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * w[mb];
+    if constexpr (HASG) add_to<V, NB>(v, g[j]);
+    if (MODE == SWEEP_CORRF && on) Lt::store(X + (size_t)(top - 1 - j) * slice + row, v);
+  }
+
+  if (MODE == SWEEP_FC) {
+    if (on) Lt::store(static_cast<float*>(a.S) + (size_t)k * slice + row, v);
+  } else if (MODE == SWEEP_FRES) {
+    double acc = 0.0;
+    if (on) {
+      acc = sq_diff<V, NB, NV>(v, ck);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb] - cu[mb];  // g_{l+1}^k
+      Lt::store(static_cast<float*>(a.Gn) + (size_t)k * slice + row, cu);
+      if (a.xn_every > 0 && k % a.xn_every == 0)
+        Lt::store(static_cast<float*>(a.Xn) + (size_t)k * slice + row, ck);
+      if (k == Nc - 1) {
+        Lt::load(ck, Cs + (size_t)Nc * a.cs_stride * slice + row);
+        Lt::store(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, ck);
+      }
+    }
+    if (a.partial) {
+      const double s = wg_sum<WAVES>(acc, red);
+      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
+    }
+  } else if (MODE == SWEEP_CORRF) {
+    if (on && k == 0) {
+      correct<Lt>(v, Cs + row, Vn + row);
+      Lt::store(X + row, v);
+    }
+  }
+}
+
 // ------------------------------------------------------------------ gradient
 // Workgroup (layer n, batch chunk). Each wave takes 32 examples at a time:
 // s = sigma'(K_n u + b_n) * lam^{n+1} in accumulator layout (one matrix-core
@@ -786,6 +1120,41 @@ constexpr int SERIAL_WAVES = 1;  // one wave per serial workgroup (more workgrou
 // per wave and twice the waves.
 constexpr int SWEEP_EX = 16;
 
+// Interval-resident sweeps (c = 4): the level's right-hand side and the record
+// kind select the instantiation.
+template <int Q, bool HASG>
+void sweep_iv(int dir, const SweepArgs& a, dim3 grid, hipStream_t st) {
+  constexpr int W4 = SWEEP_WAVES;
+  const bool rec = a.dsig != nullptr, bytes = a.act == ACT_RELU;
+  if (dir == DIR_FWD) {
+    if (a.mode == SWEEP_FC) launch(k_fwd_iv<Q, SWEEP_FC, W4, false, HASG>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_fwd_iv<Q, SWEEP_FRES, W4, false, HASG>, grid, 64 * W4, 0, st, a);
+    else if (rec) launch(k_fwd_iv<Q, SWEEP_CORRF, W4, true, HASG>, grid, 64 * W4, 0, st, a);
+    else launch(k_fwd_iv<Q, SWEEP_CORRF, W4, false, HASG>, grid, 64 * W4, 0, st, a);
+    return;
+  }
+#define LP_ADJ_IV(MODE)                                                                                    \
+  do {                                                                                                     \
+    if (!rec) launch(k_adj_iv<Q, MODE, W4, false, false, HASG>, grid, 64 * W4, 0, st, a);                  \
+    else if (bytes) launch(k_adj_iv<Q, MODE, W4, true, true, HASG>, grid, 64 * W4, 0, st, a);              \
+    else launch(k_adj_iv<Q, MODE, W4, true, false, HASG>, grid, 64 * W4, 0, st, a);                        \
+  } while (0)
+  if (a.mode == SWEEP_FC) LP_ADJ_IV(SWEEP_FC);
+  else if (a.mode == SWEEP_FRES) LP_ADJ_IV(SWEEP_FRES);
+  else LP_ADJ_IV(SWEEP_CORRF);
+#undef LP_ADJ_IV
+}
+
+// LP_DENSE_SWEEP=staged keeps the double-buffered per-step kernels for c = 4 as
+// well (for comparing the two designs).
+bool iv_enabled() {
+  static const bool on = [] {
+    const char* e = getenv("LP_DENSE_SWEEP");
+    return !(e && strcmp(e, "staged") == 0);
+  }();
+  return on;
+}
+
 template <int Q>
 hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   constexpr int W4 = SWEEP_WAVES, EX = SWEEP_EX;
@@ -793,6 +1162,13 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   if (Nc > 65535) return hipErrorNotSupported;  // intervals index the grid's y dimension
   const dim3 grid((a.B + EX * W4 - 1) / (EX * W4), (unsigned)Nc);
   if (partials) *partials = (int)(grid.x * grid.y);
+  if constexpr (Q == 32) {
+    if (a.c == IV_CF && iv_enabled()) {
+      if (a.G) sweep_iv<Q, true>(dir, a, grid, st);
+      else sweep_iv<Q, false>(dir, a, grid, st);
+      return hipGetLastError();
+    }
+  }
   const bool rec = a.dsig != nullptr;
   if (dir == DIR_FWD) {
     // only the final F-relaxation writes the sigma' record
