@@ -67,7 +67,8 @@ namespace {
 hipEvent_t pool_event() {
   if (g_pool_used == g_event_pool.size()) {
     hipEvent_t e;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    // timing-only events: no system-scope fence (cache writeback) around the traced kernels
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     g_event_pool.push_back(e);
   }
   return g_event_pool[g_pool_used++];
