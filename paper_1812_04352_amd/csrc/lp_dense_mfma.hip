@@ -743,7 +743,8 @@ struct RecRow<Lt, false> {
 // REC: the final F-relaxation writes the sigma' record (CORRF only).
 // HASG: the level has right-hand-side rows (every level but the finest).
 template <int Q, int MODE, int WAVES, bool REC, bool HASG>
-__global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(HASG ? 1 : 8, 8)))
+void k_fwd_iv(SweepArgs a) {
   constexpr int EX = 16;
   using C = Cfg<Q, WAVES>;
   using Lt = Lay<Q, EX>;
@@ -853,7 +854,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
 // REC: sigma' comes from the record (ReLU: RBYTES, one byte per value) instead of
 // the layer product at the primal state.
 template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG>
-__global__ __launch_bounds__(64 * WAVES) void k_adj_iv(SweepArgs a) {
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(!HASG && REC && RBYTES ? 8 : 1, 8)))
+void k_adj_iv(SweepArgs a) {
   constexpr int EX = 16;
   using C = Cfg<Q, WAVES>;
   using Lt = Lay<Q, EX>;
@@ -886,7 +888,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj_iv(SweepArgs a) {
     else Lt::load(v, X + top * slice + row);
   } else if (MODE == SWEEP_FRES) {
     Lt::load(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
-    Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
+    // at eight waves per SIMD (finest level, byte record) the registers go to
+    // occupancy, and the lower C-point is read after the steps
+    if (!(!HASG && REC && RBYTES)) Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
   } else {
     correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
   }
@@ -949,6 +953,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj_iv(SweepArgs a) {
   } else if (MODE == SWEEP_FRES) {
     double acc = 0.0;
     if (on) {
+      if (!HASG && REC && RBYTES) Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
       acc = sq_diff<V, NB, NV>(v, ck);
 #pragma unroll
       for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb] - cu[mb];  // g_{l+1}^k
