@@ -226,30 +226,73 @@ __device__ __forceinline__ float dact_one(float z, int act) {
   }
 }
 
-// The sigma' record at the lane's own output pixels (same layout as the state):
-// a byte 0/1 for ReLU, fp32 otherwise. rec_put takes the pre-activation.
-__device__ __forceinline__ void rec_put(void* rec, size_t off, f32x4 z, const SGeo& g, const Px& p, int act) {
-  if (act == ACT_RELU) {
-    uint8_t* r8 = static_cast<uint8_t*>(rec) + off;
+// The sigma' record of one (layer, example) is a block in the kernels' own tile
+// order: slot (wave w, tile tt, lane) = (w TPW + tt) 64 + lane holds the lane's
+// four values of that tile (its accumulator registers r = 0..3), as one word of
+// four 0/1 bytes for ReLU or as four fp32 values otherwise. Every lane of every
+// tile, ghost tiles included, writes its slot, so a block is whole once written
+// and each lane reads its values with one vector load. Blocks are indexed by
+// layer * B + example.
+__host__ __device__ constexpr size_t rec_block_bytes(const SGeo& g, bool bytes) {
+  return (size_t)g.NW * TPW * 64 * (bytes ? 4 : 16);
+}
+
+// The record values of one lane and tile as loaded (kept packed until used):
+// RB, ReLU's four 0/1 bytes in one word; else four fp32 values.
+template <bool RB>
+struct RecW;
+template <>
+struct RecW<true> {
+  uint32_t w;
+};
+template <>
+struct RecW<false> {
+  f32x4 f;
+};
+
+__device__ __forceinline__ size_t rec_slot(int t, int lane) { return (size_t)t * 64 + lane; }
+
+// rec_put takes the pre-activation of the lane's four values in tile t
+template <bool RB>
+__device__ __forceinline__ void rec_put(void* rec, size_t blk, const SGeo& g, int t, int lane, f32x4 z, int act) {
+  uint8_t* base = static_cast<uint8_t*>(rec) + blk * rec_block_bytes(g, RB);
+  if constexpr (RB) {
+    uint32_t w = 0;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) r8[gl_r(g, p, r)] = z[r] > 0.f ? 1 : 0;
+    for (int r = 0; r < 4; ++r) w |= (z[r] > 0.f ? 1u : 0u) << (8 * r);
+    reinterpret_cast<uint32_t*>(base)[rec_slot(t, lane)] = w;
   } else {
-    float* rf = static_cast<float*>(rec) + off;
+    f32x4 d;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) rf[gl_r(g, p, r)] = dact_one(z[r], act);
+    for (int r = 0; r < 4; ++r) d[r] = dact_one(z[r], act);
+    reinterpret_cast<f32x4*>(base)[rec_slot(t, lane)] = d;
   }
 }
 
-__device__ __forceinline__ f32x4 rec_get(const void* rec, size_t off, const SGeo& g, const Px& p, int act) {
-  f32x4 d;
-  if (act == ACT_RELU) {
-    const uint8_t* r8 = static_cast<const uint8_t*>(rec) + off;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) d[r] = r8[gl_r(g, p, r)] ? 1.f : 0.f;
+template <bool RB>
+__device__ __forceinline__ RecW<RB> rec_load(const void* rec, size_t blk, const SGeo& g, int t, int lane) {
+  const uint8_t* base = static_cast<const uint8_t*>(rec) + blk * rec_block_bytes(g, RB);
+  RecW<RB> r;
+  if constexpr (RB) r.w = reinterpret_cast<const uint32_t*>(base)[rec_slot(t, lane)];
+  else r.f = reinterpret_cast<const f32x4*>(base)[rec_slot(t, lane)];
+  return r;
+}
+
+template <bool RB>
+__device__ __forceinline__ f32x4 rec_val(const RecW<RB>& r) {
+  if constexpr (!RB) {
+    return r.f;
   } else {
-    d = ld_px(static_cast<const float*>(rec) + off, g, p);
+    f32x4 d;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) d[q] = (r.w >> (8 * q)) & 0xffu ? 1.f : 0.f;
+    return d;
   }
-  return d;
+}
+
+template <bool RB>
+__device__ __forceinline__ f32x4 rec_get(const void* rec, size_t blk, const SGeo& g, int t, int lane) {
+  return rec_val<RB>(rec_load<RB>(rec, blk, g, t, lane));
 }
 
 __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
@@ -263,8 +306,10 @@ __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
   return s;
 }
 
-template <int MODE, int GH, int GW, bool REC>
+// RK: the sigma' record kind (0 none, 1 ReLU bytes, 2 fp32 values)
+template <int MODE, int GH, int GW, int RK>
 __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
+  constexpr bool REC = RK != 0, RB = RK == 1;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
   float* buf = lds;               // CH * CS
@@ -341,11 +386,9 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
       conv_tiles(z, wr, buf, g, t0, lane, bias);
     }
     if constexpr (rec) {
+      const size_t blk = (size_t)(kc + j) * a.stride * a.B + blockIdx.y;
 #pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) {
-        const Px p = px_of(g, t0 + tt, lane);
-        if (p.ok) rec_put(a.dsig, (size_t)(kc + j) * a.stride * slice + eo, z[tt], g, p, a.act);
-      }
+      for (int tt = 0; tt < TPW; ++tt) rec_put<RB>(a.dsig, blk, g, t0 + tt, lane, z[tt], a.act);
     }
     act_tiles<false>(z, a.act);
     const float* gi = G ? G + (kc + j + 1) * slice + eo : nullptr;
@@ -376,11 +419,9 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
     float wr[24];
     gather_w<false>(wr, swc, lane);
     conv_tiles(z, wr, buf, g, t0, lane, bias_px(swc, lane));
+    const size_t blk = (size_t)(kc + nsteps) * a.stride * a.B + blockIdx.y;
 #pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) {
-      const Px p = px_of(g, t0 + tt, lane);
-      if (p.ok) rec_put(a.dsig, (size_t)(kc + nsteps) * a.stride * slice + eo, z[tt], g, p, a.act);
-    }
+    for (int tt = 0; tt < TPW; ++tt) rec_put<RB>(a.dsig, blk, g, t0 + tt, lane, z[tt], a.act);
   }
   if (MODE == SWEEP_FC) {
     float* so = static_cast<float*>(a.S) + (size_t)(k + 1) * slice + eo;
@@ -423,8 +464,10 @@ __global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
 // Adjoint step at level point i: d = sigma'(K u + b) with u the fine primal state
 // of point i (or d read from the sigma' record: REC), s = d * lam,
 // lam' = lam + h K^T s (+ g).
-template <int MODE, int GH, int GW, bool REC>
-__global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
+template <int MODE, int GH, int GW, int RK>
+__global__ __launch_bounds__(64 * MAXW) __attribute__((amdgpu_waves_per_eu(RK == 1 ? 4 : RK == 2 ? 3 : 1, 8)))
+void k_adj(SweepArgs a, SGeo ga) {
+  constexpr bool REC = RK != 0, RB = RK == 1;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
   float* buf = lds;               // CH * CS: u, then s
@@ -483,6 +526,12 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
   __syncthreads();
 
   f32x4 dd[TPW];  // sigma'(z) of the step (after the loop: of the last one)
+  // with the record, the words of step j + 1 are requested during step j
+  RecW<RB> rn[REC ? TPW : 1];
+  if constexpr (REC) {
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) rn[tt] = rec_load<RB>(a.dsig, (size_t)(top - 1) * a.stride * a.B + blockIdx.y, g, t0 + tt, lane);
+  }
   for (int j = 0; j < nsteps; ++j) {
     // tile offsets recomputed each step (see k_fwd) where that lowers the
     // register count (compiler-measured per variant)
@@ -495,7 +544,11 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
     // d = sigma'(K u + b)
     if constexpr (REC) {
 #pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) dd[tt] = rec_get(a.dsig, (size_t)i * ustep + eo, g, px_of(g, t0 + tt, lane), a.act);
+      for (int tt = 0; tt < TPW; ++tt) dd[tt] = rec_val<RB>(rn[tt]);
+      if (more) {
+#pragma unroll
+        for (int tt = 0; tt < TPW; ++tt) rn[tt] = rec_load<RB>(a.dsig, (size_t)(i - 1) * a.stride * a.B + blockIdx.y, g, t0 + tt, lane);
+      }
     } else {
       float wr[24];
       gather_w<false>(wr, swc, lane);
@@ -560,7 +613,8 @@ __global__ __launch_bounds__(64 * MAXW) void k_adj(SweepArgs a, SGeo ga) {
       cu[tt] = ld_px(src, g, p);
       // with the record, sigma' of the last step is read again rather than kept
       // live in registers through the loop
-      const f32x4 d = REC ? rec_get(a.dsig, (size_t)(top - nsteps) * ustep + eo, g, p, a.act) : dd[tt];
+      const f32x4 d = REC ? rec_get<RB>(a.dsig, (size_t)(top - nsteps) * a.stride * a.B + blockIdx.y, g, t0 + tt, lane)
+                          : dd[tt];
       if (p.ok) put_px(buf, d * cu[tt], g, p);
     }
     float wt[24];
@@ -683,8 +737,9 @@ __global__ __launch_bounds__(64 * MAXW) void k_resid(ResidArgs a, SGeo g) {
 // and lanes are combined in a fixed order.
 constexpr int GOUT = 16 * 96 + CH;  // dWbig then db per chunk
 
-template <int GH, int GW, bool REC>
+template <int GH, int GW, int RK>
 __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
+  constexpr bool REC = RK != 0, RB = RK == 1;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
   float* bu = lds;                   // CH * CS: u
@@ -743,7 +798,7 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
     if constexpr (REC) {
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt)
-        z[tt] = rec_get(a.dsig, (size_t)n * slice + (size_t)e * g.q, g, px_of(g, t0 + tt, lane), a.act);
+        z[tt] = rec_get<RB>(a.dsig, (size_t)n * a.B + e, g, t0 + tt, lane);
     } else {
       conv_tiles(z, wf, bu, g, t0, lane, bias);
       act_tiles<true>(z, a.act);
@@ -852,32 +907,34 @@ size_t sweep_lds(const conv::SGeo& g) { return (size_t)(conv::CH * g.CS + 2 * co
 // Sweep kernels with the geometry as template arguments (0, 0: runtime).
 // Only the forward CORRF and serial kernels write the record; every adjoint
 // kernel can read it.
-template <int GH, int GW, bool REC>
+template <int GH, int GW, int RK>
 void sweep_kernels(int dir, int mode, void (*&f)(SweepArgs, conv::SGeo)) {
   using namespace conv;
   if (dir == DIR_FWD) {
-    if (mode == SWEEP_FC) f = k_fwd<SWEEP_FC, GH, GW, false>;
-    else if (mode == SWEEP_FRES) f = k_fwd<SWEEP_FRES, GH, GW, false>;
-    else if (mode == SWEEP_CORRF) f = k_fwd<SWEEP_CORRF, GH, GW, REC>;
-    else f = k_fwd<MODE_SERIAL, GH, GW, REC>;
+    if (mode == SWEEP_FC) f = k_fwd<SWEEP_FC, GH, GW, 0>;
+    else if (mode == SWEEP_FRES) f = k_fwd<SWEEP_FRES, GH, GW, 0>;
+    else if (mode == SWEEP_CORRF) f = k_fwd<SWEEP_CORRF, GH, GW, RK>;
+    else f = k_fwd<MODE_SERIAL, GH, GW, RK>;
   } else {
-    if (mode == SWEEP_FC) f = k_adj<SWEEP_FC, GH, GW, REC>;
-    else if (mode == SWEEP_FRES) f = k_adj<SWEEP_FRES, GH, GW, REC>;
-    else if (mode == SWEEP_CORRF) f = k_adj<SWEEP_CORRF, GH, GW, REC>;
-    else f = k_adj<MODE_SERIAL, GH, GW, REC>;
+    if (mode == SWEEP_FC) f = k_adj<SWEEP_FC, GH, GW, RK>;
+    else if (mode == SWEEP_FRES) f = k_adj<SWEEP_FRES, GH, GW, RK>;
+    else if (mode == SWEEP_CORRF) f = k_adj<SWEEP_CORRF, GH, GW, RK>;
+    else f = k_adj<MODE_SERIAL, GH, GW, RK>;
   }
 }
 
 hipError_t launch_conv_sweep(const Shape& s, int dir, const SweepArgs& a, dim3 grid, hipStream_t st) {
   const conv::SGeo g = sweep_geo(s);
   void (*f)(SweepArgs, conv::SGeo) = nullptr;
-  const bool rec = a.dsig != nullptr;
+  const int rk = a.dsig == nullptr ? 0 : a.act == ACT_RELU ? 1 : 2;
   if (s.H == 28 && s.W == 28) {  // MNIST-sized images
-    if (rec) sweep_kernels<28, 28, true>(dir, a.mode, f);
-    else sweep_kernels<28, 28, false>(dir, a.mode, f);
+    if (rk == 1) sweep_kernels<28, 28, 1>(dir, a.mode, f);
+    else if (rk == 2) sweep_kernels<28, 28, 2>(dir, a.mode, f);
+    else sweep_kernels<28, 28, 0>(dir, a.mode, f);
   } else {
-    if (rec) sweep_kernels<0, 0, true>(dir, a.mode, f);
-    else sweep_kernels<0, 0, false>(dir, a.mode, f);
+    if (rk == 1) sweep_kernels<0, 0, 1>(dir, a.mode, f);
+    else if (rk == 2) sweep_kernels<0, 0, 2>(dir, a.mode, f);
+    else sweep_kernels<0, 0, 0>(dir, a.mode, f);
   }
   launch(f, grid, dim3(64 * g.NW), sweep_lds(g), st, a, g);
   return hipGetLastError();
@@ -895,6 +952,8 @@ bool conv_supported(const Shape& s) {
 }
 
 int conv_tile(const Shape&) { return 1; }
+
+size_t conv_dsig_block_bytes(const Shape& s) { return conv::rec_block_bytes(sweep_geo(s), s.act == ACT_RELU); }
 
 int conv_grad_chunks(int B, int N) {
   const int want = (2048 + N - 1) / N;
@@ -941,8 +1000,10 @@ hipError_t conv_grad(const Shape& s, const GradArgs& a, hipStream_t st) {
   const int fl = 2 * conv::CH * g.CS + conv::WV, red = conv::GOUT + 2 * 64 * g.NW;
   const size_t sh = (size_t)(fl > red ? fl : red) * sizeof(float);
   void (*f)(GradArgs, conv::SGeo);
-  if (s.H == 28 && s.W == 28) f = a.dsig ? conv::k_grad<28, 28, true> : conv::k_grad<28, 28, false>;
-  else f = a.dsig ? conv::k_grad<0, 0, true> : conv::k_grad<0, 0, false>;
+  const int rk = a.dsig == nullptr ? 0 : a.act == ACT_RELU ? 1 : 2;
+  if (s.H == 28 && s.W == 28)
+    f = rk == 1 ? conv::k_grad<28, 28, 1> : rk == 2 ? conv::k_grad<28, 28, 2> : conv::k_grad<28, 28, 0>;
+  else f = rk == 1 ? conv::k_grad<0, 0, 1> : rk == 2 ? conv::k_grad<0, 0, 2> : conv::k_grad<0, 0, 0>;
   launch(f, dim3(a.N, a.nchunks), 64 * g.NW, sh, st, a, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;

@@ -546,6 +546,7 @@ size_t lp_dsig_bytes(const lp_problem* p) {
   if (check_problem(p) != LP_OK) return 0;
   g_err.clear();
   if (!lp::dsig_supported(shape_of(p))) return 0;
+  if (p->layer == LP_CONV3X3) return (size_t)p->N * p->B * lp::conv_dsig_block_bytes(shape_of(p));
   const size_t per = p->act == LP_RELU ? 1 : esize(p);
   return (size_t)p->N * p->B * qdim(p) * per;
 }

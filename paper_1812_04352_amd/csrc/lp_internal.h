@@ -62,7 +62,7 @@ struct SweepArgs {
   const void* V;       // CORRF: next level solution
   double* partial;     // FRES: per-workgroup sum of squared residuals (nullable)
   int finest;          // 1 on level 0: the fixed boundary row (u^0 or lam^N) is never written
-  void* dsig;          // sigma' record [N][B][q] (nullable): forward level-0 CORRF writes it
+  void* dsig;          // sigma' record (nullable; dense [N][B][q], conv per-(layer, example) tile blocks): forward level-0 CORRF writes it
                        // (every layer of its intervals), the adjoint reads it at i*stride
 };
 
@@ -155,6 +155,7 @@ hipError_t conv_grad(const Shape& s, const GradArgs& a, hipStream_t st);
 bool conv_supported(const Shape& s);
 int conv_grad_chunks(int B, int N);
 int conv_tile(const Shape& s);
+size_t conv_dsig_block_bytes(const Shape& s);  // sigma' record bytes per (layer, example)
 
 // Common kernels (lp_common.hip)
 hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_row0,

@@ -317,6 +317,28 @@ RECORDED = [DENSE[1], DENSE[2], DENSE[3],
             DENSE[6], DENSE[7]]
 
 
+def _conv_record(rec, N, B, C, H, W, relu):
+    """The convolution record ([N][B] blocks in the kernels' tile order, see
+    lp_dsig_bytes in include/lp.h) rearranged to [N][B][C][H][W]: tile t of 16
+    pair-pixels, lane l: pair-pixel P = 16 t + l % 16 (ghost lanes P >= H/2 W are
+    skipped), value r of the lane = channel 2 (l // 16) + r // 2, row 2 (P // W) +
+    r % 2, column P % W."""
+    npp = H // 2 * W
+    T = -(-(-(-npp // 16)) // 7) * 7
+    raw = rec[: N * B * T * 64 * (4 if relu else 16)].cpu()
+    vals = (raw if relu else raw.view(torch.float32)).numpy().reshape(N, B, T, 64, 4)
+    out = np.zeros((N, B, C, H, W), dtype=vals.dtype)
+    for t in range(T):
+        for l in range(64):
+            P = 16 * t + l % 16
+            if P >= npp:
+                continue
+            Y, x = divmod(P, W)
+            for r in range(4):
+                out[:, :, 2 * (l // 16) + r // 2, 2 * Y + r % 2, x] = vals[:, :, t, l, r]
+    return out.reshape(N, B, C * H * W)
+
+
 def _check_record(c, U, rec):
     """The record against sigma'(K_n u_n + b_n) evaluated by the oracle in fp64 at
     the trajectory the GPU returned. ReLU's 0/1 bytes may differ from the fp64
@@ -325,6 +347,15 @@ def _check_record(c, U, rec):
     Uh = U.double().cpu().numpy()
     z = np.stack([O.preact(c.d["K"][n], c.d["b"][n], Uh[n]) for n in range(wl.N)])
     want = O.dact(z, wl.act)
+    if wl.layer == "conv3x3":
+        got = _conv_record(rec, wl.N, wl.B, wl.C, wl.H, wl.W, wl.act == "relu").reshape(z.shape)
+        if wl.act == "relu":
+            assert set(np.unique(got)) <= {0, 1}
+            bad = got != want
+            assert np.all(np.abs(z[bad]) <= 1e-5 * np.abs(z).max()), f"{bad.sum()} wrong record bytes"
+        else:
+            np.testing.assert_allclose(got, want, rtol=0, atol=2e-5)
+        return
     if wl.act == "relu":
         got = rec[: z.size].cpu().numpy().reshape(z.shape)
         assert set(np.unique(got)) <= {0, 1}
