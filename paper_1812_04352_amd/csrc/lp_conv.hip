@@ -308,7 +308,8 @@ __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
 
 // RK: the sigma' record kind (0 none, 1 ReLU bytes, 2 fp32 values)
 template <int MODE, int GH, int GW, int RK>
-__global__ __launch_bounds__(64 * MAXW) void k_fwd(SweepArgs a, SGeo ga) {
+__global__ __launch_bounds__(64 * MAXW)
+__attribute__((amdgpu_waves_per_eu(MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 4 : 1, 8))) void k_fwd(SweepArgs a, SGeo ga) {
   constexpr bool REC = RK != 0, RB = RK == 1;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
