@@ -497,7 +497,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
 // Interval k runs from its upper C-point (k+1)c down to kc; step j produces level
 // point i = (k+1)c-1-j, linearised at the fine state of index i*stride.
 template <int Q, int MODE, int WAVES, int EX, bool REC>
-__global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
+__global__ __launch_bounds__(64 * WAVES)
+__attribute__((amdgpu_waves_per_eu(Q == 64 && REC && MODE != MODE_SERIAL ? (MODE == SWEEP_FRES ? 3 : 4) : 1, 8))) void k_adj(SweepArgs a) {
   using C = Cfg<Q, WAVES>;
   using Lt = Lay<Q, EX>;
   using V = typename Lt::V;
@@ -553,11 +554,16 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
   // stored); the sweeps keep the registers for occupancy instead.
   constexpr bool PF = MODE == MODE_SERIAL;
   constexpr bool rec = REC;  // sigma' from the record instead of K u + b
-  V un[NB], gn[NB];
+  // the record row of the next step is requested one step ahead by the serial
+  // solve and, at width 64, by the sweeps (whose occupancy the extra registers
+  // do not lower there)
+  constexpr bool PFR = rec && (PF || Q == 64);
+  V un[NB], gn[NB], rn[NB];
   if (PF) {
     if (!rec) Lt::load(un, Uf + (size_t)(top - 1) * a.stride * slice + row);
     if (G) Lt::load(gn, G + (size_t)(top - 1) * slice + row);
   }
+  if (PFR) load_dsig<Lt>(rn, a.dsig, (size_t)(top - 1) * a.stride * slice + row, a.act);
   for (int j = 0; j < nsteps; ++j) {
     const long i = top - 1 - j;
     w_fetch<Q, WAVES>(wr, K, bb, (size_t)(j + 1 < nsteps ? i - 1 : i) * a.stride);
@@ -569,7 +575,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_adj(SweepArgs a) {
     }
     if constexpr (rec) {
       // every lane reads a valid row; columns of lanes past the batch are never stored
-      load_dsig<Lt>(d, a.dsig, (size_t)i * a.stride * slice + row, a.act);
+      if constexpr (PFR) {
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) d[mb] = rn[mb];
+        if (j + 1 < nsteps) load_dsig<Lt>(rn, a.dsig, (size_t)(i - 1) * a.stride * slice + row, a.act);
+      } else {
+        load_dsig<Lt>(d, a.dsig, (size_t)i * a.stride * slice + row, a.act);
+      }
     } else {
       V u[NB];
       if (PF) {
