@@ -154,7 +154,7 @@ def kernel_kind(name: str):
     import re
     if "k_grad<" in name or "k_grad_partial<" in name:
         return "gradient"
-    m = re.search(r"lp::(mfma|conv|dense)::k_(fwd|adj)(_sweep|_serial)?<([^>]*)>", name)
+    m = re.search(r"lp::(mfma|conv|dense)::k_(fwd|adj)(_sweep|_serial|_iv)?<([^>]*)>", name)
     if not m:
         return None
     fam, d, suffix, targs = m.groups()
