@@ -755,8 +755,7 @@ struct RecRow<Lt, false> {
 // REC: the final F-relaxation writes the sigma' record (CORRF only).
 // HASG: the level has right-hand-side rows (every level but the finest).
 template <int Q, int MODE, int WAVES, bool REC, bool HASG>
-__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(HASG ? 1 : 8, 8)))
-void k_fwd_iv(SweepArgs a) {
+__global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
   constexpr int EX = 16;
   using C = Cfg<Q, WAVES>;
   using Lt = Lay<Q, EX>;
