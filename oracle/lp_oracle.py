@@ -352,8 +352,26 @@ def _fwd_C_relax(H, K, b, kind, l):
         u[k * c] = new[k - 1]
 
 
-def _fwd_cycle(H, K, b, kind, relax, l, rho_out):
-    """One FAS V-cycle on level l (Algorithm 1, with step 3 a recursive call)."""
+# C-relaxations in one relaxation sweep: F, FCF (the paper's default, Section
+# 3.1.1) and FCFCF (one more C- and F-relaxation pair)
+C_SWEEPS = {"F": 0, "FCF": 1, "FCFCF": 2}
+
+
+def _coarse_solves(cycle, l, L):
+    """Cycles that solve the coarse problem of level l (Algorithm 1, step 3) on level
+    l + 1: a V-cycle is one recursive V-cycle; an F-cycle (the multigrid F-cycle the
+    paper mentions for visiting coarse grids more often) is a recursive F-cycle
+    followed by a V-cycle, the latter left out when level l + 1 is the coarsest
+    (whose solve is exact, so a second one changes nothing)."""
+    if cycle == "V":
+        return ["V"]
+    if cycle == "F":
+        return ["F"] if l + 1 == L - 1 else ["F", "V"]
+    raise ValueError(f"unknown cycle {cycle!r}")
+
+
+def _fwd_cycle(H, K, b, kind, relax, l, rho_out, cycle="V"):
+    """One FAS cycle on level l (Algorithm 1, with step 3 recursive: V- or F-cycle)."""
     c, L = H.cf, len(H.sizes)
     u, g = H.u[l], H.g[l]
     Nl = H.sizes[l]
@@ -362,9 +380,9 @@ def _fwd_cycle(H, K, b, kind, relax, l, rho_out):
         for i in range(1, Nl + 1):
             u[i] = _fwd_step(H, K, b, kind, l, i - 1, u[i - 1]) + g[i]
         return
-    # Step 1: F- or FCF-relaxation.
+    # Step 1: F-, FCF- or FCFCF-relaxation.
     _fwd_F_relax(H, K, b, kind, l)
-    if relax == "FCF":
+    for _ in range(C_SWEEPS[relax]):
         _fwd_C_relax(H, K, b, kind, l)
         _fwd_F_relax(H, K, b, kind, l)
     # Step 2: residual at the C-points and restriction by injection.
@@ -388,8 +406,9 @@ def _fwd_cycle(H, K, b, kind, relax, l, rho_out):
     for k in range(1, Nc + 1):
         gc[k] = f[k] - _fwd_step(H, K, b, kind, l + 1, k - 1, uc[k - 1])
     H.u[l + 1], H.g[l + 1] = uc, gc
-    # Step 3: solve the coarse residual equation (recursively: V-cycle).
-    _fwd_cycle(H, K, b, kind, relax, l + 1, rho_out)
+    # Step 3: solve the coarse residual equation (recursively).
+    for cyc in _coarse_solves(cycle, l, L):
+        _fwd_cycle(H, K, b, kind, relax, l + 1, rho_out, cyc)
     # Steps 4-5: E = V - U at the C-points, U^{kc} <- U^{kc} + E^k, then F-relaxation.
     V = H.u[l + 1]
     for k in range(1, Nc + 1):
@@ -399,8 +418,9 @@ def _fwd_cycle(H, K, b, kind, relax, l, rho_out):
 
 
 def mgrit_forward(U, K, b, h, kind, cf=4, max_levels=2, min_coarse=1, relax="FCF",
-                  max_iter=1, rtol=0.0, stag=0.0, warm_start=False):
-    """Solve A(U, theta) = G (eq. nonlinear_mgrit) with MGRIT/FAS iterations.
+                  max_iter=1, rtol=0.0, stag=0.0, warm_start=False, cycle="V"):
+    """Solve A(U, theta) = G (eq. nonlinear_mgrit) with MGRIT/FAS iterations: V- or
+    F-cycles (cycle "V" | "F"), with F-, FCF- or FCFCF-relaxation.
 
     U [N+1][...] holds u^0 in row 0; with warm_start the other rows are the initial
     guess, else the C-points start as copies of u^0 (a generic initial condition,
@@ -423,7 +443,7 @@ def mgrit_forward(U, K, b, h, kind, cf=4, max_levels=2, min_coarse=1, relax="FCF
     hist = []
     it = 0
     for m in range(1, max_iter + 1):
-        _fwd_cycle(H, K, b, kind, relax, 0, hist)
+        _fwd_cycle(H, K, b, kind, relax, 0, hist, cycle)
         it = m
         if len(sizes) == 1:
             hist.append(0.0)
@@ -461,7 +481,7 @@ def _adj_C_relax(H, U, K, b, kind, l):
         lam[k * c] = new[k]
 
 
-def _adj_cycle(H, U, K, b, kind, relax, l, rho_out):
+def _adj_cycle(H, U, K, b, kind, relax, l, rho_out, cycle="V"):
     """Algorithm 1 on the adjoint system A_U(Lam) = G_U (eq. adjointMGRIT), whose
     block rows run backwards in the layer index."""
     c, L = H.cf, len(H.sizes)
@@ -472,7 +492,7 @@ def _adj_cycle(H, U, K, b, kind, relax, l, rho_out):
             lam[i] = _adj_step(H, U, K, b, kind, l, i, lam[i + 1]) + g[i]
         return
     _adj_F_relax(H, U, K, b, kind, l)
-    if relax == "FCF":
+    for _ in range(C_SWEEPS[relax]):
         _adj_C_relax(H, U, K, b, kind, l)
         _adj_F_relax(H, U, K, b, kind, l)
     Nc = Nl // c
@@ -492,7 +512,8 @@ def _adj_cycle(H, U, K, b, kind, relax, l, rho_out):
     for k in range(Nc):
         gc[k] = f[k] - _adj_step(H, U, K, b, kind, l + 1, k, lc[k + 1])
     H.u[l + 1], H.g[l + 1] = lc, gc
-    _adj_cycle(H, U, K, b, kind, relax, l + 1, rho_out)
+    for cyc in _coarse_solves(cycle, l, L):
+        _adj_cycle(H, U, K, b, kind, relax, l + 1, rho_out, cyc)
     V = H.u[l + 1]
     for k in range(Nc):
         E = V[k] - lam[k * c]
@@ -501,7 +522,7 @@ def _adj_cycle(H, U, K, b, kind, relax, l, rho_out):
 
 
 def mgrit_adjoint(U, Lam, K, b, h, kind, cf=4, max_levels=2, min_coarse=1, relax="FCF",
-                  max_iter=1, rtol=0.0, stag=0.0, warm_start=False):
+                  max_iter=1, rtol=0.0, stag=0.0, warm_start=False, cycle="V"):
     """Solve the adjoint system (eq. adjointMGRIT) with MGRIT, the primal trajectory U
     fixed. Lam [N+1][...] holds the terminal value lam^N in row N; with warm_start
     the other rows are the initial guess, else the C-points kc (k < N/c) start as
@@ -520,7 +541,7 @@ def mgrit_adjoint(U, Lam, K, b, h, kind, cf=4, max_levels=2, min_coarse=1, relax
     hist = []
     it = 0
     for m in range(1, max_iter + 1):
-        _adj_cycle(H, U, K, b, kind, relax, 0, hist)
+        _adj_cycle(H, U, K, b, kind, relax, 0, hist, cycle)
         it = m
         if len(sizes) == 1:
             hist.append(0.0)

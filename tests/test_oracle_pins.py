@@ -283,15 +283,17 @@ def _mgrit_case(seed=20, N=32, B=6, q=5, act="tanh", kscale=0.4):
     return K, b, u0, 5.0 / N
 
 
-@pytest.mark.parametrize("relax,gain", [("F", 1), ("FCF", 2)])
+@pytest.mark.parametrize("relax,gain", [("F", 1), ("FCF", 2), ("FCFCF", 3)])
 def test_two_level_finite_step_exactness_forward(relax, gain):
-    # two-level F: after m iterations points n <= (m+1)c-1 are exact; FCF: n <= (2m+1)c-1
+    # two-level F: after m iterations points n <= (m+1)c-1 are exact; FCF: n <= (2m+1)c-1;
+    # FCFCF: n <= (3m+1)c-1 (each C-relaxation moves the exact front by one interval,
+    # the coarse-grid correction by one more)
     K, b, u0, h = _mgrit_case()
     N, c = K.shape[0], 4
     S = O.serial_forward(u0, K, b, h, "tanh")
     U = np.zeros_like(S)
     U[0] = u0
-    full = N // c if relax == "F" else -(-N // (2 * c))
+    full = -(-N // (gain * c))
     for m in range(1, full + 1):
         Um, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=c, max_levels=2, relax=relax, max_iter=m)
         exact = min((gain * m + 1) * c - 1, N)
@@ -302,7 +304,7 @@ def test_two_level_finite_step_exactness_forward(relax, gain):
     assert np.abs(Um - S).max() < 1e-14
 
 
-@pytest.mark.parametrize("relax,gain", [("F", 1), ("FCF", 2)])
+@pytest.mark.parametrize("relax,gain", [("F", 1), ("FCF", 2), ("FCFCF", 3)])
 def test_two_level_finite_step_exactness_adjoint(relax, gain):
     K, b, u0, h = _mgrit_case(seed=21)
     N, c = K.shape[0], 4
@@ -311,7 +313,7 @@ def test_two_level_finite_step_exactness_adjoint(relax, gain):
     S = O.serial_adjoint(U, lamN, K, b, h, "tanh")
     L = np.zeros_like(S)
     L[N] = lamN
-    full = N // c if relax == "F" else -(-N // (2 * c))
+    full = -(-N // (gain * c))
     for m in range(1, full + 1):
         Lm, _, _ = O.mgrit_adjoint(U, L, K, b, h, "tanh", cf=c, max_levels=2, relax=relax, max_iter=m)
         exact = min((gain * m + 1) * c - 1, N)
@@ -528,8 +530,9 @@ def test_workload_generator_is_deterministic_and_rounded():
     assert s.shape == (1, 10, 32) and s.dtype == np.float32
 
 
-@pytest.mark.parametrize("levels,relax", [(2, "F"), (3, "F"), (3, "FCF"), (4, "FCF")])
-def test_exact_coarse_propagators_solve_in_one_vcycle(levels, relax):
+@pytest.mark.parametrize("levels,relax,cycle", [(2, "F", "V"), (3, "F", "V"), (3, "FCF", "V"), (4, "FCF", "V"),
+                                                (3, "F", "F"), (4, "FCFCF", "F"), (4, "FCFCF", "V")])
+def test_exact_coarse_propagators_solve_in_one_vcycle(levels, relax, cycle):
     # Affine steps with a nilpotent K (K^2 = 0) and a bias in K's null space: c^l fine
     # steps of size h equal exactly one step of size c^l h, so the coarse grids of every
     # level represent their fine grids exactly and one V-cycle reaches the serial
@@ -549,14 +552,14 @@ def test_exact_coarse_propagators_solve_in_one_vcycle(levels, relax):
     U = r.standard_normal(S.shape)
     U[0] = u0
     Um, _, _ = O.mgrit_forward(U, K, b, h, "identity", cf=4, max_levels=levels, relax=relax,
-                               max_iter=1, warm_start=True)
+                               max_iter=1, warm_start=True, cycle=cycle)
     assert rel(Um, S) < 1e-13
     lamN = r.standard_normal((B, q))
     Ls = O.serial_adjoint(S, lamN, K, b, h, "identity")
     L0 = r.standard_normal(S.shape)
     L0[N] = lamN
     Lm, _, _ = O.mgrit_adjoint(S, L0, K, b, h, "identity", cf=4, max_levels=levels, relax=relax,
-                               max_iter=1, warm_start=True)
+                               max_iter=1, warm_start=True, cycle=cycle)
     assert rel(Lm, Ls) < 1e-13
 
 
@@ -617,3 +620,77 @@ def test_reported_residual_is_full_grid_residual_of_relaxed_iterate(levels, rela
             for n in range((k + 1) * 4 - 1, k * 4, -1):
                 Lr[n] = O.phibar(Lr[n + 1], S[n], K[n], b[n], h, kind)
     assert abs(hist[0] - O.residual_norm_adjoint(S, Lr, K, b, h, kind)) <= 1e-12 * hist[0]
+
+
+# ---------------------------------------------------------------- F-cycles
+
+@pytest.mark.parametrize("relax,N", [("F", 32), ("FCF", 64)])
+def test_fcycle_with_exactly_solved_level_one_equals_two_level(relax, N):
+    # c = 4, three levels: level 1 has N/4 points in N/16 coarse intervals. An
+    # F-cycle solves level 1's coarse problem with two two-level cycles (the
+    # recursive F-cycle, then the V-cycle), and two-level MGRIT with F-relaxation is
+    # exact on 2 intervals after 2 iterations (FCF: on 4 intervals after 2), so the
+    # three-level F-cycle must coincide with the two-level V-cycle, iterate by
+    # iterate, forward and adjoint. A three-level V-cycle (one level-1 cycle) does not.
+    K, b, u0, h = _mgrit_case(seed=31, N=N)
+    N = K.shape[0]
+    U = np.zeros((N + 1,) + u0.shape)
+    U[0] = u0
+    for m in (1, 2, 3):
+        F3, hF, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=3, relax=relax, max_iter=m, cycle="F")
+        V2, hV, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=2, relax=relax, max_iter=m)
+        V3, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=3, relax=relax, max_iter=m)
+        assert rel(F3, V2) < 1e-13 and np.allclose(hF, hV, rtol=1e-12, atol=0), m
+        if m == 1:
+            assert rel(V3, V2) > 1e-8
+    S = O.serial_forward(u0, K, b, h, "tanh")
+    lamN = np.random.default_rng(3).standard_normal(u0.shape)
+    Lm = np.zeros_like(S)
+    Lm[N] = lamN
+    for m in (1, 2):
+        F3, _, _ = O.mgrit_adjoint(S, Lm, K, b, h, "tanh", cf=4, max_levels=3, relax=relax, max_iter=m, cycle="F")
+        V2, _, _ = O.mgrit_adjoint(S, Lm, K, b, h, "tanh", cf=4, max_levels=2, relax=relax, max_iter=m)
+        assert rel(F3, V2) < 1e-13, m
+
+
+def test_fcycle_on_two_levels_is_the_vcycle():
+    K, b, u0, h = _mgrit_case(seed=32, N=24)
+    U = np.zeros((25,) + u0.shape)
+    U[0] = u0
+    a, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=2, max_iter=2, cycle="F")
+    v, _, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=2, max_iter=2, cycle="V")
+    assert np.array_equal(a, v)
+
+
+@pytest.mark.parametrize("act", ["tanh", "relu", "smoothrelu"])
+@pytest.mark.parametrize("relax,cycle", [("FCFCF", "V"), ("FCF", "F"), ("F", "F")])
+def test_cycle_variants_converge_to_the_serial_solution(act, relax, cycle):
+    # the serial trajectory is the fixed point of every cycle (FAS), and with five
+    # levels the iteration reaches it
+    K, b, u0, h = _mgrit_case(seed=33, N=256, B=4, q=6, act=act, kscale=0.3)
+    N = K.shape[0]
+    S = O.serial_forward(u0, K, b, h, act)
+    U = np.zeros_like(S)
+    U[0] = u0
+    Um, hist, it = O.mgrit_forward(U, K, b, h, act, cf=4, max_levels=5, relax=relax, cycle=cycle, max_iter=40,
+                                   rtol=1e-13)
+    assert rel(Um, S) < 1e-11, (it, hist[-3:])
+    lamN = np.random.default_rng(4).standard_normal(u0.shape)
+    Ls = O.serial_adjoint(S, lamN, K, b, h, act)
+    L0 = np.zeros_like(S)
+    L0[N] = lamN
+    Lm, _, it = O.mgrit_adjoint(S, L0, K, b, h, act, cf=4, max_levels=5, relax=relax, cycle=cycle, max_iter=40,
+                                rtol=1e-13)
+    assert rel(Lm, Ls) < 1e-11, it
+
+
+def test_fcycle_converges_no_slower_than_the_vcycle():
+    # more work on the coarse grids per cycle: after a few cycles the F-cycle's
+    # residual is below the V-cycle's on a five-level hierarchy
+    K, b, u0, h = _mgrit_case(seed=34, N=1024, B=3, q=5, kscale=0.5)
+    U = np.zeros((1025,) + u0.shape)
+    U[0] = u0
+    _, hV, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=5, relax="FCF", max_iter=4, cycle="V")
+    _, hF, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=5, relax="FCF", max_iter=4, cycle="F")
+    assert hF[0] == hV[0]  # the first residual is taken before any coarse-grid work
+    assert hF[-1] < hV[-1]
