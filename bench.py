@@ -15,6 +15,7 @@ the library on the launch stream over the timed steps, and compared with its
 algorithmic bytes or flops (the model below) to give the roofline fraction.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--no-cpu]
+                       [--relax F|FCF|FCFCF] [--cycle V|F] [--no-record]
 """
 from __future__ import annotations
 
@@ -41,6 +42,24 @@ def level_sizes(N, cf, max_levels, min_coarse):
     while len(sizes) < max_levels and sizes[-1] > min_coarse:
         sizes.append(sizes[-1] // cf)
     return sizes
+
+
+def level_visits(L: int, cycle: str):
+    """Times each level is visited by one cycle from the finest level: a V-cycle
+    visits every level once; an F-cycle solves each coarse problem with an F-cycle
+    and then a V-cycle (the V-cycle left out above the coarsest level)."""
+    v = [0] * L
+
+    def go(l, cyc):
+        v[l] += 1
+        if l == L - 1:
+            return
+        go(l + 1, "F" if cyc == "F" else "V")
+        if cyc == "F" and l + 2 < L:
+            go(l + 1, "V")
+
+    go(0, cycle)
+    return v
 
 
 def record_bytes(wl) -> int:
@@ -74,7 +93,9 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
     row = B * q * e
     sizes = level_sizes(wl.N, c, wl.max_levels, wl.min_coarse)
     L = len(sizes)
-    fcf = wl.relax == "FCF"
+    fcf = wl.relax != "F"
+    nfc = {"F": 0, "FCF": 1, "FCFCF": 2}[wl.relax]  # FC sweeps per relaxation
+    visits = level_visits(L, wl.cycle)
     adj = kind.startswith("adj")
     iters = adj_iters if adj else fwd_iters
     # multiply-adds of one layer product K v per example: q^2 dense, 9 C^2 H W conv
@@ -96,31 +117,36 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
         for l, Nl in enumerate(sizes):
             wbytes = Nl * nweights * e
             g = 1 if l >= 1 else 0
+            nv = visits[l]
             if l == L - 1:
                 if kind.endswith("coarsest"):
-                    byts += (1 + g * Nl + Nl + (Nl * arow if adj else 0)) * row + wbytes
-                    flops += Nl * fstep * B
-                    launches += 1
+                    byts += nv * ((1 + g * Nl + Nl + (Nl * arow if adj else 0)) * row + wbytes)
+                    flops += nv * Nl * fstep * B
+                    launches += nv
                 continue
             Nc = Nl // c
             xn = (1.0 / c) if (l + 1 < L - 1) else 0.0
             deferred = l == 0 and fcf
             if kind.endswith("_fc") and fcf:
-                byts += Nc * (2 + g * c + (c * arow if adj else 0) + (1 if deferred and m > 0 else 0)) * row + wbytes
-                flops += Nc * c * fstep * B
-                launches += 1
+                # the first FC sweep reads the pending correction on the finest level
+                # from the second cycle on; a second one (FCFCF) reads staged C-points
+                first = Nc * (2 + g * c + (c * arow if adj else 0) + (1 if deferred and m > 0 else 0)) * row
+                again = Nc * (2 + g * c + (c * arow if adj else 0)) * row
+                byts += nv * (first + (nfc - 1) * again + nfc * wbytes)
+                flops += nv * nfc * Nc * c * fstep * B
+                launches += nv * nfc
             elif kind.endswith("_fres"):
-                byts += Nc * (3 + xn + g * c + (c * arow if adj else 0)) * row + wbytes
-                flops += Nc * (c * fstep + (2 * mac if adj else 0)) * B
-                launches += 1
+                byts += nv * (Nc * (3 + xn + g * c + (c * arow if adj else 0)) * row + wbytes)
+                flops += nv * Nc * (c * fstep + (2 * mac if adj else 0)) * B
+                launches += nv
             elif kind.endswith("_corrf") and (not deferred or m == iters - 1):
-                byts += Nc * (2 + c + g * (c - 1) + ((c - 1) * arow if adj else 0)) * row + wbytes
-                flops += Nc * (c - 1) * fstep * B
+                byts += nv * (Nc * (2 + c + g * (c - 1) + ((c - 1) * arow if adj else 0)) * row + wbytes)
+                flops += nv * Nc * (c - 1) * fstep * B
                 if rec and not adj and l == 0:
                     # the final finest sweep keeps the record of all c layers
                     byts += Nc * c * rrow
                     flops += Nc * 2 * mac * B
-                launches += 1
+                launches += nv
     return byts, flops, launches
 
 
@@ -239,7 +265,8 @@ def cpu_baseline(wl, budget_s: float = 12.0):
         u0 = O.open_forward(d["y"], d["L_in"], wl.act, wl.opening)
         U = np.zeros((wl.N + 1,) + u0.shape)
         U[0] = u0
-        args = dict(cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=1)
+        args = dict(cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=1,
+                    cycle=wl.cycle)
         t0 = time.perf_counter()
         reps = 0
         while True:
@@ -277,6 +304,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (to scale HBM byte counters)")
+    ap.add_argument("--relax", choices=["F", "FCF", "FCFCF"], help="relaxation (default: the workload's)")
+    ap.add_argument("--cycle", choices=["V", "F"], help="MGRIT cycle (default: the workload's V-cycle)")
     ap.add_argument("--traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="summarise rocprofv3 FETCH_SIZE / WRITE_SIZE runs of --config into profiles/traffic.json "
                          "(no GPU needed)")
@@ -307,6 +336,8 @@ def main():
     from workloads import WORKLOADS, generate
 
     wl = WORKLOADS[args.config]
+    if args.relax or args.cycle:
+        wl = wl.with_overrides(**{k: v for k, v in (("relax", args.relax), ("cycle", args.cycle)) if v})
 
     def note(msg):
         print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -335,16 +366,17 @@ def main():
     # iteration counts: fixed by the workload, or found once with its stop rule
     fwd_iters, adj_iters = wl.fwd_iters, wl.adj_iters
     if wl.rtol > 0 or wl.stag > 0:
-        mg = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, wl.fwd_iters, False, wl.rtol, wl.stag)
+        mg = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, wl.fwd_iters, False, wl.rtol, wl.stag,
+                     wl.cycle)
         ws = L.alloc_workspace(p, mg)
         fwd_iters, _ = L.lp_mgrit_forward(p, mg, K, b, U, ws, dsig=rec)
         L.lp_loss_terminal(p, wl.n_classes, U[-1], W, mu, c, J, Lam[-1], dW, dmu, ws)
         adj_iters, _ = L.lp_mgrit_adjoint(p, L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax,
-                                                     wl.adj_iters, False, wl.rtol, wl.stag), K, b, U, Lam, ws,
+                                                     wl.adj_iters, False, wl.rtol, wl.stag, wl.cycle), K, b, U, Lam, ws,
                                           dsig=rec)
         del ws
-    mgF = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, fwd_iters)
-    mgA = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, adj_iters)
+    mgF = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, fwd_iters, cycle=wl.cycle)
+    mgA = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, adj_iters, cycle=wl.cycle)
     ws = L.alloc_workspace(p, mgF if fwd_iters >= adj_iters else mgA)
     hist = {}
 
@@ -440,7 +472,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"cfg{wl.cfg}: {wl.name}", "N": wl.N, "B": wl.B, "width": wl.q,
                    "activation": wl.act, "mgrit": {"cf": wl.cf, "levels": len(level_sizes(
-                       wl.N, wl.cf, wl.max_levels, wl.min_coarse)), "relax": wl.relax,
+                       wl.N, wl.cf, wl.max_levels, wl.min_coarse)), "relax": wl.relax, "cycle": wl.cycle,
                        "fwd_iters": fwd_iters, "adj_iters": adj_iters},
                    "sigma_record": {0: None, 1: "u8", 4: "f32"}[rec_e],
                    "step": "MGRIT forward iterations + loss + MGRIT adjoint iterations + gradient"},

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LP_ABI_VERSION 2
+#define LP_ABI_VERSION 3
 
 typedef enum {
   LP_OK = 0,
@@ -61,7 +61,8 @@ typedef enum {
 enum { LP_F32 = 0, LP_F64 = 1 };                       /* dtype */
 enum { LP_DENSE = 0, LP_CONV3X3 = 1 };                 /* layer */
 enum { LP_TANH = 0, LP_RELU = 1, LP_SMOOTHRELU = 2, LP_IDENTITY = 3 }; /* activation sigma */
-enum { LP_RELAX_F = 0, LP_RELAX_FCF = 1 };             /* MGRIT relaxation */
+enum { LP_RELAX_F = 0, LP_RELAX_FCF = 1, LP_RELAX_FCFCF = 2 }; /* MGRIT relaxation */
+enum { LP_CYCLE_V = 0, LP_CYCLE_F = 1 };               /* MGRIT cycle */
 enum { LP_STATE = 0, LP_ADJOINT = 1 };                 /* which system */
 enum { LP_OPEN_IDENTITY = 0, LP_OPEN_DENSE_ACT = 1, LP_OPEN_CONV_ACT = 2 }; /* opening layer */
 
@@ -78,20 +79,28 @@ typedef struct {
   double h;              /* step size */
 } lp_problem;
 
-/* MGRIT schedule (Section 3.1, Algorithm 1, as a recursive V-cycle).
+/* MGRIT schedule (Section 3.1, Algorithm 1, applied recursively).
  * Level l has N_l = N / cf^l steps of size cf^l h and uses the injected weights
  * theta^{i cf^l}. Levels are added while l+1 < max_levels and N_l > min_coarse;
  * every coarsened level must satisfy N_l % cf == 0 (else LP_EINVAL). The
- * coarsest level is solved by forward (adjoint: backward) substitution. */
+ * coarsest level is solved by forward (adjoint: backward) substitution.
+ * Step 3 of Algorithm 1 (the coarse solve) is one recursive cycle on the next
+ * level for LP_CYCLE_V (a V-cycle); for LP_CYCLE_F it is a recursive F-cycle
+ * followed by a V-cycle, the V-cycle left out when the next level is the
+ * coarsest (the multigrid F-cycle, which visits the coarse levels more often;
+ * Section 3.1.1 mentions it). Relaxation on every non-coarsest level:
+ * LP_RELAX_F (F), LP_RELAX_FCF (F, C, F; the paper's default) or
+ * LP_RELAX_FCFCF (F, C, F, C, F). */
 typedef struct {
   int32_t cf;            /* coarsening factor c >= 2 */
   int32_t max_levels;    /* >= 1; 1 means a serial solve */
   int32_t min_coarse;    /* stop coarsening at N_l <= min_coarse (>= 1) */
-  int32_t relax;         /* LP_RELAX_F | LP_RELAX_FCF, on every non-coarsest level */
-  int32_t max_iter;      /* >= 1 V-cycles */
+  int32_t relax;         /* LP_RELAX_F | LP_RELAX_FCF | LP_RELAX_FCFCF, on every non-coarsest level */
+  int32_t max_iter;      /* >= 1 cycles */
   int32_t warm_start;    /* 0: C-points start as copies of u^0 (adjoint: lam^N); 1: caller's array is the guess */
   double rtol;           /* stop after iteration m when rho_m <= rtol * rho_1 (0: off) */
   double stag;           /* stop after iteration m > 1 when rho_m > stag * rho_{m-1} (0: off) */
+  int32_t cycle;         /* LP_CYCLE_V | LP_CYCLE_F */
 } lp_mgrit;
 
 int32_t lp_abi_version(void);

@@ -144,7 +144,9 @@ int check_mgrit(const lp_problem* p, const lp_mgrit* m, std::vector<int>& sizes)
   if (m->cf < 2) return fail(LP_EINVAL, "coarsening factor %d < 2", m->cf);
   if (m->max_levels < 1) return fail(LP_EINVAL, "max_levels %d < 1", m->max_levels);
   if (m->min_coarse < 1) return fail(LP_EINVAL, "min_coarse %d < 1", m->min_coarse);
-  if (m->relax != LP_RELAX_F && m->relax != LP_RELAX_FCF) return fail(LP_EINVAL, "bad relax %d", m->relax);
+  if (m->relax != LP_RELAX_F && m->relax != LP_RELAX_FCF && m->relax != LP_RELAX_FCFCF)
+    return fail(LP_EINVAL, "bad relax %d", m->relax);
+  if (m->cycle != LP_CYCLE_V && m->cycle != LP_CYCLE_F) return fail(LP_EINVAL, "bad cycle %d", m->cycle);
   if (m->max_iter < 1) return fail(LP_EINVAL, "max_iter %d < 1", m->max_iter);
   if (!(m->rtol >= 0.0) || !(m->stag >= 0.0)) return fail(LP_EINVAL, "rtol and stag must be >= 0");
   sizes.assign(1, p->N);
@@ -160,6 +162,7 @@ int check_mgrit(const lp_problem* p, const lp_mgrit* m, std::vector<int>& sizes)
 // Workspace layout for one MGRIT solve.
 struct Layout {
   std::vector<size_t> X, G, S;  // byte offsets per level (X[0], G[0] unused)
+  std::vector<size_t> S2;       // FCFCF: second staging buffer of the coarse levels
   size_t S0b = 0;               // second finest-level staging buffer
   size_t partial = 0, rho = 0, total = 0;
   int partial_cap = 0;
@@ -178,6 +181,7 @@ Layout mgrit_layout(const lp_problem* p, const lp_mgrit* m, const std::vector<in
   L.X.assign(nl, 0);
   L.G.assign(nl, 0);
   L.S.assign(nl, 0);
+  L.S2.assign(nl, 0);
   size_t off = 0;
   for (int l = 1; l < nl; ++l) {
     L.X[l] = off;
@@ -185,7 +189,7 @@ Layout mgrit_layout(const lp_problem* p, const lp_mgrit* m, const std::vector<in
     L.G[l] = off;
     off = up(off + (size_t)(sizes[l] + 1) * sl);
   }
-  if (m->relax == LP_RELAX_FCF) {
+  if (m->relax != LP_RELAX_F) {
     for (int l = 0; l + 1 < nl; ++l) {
       L.S[l] = off;
       off = up(off + (size_t)(sizes[l + 1] + 1) * sl);
@@ -193,6 +197,12 @@ Layout mgrit_layout(const lp_problem* p, const lp_mgrit* m, const std::vector<in
     if (nl > 1) {  // second finest-level staging buffer
       L.S0b = off;
       off = up(off + (size_t)(sizes[1] + 1) * sl);
+    }
+    if (m->relax == LP_RELAX_FCFCF) {  // the second C-relaxation stages into another buffer
+      for (int l = 1; l + 1 < nl; ++l) {
+        L.S2[l] = off;
+        off = up(off + (size_t)(sizes[l + 1] + 1) * sl);
+      }
     }
   }
   L.partial_cap = partial_capacity(p);
@@ -233,8 +243,8 @@ struct Solver {
   const void* Uf;  // fine primal trajectory (adjoint)
   void* dsig = nullptr;  // sigma' record (written by the forward's final level-0 F-relaxation, read by the adjoint)
   std::vector<int> sizes;
-  std::vector<void*> X, G, S;
-  void* S0[2] = {nullptr, nullptr};  // finest-level staging buffers (FCF), used alternately
+  std::vector<void*> X, G, S, S2;
+  void* S0[2] = {nullptr, nullptr};  // finest-level staging buffers (FCF, FCFCF), used alternately
   int cur0 = 0;
   bool pending = false;              // finest-level correction not yet written back
   double* partial;
@@ -247,7 +257,10 @@ struct Solver {
     return s;
   }
 
-  int cycle(int l) {
+  // One cycle on level l (Algorithm 1 with step 3 recursive): cyc is LP_CYCLE_V or
+  // LP_CYCLE_F (coarse problem solved by an F-cycle and then a V-cycle, the latter
+  // left out above the coarsest level, whose solve is exact).
+  int cycle(int l, int cyc) {
     const int L = (int)sizes.size();
     const double hl = p->h * (double)stride(l);
     const int kb = dir == lp::DIR_FWD ? LP_TRACE_FWD_FC : LP_TRACE_ADJ_FC;  // first kind of this direction
@@ -258,7 +271,7 @@ struct Solver {
       LP_TRY(lp::launch_serial(sh, dir, a, st), "coarsest-level solve");
       return LP_OK;
     }
-    const bool fcf = m->relax == LP_RELAX_FCF;
+    const bool fcf = m->relax != LP_RELAX_F;  // at least one C-relaxation
     lp::SweepArgs a{};
     a.act = p->act;
     a.K = K;
@@ -292,6 +305,22 @@ struct Solver {
       TraceScope ts(kb + 0, l, st);
       LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "FC-relaxation");
     }
+    if (m->relax == LP_RELAX_FCFCF) {
+      // F- and C-relaxation again, from the staged C-points into the other staging
+      // buffer (on the finest level the one the previous cycle used, now free);
+      // reading them as C + (C - C) = C reuses the correcting form of the sweep
+      void* Sn = defer ? S0[cur0 ^ 1] : S2[l];
+      a.Cs = Sl;
+      a.cs_stride = 1;
+      a.V = Sl;
+      a.S = Sn;
+      {
+        TraceScope ts(kb + 0, l, st);
+        LP_TRY(lp::launch_sweep(sh, dir, a, st, nullptr), "FC-relaxation");
+      }
+      Sl = Sn;
+      if (defer) cur0 ^= 1;  // S0[cur0] holds the relaxed C-points again
+    }
     a.V = nullptr;
     a.Cs = fcf ? Sl : X[l];
     a.cs_stride = fcf ? 1 : m->cf;
@@ -306,8 +335,12 @@ struct Solver {
       LP_TRY(lp::launch_sweep(sh, dir, a, st, &np), "F-relaxation and restriction");
     }
     if (l == 0) partials_used = np;
-    int rc = cycle(l + 1);
+    int rc = cycle(l + 1, cyc);
     if (rc != LP_OK) return rc;
+    if (cyc == LP_CYCLE_F && l + 2 < L) {
+      rc = cycle(l + 1, LP_CYCLE_V);
+      if (rc != LP_OK) return rc;
+    }
     if (defer) {
       pending = true;
       cur0 ^= 1;
@@ -384,15 +417,18 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
   s.X.assign(L, nullptr);
   s.G.assign(L, nullptr);
   s.S.assign(L, nullptr);
+  s.S2.assign(L, nullptr);
   s.X[0] = Xuser;
   for (int l = 1; l < L; ++l) {
     s.X[l] = w + lay.X[l];
     s.G[l] = w + lay.G[l];
   }
-  if (m->relax == LP_RELAX_FCF && L > 1) {
+  if (m->relax != LP_RELAX_F && L > 1) {
     for (int l = 0; l + 1 < L; ++l) s.S[l] = w + lay.S[l];
     s.S0[0] = s.S[0];
     s.S0[1] = w + lay.S0b;
+    if (m->relax == LP_RELAX_FCFCF)
+      for (int l = 1; l + 1 < L; ++l) s.S2[l] = w + lay.S2[l];
   }
   s.partial = reinterpret_cast<double*>(w + lay.partial);
   s.st = st;
@@ -410,7 +446,7 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
   std::vector<double> hist;
   int it = 0;
   for (int mi = 0; mi < m->max_iter; ++mi) {
-    rc = s.cycle(0);
+    rc = s.cycle(0, m->cycle);
     if (rc) return rc;
     if (L > 1) LP_TRY(lp::launch_norm_reduce(s.partial, s.partials_used, rho + mi, st), "residual norm");
     else LP_TRY(lp::launch_zero(rho + mi, sizeof(double), st), "residual norm");

@@ -17,18 +17,20 @@ from typing import Optional, Sequence, Tuple
 # compare kernel variants under the same tests)
 LIB_PATH = os.environ.get("LP_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblp.so")
 
-LP_ABI_VERSION = 2
+LP_ABI_VERSION = 3
 LP_OK, LP_EINVAL, LP_EUNSUPPORTED, LP_EWORKSPACE, LP_EHIP, LP_ENONFINITE = range(6)
 LP_F32, LP_F64 = 0, 1
 LP_DENSE, LP_CONV3X3 = 0, 1
 LP_TANH, LP_RELU, LP_SMOOTHRELU, LP_IDENTITY = 0, 1, 2, 3
-LP_RELAX_F, LP_RELAX_FCF = 0, 1
+LP_RELAX_F, LP_RELAX_FCF, LP_RELAX_FCFCF = 0, 1, 2
+LP_CYCLE_V, LP_CYCLE_F = 0, 1
 LP_STATE, LP_ADJOINT = 0, 1
 LP_OPEN_IDENTITY, LP_OPEN_DENSE_ACT, LP_OPEN_CONV_ACT = 0, 1, 2
 
 ACT = {"tanh": LP_TANH, "relu": LP_RELU, "smoothrelu": LP_SMOOTHRELU, "identity": LP_IDENTITY}
 LAYER = {"dense": LP_DENSE, "conv3x3": LP_CONV3X3}
-RELAX = {"F": LP_RELAX_F, "FCF": LP_RELAX_FCF}
+RELAX = {"F": LP_RELAX_F, "FCF": LP_RELAX_FCF, "FCFCF": LP_RELAX_FCFCF}
+CYCLE = {"V": LP_CYCLE_V, "F": LP_CYCLE_F}
 OPENING = {"identity": LP_OPEN_IDENTITY, "dense_act": LP_OPEN_DENSE_ACT, "conv_act": LP_OPEN_CONV_ACT}
 
 # Every symbol the header declares (checked by the CPU test suite).
@@ -54,7 +56,7 @@ class LpProblem(ctypes.Structure):
 class LpMgrit(ctypes.Structure):
     _fields_ = [("cf", ctypes.c_int32), ("max_levels", ctypes.c_int32), ("min_coarse", ctypes.c_int32),
                 ("relax", ctypes.c_int32), ("max_iter", ctypes.c_int32), ("warm_start", ctypes.c_int32),
-                ("rtol", ctypes.c_double), ("stag", ctypes.c_double)]
+                ("rtol", ctypes.c_double), ("stag", ctypes.c_double), ("cycle", ctypes.c_int32)]
 
 
 class LpError(RuntimeError):
@@ -124,8 +126,9 @@ def problem(dtype: str, layer: str, act: str, N: int, B: int, C: int, H: int = 1
 
 
 def mgrit(cf: int = 4, max_levels: int = 2, min_coarse: int = 1, relax: str = "FCF", max_iter: int = 1,
-          warm_start: bool = False, rtol: float = 0.0, stag: float = 0.0) -> LpMgrit:
-    return LpMgrit(cf, max_levels, min_coarse, RELAX[relax], max_iter, int(bool(warm_start)), rtol, stag)
+          warm_start: bool = False, rtol: float = 0.0, stag: float = 0.0, cycle: str = "V") -> LpMgrit:
+    return LpMgrit(cf, max_levels, min_coarse, RELAX[relax], max_iter, int(bool(warm_start)), rtol, stag,
+                   CYCLE[cycle])
 
 
 # ---------------------------------------------------------------- tensor marshalling

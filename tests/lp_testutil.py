@@ -50,10 +50,10 @@ def prob(wl: Workload, B: int | None = None) -> L.LpProblem:
 
 
 def sched(wl: Workload, iters: int, relax: str | None = None, levels: int | None = None, warm=False,
-          rtol=0.0, stag=0.0) -> L.LpMgrit:
+          rtol=0.0, stag=0.0, cycle: str | None = None) -> L.LpMgrit:
     return L.mgrit(cf=wl.cf, max_levels=wl.max_levels if levels is None else levels, min_coarse=wl.min_coarse,
                    relax=wl.relax if relax is None else relax, max_iter=iters, warm_start=warm, rtol=rtol,
-                   stag=stag)
+                   stag=stag, cycle=wl.cycle if cycle is None else cycle)
 
 
 def state_shape(wl: Workload, rows: int, B: int | None = None):

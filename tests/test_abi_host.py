@@ -154,3 +154,22 @@ def test_binding_refuses_cpu_tensors():
     K = torch.zeros(4, 8, 8)
     with pytest.raises(ValueError):
         L.lp_serial_forward(p, K, torch.zeros(4, 8), torch.zeros(5, 3, 8))
+
+
+def test_cycle_and_relaxation_options(monkeypatch):
+    """F-cycles and FCFCF are accepted; unknown values are LP_EINVAL; FCFCF needs
+    one more staging buffer on every coarse non-coarsest level."""
+    lib = L.load()
+    p = L.problem("f32", "dense", "relu", 256, 64, 32, h=0.04)
+    fcf = L.lp_workspace_bytes(p, L.mgrit(4, 4, 1, "FCF", 2))
+    fcfcf = L.lp_workspace_bytes(p, L.mgrit(4, 4, 1, "FCFCF", 2))
+    slice_ = 64 * 32 * 4
+    # levels 256 -> 64 -> 16 -> 4: the extra buffers sit on levels 1 and 2 (17 and 5 slices)
+    assert fcfcf - fcf >= (17 + 5) * slice_
+    assert L.lp_workspace_bytes(p, L.mgrit(4, 4, 1, "FCF", 2, cycle="F")) == fcf
+    m = L.mgrit(4, 4, 1, "FCF", 2)
+    m.cycle = 7
+    assert lib.lp_workspace_bytes(ctypes.byref(p), ctypes.byref(m)) == 0
+    m = L.mgrit(4, 4, 1, "FCF", 2)
+    m.relax = 3
+    assert lib.lp_workspace_bytes(ctypes.byref(p), ctypes.byref(m)) == 0

@@ -311,6 +311,53 @@ def test_one_shot_training_matches_oracle():
         assert_close(params[k].cpu().numpy(), wo[k], wl.dtype, f"{k} after {updates} updates", scale=10)
 
 
+def _deepest(wl, most=4):
+    """The most levels (up to `most`) the workload's N allows with its cf."""
+    for lv in range(most, 1, -1):
+        try:
+            O.level_sizes(wl.N, wl.cf, lv, wl.min_coarse)
+            return lv
+        except ValueError:
+            pass
+    return 2
+
+
+@pytest.mark.parametrize("relax,cycle", [("FCFCF", "V"), ("FCF", "F"), ("F", "F"), ("FCFCF", "F")])
+@pytest.mark.parametrize("name,wl", DENSE, ids=IDS)
+def test_mgrit_cycle_variants(name, wl, relax, cycle):
+    """F-cycles and FCFCF relaxation on the deepest hierarchy the size allows:
+    forward and adjoint iterates and residual histories against the oracle."""
+    c = case(wl)
+    levels = _deepest(wl)
+    iters = 3
+    mg = sched(wl, iters, relax=relax, levels=levels, cycle=cycle)
+    ws = L.alloc_workspace(c.p, mg)
+    U = c.new_traj()
+    it, hist = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws)
+    assert it == iters
+    Ur, hr, _ = O.mgrit_forward(c.ref_traj(), c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=levels,
+                                min_coarse=wl.min_coarse, relax=relax, max_iter=iters, cycle=cycle)
+    assert_close(U.cpu().numpy(), Ur, wl.dtype, "U iterate")
+    floor = {"f32": 3e-5, "f64": 1e-11}[wl.dtype]
+    for m in range(iters):
+        assert abs(hist[m] - hr[m]) <= floor * hr[0] + 1e-5 * hr[m], (m, hist, hr)
+    # adjoint, linearised at the serial trajectory on each side
+    L.lp_serial_forward(c.p, c.K, c.b, U)
+    lamN, _, _, _ = _lamN(c, U)
+    Us = O.serial_forward(c.u0_ref, c.d["K"], c.d["b"], wl.h, wl.act)
+    lamNr = O.loss_terminal(Us[-1], c.d["W"], c.d["mu"], c.d["onehot"])[1]
+    Lam = torch.zeros_like(U)
+    Lam[-1] = lamN
+    it, hist = L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, Lam, ws)
+    Lr0 = np.zeros_like(Us)
+    Lr0[-1] = lamNr
+    Lr, hr, _ = O.mgrit_adjoint(Us, Lr0, c.d["K"], c.d["b"], wl.h, wl.act, cf=wl.cf, max_levels=levels,
+                                min_coarse=wl.min_coarse, relax=relax, max_iter=iters, cycle=cycle)
+    assert_close(Lam.cpu().numpy(), Lr, wl.dtype, "Lam iterate")
+    for m in range(iters):
+        assert abs(hist[m] - hr[m]) <= floor * hr[0] + 1e-5 * hr[m], (m, hist, hr)
+
+
 # fp32 widths on the matrix cores with a non-identity activation: the ones that keep a sigma' record
 RECORDED = [DENSE[1], DENSE[2], DENSE[3],
             ("srelu32", WORKLOADS[2].with_overrides(act="smoothrelu", N=32, B=77, max_levels=2)),

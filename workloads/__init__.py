@@ -49,7 +49,8 @@ class Workload:
     cf: int = 4
     max_levels: int = 2
     min_coarse: int = 1
-    relax: str = "FCF"    # "F" or "FCF"
+    relax: str = "FCF"    # "F", "FCF" or "FCFCF"
+    cycle: str = "V"      # "V" or "F"
     fwd_iters: int = 2
     adj_iters: int = 2
     rtol: float = 0.0
