@@ -24,7 +24,7 @@ def sample_of(B, n_rand, seed=0):
     return np.array(sorted(idx))
 
 
-@pytest.fixture(scope="module", params=[1, 2, 3, 4, 5], ids=lambda c: f"cfg{c}")
+@pytest.fixture(scope="module", params=[1, 2, 3, 4, 5, 6], ids=lambda c: f"cfg{c}")
 def full(request):
     wl = WORKLOADS[request.param]
     print(f"[fullsize] cfg{wl.cfg} {wl.name}", flush=True)
@@ -98,7 +98,7 @@ def test_mgrit_forward_and_adjoint_full_size(full):
     # gradient: full oracle comparison where cheap, else additivity over the batch
     dK, db = torch.empty_like(c.K), torch.empty_like(c.b)
     L.lp_gradient(c.p, c.K, c.b, U, Lam, dK, db, ws)
-    if wl.cfg in (1, 2):
+    if wl.cfg in (1, 2, 6):
         Uf, _, _ = O.mgrit_forward(
             np.concatenate([c.u0_ref[None], np.zeros((wl.N,) + c.u0_ref.shape)]), c.d["K"], c.d["b"], wl.h,
             wl.act, cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=itF)
