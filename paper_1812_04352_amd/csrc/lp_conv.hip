@@ -162,6 +162,24 @@ __device__ __forceinline__ void put_px(float* buf, f32x4 v, const SGeo& g, const
   for (int r = 0; r < 4; ++r) buf[lds_r(g, p, r)] = v[r];
 }
 
+// The interior of the zero-halo LDS image (channel stride CS, padded rows PW) to a
+// state row [C][H][W] in global memory: thread i takes values 4i .. 4i+3, which lie
+// in one image row when W % 4 == 0 (else one value at a time).
+__device__ __forceinline__ void store_img(float* __restrict__ dst, const float* buf, const SGeo& g, int nt) {
+  if (g.W % 4 == 0) {
+    for (int i = 4 * (int)threadIdx.x; i < g.q; i += 4 * nt) {
+      const int c = i / g.HW, r = i - c * g.HW, y = r / g.W, x = r - y * g.W;
+      const float* s = buf + c * g.CS + (y + 1) * g.PW + x + 1;
+      *reinterpret_cast<f32x4*>(dst + i) = f32x4{s[0], s[1], s[2], s[3]};
+    }
+  } else {
+    for (int i = threadIdx.x; i < g.q; i += nt) {
+      const int c = i / g.HW, r = i - c * g.HW, y = r / g.W, x = r - y * g.W;
+      dst[i] = buf[c * g.CS + (y + 1) * g.PW + x + 1];
+    }
+  }
+}
+
 // Products of the wave's tiles, z[tt] = init + Wbig^T x patches.
 __device__ __forceinline__ void conv_tiles(f32x4 (&z)[TPW], const float (&wr)[24], const float* buf, const SGeo& g,
                                            int t0, int lane, f32x4 init) {
@@ -400,16 +418,16 @@ __attribute__((amdgpu_waves_per_eu(MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 
       if (gi) v[tt] += ld_px(gi, g, px_of(g, t0 + tt, lane));
     }
     __syncthreads();  // every read of the step's input is done
-    float* xo = (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) ? X + (kc + j + 1) * slice + eo : nullptr;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
       const Px p = px_of(g, t0 + tt, lane);
-      if (p.ok) {
-        put_px(buf, v[tt], g, p);
-        if (xo) st_px(xo, v[tt], g, p);
-      }
+      if (p.ok) put_px(buf, v[tt], g, p);
     }
     __syncthreads();
+    // the new state is written out from the LDS image in row order, four values
+    // per thread and store (the next write of the buffer is a step away, behind
+    // that step's first barrier)
+    if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) store_img(X + (kc + j + 1) * slice + eo, buf, g, nt);
   }
 
   if constexpr (extra != 0) {
