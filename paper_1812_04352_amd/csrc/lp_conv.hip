@@ -324,10 +324,14 @@ __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
   return s;
 }
 
-// RK: the sigma' record kind (0 none, 1 ReLU bytes, 2 fp32 values)
-template <int MODE, int GH, int GW, int RK>
+// RK: the sigma' record kind (0 none, 1 ReLU bytes, 2 fp32 values). HG: the level
+// has right-hand-side rows (every level but the finest); a step requests its row
+// before the product, so the load overlaps the matrix-core work (three waves per
+// SIMD leave room for it).
+template <int MODE, int GH, int GW, int RK, bool HG>
 __global__ __launch_bounds__(64 * MAXW)
-__attribute__((amdgpu_waves_per_eu(MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 4 : 1, 8))) void k_fwd(SweepArgs a, SGeo ga) {
+__attribute__((amdgpu_waves_per_eu(HG ? 3 : MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 4 : 1, 8)))
+void k_fwd(SweepArgs a, SGeo ga) {
   constexpr bool REC = RK != 0, RB = RK == 1;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
@@ -397,7 +401,11 @@ __attribute__((amdgpu_waves_per_eu(MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 
     asm volatile("" : "+v"(lane));
     const float* swc = sw + (j & 1) * WV;
     stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j + extra)) * a.stride, nt);
-    f32x4 z[TPW];
+    f32x4 z[TPW], gv[HG ? TPW : 1];
+    if constexpr (HG) {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) gv[tt] = ld_px(G + (kc + j + 1) * slice + eo, g, px_of(g, t0 + tt, lane));
+    }
     {
       float wr[24];
       gather_w<false>(wr, swc, lane);
@@ -410,12 +418,15 @@ __attribute__((amdgpu_waves_per_eu(MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 
       for (int tt = 0; tt < TPW; ++tt) rec_put<RB>(a.dsig, blk, g, t0 + tt, lane, z[tt], a.act);
     }
     act_tiles<false>(z, a.act);
-    const float* gi = G ? G + (kc + j + 1) * slice + eo : nullptr;
+    // (without HG the kernel keeps the form it was tuned in: a run-time test that
+    // is false on the finest level)
+    const float* gi = !HG && G ? G + (kc + j + 1) * slice + eo : nullptr;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
       if (MODE == SWEEP_FRES && j == 0) coarse[tt] = v[tt] + hc * z[tt];
       v[tt] = v[tt] + hl * z[tt];
-      if (gi) v[tt] += ld_px(gi, g, px_of(g, t0 + tt, lane));
+      if constexpr (HG) v[tt] += gv[tt];
+      else if (gi) v[tt] += ld_px(gi, g, px_of(g, t0 + tt, lane));
     }
     __syncthreads();  // every read of the step's input is done
 #pragma unroll
@@ -483,8 +494,9 @@ __attribute__((amdgpu_waves_per_eu(MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 
 // Adjoint step at level point i: d = sigma'(K u + b) with u the fine primal state
 // of point i (or d read from the sigma' record: REC), s = d * lam,
 // lam' = lam + h K^T s (+ g).
-template <int MODE, int GH, int GW, int RK>
-__global__ __launch_bounds__(64 * MAXW) __attribute__((amdgpu_waves_per_eu(RK == 1 ? 4 : RK == 2 ? 3 : 1, 8)))
+template <int MODE, int GH, int GW, int RK, bool HG>
+__global__ __launch_bounds__(64 * MAXW)
+__attribute__((amdgpu_waves_per_eu(HG ? 3 : RK == 1 ? 4 : RK == 2 ? 3 : 1, 8)))
 void k_adj(SweepArgs a, SGeo ga) {
   constexpr bool REC = RK != 0, RB = RK == 1;
   const SGeo g = geo_of<GH, GW>(ga);
@@ -591,15 +603,20 @@ void k_adj(SweepArgs a, SGeo ga) {
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) un[tt] = ld_px(Uf + (size_t)(i - 1) * ustep + eo, g, px_of(g, t0 + tt, lane));
     }
-    f32x4 w[TPW];
+    f32x4 w[TPW], gv[HG ? TPW : 1];
+    if constexpr (HG) {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) gv[tt] = ld_px(G + (size_t)i * slice + eo, g, px_of(g, t0 + tt, lane));
+    }
     conv_tiles(w, wt, buf, g, t0, lane, f32x4{0.f, 0.f, 0.f, 0.f});
-    const float* gi = G ? G + (size_t)i * slice + eo : nullptr;
+    const float* gi = !HG && G ? G + (size_t)i * slice + eo : nullptr;
     float* xo = (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) ? X + (size_t)i * slice + eo : nullptr;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
       const Px p = px_of(g, t0 + tt, lane);
       lam[tt] = lam[tt] + hl * w[tt];
-      if (gi) lam[tt] += ld_px(gi, g, p);
+      if constexpr (HG) lam[tt] += gv[tt];
+      else if (gi) lam[tt] += ld_px(gi, g, p);
       if (xo && p.ok) st_px(xo, lam[tt], g, p);
     }
     __syncthreads();  // every read of s is done
@@ -926,19 +943,19 @@ size_t sweep_lds(const conv::SGeo& g) { return (size_t)(conv::CH * g.CS + 2 * co
 // Sweep kernels with the geometry as template arguments (0, 0: runtime).
 // Only the forward CORRF and serial kernels write the record; every adjoint
 // kernel can read it.
-template <int GH, int GW, int RK>
+template <int GH, int GW, int RK, bool HG>
 void sweep_kernels(int dir, int mode, void (*&f)(SweepArgs, conv::SGeo)) {
   using namespace conv;
   if (dir == DIR_FWD) {
-    if (mode == SWEEP_FC) f = k_fwd<SWEEP_FC, GH, GW, 0>;
-    else if (mode == SWEEP_FRES) f = k_fwd<SWEEP_FRES, GH, GW, 0>;
-    else if (mode == SWEEP_CORRF) f = k_fwd<SWEEP_CORRF, GH, GW, RK>;
-    else f = k_fwd<MODE_SERIAL, GH, GW, RK>;
+    if (mode == SWEEP_FC) f = k_fwd<SWEEP_FC, GH, GW, 0, HG>;
+    else if (mode == SWEEP_FRES) f = k_fwd<SWEEP_FRES, GH, GW, 0, HG>;
+    else if (mode == SWEEP_CORRF) f = k_fwd<SWEEP_CORRF, GH, GW, RK, HG>;
+    else f = k_fwd<MODE_SERIAL, GH, GW, RK, HG>;
   } else {
-    if (mode == SWEEP_FC) f = k_adj<SWEEP_FC, GH, GW, RK>;
-    else if (mode == SWEEP_FRES) f = k_adj<SWEEP_FRES, GH, GW, RK>;
-    else if (mode == SWEEP_CORRF) f = k_adj<SWEEP_CORRF, GH, GW, RK>;
-    else f = k_adj<MODE_SERIAL, GH, GW, RK>;
+    if (mode == SWEEP_FC) f = k_adj<SWEEP_FC, GH, GW, RK, HG>;
+    else if (mode == SWEEP_FRES) f = k_adj<SWEEP_FRES, GH, GW, RK, HG>;
+    else if (mode == SWEEP_CORRF) f = k_adj<SWEEP_CORRF, GH, GW, RK, HG>;
+    else f = k_adj<MODE_SERIAL, GH, GW, RK, HG>;
   }
 }
 
@@ -946,14 +963,27 @@ hipError_t launch_conv_sweep(const Shape& s, int dir, const SweepArgs& a, dim3 g
   const conv::SGeo g = sweep_geo(s);
   void (*f)(SweepArgs, conv::SGeo) = nullptr;
   const int rk = a.dsig == nullptr ? 0 : a.act == ACT_RELU ? 1 : 2;
+  const bool hg = a.G != nullptr;
   if (s.H == 28 && s.W == 28) {  // MNIST-sized images
-    if (rk == 1) sweep_kernels<28, 28, 1>(dir, a.mode, f);
-    else if (rk == 2) sweep_kernels<28, 28, 2>(dir, a.mode, f);
-    else sweep_kernels<28, 28, 0>(dir, a.mode, f);
+    if (hg) {
+      if (rk == 1) sweep_kernels<28, 28, 1, true>(dir, a.mode, f);
+      else if (rk == 2) sweep_kernels<28, 28, 2, true>(dir, a.mode, f);
+      else sweep_kernels<28, 28, 0, true>(dir, a.mode, f);
+    } else {
+      if (rk == 1) sweep_kernels<28, 28, 1, false>(dir, a.mode, f);
+      else if (rk == 2) sweep_kernels<28, 28, 2, false>(dir, a.mode, f);
+      else sweep_kernels<28, 28, 0, false>(dir, a.mode, f);
+    }
   } else {
-    if (rk == 1) sweep_kernels<0, 0, 1>(dir, a.mode, f);
-    else if (rk == 2) sweep_kernels<0, 0, 2>(dir, a.mode, f);
-    else sweep_kernels<0, 0, 0>(dir, a.mode, f);
+    if (hg) {
+      if (rk == 1) sweep_kernels<0, 0, 1, true>(dir, a.mode, f);
+      else if (rk == 2) sweep_kernels<0, 0, 2, true>(dir, a.mode, f);
+      else sweep_kernels<0, 0, 0, true>(dir, a.mode, f);
+    } else {
+      if (rk == 1) sweep_kernels<0, 0, 1, false>(dir, a.mode, f);
+      else if (rk == 2) sweep_kernels<0, 0, 2, false>(dir, a.mode, f);
+      else sweep_kernels<0, 0, 0, false>(dir, a.mode, f);
+    }
   }
   launch(f, grid, dim3(64 * g.NW), sweep_lds(g), st, a, g);
   return hipGetLastError();
