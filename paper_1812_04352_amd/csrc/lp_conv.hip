@@ -44,6 +44,28 @@ __device__ __forceinline__ void stage_w(float* sw, const float* __restrict__ K, 
   for (int i = threadIdx.x; i < WV; i += nt) sw[i] = i < KW ? K[n * KW + i] : b[n * CH + (i - KW)];
 }
 
+// A layer's weights and bias on their way to LDS in a sweep: thread t carries
+// entries t, t + nt, ... (WPT of them), fetched at the start of a step and
+// written after its product, so the load's latency overlaps the matrix-core work.
+template <int WPT>
+__device__ __forceinline__ void stage_fetch(float (&r)[WPT], const float* __restrict__ K,
+                                            const float* __restrict__ b, size_t n, int nt) {
+#pragma unroll
+  for (int p = 0; p < WPT; ++p) {
+    const int i = threadIdx.x + p * nt;
+    r[p] = i < KW ? K[n * KW + i] : i < WV ? b[n * CH + (i - KW)] : 0.f;
+  }
+}
+
+template <int WPT>
+__device__ __forceinline__ void stage_put(float* sw, const float (&r)[WPT], int nt) {
+#pragma unroll
+  for (int p = 0; p < WPT; ++p) {
+    const int i = threadIdx.x + p * nt;
+    if (i < WV) sw[i] = r[p];
+  }
+}
+
 __device__ __forceinline__ void zero_buf(float* buf, int n, int nt = NT) {
   for (int i = threadIdx.x; i < n; i += nt) buf[i] = 0.f;
 }
@@ -330,9 +352,11 @@ __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
 // SIMD leave room for it).
 template <int MODE, int GH, int GW, int RK, bool HG>
 __global__ __launch_bounds__(64 * MAXW)
-__attribute__((amdgpu_waves_per_eu(HG ? 3 : MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 4 : 1, 8)))
+__attribute__((amdgpu_waves_per_eu(HG || MODE == SWEEP_FRES ? 3 : MODE == SWEEP_CORRF || MODE == MODE_SERIAL ? 4 : 1, 8)))
 void k_fwd(SweepArgs a, SGeo ga) {
   constexpr bool REC = RK != 0, RB = RK == 1;
+  // weight entries per thread while staging (the specialised geometry fixes the thread count)
+  constexpr int WPT = GH ? (WV + 64 * make_geo(GH, GW).NW - 1) / (64 * make_geo(GH, GW).NW) : (WV + 63) / 64;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
   float* buf = lds;               // CH * CS
@@ -400,7 +424,12 @@ void k_fwd(SweepArgs a, SGeo ga) {
     // live in registers through the loop (fewer registers, more resident waves)
     asm volatile("" : "+v"(lane));
     const float* swc = sw + (j & 1) * WV;
-    stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j + extra)) * a.stride, nt);
+    // the serial solve stages in one go (measured faster there)
+    constexpr bool SPLIT = MODE != MODE_SERIAL;
+    const size_t nxt = (size_t)(kc + (j + 1 < nsteps ? j + 1 : j + extra)) * a.stride;
+    float wreg[SPLIT ? WPT : 1];
+    if constexpr (SPLIT) stage_fetch<WPT>(wreg, K, bb, nxt, nt);
+    else stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, nxt, nt);
     f32x4 z[TPW], gv[HG ? TPW : 1];
     if constexpr (HG) {
 #pragma unroll
@@ -434,6 +463,7 @@ void k_fwd(SweepArgs a, SGeo ga) {
       const Px p = px_of(g, t0 + tt, lane);
       if (p.ok) put_px(buf, v[tt], g, p);
     }
+    if constexpr (SPLIT) stage_put<WPT>(sw + ((j & 1) ^ 1) * WV, wreg, nt);
     __syncthreads();
     // the new state is written out from the LDS image in row order, four values
     // per thread and store (the next write of the buffer is a step away, behind
@@ -499,6 +529,8 @@ __global__ __launch_bounds__(64 * MAXW)
 __attribute__((amdgpu_waves_per_eu(HG ? 3 : RK == 1 ? 4 : RK == 2 ? 3 : 1, 8)))
 void k_adj(SweepArgs a, SGeo ga) {
   constexpr bool REC = RK != 0, RB = RK == 1;
+  // weight entries per thread while staging (the specialised geometry fixes the thread count)
+  constexpr int WPT = GH ? (WV + 64 * make_geo(GH, GW).NW - 1) / (64 * make_geo(GH, GW).NW) : (WV + 63) / 64;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
   float* buf = lds;               // CH * CS: u, then s
@@ -571,7 +603,11 @@ void k_adj(SweepArgs a, SGeo ga) {
     const long i = top - 1 - j;
     const bool more = j + 1 < nsteps;
     const float* swc = sw + (j & 1) * WV;
-    stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(more ? i - 1 : i) * a.stride, nt);
+    // the correction and serial sweeps stage in one go: their registers are spoken for
+    constexpr bool SPLIT = MODE == SWEEP_FC || MODE == SWEEP_FRES;
+    float wreg[SPLIT ? WPT : 1];
+    if constexpr (SPLIT) stage_fetch<WPT>(wreg, K, bb, (size_t)(more ? i - 1 : i) * a.stride, nt);
+    else stage_w(sw + ((j & 1) ^ 1) * WV, K, bb, (size_t)(more ? i - 1 : i) * a.stride, nt);
     // d = sigma'(K u + b)
     if constexpr (REC) {
 #pragma unroll
@@ -619,6 +655,7 @@ void k_adj(SweepArgs a, SGeo ga) {
       else if (gi) lam[tt] += ld_px(gi, g, p);
       if (xo && p.ok) st_px(xo, lam[tt], g, p);
     }
+    if constexpr (SPLIT) stage_put<WPT>(sw + ((j & 1) ^ 1) * WV, wreg, nt);
     __syncthreads();  // every read of s is done
     if (!REC) {
       if (more) {
@@ -776,6 +813,8 @@ constexpr int GOUT = 16 * 96 + CH;  // dWbig then db per chunk
 template <int GH, int GW, int RK>
 __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   constexpr bool REC = RK != 0, RB = RK == 1;
+  // weight entries per thread while staging (the specialised geometry fixes the thread count)
+  constexpr int WPT = GH ? (WV + 64 * make_geo(GH, GW).NW - 1) / (64 * make_geo(GH, GW).NW) : (WV + 63) / 64;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
   float* bu = lds;                   // CH * CS: u
