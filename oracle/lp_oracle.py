@@ -616,3 +616,117 @@ def serial_training(y, onehot, L_in, K, b, W, mu, h, kind, opening, updates, lr)
         if dL is not None:
             L_in -= lr * dL
     return losses, dict(L_in=L_in, K=K, b=b, W=W, mu=mu)
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 2 in full: m1 state and m2 adjoint MGRIT iterations per design
+# update, a limited-memory BFGS approximation of the Hessian, a backtracking line
+# search on the objective, and a validation-accuracy stop (Section 4)
+# ---------------------------------------------------------------------------
+
+def _vdot(a, b):
+    return float(sum(np.sum(x * y) for x, y in zip(a, b)))
+
+
+def lbfgs_direction(g, pairs):
+    """H g by the limited-memory BFGS two-loop recursion over the stored pairs
+    (s_i, y_i), oldest first, with the initial matrix gamma I, gamma = s.y / y.y of
+    the newest pair (1 without pairs). Vectors are lists of arrays."""
+    q = [x.copy() for x in g]
+    alphas = []
+    for s_i, y_i in reversed(pairs):
+        a = _vdot(s_i, q) / _vdot(y_i, s_i)
+        alphas.append(a)
+        q = [x - a * y for x, y in zip(q, y_i)]
+    gamma = _vdot(pairs[-1][0], pairs[-1][1]) / _vdot(pairs[-1][1], pairs[-1][1]) if pairs else 1.0
+    r = [gamma * x for x in q]
+    for (s_i, y_i), a in zip(pairs, reversed(alphas)):
+        beta = _vdot(y_i, r) / _vdot(y_i, s_i)
+        r = [x + (a - beta) * s for x, s in zip(r, s_i)]
+    return r
+
+
+def one_shot_lbfgs(y, onehot, L_in, K, b, W, mu, h, kind, opening, cf, max_levels, min_coarse, relax,
+                   updates, m1=2, m2=2, memory=5, alpha0=1e-2, c1=1e-4, shrink=0.5, max_ls=8,
+                   y_val=None, onehot_val=None, target_acc=None, cycle="V"):
+    """Algorithm 2 with its Hessian approximated by limited-memory BFGS. Per design
+    update: m1 state and m2 adjoint MGRIT iterations, warm-started from the previous
+    update's iterates (cold at the first); the reduced gradient g of J at those
+    inexact iterates; the pair (s, y) = (design change, gradient change) is kept when
+    s.y > 0 (at most `memory` pairs); the direction d = -H g (two-loop recursion);
+    a backtracking line search: trial steps alpha = alpha_start * shrink^t, t < max_ls,
+    the objective at a trial design being the loss of the state after m1 MGRIT
+    iterations warm-started from the current state, accepted at the first trial with
+    J_t <= J + c1 alpha g.d (the last trial is taken if none is); alpha_start is alpha0
+    at the first update (no curvature yet) and 1 afterwards. The accepted trial's
+    state becomes the current one. With validation data, the validation accuracy of
+    the new design (its exact forward propagation) is taken after every update and the
+    run stops once it reaches target_acc.
+    Design vector order: L_in (unless the opening is the identity), K, b, W, mu.
+    Returns dict(losses, alphas, trials, accuracies, weights)."""
+    L_in, K, b, W, mu = (None if a is None else np.array(a, dtype=np.float64, copy=True)
+                         for a in (L_in, K, b, W, mu))
+    y, onehot = _f64(y, onehot)
+    N = K.shape[0]
+    has_open = opening != "identity"
+    sched = dict(cf=cf, max_levels=max_levels, min_coarse=min_coarse, relax=relax, cycle=cycle)
+
+    def design():
+        return ([L_in] if has_open else []) + [K, b, W, mu]
+
+    def unpack(v):
+        v = list(v)
+        return (v.pop(0) if has_open else None), v[0], v[1], v[2], v[3]
+
+    def state_after(Lt, Kt, bt, Ustart, warm):
+        U = Ustart.copy()
+        U[0] = open_forward(y, Lt, kind, opening)
+        U, _, _ = mgrit_forward(U, Kt, bt, h, kind, max_iter=m1, warm_start=warm, **sched)
+        return U
+
+    u0 = open_forward(y, L_in, kind, opening)
+    U = np.zeros((N + 1,) + u0.shape)
+    Lam = np.zeros_like(U)
+    pairs = []
+    prev = None  # (design, gradient) of the previous update
+    out = dict(losses=[], alphas=[], trials=[], accuracies=[])
+    U = state_after(L_in, K, b, U, False)
+    for it in range(updates):
+        if it > 0:
+            U = state_after(L_in, K, b, U, True)
+        J, lamN, dW, dmu = loss_terminal(U[N], W, mu, onehot)
+        Lam[N] = lamN
+        Lam, _, _ = mgrit_adjoint(U, Lam, K, b, h, kind, max_iter=m2, warm_start=(it > 0), **sched)
+        dK, db = gradient(U, Lam, K, b, h, kind)
+        g = ([open_grad(y, L_in, Lam[0], kind, opening)] if has_open else []) + [dK, db, dW, dmu]
+        x = design()
+        if prev is not None:
+            s_v = [a - c for a, c in zip(x, prev[0])]
+            y_v = [a - c for a, c in zip(g, prev[1])]
+            if _vdot(s_v, y_v) > 0.0:
+                pairs.append((s_v, y_v))
+                pairs = pairs[-memory:]
+        d = [-v for v in lbfgs_direction(g, pairs)]
+        gd = _vdot(g, d)
+        alpha = alpha0 if it == 0 else 1.0
+        for t in range(max_ls):
+            Lt, Kt, bt, Wt, mut = unpack([a + alpha * v for a, v in zip(x, d)])
+            Ut = state_after(Lt, Kt, bt, U, True)
+            Jt = loss_terminal(Ut[N], Wt, mut, onehot)[0]
+            if Jt <= J + c1 * alpha * gd or t == max_ls - 1:
+                break
+            alpha *= shrink
+        prev = (x, g)
+        L_in, K, b, W, mu = Lt, Kt, bt, Wt, mut
+        U = Ut
+        out["losses"].append(J)
+        out["alphas"].append(alpha)
+        out["trials"].append(t + 1)
+        if y_val is not None:
+            uv = serial_forward(open_forward(_f64(y_val), L_in, kind, opening), K, b, h, kind)[N]
+            acc = accuracy(uv, W, mu, np.argmax(_f64(onehot_val), axis=1))
+            out["accuracies"].append(acc)
+            if target_acc is not None and acc >= target_acc:
+                break
+    out["weights"] = dict(L_in=L_in, K=K, b=b, W=W, mu=mu)
+    return out

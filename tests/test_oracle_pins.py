@@ -694,3 +694,84 @@ def test_fcycle_converges_no_slower_than_the_vcycle():
     _, hF, _ = O.mgrit_forward(U, K, b, h, "tanh", cf=4, max_levels=5, relax="FCF", max_iter=4, cycle="F")
     assert hF[0] == hV[0]  # the first residual is taken before any coarse-grid work
     assert hF[-1] < hV[-1]
+
+
+# ---------------------------------------------------------------- Algorithm 2 with L-BFGS
+
+def _pairs(seed, n, m):
+    r = np.random.default_rng(seed)
+    A = r.standard_normal((n, n))
+    A = A @ A.T + n * np.eye(n)  # SPD: y = A s gives s.y > 0
+    pairs = []
+    for _ in range(m):
+        s = r.standard_normal(n)
+        pairs.append(([s[:3], s[3:]], [(A @ s)[:3], (A @ s)[3:]]))
+    return pairs, r
+
+
+def test_lbfgs_two_loop_applies_the_dense_bfgs_updates():
+    # textbook BFGS inverse update H <- (I - rho s y^T) H (I - rho y s^T) + rho s s^T,
+    # applied to H0 = gamma I (gamma from the newest pair) for the stored pairs in order
+    n = 7
+    pairs, r = _pairs(40, n, 4)
+    flat = [(np.concatenate(s), np.concatenate(y)) for s, y in pairs]
+    gamma = flat[-1][0] @ flat[-1][1] / (flat[-1][1] @ flat[-1][1])
+    H = gamma * np.eye(n)
+    for s, y in flat:
+        rho = 1.0 / (s @ y)
+        V = np.eye(n) - rho * np.outer(y, s)
+        H = V.T @ H @ V + rho * np.outer(s, s)
+    g = r.standard_normal(n)
+    got = np.concatenate(O.lbfgs_direction([g[:3], g[3:]], pairs))
+    assert np.allclose(got, H @ g, rtol=1e-12, atol=1e-12)
+    # the newest secant equation H y = s, and no pairs: H = I
+    s_new, y_new = pairs[-1]
+    assert np.allclose(np.concatenate(O.lbfgs_direction(y_new, pairs)), np.concatenate(s_new), rtol=1e-12)
+    assert np.array_equal(np.concatenate(O.lbfgs_direction([g[:3], g[3:]], [])), g)
+
+
+def test_accuracy_counts_argmax_hits():
+    r = np.random.default_rng(41)
+    uN, W, mu = r.standard_normal((50, 6)), r.standard_normal((4, 6)), r.standard_normal(4)
+    labels = r.integers(0, 4, 50)
+    hits = sum(int(np.argmax(W @ uN[k] + mu) == labels[k]) for k in range(50))
+    assert O.accuracy(uN, W, mu, labels) == hits / 50
+
+
+def _lbfgs_case():
+    wl = WORKLOADS[5].with_overrides(N=32, B=120, n_features=20)
+    d = generate(wl.with_overrides(B=wl.B + 80))
+    tr = {k: (v[:wl.B] if k in ("y", "onehot", "labels") else v) for k, v in d.items()}
+    va = {k: d[k][wl.B:] for k in ("y", "onehot", "labels")}
+    return wl, tr, va
+
+
+def test_one_shot_lbfgs_converges_on_the_training_set_and_stops_on_validation():
+    wl, d, va = _lbfgs_case()
+    args = (d["y"], d["onehot"], d["L_in"], d["K"], d["b"], d["W"], d["mu"], wl.h, wl.act, wl.opening)
+    kw = dict(cf=4, max_levels=3, min_coarse=1, relax="FCF", m1=2, m2=2, alpha0=0.5)
+    r = O.one_shot_lbfgs(*args, updates=12, **kw)
+    assert r["losses"][-1] < 0.05 * r["losses"][0]
+    assert r["alphas"][0] <= 0.5 and all(0 < a <= 1.0 for a in r["alphas"])
+    # a stochastic-gradient run of the same length (Algorithm 2 with a scaled identity)
+    # stays far above: the curvature pairs are doing the work
+    ls, _ = O.one_shot(*args, cf=4, max_levels=3, min_coarse=1, relax="FCF", updates=12, lr=0.5, m1=2, m2=2)
+    assert r["losses"][-1] < 0.5 * ls[-1]
+    # the validation stop ends the run at the first update that reaches the target
+    full = O.one_shot_lbfgs(*args, updates=12, y_val=va["y"], onehot_val=va["onehot"], **kw)
+    target = sorted(full["accuracies"])[len(full["accuracies"]) // 2]
+    first = next(i for i, a in enumerate(full["accuracies"]) if a >= target)
+    stop = O.one_shot_lbfgs(*args, updates=12, y_val=va["y"], onehot_val=va["onehot"], target_acc=target, **kw)
+    assert len(stop["losses"]) == first + 1 and stop["accuracies"] == full["accuracies"][:first + 1]
+
+
+def test_one_shot_lbfgs_with_exact_inner_solves_takes_exact_gradients():
+    # with many inner iterations the MGRIT states are the serial ones, so the first
+    # direction is -alpha0 times the exact reduced gradient (serial backpropagation)
+    wl, d, _ = _lbfgs_case()
+    args = (d["y"], d["onehot"], d["L_in"], d["K"], d["b"], d["W"], d["mu"], wl.h, wl.act, wl.opening)
+    r = O.one_shot_lbfgs(*args, updates=1, cf=4, max_levels=3, min_coarse=1, relax="FCF", m1=30, m2=30,
+                         alpha0=0.25, max_ls=1)
+    _, wo = O.serial_training(*args, updates=1, lr=0.25)
+    for k in ("K", "b", "W", "mu", "L_in"):
+        assert rel(r["weights"][k], wo[k]) < 1e-10, k
