@@ -240,6 +240,26 @@ int32_t lp_loss_terminal(const lp_problem* prob, int32_t nc, const void* uN, con
  * design update of Algorithm 2 with a scaled-identity Hessian approximation). */
 int32_t lp_sgd_update(int32_t dtype, size_t n, double lr, const void* g, void* x, void* stream);
 
+/* Vector algebra of the design update of Algorithm 2 with a limited-memory
+ * BFGS Hessian approximation (Section 4; the two-loop recursion runs on the
+ * host over these calls), on n elements of the given dtype:
+ *   lp_vec_axpby: y <- a x + b y (b = 0: y <- a x, whatever y held);
+ *   lp_vec_dot:   out[0] <- sum_i x_i y_i, accumulated in fp64 in a fixed order
+ *                 (bitwise reproducible); out is a device array of at least
+ *                 1 + LP_DOT_PARTIALS doubles, out[1..] being scratch. */
+#define LP_DOT_PARTIALS 256
+int32_t lp_vec_axpby(int32_t dtype, size_t n, double a, const void* x, double b, void* y, void* stream);
+int32_t lp_vec_dot(int32_t dtype, size_t n, const void* x, const void* y, double* out, void* stream);
+
+/* Classification accuracy at the network output (the validation measure of
+ * Algorithm 2's stopping test, Section 4): the fraction of the B examples
+ * whose predicted class argmax_j (W u_k^N + mu)_j, logits in fp64, equals the
+ * class of their one-hot row c (first index on ties, on both sides).
+ * uN [B][q], W [nc][q], mu [nc], c [B][nc] (problem dtype); acc: one device
+ * double. ws: device workspace of at least lp_workspace_bytes(prob, NULL) bytes. */
+int32_t lp_accuracy(const lp_problem* prob, int32_t nc, const void* uN, const void* W, const void* mu,
+                    const void* c, double* acc, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- tracing (a profiling aid, not part of the method) ----
  * When enabled for a kernel kind, every launch of that kind records a pair of
  * HIP events on the launch's stream; lp_trace_read sums their elapsed times.

@@ -231,6 +231,47 @@ hipError_t launch_open_grad(const Shape& s, int opening, int nf, int B, const vo
                       : open_grad_t<double>(s, opening, nf, B, y, L, lam0, dL, st);
 }
 
+// y <- a x + b y (b == 0: y <- a x, whatever y held)
+template <typename T>
+__global__ __launch_bounds__(NT) void k_axpby(size_t n, double a, const T* x, double b, T* y) {
+  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < n; i += (size_t)gridDim.x * NT)
+    y[i] = b == 0.0 ? (T)(a * (double)x[i]) : (T)(a * (double)x[i] + b * (double)y[i]);
+}
+
+// Dot product in fp64 and in a fixed order: workgroup w sums the elements
+// w NT + t (+ k DOT_BLOCKS NT) per thread, then its threads in a fixed tree; the
+// second pass adds the DOT_BLOCKS partials in order.
+template <typename T>
+__global__ __launch_bounds__(NT) void k_dot_part(size_t n, const T* x, const T* y, double* part) {
+  __shared__ double sh[NT];
+  double s = 0.0;
+  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < n; i += (size_t)DOT_BLOCKS * NT)
+    s += (double)x[i] * (double)y[i];
+  s = block_sum<NT>(s, sh);
+  if (threadIdx.x == 0) part[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(64) void k_dot_final(const double* part, double* out) {
+  if (threadIdx.x != 0) return;
+  double s = 0.0;
+  for (int w = 0; w < DOT_BLOCKS; ++w) s += part[w];
+  out[0] = s;
+}
+
+hipError_t launch_axpby(int dtype, size_t n, double a, const void* x, double b, void* y, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  if (dtype == 0) k_axpby<float><<<grid_for(n), NT, 0, st>>>(n, a, (const float*)x, b, (float*)y);
+  else k_axpby<double><<<grid_for(n), NT, 0, st>>>(n, a, (const double*)x, b, (double*)y);
+  return hipGetLastError();
+}
+
+hipError_t launch_dot(int dtype, size_t n, const void* x, const void* y, double* out, hipStream_t st) {
+  if (dtype == 0) k_dot_part<float><<<DOT_BLOCKS, NT, 0, st>>>(n, (const float*)x, (const float*)y, out + 1);
+  else k_dot_part<double><<<DOT_BLOCKS, NT, 0, st>>>(n, (const double*)x, (const double*)y, out + 1);
+  k_dot_final<<<1, 64, 0, st>>>(out + 1, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_sgd(int dtype, size_t n, double lr, const void* g, void* x, hipStream_t st) {
   if (n == 0) return hipSuccess;
   if (dtype == 0) k_sgd<float><<<grid_for(n), NT, 0, st>>>(n, (float)lr, (const float*)g, (float*)x);

@@ -738,6 +738,36 @@ int32_t lp_sgd_update(int32_t dtype, size_t n, double lr, const void* g, void* x
   return LP_OK;
 }
 
+int32_t lp_vec_axpby(int32_t dtype, size_t n, double a, const void* x, double b, void* y, void* stream) {
+  if (dtype != LP_F32 && dtype != LP_F64) return fail(LP_EINVAL, "bad dtype %d", dtype);
+  if (n && (!x || !y)) return fail(LP_EINVAL, "NULL array argument");
+  LP_TRY(lp::launch_axpby(dtype, n, a, x, b, y, static_cast<hipStream_t>(stream)), "axpby");
+  return LP_OK;
+}
+
+int32_t lp_vec_dot(int32_t dtype, size_t n, const void* x, const void* y, double* out, void* stream) {
+  static_assert(LP_DOT_PARTIALS == lp::DOT_BLOCKS, "dot partial count");
+  if (dtype != LP_F32 && dtype != LP_F64) return fail(LP_EINVAL, "bad dtype %d", dtype);
+  if (!out || (n && (!x || !y))) return fail(LP_EINVAL, "NULL array argument");
+  LP_TRY(lp::launch_dot(dtype, n, x, y, out, static_cast<hipStream_t>(stream)), "dot");
+  return LP_OK;
+}
+
+int32_t lp_accuracy(const lp_problem* p, int32_t nc, const void* uN, const void* W, const void* mu, const void* c,
+                    double* acc, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  if (nc < 1 || nc > 64) return fail(LP_EINVAL, "need 1 <= nc <= 64, nc = %d", nc);
+  if (!uN || !W || !mu || !c || !acc) return fail(LP_EINVAL, "NULL array argument");
+  if (p->B == 0) return fail(LP_EINVAL, "the accuracy needs B >= 1");
+  rc = check_ws(ws, ws_bytes, lp::loss_workspace_bytes(p->B, (int)qdim(p), nc));
+  if (rc) return rc;
+  LP_TRY(lp::launch_accuracy(p->dtype, p->B, (int)qdim(p), nc, uN, W, mu, c, acc, ws,
+                             static_cast<hipStream_t>(stream)),
+         "accuracy");
+  return LP_OK;
+}
+
 int32_t lp_trace_enable(uint32_t kind_mask) {
   std::lock_guard<std::mutex> lk(g_trace_mu);
   // earlier records may still be pending on some stream: wait before reusing their events

@@ -170,5 +170,10 @@ hipError_t launch_loss(int dtype, int B, int q, int nc, const void* uN, const vo
                        const void* c, double* J, void* lamN, void* dW, void* dmu, void* ws, hipStream_t st);
 size_t loss_workspace_bytes(int B, int q, int nc);  // lp_loss.hip
 hipError_t launch_sgd(int dtype, size_t n, double lr, const void* g, void* x, hipStream_t st);
+constexpr int DOT_BLOCKS = 256;  // partials of lp_vec_dot (out[1 .. DOT_BLOCKS])
+hipError_t launch_axpby(int dtype, size_t n, double a, const void* x, double b, void* y, hipStream_t st);
+hipError_t launch_dot(int dtype, size_t n, const void* x, const void* y, double* out, hipStream_t st);
+hipError_t launch_accuracy(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,
+                           const void* c, double* acc, void* ws, hipStream_t st);  // lp_loss.hip
 
 }  // namespace lp

@@ -109,6 +109,36 @@ __global__ __launch_bounds__(NT) void k_wfinal(const double* part, int nch, T* d
   else dmu[j] = (T)t;
 }
 
+// Classification hit of each example: 1 when argmax_j (W u + mu)_j equals
+// argmax_j c_j (the first index on ties, on both), else 0. One segment of S
+// lanes per example as in k_head; logits in fp64.
+template <typename T>
+__global__ __launch_bounds__(NT) void k_hits(const T* uN, const T* Wc, const T* mu, const T* c, double* hit, int B,
+                                             int q, int nc, int S) {
+  const int t = threadIdx.x, j = t & (S - 1);
+  const int e = blockIdx.x * (NT / S) + t / S;
+  const bool on = e < B;
+  const T* u = uN + (size_t)(on ? e : B - 1) * q;
+  double zj = -INFINITY;
+  for (int jj = 0; jj < nc; ++jj) {
+    double p = 0.0;
+    for (int i = j; i < q; i += S) p += (double)Wc[(size_t)jj * q + i] * (double)u[i];
+    for (int off = S / 2; off > 0; off >>= 1) p += __shfl_xor(p, off, 64);
+    if (j == jj) zj = p + (double)mu[jj];
+  }
+  const double cj = j < nc && on ? (double)c[(size_t)(on ? e : 0) * nc + j] : -INFINITY;
+  // (value, index) arg-max over the segment: larger value wins, the lower index on ties
+  double zv = zj, cv = cj;
+  int zi = j, ci = j;
+  for (int off = S / 2; off > 0; off >>= 1) {
+    const double zo = __shfl_xor(zv, off, 64), co = __shfl_xor(cv, off, 64);
+    const int zio = __shfl_xor(zi, off, 64), cio = __shfl_xor(ci, off, 64);
+    if (zo > zv || (zo == zv && zio < zi)) zv = zo, zi = zio;
+    if (co > cv || (co == cv && cio < ci)) cv = co, ci = cio;
+  }
+  if (on && j == 0) hit[e] = zi == ci ? 1.0 : 0.0;
+}
+
 size_t up(size_t x) { return (x + 255) / 256 * 256; }
 
 template <typename T>
@@ -131,7 +161,26 @@ hipError_t loss_t(int B, int q, int nc, const void* uN, const void* Wc, const vo
   return hipGetLastError();
 }
 
+template <typename T>
+hipError_t accuracy_t(int B, int q, int nc, const void* uN, const void* Wc, const void* mu, const void* c,
+                      double* acc, void* ws, hipStream_t st) {
+  double* hit = static_cast<double*>(ws);
+  int S = 1;
+  while (S < nc) S *= 2;
+  const int per = NT / S;
+  k_hits<T><<<(B + per - 1) / per, NT, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu, (const T*)c, hit, B, q,
+                                                nc, S);
+  k_mean<<<1, NT_MEAN, 0, st>>>(hit, B, acc);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_accuracy(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,
+                           const void* c, double* acc, void* ws, hipStream_t st) {
+  return dtype == 0 ? accuracy_t<float>(B, q, nc, uN, Wc, mu, c, acc, ws, st)
+                    : accuracy_t<double>(B, q, nc, uN, Wc, mu, c, acc, ws, st);
+}
 
 size_t loss_workspace_bytes(int B, int q, int nc) {
   const size_t nch = (size_t)(B + CHUNK - 1) / CHUNK;

@@ -38,7 +38,8 @@ EXPORTS = (
     "lp_abi_version", "lp_status_string", "lp_last_error", "lp_workspace_bytes",
     "lp_dsig_bytes", "lp_serial_forward", "lp_serial_adjoint", "lp_mgrit_forward", "lp_mgrit_adjoint",
     "lp_gradient", "lp_residual_norm", "lp_open_forward", "lp_open_grad",
-    "lp_loss_terminal", "lp_sgd_update", "lp_trace_enable", "lp_trace_read",
+    "lp_loss_terminal", "lp_sgd_update", "lp_vec_axpby", "lp_vec_dot", "lp_accuracy",
+    "lp_trace_enable", "lp_trace_read",
 )
 
 
@@ -91,6 +92,9 @@ _SIGS = {
     "lp_open_grad": ([_P, _i32, _i32, _v, _v, _v, _v, _v], _i32),
     "lp_loss_terminal": ([_P, _i32, _v, _v, _v, _v, _v, _v, _v, _v, _v, _sz, _v], _i32),
     "lp_sgd_update": ([_i32, _sz, ctypes.c_double, _v, _v, _v], _i32),
+    "lp_vec_axpby": ([_i32, _sz, ctypes.c_double, _v, ctypes.c_double, _v, _v], _i32),
+    "lp_vec_dot": ([_i32, _sz, _v, _v, _v, _v], _i32),
+    "lp_accuracy": ([_P, _i32, _v, _v, _v, _v, _v, _v, _sz, _v], _i32),
     "lp_trace_enable": ([ctypes.c_uint32], _i32),
     "lp_trace_read": ([_i32, _i32, _ip, _dp], _i32),
 }
@@ -323,3 +327,44 @@ def lp_sgd_update(x, g, lr: float) -> None:
     n = x.numel()
     dtype = LP_F32 if x.dtype == torch.float32 else LP_F64
     _check(load().lp_sgd_update(dtype, n, lr, _arr(g, n, "g"), _arr(x, n, "x"), _stream()), "lp_sgd_update")
+
+
+LP_DOT_PARTIALS = 256
+
+
+def _vec_dtype(*ts):
+    import torch
+    dt = ts[0].dtype
+    if dt not in (torch.float32, torch.float64) or any(t.dtype != dt for t in ts):
+        raise ValueError("vectors must share dtype float32 or float64")
+    return LP_F32 if dt == torch.float32 else LP_F64
+
+
+def lp_vec_axpby(y, x, a: float, b: float) -> None:
+    """y <- a x + b y over all elements (b = 0: y <- a x)."""
+    n = y.numel()
+    if x.numel() != n:
+        raise ValueError("x and y differ in size")
+    _check(load().lp_vec_axpby(_vec_dtype(x, y), n, a, _arr(x, n, "x"), b, _arr(y, n, "y"), _stream()),
+           "lp_vec_axpby")
+
+
+def lp_vec_dot(x, y, out) -> None:
+    """out[0] <- x . y in fp64 (out: a device float64 tensor of 1 + LP_DOT_PARTIALS
+    elements; the value is left on the device)."""
+    import torch
+    n = x.numel()
+    if y.numel() != n:
+        raise ValueError("x and y differ in size")
+    _check(load().lp_vec_dot(_vec_dtype(x, y), n, _arr(x, n, "x"), _arr(y, n, "y"),
+                             _arr(out, 1 + LP_DOT_PARTIALS, "out", torch.float64), _stream()), "lp_vec_dot")
+
+
+def lp_accuracy(p: LpProblem, nc: int, uN, W, mu, c, acc, ws) -> None:
+    """acc[0] <- fraction of examples whose predicted class is their one-hot class."""
+    import torch
+    dt = _elem_dtype(p)
+    wp, wn = _ws(ws, 1)
+    _check(load().lp_accuracy(ctypes.byref(p), nc, _arr(uN, p.B * p.q, "uN", dt), _arr(W, nc * p.q, "W", dt),
+                              _arr(mu, nc, "mu", dt), _arr(c, p.B * nc, "c", dt), _arr(acc, 1, "acc", torch.float64),
+                              wp, wn, _stream()), "lp_accuracy")
