@@ -150,10 +150,23 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
     return byts, flops, launches
 
 
-def source_hash() -> str:
+# Source files that define each kernel family (besides the shared headers).
+_FAMILY_SOURCES = {
+    "lp::conv::": ["lp_conv.hip"],
+    "lp::mfma::": ["lp_dense_mfma.hip"],
+    "lp::dense::": ["lp_dense_impl.h", "lp_dense_f32.hip", "lp_dense_f64.hip"],
+}
+_SHARED_SOURCES = ["lp_internal.h", "lp_device.h"]
+
+
+def source_hash(kernels: str = "") -> str:
+    """Hash of the sources of the kernel family named in `kernels` (all sources if
+    it names none), so a counter summary goes stale only when its kernels change."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1812_04352_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    fams = [f for ns, fs in _FAMILY_SOURCES.items() if ns in kernels for f in fs]
+    files = sorted(set(fams + _SHARED_SOURCES)) if fams else sorted(os.listdir(csrc))
+    for f in files:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
@@ -170,7 +183,7 @@ def measured_traffic(kernel: str, workload: str):
     except (OSError, ValueError):
         return None
     ent = rec.get(workload, {}).get(kernel)
-    if not ent or ent.get("source_hash") != source_hash():
+    if not ent or ent.get("source_hash") != source_hash(ent.get("kernel", "")):
         return None
     return ent.get("bytes_per_launch")
 
@@ -237,7 +250,8 @@ def summarize_traffic(workload: str, fetch_dir: str, write_dir: str, copy_fetch_
     for kind, (n, fs, ws, names) in sorted(by_kind.items(), key=lambda t: -(t[1][1] + t[1][2])):
         fk, wk = fs / n, ws / n
         byts = (fk * f_scale + wk * w_scale) * 1024.0
-        ent[kind] = {"bytes_per_launch": byts, "source_hash": source_hash(), "kernel": " / ".join(names)}
+        kn = " / ".join(names)
+        ent[kind] = {"bytes_per_launch": byts, "source_hash": source_hash(kn), "kernel": kn}
         print(f"| {kind} | `{' / '.join(names)}` | {n} | {fk:.0f} | {wk:.0f} | {byts / 1e6:.1f} |")
     rec[workload] = ent
     with open(path, "w") as fh:
