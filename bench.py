@@ -272,7 +272,7 @@ def cpu_baseline(wl, budget_s: float = 12.0):
     except ImportError:  # pragma: no cover
         threadpool_info = threadpool_limits = None
     ncores = len(os.sched_getaffinity(0))
-    Bs = min(wl.B, 1024 if wl.layer == "dense" else 16)
+    Bs = min(wl.B, 1024 if wl.layer == "dense" else 8)
     d = generate(wl.with_overrides(B=Bs))
     ctx = threadpool_limits(ncores) if threadpool_limits else None
     try:
