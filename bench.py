@@ -33,6 +33,9 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "f64": 78.6}  # dense MFMA / fp32 vector (packed), fp64
 
+# dense fp32 widths the library runs on the matrix cores (the others on the vector ALUs)
+MATRIX_CORE_WIDTHS = (32, 64, 220)
+
 KIND_NAMES = ["fwd_fc", "fwd_fres", "fwd_corrf", "fwd_coarsest", "adj_fc", "adj_fres", "adj_corrf",
               "adj_coarsest", "gradient", "residual", "serial"]
 
@@ -64,7 +67,7 @@ def level_visits(L: int, cycle: str):
 
 def record_bytes(wl) -> int:
     """Bytes per value of the sigma' record the step keeps (0: none is kept)."""
-    if wl.dtype != "f32" or wl.act == "identity" or (wl.layer == "dense" and wl.q not in (32, 64)):
+    if wl.dtype != "f32" or wl.act == "identity" or (wl.layer == "dense" and wl.q not in MATRIX_CORE_WIDTHS):
         return 0
     return 1 if wl.act == "relu" else 4
 
@@ -155,6 +158,7 @@ _FAMILY_SOURCES = {
     "lp::conv::": ["lp_conv.hip"],
     "lp::mfma::": ["lp_dense_mfma.hip"],
     "lp::dense::": ["lp_dense_impl.h", "lp_dense_f32.hip", "lp_dense_f64.hip"],
+    "lp::wide::": ["lp_dense_wide.hip"],
 }
 _SHARED_SOURCES = ["lp_internal.h", "lp_device.h"]
 
@@ -193,7 +197,7 @@ def kernel_kind(name: str):
     import re
     if "k_grad<" in name or "k_grad_partial<" in name:
         return "gradient"
-    m = re.search(r"lp::(mfma|conv|dense)::k_(fwd|adj)(_sweep|_serial|_iv)?<([^>]*)>", name)
+    m = re.search(r"lp::(mfma|conv|dense|wide)::k_(fwd|adj)(_sweep|_serial|_iv)?<([^>]*)>", name)
     if not m:
         return None
     fam, d, suffix, targs = m.groups()
@@ -201,7 +205,7 @@ def kernel_kind(name: str):
     if suffix == "_serial":
         mode = 3
     else:
-        mode = int(args[{"mfma": 1, "conv": 0, "dense": 2}[fam]])
+        mode = int(args[{"mfma": 1, "conv": 0, "dense": 2, "wide": 1}[fam]])
     return f"{d}_" + ["fc", "fres", "corrf", "coarsest"][mode]
 
 
@@ -311,7 +315,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default: the second workload)")
+    ap.add_argument("--config", type=int, default=2, help="workload 1..7 (default: the second workload)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-record", action="store_true",
                     help="let the adjoint and the gradient recompute sigma' instead of reading the record")
@@ -449,7 +453,7 @@ def main():
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     else:
         achieved = flops / launches / (avg_ms / 1e3) / 1e12
-        on_mfma = wl.dtype == "f32" and (wl.layer == "conv3x3" or wl.q in (32, 64)) and \
+        on_mfma = wl.dtype == "f32" and (wl.layer == "conv3x3" or wl.q in MATRIX_CORE_WIDTHS) and \
             os.environ.get("LP_DENSE_PATH") != "valu"
         roof = {"bound": "mfma" if on_mfma else "alu", "achieved": achieved, "peak": PEAK_TFLOPS[wl.dtype],
                 "unit": "TFLOP/s"}

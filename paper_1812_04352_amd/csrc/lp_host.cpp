@@ -492,7 +492,9 @@ int dense_grad_chunks(int B, int N) {
 }
 
 bool shape_supported(const Shape& s) {
-  if (s.layer == 0) return s.H == 1 && s.W == 1 && dense_width_supported(s.C) && !(s.dtype == 1 && s.C > 32);
+  if (s.layer == 0)
+    return s.H == 1 && s.W == 1 &&
+           ((dense_width_supported(s.C) && !(s.dtype == 1 && s.C > 32)) || (s.dtype == 0 && wide_width_supported(s.C)));
   return conv_supported(s);
 }
 
@@ -517,31 +519,38 @@ bool use_mfma(const Shape& s) {
   return !(e && strcmp(e, "valu") == 0);
 }
 
+// fp32 dense layers too wide for the per-thread and whole-layer-in-LDS kernels
+bool use_wide(const Shape& s) { return s.layer == 0 && s.dtype == 0 && wide_width_supported(s.C); }
+
 // the sigma' record is written and read by the dense matrix-core kernels and
 // the convolution kernels (no record exists for the identity activation)
 bool dsig_supported(const Shape& s) {
-  return s.act != LP_IDENTITY && (use_mfma(s) || (s.layer == 1 && conv_supported(s)));
+  return s.act != LP_IDENTITY && (use_mfma(s) || use_wide(s) || (s.layer == 1 && conv_supported(s)));
 }
 
 hipError_t launch_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   if (s.layer != 0) return conv_sweep(s, dir, a, st, partials);
+  if (use_wide(s)) return wide_sweep(s.C, dir, a, st, partials);
   if (use_mfma(s)) return mfma_sweep(s.C, dir, a, st, partials);
   return s.dtype == 0 ? dense_sweep_f32(s.C, dir, a, st, partials) : dense_sweep_f64(s.C, dir, a, st, partials);
 }
 
 hipError_t launch_serial(const Shape& s, int dir, const SerialArgs& a, hipStream_t st) {
   if (s.layer != 0) return conv_serial(s, dir, a, st);
+  if (use_wide(s)) return wide_serial(s.C, dir, a, st);
   if (use_mfma(s)) return mfma_serial(s.C, dir, a, st);
   return s.dtype == 0 ? dense_serial_f32(s.C, dir, a, st) : dense_serial_f64(s.C, dir, a, st);
 }
 
 hipError_t launch_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t st, int* partials) {
   if (s.layer != 0) return conv_resid(s, dir, a, st, partials);
+  if (use_wide(s)) return wide_resid(s.C, dir, a, st, partials);
   return s.dtype == 0 ? dense_resid_f32(s.C, dir, a, st, partials) : dense_resid_f64(s.C, dir, a, st, partials);
 }
 
 hipError_t launch_grad(const Shape& s, const GradArgs& a, hipStream_t st) {
   if (s.layer != 0) return conv_grad(s, a, st);
+  if (use_wide(s)) return wide_grad(s.C, a, st);
   if (use_mfma(s)) return mfma_grad(s.C, a, st);
   return s.dtype == 0 ? dense_grad_f32(s.C, a, st) : dense_grad_f64(s.C, a, st);
 }

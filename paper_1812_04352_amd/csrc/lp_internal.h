@@ -147,6 +147,14 @@ hipError_t mfma_serial(int q, int dir, const SerialArgs& a, hipStream_t st);
 hipError_t mfma_grad(int q, const GradArgs& a, hipStream_t st);
 int dense_grad_chunks(int B, int N);
 
+// Dense fp32 matrix-core family for wide layers (lp_dense_wide.hip), width 220:
+// the layer weights stream through LDS in panels
+bool wide_width_supported(int q);
+hipError_t wide_sweep(int q, int dir, const SweepArgs& a, hipStream_t st, int* partials);
+hipError_t wide_serial(int q, int dir, const SerialArgs& a, hipStream_t st);
+hipError_t wide_resid(int q, int dir, const ResidArgs& a, hipStream_t st, int* partials);
+hipError_t wide_grad(int q, const GradArgs& a, hipStream_t st);
+
 // Conv family (lp_conv.hip)
 hipError_t conv_sweep(const Shape& s, int dir, const SweepArgs& a, hipStream_t st, int* partials);
 hipError_t conv_serial(const Shape& s, int dir, const SerialArgs& a, hipStream_t st);

@@ -24,7 +24,7 @@ def sample_of(B, n_rand, seed=0):
     return np.array(sorted(idx))
 
 
-@pytest.fixture(scope="module", params=[1, 2, 3, 4, 5, 6], ids=lambda c: f"cfg{c}")
+@pytest.fixture(scope="module", params=[1, 2, 3, 4, 5, 6, 7], ids=lambda c: f"cfg{c}")
 def full(request):
     wl = WORKLOADS[request.param]
     print(f"[fullsize] cfg{wl.cfg} {wl.name}", flush=True)

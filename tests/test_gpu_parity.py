@@ -23,6 +23,11 @@ DENSE = [
     ("relu8_f32", WORKLOADS[2].with_overrides(C=8, N=32, B=77, n_features=12, n_classes=5)),
     ("conv_relu12", WORKLOADS[4].with_overrides(N=16, B=5, H=12, W=12, n_features=144, max_levels=3)),
     ("conv_tanh28", WORKLOADS[4].with_overrides(N=16, B=3, act="tanh", max_levels=3)),
+    # width 220 (weights streamed through LDS in panels): ragged batch tiles, the
+    # padded last feature block, every activation and record kind
+    ("srelu220", WORKLOADS[7].with_overrides(N=32, B=100, max_levels=3)),
+    ("relu220", WORKLOADS[7].with_overrides(act="relu", N=16, B=70, max_levels=2)),
+    ("tanh220", WORKLOADS[7].with_overrides(act="tanh", N=16, B=33, max_levels=2)),
 ]
 IDS = [n for n, _ in DENSE]
 
@@ -361,7 +366,7 @@ def test_mgrit_cycle_variants(name, wl, relax, cycle):
 # fp32 widths on the matrix cores with a non-identity activation: the ones that keep a sigma' record
 RECORDED = [DENSE[1], DENSE[2], DENSE[3],
             ("srelu32", WORKLOADS[2].with_overrides(act="smoothrelu", N=32, B=77, max_levels=2)),
-            DENSE[6], DENSE[7]]
+            DENSE[6], DENSE[7], DENSE[8], DENSE[9]]
 
 
 def _conv_record(rec, N, B, C, H, W, relu):

@@ -511,7 +511,7 @@ def test_one_shot_with_many_inner_iterations_is_serial_training():
 
 def test_level_sizes_of_workloads():
     expect = {1: [32, 8], 2: [256, 64, 16], 3: [2048, 512, 128, 32, 8], 4: [512, 128, 32, 8],
-              5: [1024, 256, 64], 6: [2048, 512, 128, 32, 8]}
+              5: [1024, 256, 64], 6: [2048, 512, 128, 32, 8], 7: [2048, 512, 128, 32, 8]}
     for cfg, sizes in expect.items():
         wl = WORKLOADS[cfg]
         assert O.level_sizes(wl.N, wl.cf, wl.max_levels, wl.min_coarse) == sizes

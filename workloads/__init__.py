@@ -74,7 +74,7 @@ class Workload:
         return dataclasses.replace(self, **kw)
 
 
-# Workload table. Sizes, activations and schedules of the five synthetic stand-ins.
+# Workload table. Sizes, activations and schedules of the synthetic stand-ins.
 WORKLOADS = {
     1: Workload(cfg=1, name="tiny dense tanh fp64 (q=8, N=32, B=512)", dtype="f64",
                 layer=DENSE, act=TANH, N=32, B=512, C=8, H=1, W=1, T=5.0,
@@ -103,6 +103,15 @@ WORKLOADS = {
     6: Workload(cfg=6, name="Peaks-shaped dense smoothed ReLU fp64 (q=8, N=2048, B=5000)", dtype="f64",
                 layer=DENSE, act=SMOOTHRELU, N=2048, B=5000, C=8, H=1, W=1, T=5.0,
                 n_features=2, n_classes=5, opening="dense_act",
+                cf=4, max_levels=16, min_coarse=8, relax="FCF", fwd_iters=20, adj_iters=20, rtol=1e-5),
+    # The hyperspectral network of Section 5.1 (width 220 = the spectral bands,
+    # identity opening, smoothed ReLU, 16 classes, T = 20) at its largest depth,
+    # N = 2048, with the batch of Section 5.2 (1000 pixels), solved to a relative
+    # residual drop of five orders of magnitude; fp32 so that the layer products
+    # run on the matrix cores.
+    7: Workload(cfg=7, name="hyperspectral-shaped dense smoothed ReLU fp32 (q=220, N=2048, B=1000)", dtype="f32",
+                layer=DENSE, act=SMOOTHRELU, N=2048, B=1000, C=220, H=1, W=1, T=20.0,
+                n_features=220, n_classes=16, opening="identity",
                 cf=4, max_levels=16, min_coarse=8, relax="FCF", fwd_iters=20, adj_iters=20, rtol=1e-5),
 }
 
@@ -153,6 +162,16 @@ def generate(wl: Workload, data_seed: Optional[int] = None,
     elif wl.cfg == 3:
         y = rd.standard_normal((B, wl.n_features))
         labels = rd.integers(0, nc, size=B)
+    elif wl.cfg == 7:
+        # per class a smooth spectrum (three Gaussian bumps over the bands); each
+        # pixel scales its class spectrum by a brightness in [0.8, 1.2] and adds noise
+        bands = np.arange(wl.n_features, dtype=np.float64)
+        centers = rd.uniform(0.0, wl.n_features, size=(nc, 3, 1))
+        widths = rd.uniform(10.0, 40.0, size=(nc, 3, 1))
+        amps = rd.uniform(0.3, 1.0, size=(nc, 3, 1))
+        means = np.sum(amps * np.exp(-((bands - centers) / widths) ** 2), axis=1)
+        labels = rd.integers(0, nc, size=B)
+        y = means[labels] * rd.uniform(0.8, 1.2, size=(B, 1)) + 0.05 * rd.standard_normal((B, wl.n_features))
     elif wl.cfg == 4:
         patterns = rd.uniform(0.0, 1.0, size=(nc, 5, 5))
         offsets = np.stack([rd.integers(0, wl.H - 4, size=nc), rd.integers(0, wl.W - 4, size=nc)], axis=1) \
@@ -189,6 +208,11 @@ def generate(wl: Workload, data_seed: Optional[int] = None,
         K = _normal(rw, (N, q, q), 0.3)
         b = _normal(rw, (N, q), 0.05)
         W = _normal(rw, (nc, q), 0.5)
+    elif wl.cfg == 7:
+        L_in = None
+        K = _normal(rw, (N, q, q), 0.003)
+        b = _normal(rw, (N, q), 0.01)
+        W = _normal(rw, (nc, q), 0.1)
     elif wl.cfg == 4:
         L_in = _kaiming(rw, (C, 1, 3, 3), 9, 0.1)
         K = _kaiming(rw, (N, C, C, 3, 3), 9 * C, 0.1)
