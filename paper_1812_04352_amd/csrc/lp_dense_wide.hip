@@ -195,12 +195,13 @@ struct Pan {
 template <int Q>
 __device__ __forceinline__ void fetch_f(Pan<Q>& pr, const float* __restrict__ Kn, int p) {
   using G = Geo<Q>;
+  const float* base = Kn + 32 * p;  // workgroup-uniform; 32-bit per-slot offsets
 #pragma unroll
   for (int s = 0; s < G::PPT; ++s) {
     const int idx = threadIdx.x + s * NT;
-    const int o = idx >> 3, col = 32 * p + 4 * (idx & 7);
-    pr.r[s] = (idx < G::PV && o < Q && col < Q) ? *reinterpret_cast<const f32x4*>(Kn + (size_t)o * Q + col)
-                                                 : f32x4{};
+    const int o = idx >> 3, c4 = idx & 7;
+    const bool ok = idx < G::PV && o < Q && 32 * p + 4 * c4 < Q;
+    pr.r[s] = ok ? *reinterpret_cast<const f32x4*>(base + (o * Q + 4 * c4)) : f32x4{};
   }
 }
 
@@ -214,29 +215,32 @@ __device__ __forceinline__ void put_f(float* buf, const Pan<Q>& pr) {
   }
 }
 
-// adjoint panel p of K_n: slot = (row ii, 4 columns o4) of K_n[32p + ii][4 o4 ..]
-template <int Q>
-__device__ __forceinline__ void fetch_a(Pan<Q>& pr, const float* __restrict__ Kn, int p) {
+// adjoint panel p of K_n: slot = (row ii, 4 columns o4) of K_n[32p + ii][4 o4 ..];
+// slots S0 .. S1-1 of this thread (the adjoint moves a panel in two parts)
+template <int Q, int S0, int S1>
+__device__ __forceinline__ void fetch_a(f32x4 (&r)[S1 - S0], const float* __restrict__ Kn, int p) {
   using G = Geo<Q>;
   constexpr int RW = G::QP / 4;  // slots per panel row
+  // a workgroup-uniform panel base and 32-bit per-slot offsets (few registers)
+  const float* base = Kn + (size_t)(32 * p) * Q;
 #pragma unroll
-  for (int s = 0; s < G::PPT; ++s) {
+  for (int s = S0; s < S1; ++s) {
     const int idx = threadIdx.x + s * NT;
-    const int ii = idx / RW, o4 = idx - ii * RW, i = 32 * p + ii;
-    pr.r[s] = (idx < G::PV && i < Q && 4 * o4 < Q) ? *reinterpret_cast<const f32x4*>(Kn + (size_t)i * Q + 4 * o4)
-                                                    : f32x4{};
+    const int ii = idx / RW, o4 = idx - ii * RW;
+    const bool ok = idx < G::PV && 32 * p + ii < Q && 4 * o4 < Q;
+    r[s - S0] = ok ? *reinterpret_cast<const f32x4*>(base + (ii * Q + 4 * o4)) : f32x4{};
   }
 }
 
-template <int Q>
-__device__ __forceinline__ void put_a(float* buf, const Pan<Q>& pr) {
+template <int Q, int S0, int S1>
+__device__ __forceinline__ void put_a(float* buf, const f32x4 (&r)[S1 - S0]) {
   using G = Geo<Q>;
   constexpr int RW = G::QP / 4;
 #pragma unroll
-  for (int s = 0; s < G::PPT; ++s) {
+  for (int s = S0; s < S1; ++s) {
     const int idx = threadIdx.x + s * NT;
     const int ii = idx / RW, o4 = idx - ii * RW;
-    if (idx < G::PV) *reinterpret_cast<f32x4*>(buf + ii * G::PLA + 4 * o4) = pr.r[s];
+    if (idx < G::PV) *reinterpret_cast<f32x4*>(buf + ii * G::PLA + 4 * o4) = r[s - S0];
   }
 }
 
@@ -279,25 +283,36 @@ __device__ __forceinline__ void prod(f32x4 (&z)[Geo<Q>::NB], const f32x4 (&v)[Ge
   }
 }
 
-// w = K_n^T s (same calling rules as prod)
+// w = K_n^T s (same calling rules as prod). The next panel moves in two parts,
+// each fetched before half of the current panel's products and written after it,
+// so only half a panel is held in registers at a time.
 template <int Q>
 __device__ __forceinline__ void prod_t(f32x4 (&w)[Geo<Q>::NB], const f32x4 (&s)[Geo<Q>::NB],
                                        const float* __restrict__ Kn, float* buf, int lane) {
   using G = Geo<Q>;
-  constexpr int NB = G::NB;
+  constexpr int NB = G::NB, H1 = (G::PPT + 1) / 2;
   const int g = lane >> 4, i = lane & 15;
-  Pan<Q> pr;
-  fetch_a<Q>(pr, Kn, 0);
+  {
+    f32x4 r0[H1], r1[G::PPT - H1];
+    fetch_a<Q, 0, H1>(r0, Kn, 0);
+    fetch_a<Q, H1, G::PPT>(r1, Kn, 0);
+    put_a<Q, 0, H1>(buf, r0);
+    put_a<Q, H1, G::PPT>(buf, r1);
+  }
 #pragma unroll
   for (int ob = 0; ob < NB; ++ob) w[ob] = 0.f;
-  put_a<Q>(buf, pr);
   __syncthreads();
 #pragma unroll
   for (int p = 0; p < G::NP; ++p) {
-    if (p + 1 < G::NP) fetch_a<Q>(pr, Kn, p + 1);
     const float* P = buf + (p & 1) * G::PSZ + 4 * g * G::PLA + i;
+    float* nxt = buf + ((p + 1) & 1) * G::PSZ;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
+      f32x4 r0[H1], r1[G::PPT - H1];
+      if (p + 1 < G::NP) {
+        if (h == 0) fetch_a<Q, 0, H1>(r0, Kn, p + 1);
+        else fetch_a<Q, H1, G::PPT>(r1, Kn, p + 1);
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float av[NB];
@@ -306,9 +321,14 @@ __device__ __forceinline__ void prod_t(f32x4 (&w)[Geo<Q>::NB], const f32x4 (&s)[
 #pragma unroll
         for (int ob = 0; ob < NB; ++ob)
           w[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[ob], s[2 * p + h][r], w[ob], 0, 0, 0);
+        // keep the next slice's reads from being hoisted here (registers)
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (p + 1 < G::NP) {
+        if (h == 0) put_a<Q, 0, H1>(nxt, r0);
+        else put_a<Q, H1, G::PPT>(nxt, r1);
       }
     }
-    if (p + 1 < G::NP) put_a<Q>(buf + ((p + 1) & 1) * G::PSZ, pr);
     __syncthreads();
   }
 }
@@ -327,7 +347,7 @@ __device__ __forceinline__ void xcd_item(int& tile, int& itv) {
 
 // ------------------------------------------------------------------ forward
 template <int Q, int MODE, bool REC>
-__global__ __launch_bounds__(NT) void k_fwd(SweepArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_fwd(SweepArgs a) {
   using G = Geo<Q>;
   constexpr int NB = G::NB;
   __shared__ __attribute__((aligned(16))) float buf[2 * G::PSZ];
@@ -468,7 +488,7 @@ __device__ __forceinline__ void sigma_prime(f32x4 (&d)[Geo<Q>::NB], const SweepA
 // Interval k runs from its upper C-point (k+1)c down to kc; step j produces level
 // point i = (k+1)c-1-j, linearised at the fine state of index i*stride.
 template <int Q, int MODE, bool REC>
-__global__ __launch_bounds__(NT) void k_adj(SweepArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_adj(SweepArgs a) {
   using G = Geo<Q>;
   constexpr int NB = G::NB;
   __shared__ __attribute__((aligned(16))) float buf[2 * G::PSZ];
@@ -507,7 +527,7 @@ __global__ __launch_bounds__(NT) void k_adj(SweepArgs a) {
       if (k + 1 < Nc) store_row<Q>(X + top * slice + row, v, g);
     }
   }
-  f32x4 w2[NB];  // FRES: K^T (sigma' * upper C-point) of the interval's last layer
+  double acc = 0.0;  // FRES: squared residual of the lower C-point
   for (int j = 0; j < nsteps; ++j) {
     const long i = top - 1 - j;
     const size_t n = (size_t)i * a.stride;
@@ -527,39 +547,42 @@ __global__ __launch_bounds__(NT) void k_adj(SweepArgs a) {
       }
       if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) store_row<Q>(X + (size_t)i * slice + row, v, g);
     }
-    if (MODE == SWEEP_FRES && j == nsteps - 1) {
-      // coarse adjoint step from the upper C-point, linearised at the same fine
-      // state; sigma' is taken again (same operands, same result) rather than kept
-      sigma_prime<Q, REC>(d, a, n, slice, row, on, buf, lane);
-      f32x4 t[NB];
+  }
+  if constexpr (MODE == SWEEP_FRES) {
+    // coarse adjoint step from the upper C-point, linearised at the fine state of
+    // the interval's last step (sigma' is taken again: same operands, same
+    // result), then the residual and the FAS restriction with v the relaxed
+    // lower C-point
+    const size_t n = (size_t)(top - nsteps) * a.stride;
+    f32x4 d[NB], w[NB], t[NB];
+    sigma_prime<Q, REC>(d, a, n, slice, row, on, buf, lane);
+    const float* cup = Cs + (size_t)(k + 1) * a.cs_stride * slice + row;
 #pragma unroll
-      for (int mb = 0; mb < NB; ++mb) t[mb] = 0.f;
-      if (on) load_row<Q>(t, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, g);
+    for (int mb = 0; mb < NB; ++mb) t[mb] = 0.f;
+    if (on) load_row<Q>(t, cup, g);
 #pragma unroll
-      for (int mb = 0; mb < NB; ++mb) t[mb] = d[mb] * t[mb];
-      prod_t<Q>(w2, t, K + n * (Q * Q), buf, lane);
+    for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * t[mb];
+    prod_t<Q>(w, d, K + n * (Q * Q), buf, lane);
+    if (on) {
+      f32x4 ck[NB];
+      load_row<Q>(ck, Cs + (size_t)k * a.cs_stride * slice + row, g);
+      acc = sq_diff<Q>(v, ck);
+      if (a.xn_every > 0 && k % a.xn_every == 0)
+        store_row<Q>(static_cast<float*>(a.Xn) + (size_t)k * slice + row, ck, g);
+      load_row<Q>(t, cup, g);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) t[mb] = v[mb] - (t[mb] + hc * w[mb]);  // g_{l+1}^k
+      store_row<Q>(static_cast<float*>(a.Gn) + (size_t)k * slice + row, t, g);
+      if (k == Nc - 1) {
+        load_row<Q>(ck, Cs + (size_t)Nc * a.cs_stride * slice + row, g);
+        store_row<Q>(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, ck, g);
+      }
     }
   }
 
   if (MODE == SWEEP_FC) {
     if (on) store_row<Q>(static_cast<float*>(a.S) + (size_t)k * slice + row, v, g);
   } else if (MODE == SWEEP_FRES) {
-    double acc = 0.0;
-    if (on) {
-      f32x4 ck[NB], cu[NB];
-      load_row<Q>(ck, Cs + (size_t)k * a.cs_stride * slice + row, g);
-      acc = sq_diff<Q>(v, ck);
-      load_row<Q>(cu, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, g);
-#pragma unroll
-      for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb] - (cu[mb] + hc * w2[mb]);  // g_{l+1}^k
-      store_row<Q>(static_cast<float*>(a.Gn) + (size_t)k * slice + row, cu, g);
-      if (a.xn_every > 0 && k % a.xn_every == 0)
-        store_row<Q>(static_cast<float*>(a.Xn) + (size_t)k * slice + row, ck, g);
-      if (k == Nc - 1) {
-        load_row<Q>(ck, Cs + (size_t)Nc * a.cs_stride * slice + row, g);
-        store_row<Q>(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, ck, g);
-      }
-    }
     if (a.partial) {
       const double s = wg_sum(acc, red);
       if (threadIdx.x == 0) a.partial[(size_t)k * gridDim.x + tile] = s;
