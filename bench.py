@@ -276,7 +276,8 @@ def cpu_baseline(wl, budget_s: float = 12.0):
     except ImportError:  # pragma: no cover
         threadpool_info = threadpool_limits = None
     ncores = len(os.sched_getaffinity(0))
-    Bs = min(wl.B, 1024 if wl.layer == "dense" else 8)
+    # about 10-30 s of oracle work: wide dense layers and convolutions take a smaller sample
+    Bs = min(wl.B, (1024 if wl.q <= 64 else 64) if wl.layer == "dense" else 8)
     d = generate(wl.with_overrides(B=Bs))
     ctx = threadpool_limits(ncores) if threadpool_limits else None
     try:

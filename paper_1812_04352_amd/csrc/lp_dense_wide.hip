@@ -552,7 +552,11 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     // coarse adjoint step from the upper C-point, linearised at the fine state of
     // the interval's last step (sigma' is taken again: same operands, same
     // result), then the residual and the FAS restriction with v the relaxed
-    // lower C-point
+    // lower C-point. The step is evaluated exactly as the coarse level evaluates
+    // its own steps (c + h_c K_n^T (sigma' * c), the product accumulated from
+    // zero), so the FAS right-hand side matches the coarse operator bit for bit;
+    // accumulating the product onto c instead rounds every partial sum at the
+    // size of c and leaves the iteration a residual floor two orders higher.
     const size_t n = (size_t)(top - nsteps) * a.stride;
     f32x4 d[NB], w[NB], t[NB];
     sigma_prime<Q, REC>(d, a, n, slice, row, on, buf, lane);
