@@ -67,7 +67,11 @@ enum { LP_STATE = 0, LP_ADJOINT = 1 };                 /* which system */
 enum { LP_OPEN_IDENTITY = 0, LP_OPEN_DENSE_ACT = 1, LP_OPEN_CONV_ACT = 2 }; /* opening layer */
 
 /* The network and batch (Section 2.2). Dense: C = width q, H = W = 1.
- * Conv: C channels of H x W pixels. h = T / N is the step size. */
+ * Conv: C channels of H x W pixels. h = T / N is the step size.
+ * Kernels exist for dense widths 8, 16, 32, 64 (fp32 and fp64; fp64 up to 32)
+ * and 220 (fp32, the hyperspectral network of Section 5.1), and for 3x3
+ * convolutions with C = 8 channels and an even image height (fp32); other
+ * shapes return LP_EUNSUPPORTED. */
 typedef struct {
   int32_t abi_version;   /* must equal LP_ABI_VERSION */
   int32_t dtype;         /* LP_F32 | LP_F64 */
@@ -132,7 +136,7 @@ size_t lp_workspace_bytes(const lp_problem* prob, const lp_mgrit* mg);
  * call receives. NULL: not written / recomputed from U.
  * Returns the record's size in bytes, or 0 where the kernels for this problem
  * keep none: an invalid problem, LP_IDENTITY, fp64, and dense widths other than
- * 32 and 64 (the fp32 matrix-core kernels). Where it returns 0 every call
+ * 32, 64 and 220 (the fp32 matrix-core kernels). Where it returns 0 every call
  * ignores `dsig`. */
 size_t lp_dsig_bytes(const lp_problem* prob);
 
