@@ -15,7 +15,7 @@ the library on the launch stream over the timed steps, and compared with its
 algorithmic bytes or flops (the model below) to give the roofline fraction.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--no-cpu]
-                       [--relax F|FCF|FCFCF] [--cycle V|F] [--no-record]
+                       [--relax F|FCF|FCFCF] [--cycle V|F] [--cf C] [--no-record]
 """
 from __future__ import annotations
 
@@ -325,6 +325,7 @@ def main():
                     help="only run a plain 1 GiB device copy 5 times (to scale HBM byte counters)")
     ap.add_argument("--relax", choices=["F", "FCF", "FCFCF"], help="relaxation (default: the workload's)")
     ap.add_argument("--cycle", choices=["V", "F"], help="MGRIT cycle (default: the workload's V-cycle)")
+    ap.add_argument("--cf", type=int, help="coarsening factor (default: the workload's, 4)")
     ap.add_argument("--traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="summarise rocprofv3 FETCH_SIZE / WRITE_SIZE runs of --config into profiles/traffic.json "
                          "(no GPU needed)")
@@ -355,8 +356,9 @@ def main():
     from workloads import WORKLOADS, generate
 
     wl = WORKLOADS[args.config]
-    if args.relax or args.cycle:
-        wl = wl.with_overrides(**{k: v for k, v in (("relax", args.relax), ("cycle", args.cycle)) if v})
+    if args.relax or args.cycle or args.cf:
+        wl = wl.with_overrides(**{k: v for k, v in (("relax", args.relax), ("cycle", args.cycle), ("cf", args.cf))
+                                  if v})
 
     def note(msg):
         print(f"[bench] {msg}", file=sys.stderr, flush=True)

@@ -363,6 +363,45 @@ def test_mgrit_cycle_variants(name, wl, relax, cycle):
         assert abs(hist[m] - hr[m]) <= floor * hr[0] + 1e-5 * hr[m], (m, hist, hr)
 
 
+@pytest.mark.parametrize("cf", [2, 8])
+@pytest.mark.parametrize("name,wl", DENSE, ids=IDS)
+def test_mgrit_coarsening_factors(name, wl, cf):
+    """Coarsening factors other than 4 (the intervals' kernels take c at run time;
+    the interval-resident width-32 kernels are built for c = 4, so other factors
+    run the per-step kernels): forward and adjoint iterates and residual
+    histories on the deepest hierarchy the size allows, the forward keeping the
+    sigma' record where the kernels support one (the adjoint then reads it)."""
+    wl = wl.with_overrides(cf=cf)
+    c = case(wl)
+    levels = _deepest(wl)
+    iters = 3
+    mg = sched(wl, iters, levels=levels)
+    ws = L.alloc_workspace(c.p, mg)
+    rec = L.alloc_dsig(c.p) if L.lp_dsig_bytes(c.p) else None
+    U = c.new_traj()
+    it, hist = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, dsig=rec)
+    assert it == iters
+    Ur, hr, _ = O.mgrit_forward(c.ref_traj(), c.d["K"], c.d["b"], wl.h, wl.act, cf=cf, max_levels=levels,
+                                min_coarse=wl.min_coarse, relax=wl.relax, max_iter=iters)
+    assert_close(U.cpu().numpy(), Ur, wl.dtype, f"U iterate, cf={cf}")
+    floor = {"f32": 3e-5, "f64": 1e-11}[wl.dtype]
+    for m in range(iters):
+        assert abs(hist[m] - hr[m]) <= floor * hr[0] + 1e-5 * hr[m], (m, hist, hr)
+    # adjoint linearised at each side's own forward iterate
+    lamN, _, _, _ = _lamN(c, U)
+    lamNr = O.loss_terminal(Ur[-1], c.d["W"], c.d["mu"], c.d["onehot"])[1]
+    Lam = torch.zeros_like(U)
+    Lam[-1] = lamN
+    it, hist = L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, Lam, ws, dsig=rec)
+    Lr0 = np.zeros_like(Ur)
+    Lr0[-1] = lamNr
+    Lr, hr, _ = O.mgrit_adjoint(Ur, Lr0, c.d["K"], c.d["b"], wl.h, wl.act, cf=cf, max_levels=levels,
+                                min_coarse=wl.min_coarse, relax=wl.relax, max_iter=iters)
+    assert_close(Lam.cpu().numpy(), Lr, wl.dtype, f"Lam iterate, cf={cf}")
+    for m in range(iters):
+        assert abs(hist[m] - hr[m]) <= floor * hr[0] + 1e-5 * hr[m], (m, hist, hr)
+
+
 # fp32 widths on the matrix cores with a non-identity activation: the ones that keep a sigma' record
 RECORDED = [DENSE[1], DENSE[2], DENSE[3],
             ("srelu32", WORKLOADS[2].with_overrides(act="smoothrelu", N=32, B=77, max_levels=2)),
