@@ -283,13 +283,14 @@ def _mgrit_case(seed=20, N=32, B=6, q=5, act="tanh", kscale=0.4):
     return K, b, u0, 5.0 / N
 
 
+@pytest.mark.parametrize("c", [2, 4, 8])
 @pytest.mark.parametrize("relax,gain", [("F", 1), ("FCF", 2), ("FCFCF", 3)])
-def test_two_level_finite_step_exactness_forward(relax, gain):
+def test_two_level_finite_step_exactness_forward(relax, gain, c):
     # two-level F: after m iterations points n <= (m+1)c-1 are exact; FCF: n <= (2m+1)c-1;
     # FCFCF: n <= (3m+1)c-1 (each C-relaxation moves the exact front by one interval,
     # the coarse-grid correction by one more)
     K, b, u0, h = _mgrit_case()
-    N, c = K.shape[0], 4
+    N = K.shape[0]
     S = O.serial_forward(u0, K, b, h, "tanh")
     U = np.zeros_like(S)
     U[0] = u0
@@ -300,14 +301,15 @@ def test_two_level_finite_step_exactness_forward(relax, gain):
         err = np.abs(Um - S).reshape(N + 1, -1).max(axis=1)
         assert err[:exact + 1].max() < 1e-14, (m, exact)
         if exact < N:
-            assert err[exact + 1:].max() > 1e-8  # not exact beyond the front
+            assert err[exact + 1:].max() > 1e-12  # not exact beyond the front (well above rounding)
     assert np.abs(Um - S).max() < 1e-14
 
 
+@pytest.mark.parametrize("c", [2, 4, 8])
 @pytest.mark.parametrize("relax,gain", [("F", 1), ("FCF", 2), ("FCFCF", 3)])
-def test_two_level_finite_step_exactness_adjoint(relax, gain):
+def test_two_level_finite_step_exactness_adjoint(relax, gain, c):
     K, b, u0, h = _mgrit_case(seed=21)
-    N, c = K.shape[0], 4
+    N = K.shape[0]
     U = O.serial_forward(u0, K, b, h, "tanh")
     lamN = np.random.default_rng(0).standard_normal(u0.shape)
     S = O.serial_adjoint(U, lamN, K, b, h, "tanh")
@@ -320,7 +322,7 @@ def test_two_level_finite_step_exactness_adjoint(relax, gain):
         err = np.abs(Lm - S).reshape(N + 1, -1).max(axis=1)[::-1]  # distance from the end
         assert err[:exact + 1].max() < 1e-14, (m, exact)
         if exact < N:
-            assert err[exact + 1:].max() > 1e-8
+            assert err[exact + 1:].max() > 1e-12
     assert np.abs(Lm - S).max() < 1e-14
 
 
