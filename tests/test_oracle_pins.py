@@ -300,8 +300,10 @@ def test_two_level_finite_step_exactness_forward(relax, gain, c):
         exact = min((gain * m + 1) * c - 1, N)
         err = np.abs(Um - S).reshape(N + 1, -1).max(axis=1)
         assert err[:exact + 1].max() < 1e-14, (m, exact)
-        if exact < N:
-            assert err[exact + 1:].max() > 1e-12  # not exact beyond the front (well above rounding)
+        if exact < N and (c >= 4 or m == 1):
+            # not exact beyond the front (at c = 2 later iterations may converge
+            # there to rounding before the front arrives)
+            assert err[exact + 1:].max() > 1e-8
     assert np.abs(Um - S).max() < 1e-14
 
 
@@ -321,8 +323,8 @@ def test_two_level_finite_step_exactness_adjoint(relax, gain, c):
         exact = min((gain * m + 1) * c - 1, N)
         err = np.abs(Lm - S).reshape(N + 1, -1).max(axis=1)[::-1]  # distance from the end
         assert err[:exact + 1].max() < 1e-14, (m, exact)
-        if exact < N:
-            assert err[exact + 1:].max() > 1e-12
+        if exact < N and (c >= 4 or m == 1):
+            assert err[exact + 1:].max() > 1e-8
     assert np.abs(Lm - S).max() < 1e-14
 
 
