@@ -1178,8 +1178,13 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   if (Nc > 65535) return hipErrorNotSupported;  // intervals index the grid's y dimension
   const dim3 grid((a.B + EX * W4 - 1) / (EX * W4), (unsigned)Nc);
   if (partials) *partials = (int)(grid.x * grid.y);
-  if constexpr (Q == 32) {
-    if (a.c == IV_CF && iv_enabled()) {
+  // Interval-resident kernels: every sweep at width 32; at width 64 (four layers,
+  // 70 KB of LDS per workgroup, two waves per SIMD) all but the adjoint FRES
+  // sweep, whose per-step kernel with the record requested a step ahead was
+  // measured faster (56.3 against 60.9 ms per step on the deep workload; the
+  // other modes gain 1-6 %).
+  if constexpr (Q == 32 || Q == 64) {
+    if (a.c == IV_CF && iv_enabled() && !(Q == 64 && dir == DIR_ADJ && a.mode == SWEEP_FRES)) {
       if (a.G) sweep_iv<Q, true>(dir, a, grid, st);
       else sweep_iv<Q, false>(dir, a, grid, st);
       return hipGetLastError();
