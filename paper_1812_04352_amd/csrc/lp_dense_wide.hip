@@ -313,16 +313,20 @@ __device__ __forceinline__ void prod_t(f32x4 (&w)[Geo<Q>::NB], const f32x4 (&s)[
         if (h == 0) fetch_a<Q, 0, H1>(r0, Kn, p + 1);
         else fetch_a<Q, H1, G::PPT>(r1, Kn, p + 1);
       }
+      // output blocks in two halves, as in the forward product: 28 A values in
+      // registers, 7 independent accumulation chains
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float av[NB];
+      for (int o0 = 0; o0 < NB; o0 += NB / 2) {
+        float av[4][NB / 2];
 #pragma unroll
-        for (int ob = 0; ob < NB; ++ob) av[ob] = P[(16 * h + r) * G::PLA + 16 * ob];
+        for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int ob = 0; ob < NB; ++ob)
-          w[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[ob], s[2 * p + h][r], w[ob], 0, 0, 0);
-        // keep the next slice's reads from being hoisted here (registers)
-        __builtin_amdgcn_sched_barrier(0);
+          for (int ob = 0; ob < NB / 2; ++ob) av[r][ob] = P[(16 * h + r) * G::PLA + 16 * (o0 + ob)];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int ob = 0; ob < NB / 2; ++ob)
+            w[o0 + ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[r][ob], s[2 * p + h][r], w[o0 + ob], 0, 0, 0);
       }
       if (p + 1 < G::NP) {
         if (h == 0) put_a<Q, 0, H1>(nxt, r0);
