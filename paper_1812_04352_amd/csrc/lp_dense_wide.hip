@@ -561,30 +561,41 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     // zero), so the FAS right-hand side matches the coarse operator bit for bit;
     // accumulating the product onto c instead rounds every partial sum at the
     // size of c and leaves the iteration a residual floor two orders higher.
+    // The residual of the lower C-point is taken first and v is parked in its Gn
+    // row, so the state's registers are free during the coarse product.
     const size_t n = (size_t)(top - nsteps) * a.stride;
-    f32x4 d[NB], w[NB], t[NB];
-    sigma_prime<Q, REC>(d, a, n, slice, row, on, buf, lane);
+    float* gn = static_cast<float*>(a.Gn) + (size_t)k * slice + row;
     const float* cup = Cs + (size_t)(k + 1) * a.cs_stride * slice + row;
-#pragma unroll
-    for (int mb = 0; mb < NB; ++mb) t[mb] = 0.f;
-    if (on) load_row<Q>(t, cup, g);
-#pragma unroll
-    for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * t[mb];
-    prod_t<Q>(w, d, K + n * (Q * Q), buf, lane);
     if (on) {
       f32x4 ck[NB];
       load_row<Q>(ck, Cs + (size_t)k * a.cs_stride * slice + row, g);
       acc = sq_diff<Q>(v, ck);
       if (a.xn_every > 0 && k % a.xn_every == 0)
         store_row<Q>(static_cast<float*>(a.Xn) + (size_t)k * slice + row, ck, g);
-      load_row<Q>(t, cup, g);
-#pragma unroll
-      for (int mb = 0; mb < NB; ++mb) t[mb] = v[mb] - (t[mb] + hc * w[mb]);  // g_{l+1}^k
-      store_row<Q>(static_cast<float*>(a.Gn) + (size_t)k * slice + row, t, g);
       if (k == Nc - 1) {
         load_row<Q>(ck, Cs + (size_t)Nc * a.cs_stride * slice + row, g);
         store_row<Q>(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, ck, g);
       }
+      store_row<Q>(gn, v, g);
+    }
+    f32x4 d[NB], w[NB], t[NB];
+    sigma_prime<Q, REC>(d, a, n, slice, row, on, buf, lane);
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) {
+      t[mb] = 0.f;
+      w[mb] = 0.f;
+    }
+    if (on) load_row<Q>(t, cup, g);
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * t[mb];
+    prod_t<Q>(w, d, K + n * (Q * Q), buf, lane);
+    if (on) {
+      f32x4 vl[NB];
+      load_row<Q>(t, cup, g);
+      load_row<Q>(vl, gn, g);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) t[mb] = vl[mb] - (t[mb] + hc * w[mb]);  // g_{l+1}^k
+      store_row<Q>(gn, t, g);
     }
   }
 
