@@ -244,24 +244,41 @@ __device__ __forceinline__ void put_a(float* buf, const f32x4 (&r)[S1 - S0]) {
   }
 }
 
-// z = K_n v + b_n. Every thread of the workgroup calls it (it holds barriers);
-// buf is two panel buffers, free on entry and on return.
+// Consecutive forward products share the two panel buffers as a chain: a
+// product's last panel fetches the next product's first panel (the next layer is
+// known), so a step does not start with a panel load the whole workgroup waits
+// for. With an odd number of panels the buffer holding a product's first panel
+// alternates; `ph` tracks it and `ready` says whether it is already loaded. (The
+// transposed product does not chain: the extra state spilled in the adjoint
+// kernels and measured slower.)
+struct Chain {
+  int ph = 0;
+  bool ready = false;
+};
+
+// z = K_n v + b_n. Every thread of the workgroup calls it (it holds barriers).
+// Knext: the next product's weights (same kind), whose first panel this product
+// loads during its last one; nullptr ends the chain.
 template <int Q>
 __device__ __forceinline__ void prod(f32x4 (&z)[Geo<Q>::NB], const f32x4 (&v)[Geo<Q>::NB],
                                      const float* __restrict__ Kn, const float* __restrict__ bn, float* buf,
-                                     int lane) {
+                                     int lane, Chain& ch, const float* __restrict__ Knext = nullptr) {
   using G = Geo<Q>;
   constexpr int NB = G::NB;
   const int g = lane >> 4, i = lane & 15;
   Pan<Q> pr;
-  fetch_f<Q>(pr, Kn, 0);
   load_row<Q>(z, bn + 4 * g, g);
-  put_f<Q>(buf, pr);
-  __syncthreads();
+  if (!ch.ready) {
+    fetch_f<Q>(pr, Kn, 0);
+    put_f<Q>(buf + ch.ph * G::PSZ, pr);
+    __syncthreads();
+  }
 #pragma unroll
   for (int p = 0; p < G::NP; ++p) {
-    if (p + 1 < G::NP) fetch_f<Q>(pr, Kn, p + 1);
-    const float* P = buf + (p & 1) * G::PSZ + i * G::PLF + 4 * g;
+    const bool more = p + 1 < G::NP;
+    if (more) fetch_f<Q>(pr, Kn, p + 1);
+    else if (Knext) fetch_f<Q>(pr, Knext, 0);
+    const float* P = buf + ((ch.ph + p) & 1) * G::PSZ + i * G::PLF + 4 * g;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       // output blocks in two halves: half the A registers, still 7 independent chains
@@ -278,9 +295,11 @@ __device__ __forceinline__ void prod(f32x4 (&z)[Geo<Q>::NB], const f32x4 (&v)[Ge
             z[o0 + ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[ob][r], v[2 * p + h][r], z[o0 + ob], 0, 0, 0);
       }
     }
-    if (p + 1 < G::NP) put_f<Q>(buf + ((p + 1) & 1) * G::PSZ, pr);
+    if (more || Knext) put_f<Q>(buf + ((ch.ph + p + 1) & 1) * G::PSZ, pr);
     __syncthreads();
   }
+  ch.ph = (ch.ph + G::NP) & 1;
+  ch.ready = Knext != nullptr;
 }
 
 // w = K_n^T s (same calling rules as prod). The next panel moves in two parts,
@@ -399,10 +418,15 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   // Gn row and finishes g_{l+1}^{k+1} = v - (that value) after the interval, so it
   // holds no extra row of registers across the steps
   float* gn = MODE == SWEEP_FRES ? static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + row : nullptr;
+  Chain ch;
   for (int j = 0; j < nsteps; ++j) {
     const size_t n = (size_t)(kc + j) * a.stride;
+    // the next product: the next step's layer, or CORRF's extra record product
+    const float* knext = j + 1 < nsteps                      ? K + (size_t)(kc + j + 1) * a.stride * (Q * Q)
+                         : (MODE == SWEEP_CORRF && rec) ? K + (size_t)(kc + nsteps) * a.stride * (Q * Q)
+                                                        : nullptr;
     f32x4 z[NB];
-    prod<Q>(z, v, K + n * (Q * Q), bb + n * Q, buf, lane);
+    prod<Q>(z, v, K + n * (Q * Q), bb + n * Q, buf, lane, ch, knext);
     if constexpr (rec) {
       f32x4 dz[NB];
 #pragma unroll
@@ -433,7 +457,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     // sigma' of the layer before the next C-point, from the last F-point
     const size_t n = (size_t)(kc + nsteps) * a.stride;
     f32x4 z[NB];
-    prod<Q>(z, v, K + n * (Q * Q), bb + n * Q, buf, lane);
+    prod<Q>(z, v, K + n * (Q * Q), bb + n * Q, buf, lane, ch);
     apply<Q>(z, a.act, true, g);
     if (on) store_dsig<Q>(a.dsig, n * slice + row, a.act, z, g);
   }
@@ -483,7 +507,9 @@ __device__ __forceinline__ void sigma_prime(f32x4 (&d)[Geo<Q>::NB], const SweepA
 #pragma unroll
     for (int mb = 0; mb < NB; ++mb) u[mb] = 0.f;
     if (on) load_row<Q>(u, static_cast<const float*>(a.Uf) + n * slice + row, g);
-    prod<Q>(d, u, static_cast<const float*>(a.K) + n * (Q * Q), static_cast<const float*>(a.b) + n * Q, buf, lane);
+    Chain own;  // loads its own first panel
+    prod<Q>(d, u, static_cast<const float*>(a.K) + n * (Q * Q), static_cast<const float*>(a.b) + n * Q, buf, lane,
+            own);
     apply<Q>(d, a.act, true, g);
   }
 }
@@ -639,7 +665,8 @@ __global__ __launch_bounds__(NT) void k_resid(ResidArgs a) {
 #pragma unroll
   for (int mb = 0; mb < NB; ++mb) v[mb] = 0.f;
   if (on) load_row<Q>(v, U + (size_t)n * slice + row, g);
-  prod<Q>(z, v, Kn, bn, buf, lane);
+  Chain ch;
+  prod<Q>(z, v, Kn, bn, buf, lane, ch);
   double acc = 0.0;
   if constexpr (DIR == DIR_FWD) {
     apply<Q>(z, a.act, false, g);
@@ -733,7 +760,8 @@ __global__ __launch_bounds__(NT) void k_grad(GradArgs a) {
     if constexpr (REC) {
       load_dsig<Q>(d, a.dsig, (size_t)n * slice + row, a.act, g);
     } else {
-      prod<Q>(d, u, Kn, bn, buf, lane);
+      Chain own;  // loads its own first panel
+      prod<Q>(d, u, Kn, bn, buf, lane, own);
       apply<Q>(d, a.act, true, g);
     }
     // lam^{n+1} is loaded after the product, which needs the registers
