@@ -546,6 +546,7 @@ LBFGS = [
     ("tanh8_f64", WORKLOADS[1].with_overrides(N=32, B=150, max_levels=3)),
     ("tanh32_f32", WORKLOADS[5].with_overrides(N=32, B=120, n_features=20)),
     ("conv_relu12", WORKLOADS[4].with_overrides(N=16, B=6, H=12, W=12, n_features=144, max_levels=3)),
+    ("srelu220", WORKLOADS[7].with_overrides(N=16, B=40, max_levels=2)),
 ]
 
 
