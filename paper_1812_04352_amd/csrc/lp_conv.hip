@@ -813,8 +813,6 @@ constexpr int GOUT = 16 * 96 + CH;  // dWbig then db per chunk
 template <int GH, int GW, int RK>
 __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   constexpr bool REC = RK != 0, RB = RK == 1;
-  // weight entries per thread while staging (the specialised geometry fixes the thread count)
-  constexpr int WPT = GH ? (WV + 64 * make_geo(GH, GW).NW - 1) / (64 * make_geo(GH, GW).NW) : (WV + 63) / 64;
   const SGeo g = geo_of<GH, GW>(ga);
   extern __shared__ float lds[];
   float* bu = lds;                   // CH * CS: u

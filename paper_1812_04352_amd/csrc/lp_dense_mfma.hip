@@ -865,7 +865,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
 // REC: sigma' comes from the record (ReLU: RBYTES, one byte per value) instead of
 // the layer product at the primal state.
 template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG>
-__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(!HASG && REC && RBYTES ? 8 : 1, 8)))
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(Q == 32 && !HASG && REC && RBYTES ? 8 : 1, 8)))
 void k_adj_iv(SweepArgs a) {
   constexpr int EX = 16;
   using C = Cfg<Q, WAVES>;
@@ -901,7 +901,7 @@ void k_adj_iv(SweepArgs a) {
     Lt::load(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
     // at eight waves per SIMD (finest level, byte record) the registers go to
     // occupancy, and the lower C-point is read after the steps
-    if (!(!HASG && REC && RBYTES)) Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
+    if (!(Q == 32 && !HASG && REC && RBYTES)) Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
   } else {
     correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
   }
@@ -964,7 +964,7 @@ void k_adj_iv(SweepArgs a) {
   } else if (MODE == SWEEP_FRES) {
     double acc = 0.0;
     if (on) {
-      if (!HASG && REC && RBYTES) Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
+      if (Q == 32 && !HASG && REC && RBYTES) Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
       acc = sq_diff<V, NB, NV>(v, ck);
 #pragma unroll
       for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb] - cu[mb];  // g_{l+1}^k

@@ -780,7 +780,7 @@ int32_t lp_accuracy(const lp_problem* p, int32_t nc, const void* uN, const void*
 int32_t lp_trace_enable(uint32_t kind_mask) {
   std::lock_guard<std::mutex> lk(g_trace_mu);
   // earlier records may still be pending on some stream: wait before reusing their events
-  for (const TraceRec& r : g_trace) hipEventSynchronize(r.b);
+  for (const TraceRec& r : g_trace) (void)hipEventSynchronize(r.b);
   g_trace.clear();
   g_pool_used = 0;
   g_trace_dropped = 0;
