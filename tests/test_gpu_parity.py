@@ -402,6 +402,39 @@ def test_mgrit_coarsening_factors(name, wl, cf):
         assert abs(hist[m] - hr[m]) <= floor * hr[0] + 1e-5 * hr[m], (m, hist, hr)
 
 
+DEGENERATE = [DENSE[0], DENSE[1], DENSE[2], DENSE[3], DENSE[6], DENSE[8]]
+
+
+@pytest.mark.parametrize("N,cf", [(4, 4), (8, 8), (1, 4)])
+@pytest.mark.parametrize("name,wl", DEGENERATE, ids=[n for n, _ in DEGENERATE])
+def test_degenerate_hierarchies(name, wl, N, cf):
+    """A single coarse interval (N = cf: one workgroup is both the first and the
+    last interval, so both boundary branches of every sweep run in it) and a
+    single layer (N = 1: one level, the serial solve): forward and adjoint iterates
+    against the oracle, with the sigma' record where the kernels keep one."""
+    wl = wl.with_overrides(N=N, cf=cf, max_levels=2, min_coarse=1, T=wl.T * N / wl.N)
+    c = case(wl)
+    iters = 2
+    mg = sched(wl, iters)
+    ws = L.alloc_workspace(c.p, mg)
+    rec = L.alloc_dsig(c.p) if L.lp_dsig_bytes(c.p) else None
+    U = c.new_traj()
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, dsig=rec)
+    Ur, _, _ = O.mgrit_forward(c.ref_traj(), c.d["K"], c.d["b"], wl.h, wl.act, cf=cf, max_levels=2,
+                               min_coarse=1, relax=wl.relax, max_iter=iters)
+    assert_close(U.cpu().numpy(), Ur, wl.dtype, f"U, N={N}, cf={cf}")
+    lamN, _, _, _ = _lamN(c, U)
+    lamNr = O.loss_terminal(Ur[-1], c.d["W"], c.d["mu"], c.d["onehot"])[1]
+    Lam = torch.zeros_like(U)
+    Lam[-1] = lamN
+    L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, Lam, ws, dsig=rec)
+    Lr0 = np.zeros_like(Ur)
+    Lr0[-1] = lamNr
+    Lr, _, _ = O.mgrit_adjoint(Ur, Lr0, c.d["K"], c.d["b"], wl.h, wl.act, cf=cf, max_levels=2, min_coarse=1,
+                               relax=wl.relax, max_iter=iters)
+    assert_close(Lam.cpu().numpy(), Lr, wl.dtype, f"Lam, N={N}, cf={cf}")
+
+
 # fp32 widths on the matrix cores with a non-identity activation: the ones that keep a sigma' record
 RECORDED = [DENSE[1], DENSE[2], DENSE[3],
             ("srelu32", WORKLOADS[2].with_overrides(act="smoothrelu", N=32, B=77, max_levels=2)),
