@@ -1128,6 +1128,174 @@ hipError_t grad(const GradArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ serial solves
+// The coarsest level (and the layer-serial baseline) runs one wave per 16
+// examples through all N_l steps in order: few waves, so each step's loads sit
+// on the critical path unless they were requested earlier. These kernels keep
+// SER_D steps of loads in flight in register rings: the layer after next
+// (weights and bias) and the right-hand-side, sigma' record or primal rows of
+// the step SER_D ahead. A step writes only the next layer into LDS (double
+// buffer, one wave: program order suffices, the barriers are nominal). The
+// arithmetic of a step is that of the interval kernels. At width 64 a layer's
+// weights take 64 registers per lane, so two layers are in flight there.
+constexpr int SER_D = 4;
+
+// Forward: U[j+1] = U[j] + h_l sigma(K_j U[j] + b_j) (+ G[j+1]), j = 0 .. N_l - 1;
+// with REC the level-0 solve records sigma'(z) of every layer.
+template <int Q, bool REC>
+__global__ __launch_bounds__(64) void k_ser_fwd(SweepArgs a) {
+  using C = Cfg<Q, 1>;
+  using Lt = Lay<Q, 16>;
+  using V = typename Lt::V;
+  constexpr int NB = Lt::NB, NV = Lt::NV, D = Q <= 32 ? SER_D : 2;
+  __shared__ float W[2][C::WSZ];
+  const int lane = threadIdx.x & 63;
+  const int e = blockIdx.x * 16 + (lane & 15);
+  const bool on = e < a.B;
+  const size_t slice = (size_t)a.B * Q;
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane >> 4);
+  const float* K = static_cast<const float*>(a.K);
+  const float* bb = static_cast<const float*>(a.b);
+  float* X = static_cast<float*>(a.X);
+  const float* G = static_cast<const float*>(a.G);
+  const int Nl = a.Nl;
+  const float hl = (float)a.hl;
+
+  // rings: slot u holds layer j+1's weights and G row j+1 for the step j = u (mod D)
+  WRegs<Q, 1> wr[D];
+  V gr[D][NB];
+  {
+    WRegs<Q, 1> w0;
+    w_fetch<Q, 1>(w0, K, bb, 0);
+    // every prefetch is issued unconditionally (indices clamped to valid rows), so
+    // the number of loads in flight is fixed and the waits stay exact
+#pragma unroll
+    for (int u = 0; u < D; ++u) w_fetch<Q, 1>(wr[u], K, bb, (size_t)min(u + 1, Nl - 1) * a.stride);
+    if (G) {
+#pragma unroll
+      for (int u = 0; u < D; ++u) Lt::load(gr[u], G + (size_t)min(u + 1, Nl) * slice + row);  // valid rows
+    }
+    w_put<Q, 1>(W[0], w0);
+  }
+  V v[NB];
+#pragma unroll
+  for (int mb = 0; mb < NB; ++mb) v[mb] = 0.f;
+  if (on) Lt::load(v, X + row);
+  __syncthreads();
+  for (int j0 = 0; j0 < Nl; j0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int j = j0 + u;
+      if (j >= Nl) break;
+      V s[NB];
+      Lt::template prod<C::LD>(s, v, W[j & 1], lane);
+      if constexpr (REC) {
+        V dz[NB];
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) dz[mb] = s[mb];
+        apply<V, NB, NV>(dz, a.act, true);
+        if (on) store_dsig<Lt>(a.dsig, (size_t)j * a.stride * slice + row, a.act, dz);
+      }
+      apply<V, NB, NV>(s, a.act, false);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * s[mb];
+      if (G) {
+        add_to<V, NB>(v, gr[u]);
+        Lt::load(gr[u], G + (size_t)min(j + 1 + D, Nl) * slice + row);
+      }
+      if (on) Lt::store(X + (size_t)(j + 1) * slice + row, v);
+      // after the last step this writes a layer nobody reads
+      w_put<Q, 1>(W[(j + 1) & 1], wr[u]);
+      w_fetch<Q, 1>(wr[u], K, bb, (size_t)min(j + 1 + D, Nl - 1) * a.stride);
+      __syncthreads();
+    }
+  }
+}
+
+// Adjoint: Lam[i] = Lam[i+1] + h_l K_i^T (sigma'(K_i U_f[i] + b_i) * Lam[i+1]) (+ G[i]),
+// i = N_l - 1 .. 0, the primal state (or the record, RK = 1 bytes, 2 fp32) at
+// fine index i * stride.
+template <int Q, int RK>
+__global__ __launch_bounds__(64) void k_ser_adj(SweepArgs a) {
+  using C = Cfg<Q, 1>;
+  using Lt = Lay<Q, 16>;
+  using V = typename Lt::V;
+  constexpr int NB = Lt::NB, NV = Lt::NV, D = Q <= 32 ? SER_D : 2;
+  constexpr bool REC = RK != 0;
+  __shared__ float W[2][C::WSZ];
+  const int lane = threadIdx.x & 63;
+  const int e = blockIdx.x * 16 + (lane & 15);
+  const bool on = e < a.B;
+  const size_t slice = (size_t)a.B * Q;
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane >> 4);
+  const float* K = static_cast<const float*>(a.K);
+  const float* bb = static_cast<const float*>(a.b);
+  const float* Uf = static_cast<const float*>(a.Uf);
+  float* X = static_cast<float*>(a.X);
+  const float* G = static_cast<const float*>(a.G);
+  const int Nl = a.Nl;
+  const float hl = (float)a.hl;
+
+  // rings, slot u for the step j = u (mod D), i = Nl - 1 - j: the weights of the
+  // next step's layer i - 1, and the step's own record (or primal) and G rows
+  WRegs<Q, 1> wr[D];
+  RecRow<Lt, RK == 1> rr[REC ? D : 1];
+  V ur[REC ? 1 : D][NB], gr[D][NB];
+  {
+    WRegs<Q, 1> w0;
+    w_fetch<Q, 1>(w0, K, bb, (size_t)(Nl - 1) * a.stride);
+    // every prefetch is issued unconditionally (indices clamped to valid rows), so
+    // the number of loads in flight is fixed and the waits stay exact
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int i = max(Nl - 1 - u, 0);  // every lane reads a valid row
+      w_fetch<Q, 1>(wr[u], K, bb, (size_t)max(i - 1, 0) * a.stride);
+      if constexpr (REC) rr[u].load(a.dsig, (size_t)i * a.stride * slice + row);
+      else Lt::load(ur[u], Uf + (size_t)i * a.stride * slice + row);
+      if (G) Lt::load(gr[u], G + (size_t)i * slice + row);
+    }
+    w_put<Q, 1>(W[0], w0);
+  }
+  V v[NB];
+#pragma unroll
+  for (int mb = 0; mb < NB; ++mb) v[mb] = 0.f;
+  if (on) Lt::load(v, X + (size_t)Nl * slice + row);
+  __syncthreads();
+  for (int j0 = 0; j0 < Nl; j0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int j = j0 + u;
+      if (j >= Nl) break;
+      const int i = Nl - 1 - j;
+      const float* Wj = W[j & 1];
+      V d[NB], w[NB];
+      const int ip = max(i - D, 0);
+      if constexpr (REC) {
+        rr[u].get(d);
+        rr[u].load(a.dsig, (size_t)ip * a.stride * slice + row);
+      } else {
+        Lt::template prod<C::LD>(d, ur[u], Wj, lane);
+        apply<V, NB, NV>(d, a.act, true);
+        Lt::load(ur[u], Uf + (size_t)ip * a.stride * slice + row);
+      }
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * v[mb];
+      Lt::template prod_t<C::LD>(w, d, Wj, lane);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * w[mb];
+      if (G) {
+        add_to<V, NB>(v, gr[u]);
+        Lt::load(gr[u], G + (size_t)ip * slice + row);
+      }
+      if (on) Lt::store(X + (size_t)i * slice + row, v);
+      // after the last step this writes a layer nobody reads
+      w_put<Q, 1>(W[(j + 1) & 1], wr[u]);
+      w_fetch<Q, 1>(wr[u], K, bb, (size_t)max(i - 1 - D, 0) * a.stride);
+      __syncthreads();
+    }
+  }
+}
+
 constexpr int SWEEP_WAVES = 4;   // waves per interval workgroup (2 and 8 measured slower or equal)
 constexpr int SERIAL_WAVES = 1;  // one wave per serial workgroup (more workgroups)
 
@@ -1211,7 +1379,6 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
 
 template <int Q>
 hipError_t serial(int dir, const SerialArgs& s, hipStream_t st) {
-  constexpr int W1 = SERIAL_WAVES;
   SweepArgs a{};
   a.act = s.act;
   a.mode = MODE_SERIAL;
@@ -1226,14 +1393,14 @@ hipError_t serial(int dir, const SerialArgs& s, hipStream_t st) {
   a.X = s.X;
   a.G = s.G;
   a.dsig = s.dsig;
-  const dim3 grid((s.B + SWEEP_EX * W1 - 1) / (SWEEP_EX * W1), 1);
-  constexpr int EX = SWEEP_EX;
+  const dim3 grid((s.B + 15) / 16, 1);
   if (dir == DIR_FWD) {
-    if (s.dsig) launch(k_fwd<Q, MODE_SERIAL, W1, EX, true>, grid, 64 * W1, 0, st, a);
-    else launch(k_fwd<Q, MODE_SERIAL, W1, EX, false>, grid, 64 * W1, 0, st, a);
+    if (s.dsig) launch(k_ser_fwd<Q, true>, grid, 64, 0, st, a);
+    else launch(k_ser_fwd<Q, false>, grid, 64, 0, st, a);
   } else {
-    if (s.dsig) launch(k_adj<Q, MODE_SERIAL, W1, EX, true>, grid, 64 * W1, 0, st, a);
-    else launch(k_adj<Q, MODE_SERIAL, W1, EX, false>, grid, 64 * W1, 0, st, a);
+    if (!s.dsig) launch(k_ser_adj<Q, 0>, grid, 64, 0, st, a);
+    else if (s.act == ACT_RELU) launch(k_ser_adj<Q, 1>, grid, 64, 0, st, a);
+    else launch(k_ser_adj<Q, 2>, grid, 64, 0, st, a);
   }
   return hipGetLastError();
 }
