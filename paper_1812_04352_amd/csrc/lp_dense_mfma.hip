@@ -26,7 +26,7 @@ namespace mfma {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int MODE_SERIAL = 3;  // whole-level serial solve (coarsest level, layer-serial)
+constexpr int MODE_SERIAL = 3;  // SweepArgs.mode of a whole-level serial solve (k_ser_fwd, k_ser_adj)
 
 // tanh(x) = sign(x) (1 - t) / (1 + t) with t = exp(-2|x|), on the hardware exp2
 // and reciprocal; absolute error a few ulp of 1.
@@ -352,7 +352,7 @@ __device__ __forceinline__ double wg_sum(double v, double* red) {
 }
 
 // ------------------------------------------------------------------ forward
-// Interval k = blockIdx.y (serial: the whole level), examples of blockIdx.x.
+// Interval k = blockIdx.y, examples of blockIdx.x.
 // Consecutive workgroups share an interval, so the round-robin dispatch over the
 // 8 XCDs gives each XCD every interval's weights once, in order, and its L2 only
 // has to hold the few intervals in flight (with the interval as the fast index,
@@ -380,9 +380,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
   const float* Cs = static_cast<const float*>(a.Cs);
   const float* Vn = static_cast<const float*>(a.V);
   const int c = a.c;
-  const int nsteps = MODE == MODE_SERIAL ? a.Nl : (MODE == SWEEP_CORRF ? c - 1 : c);
+  const int nsteps = MODE == SWEEP_CORRF ? c - 1 : c;
   const float hl = (float)a.hl, hc = (float)a.hc;
-  const long kc = MODE == MODE_SERIAL ? 0 : (long)k * c;
+  const long kc = (long)k * c;
 
   WRegs<Q, WAVES> wr;
   w_fetch<Q, WAVES>(wr, K, bb, (size_t)kc * a.stride);
@@ -393,7 +393,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
 #pragma unroll
   for (int mb = 0; mb < NB; ++mb) v[mb] = 0.f;
   if (on) {
-    if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
+    if (MODE == SWEEP_FC) {
       // a pending coarse-grid correction of the previous cycle is applied on the fly
       if (MODE == SWEEP_FC && Vn)
         correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
@@ -407,26 +407,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     }
   }
   V coarse[NB];
-  // The serial solve (one wave per workgroup, few workgroups) is latency-bound:
-  // it loads the G row of the next step one step ahead (every lane loads a valid
-  // row; columns of lanes past the batch are never stored). The sweeps keep the
-  // registers for occupancy instead.
-  constexpr bool PF = MODE == MODE_SERIAL;
-  // the final F-relaxation (and a level-0 serial solve) records sigma'(z) of every
-  // layer; CORRF then also takes the product of the layer before the next C-point
-  constexpr bool rec = REC && (MODE == SWEEP_CORRF || MODE == MODE_SERIAL);
-  constexpr int extra = MODE == SWEEP_CORRF && rec ? 1 : 0;
-  V gn[NB];
-  if (PF && G) Lt::load(gn, G + (kc + 1) * slice + row);
+  // the final F-relaxation records sigma'(z) of every layer, and also takes the
+  // product of the layer before the next C-point
+  constexpr bool rec = REC && MODE == SWEEP_CORRF;
+  constexpr int extra = rec ? 1 : 0;
   for (int j = 0; j < nsteps; ++j) {
     // prefetch the next layer (the last step re-fetches its own, or the extra one)
     w_fetch<Q, WAVES>(wr, K, bb, (size_t)(kc + (j + 1 < nsteps ? j + 1 : j + extra)) * a.stride);
-    V gc[NB];
-    if (PF && G) {
-#pragma unroll
-      for (int mb = 0; mb < NB; ++mb) gc[mb] = gn[mb];
-      if (j + 1 < nsteps) Lt::load(gn, G + (kc + j + 2) * slice + row);
-    }
     V s[NB];
     Lt::template prod<C::LD>(s, v, W[j & 1], lane);
     if constexpr (rec) {
@@ -443,14 +430,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     }
 #pragma unroll
     for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * s[mb];
-    if (PF && G) add_to<V, NB>(v, gc);
     if (on) {
-      if (!PF && G) {
+      if (G) {
         V t[NB];
         Lt::load(t, G + (kc + j + 1) * slice + row);
         add_to<V, NB>(v, t);
       }
-      if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) Lt::store(X + (kc + j + 1) * slice + row, v);
+      if (MODE == SWEEP_CORRF) Lt::store(X + (kc + j + 1) * slice + row, v);
     }
     w_put<Q, WAVES>(W[(j + 1) & 1], wr);
     __syncthreads();
@@ -498,7 +484,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
 // point i = (k+1)c-1-j, linearised at the fine state of index i*stride.
 template <int Q, int MODE, int WAVES, int EX, bool REC>
 __global__ __launch_bounds__(64 * WAVES)
-__attribute__((amdgpu_waves_per_eu(Q == 64 && REC && MODE != MODE_SERIAL ? (MODE == SWEEP_FRES ? 3 : 4) : 1, 8))) void k_adj(SweepArgs a) {
+__attribute__((amdgpu_waves_per_eu(Q == 64 && REC ? (MODE == SWEEP_FRES ? 3 : 4) : 1, 8))) void k_adj(SweepArgs a) {
   using C = Cfg<Q, WAVES>;
   using Lt = Lay<Q, EX>;
   using V = typename Lt::V;
@@ -520,9 +506,9 @@ __attribute__((amdgpu_waves_per_eu(Q == 64 && REC && MODE != MODE_SERIAL ? (MODE
   const float* Cs = static_cast<const float*>(a.Cs);
   const float* Vn = static_cast<const float*>(a.V);
   const int c = a.c;
-  const int nsteps = MODE == MODE_SERIAL ? a.Nl : (MODE == SWEEP_CORRF ? c - 1 : c);
+  const int nsteps = MODE == SWEEP_CORRF ? c - 1 : c;
   const float hl = (float)a.hl, hc = (float)a.hc;
-  const long top = MODE == MODE_SERIAL ? (long)a.Nl : (long)(k + 1) * c;
+  const long top = (long)(k + 1) * c;
 
   WRegs<Q, WAVES> wr;
   w_fetch<Q, WAVES>(wr, K, bb, (size_t)(top - 1) * a.stride);
@@ -533,8 +519,8 @@ __attribute__((amdgpu_waves_per_eu(Q == 64 && REC && MODE != MODE_SERIAL ? (MODE
 #pragma unroll
   for (int mb = 0; mb < NB; ++mb) v[mb] = 0.f;
   if (on) {
-    if (MODE == SWEEP_FC || MODE == MODE_SERIAL) {
-      if (MODE == SWEEP_FC && Vn)
+    if (MODE == SWEEP_FC) {
+      if (Vn)
         correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
       else Lt::load(v, X + top * slice + row);
       if (MODE == SWEEP_FC && k == Nc - 1) Lt::store(static_cast<float*>(a.S) + (size_t)Nc * slice + row, v);
@@ -549,30 +535,16 @@ __attribute__((amdgpu_waves_per_eu(Q == 64 && REC && MODE != MODE_SERIAL ? (MODE
 #pragma unroll
     for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb];
   }
-  // The serial solve loads the next step's primal and G rows one step ahead
-  // (every lane loads a valid row; columns of lanes past the batch are never
-  // stored); the sweeps keep the registers for occupancy instead.
-  constexpr bool PF = MODE == MODE_SERIAL;
   constexpr bool rec = REC;  // sigma' from the record instead of K u + b
-  // the record row of the next step is requested one step ahead by the serial
-  // solve and, at width 64, by the sweeps (whose occupancy the extra registers
-  // do not lower there)
-  constexpr bool PFR = rec && (PF || Q == 64);
-  V un[NB], gn[NB], rn[NB];
-  if (PF) {
-    if (!rec) Lt::load(un, Uf + (size_t)(top - 1) * a.stride * slice + row);
-    if (G) Lt::load(gn, G + (size_t)(top - 1) * slice + row);
-  }
+  // at width 64 the record row of the next step is requested one step ahead
+  // (the extra registers do not lower the occupancy there)
+  constexpr bool PFR = rec && Q == 64;
+  V rn[NB];
   if (PFR) load_dsig<Lt>(rn, a.dsig, (size_t)(top - 1) * a.stride * slice + row, a.act);
   for (int j = 0; j < nsteps; ++j) {
     const long i = top - 1 - j;
     w_fetch<Q, WAVES>(wr, K, bb, (size_t)(j + 1 < nsteps ? i - 1 : i) * a.stride);
-    V d[NB], w[NB], gc[NB];
-    if (PF && G) {
-#pragma unroll
-      for (int mb = 0; mb < NB; ++mb) gc[mb] = gn[mb];
-      if (j + 1 < nsteps) Lt::load(gn, G + (size_t)(i - 1) * slice + row);
-    }
+    V d[NB], w[NB];
     if constexpr (rec) {
       // every lane reads a valid row; columns of lanes past the batch are never stored
       if constexpr (PFR) {
@@ -584,15 +556,9 @@ __attribute__((amdgpu_waves_per_eu(Q == 64 && REC && MODE != MODE_SERIAL ? (MODE
       }
     } else {
       V u[NB];
-      if (PF) {
 #pragma unroll
-        for (int mb = 0; mb < NB; ++mb) u[mb] = un[mb];
-        if (j + 1 < nsteps) Lt::load(un, Uf + (size_t)(i - 1) * a.stride * slice + row);
-      } else {
-#pragma unroll
-        for (int mb = 0; mb < NB; ++mb) u[mb] = 0.f;
-        if (on) Lt::load(u, Uf + (size_t)i * a.stride * slice + row);
-      }
+      for (int mb = 0; mb < NB; ++mb) u[mb] = 0.f;
+      if (on) Lt::load(u, Uf + (size_t)i * a.stride * slice + row);
       Lt::template prod<C::LD>(d, u, W[j & 1], lane);
       apply<V, NB, NV>(d, a.act, true);
     }
@@ -610,14 +576,13 @@ __attribute__((amdgpu_waves_per_eu(Q == 64 && REC && MODE != MODE_SERIAL ? (MODE
     Lt::template prod_t<C::LD>(w, d, W[j & 1], lane);
 #pragma unroll
     for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * w[mb];
-    if (PF && G) add_to<V, NB>(v, gc);
     if (on) {
-      if (!PF && G) {
+      if (G) {
         V t[NB];
         Lt::load(t, G + (size_t)i * slice + row);
         add_to<V, NB>(v, t);
       }
-      if (MODE == SWEEP_CORRF || MODE == MODE_SERIAL) Lt::store(X + (size_t)i * slice + row, v);
+      if (MODE == SWEEP_CORRF) Lt::store(X + (size_t)i * slice + row, v);
     }
     w_put<Q, WAVES>(W[(j + 1) & 1], wr);
     __syncthreads();
@@ -1297,7 +1262,6 @@ __global__ __launch_bounds__(64) void k_ser_adj(SweepArgs a) {
 }
 
 constexpr int SWEEP_WAVES = 4;   // waves per interval workgroup (2 and 8 measured slower or equal)
-constexpr int SERIAL_WAVES = 1;  // one wave per serial workgroup (more workgroups)
 
 // The sweeps run on the 16-example shape: measured faster than the 32-example
 // one on every workload (q = 32 and 64, level 0 included), with fewer registers
