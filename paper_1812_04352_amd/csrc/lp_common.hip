@@ -24,13 +24,29 @@ __global__ __launch_bounds__(NT) void k_copy_rows(uint4* X, size_t units, long s
   }
 }
 
-// out[0] = sqrt(sum of partial[0..n)), summed in a fixed order.
-__global__ __launch_bounds__(NT) void k_norm_reduce(const double* partial, int n, double* out) {
-  __shared__ double sh[NT];
+// out[0] = sqrt(sum of partial[0..n)), summed in a fixed order: thread t adds
+// partial[t], partial[t + NTR], ... in index order (eight loads issued at a time,
+// so the serial chain waits once per eight), then the workgroup tree.
+constexpr int NTR = 1024;
+__global__ __launch_bounds__(NTR) void k_norm_reduce(const double* partial, int n, double* out) {
+  __shared__ double sh[NTR];
   double s = 0.0;
-  for (int i = threadIdx.x; i < n; i += NT) s += partial[i];
-  s = block_sum<NT>(s, sh);
+  int i = threadIdx.x;
+  for (; i + 7 * NTR < n; i += 8 * NTR) {
+    double v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = partial[i + k * NTR];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += v[k];
+  }
+  for (; i < n; i += NTR) s += partial[i];
+  s = block_sum<NTR>(s, sh);
   if (threadIdx.x == 0) out[0] = sqrt(s);
+}
+
+// dst[i] = src[i] over 16-byte units.
+__global__ __launch_bounds__(NT) void k_copy16(uint4* dst, const uint4* src, size_t units) {
+  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < units; i += (size_t)gridDim.x * NT) dst[i] = src[i];
 }
 
 __global__ __launch_bounds__(NT) void k_zero(uint32_t* p, size_t n) {
@@ -169,7 +185,11 @@ hipError_t open_fwd_t(const Shape& s, int opening, int nf, int B, const void* y,
                       hipStream_t st) {
   const int q = s.C * s.H * s.W;
   if (opening == 0) {
-    return hipMemcpyAsync(u0, y, (size_t)B * q * sizeof(T), hipMemcpyDeviceToDevice, st);
+    const size_t bytes = (size_t)B * q * sizeof(T);
+    if (bytes % 16 || (uintptr_t)u0 % 16 || (uintptr_t)y % 16)
+      return hipMemcpyAsync(u0, y, bytes, hipMemcpyDeviceToDevice, st);
+    k_copy16<<<grid_for(bytes / 16), NT, 0, st>>>(static_cast<uint4*>(u0), static_cast<const uint4*>(y), bytes / 16);
+    return hipGetLastError();
   }
   return with_act<T>(s.act, [&](auto ac) -> hipError_t {
     constexpr int ACT = decltype(ac)::value;
@@ -209,7 +229,7 @@ hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_
 }
 
 hipError_t launch_norm_reduce(const double* partial, int n, double* out, hipStream_t st) {
-  k_norm_reduce<<<1, NT, 0, st>>>(partial, n, out);
+  k_norm_reduce<<<1, NTR, 0, st>>>(partial, n, out);
   return hipGetLastError();
 }
 

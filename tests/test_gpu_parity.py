@@ -686,3 +686,28 @@ def test_accuracy(name, wl):
     ref = O.accuracy(Uref[-1], c.d["W"], c.d["mu"], c.d["labels"])
     slack = 0.0 if wl.dtype == "f64" else 2.0 / wl.B  # an example on a class boundary
     assert abs(acc.item() - ref) <= slack + 1e-15, (acc.item(), ref)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("q,nc,B", [(32, 1, 45), (32, 3, 257), (32, 17, 45), (32, 64, 45), (220, 10, 33),
+                                    (220, 64, 7), (8, 5, 1)])
+def test_loss_head_class_counts(q, nc, B):
+    """Softmax head, loss, terminal adjoint and classifier gradient against the
+    oracle (Section 2.1 loss, Section 2.3 terminal condition) over class counts
+    that set the lanes per example (1 .. 64) and batches that leave the last
+    workgroup partly empty; width 220 with 64 classes still stages W in LDS."""
+    rng = np.random.default_rng(1000 * q + nc + B)
+    uN = rng.standard_normal((B, q)).astype(np.float32)
+    W = (0.3 * rng.standard_normal((nc, q))).astype(np.float32)
+    mu = (0.1 * rng.standard_normal(nc)).astype(np.float32)
+    onehot = np.eye(nc, dtype=np.float32)[rng.integers(0, nc, B)]
+    p = L.problem("f32", "dense", "relu", N=4, B=B, C=q, h=0.25)
+    g = {k: torch.from_numpy(v).cuda() for k, v in dict(uN=uN, W=W, mu=mu, c=onehot).items()}
+    J = torch.zeros(1, device="cuda", dtype=torch.float64)
+    lamN, dW, dmu = torch.empty_like(g["uN"]), torch.empty_like(g["W"]), torch.empty_like(g["mu"])
+    L.lp_loss_terminal(p, nc, g["uN"], g["W"], g["mu"], g["c"], J, lamN, dW, dmu, L.alloc_workspace(p))
+    Jr, lamNr, dWr, dmur = O.loss_terminal(uN, W, mu, onehot)
+    assert abs(J.item() - Jr) <= 1e-5 * max(abs(Jr), 1e-30)
+    assert_close(lamN.cpu().numpy(), lamNr, "f32", "lamN")
+    assert_close(dW.cpu().numpy(), dWr, "f32", "dW")
+    assert_close(dmu.cpu().numpy(), dmur, "f32", "dmu")
