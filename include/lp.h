@@ -167,9 +167,9 @@ int32_t lp_serial_adjoint(const lp_problem* prob, const void* K, const void* b, 
  * iters (host, nullable): V-cycles run. Not converging within max_iter is not
  * an error.
  * With rtol = stag = 0 the call runs max_iter V-cycles; if res_hist is then
- * NULL it reads nothing back and returns without waiting for the stream (and
- * without checking the norms for non-finite values). A stopping rule makes the
- * call read rho_m after every V-cycle.
+ * NULL it reads nothing back and returns without waiting for the stream; a
+ * non-finite rho_m is then recorded on the device and reported by the next
+ * lp_check_finite. A stopping rule makes the call read rho_m after every V-cycle.
  * dsig (nullable): the sigma' record of the returned iterate is written (by the
  * final F-relaxation, which then also takes the product of the layer before each
  * C-point). */
@@ -205,13 +205,31 @@ int32_t lp_gradient(const lp_problem* prob, const void* K, const void* b, const 
                     const void* dsig, const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes,
                     void* stream);
 
-/* Full-grid residual norm (fp64, host result; the stopping quantity ||G - A(U)||):
+/* Full-grid residual norm ||G - A(U)|| of the space-time system, the quantity
+ * whose drop stops the MGRIT iteration (Algorithm 1, step 6; Section 3.1.1 for
+ * the state system, Section 3.2 for the adjoint one). fp64, summed over all
+ * examples and features in a fixed order, returned on the host (the call waits
+ * for `stream`):
  *   which = LP_STATE:   (sum_{n=1..N} ||Phi(U[n-1], theta^{n-1}) - U[n]||^2)^{1/2}
+ *                       (row 0 of A(U) = G is u^0 itself and contributes nothing)
  *   which = LP_ADJOINT: (sum_{n=0..N-1} ||Lam[n+1] + h K_n^T(sigma'(z_n) * Lam[n+1]) - Lam[n]||^2)^{1/2}
- * Lam may be NULL for LP_STATE. */
+ * U (and Lam) [N+1][B][q] are read only; Lam may be NULL for LP_STATE. ws: at
+ * least lp_workspace_bytes(prob, NULL) bytes (per-workgroup partials). Returns
+ * LP_ENONFINITE (with *norm set) when the norm is NaN or Inf. */
 int32_t lp_residual_norm(const lp_problem* prob, int32_t which, const void* K, const void* b,
                          const void* U, const void* Lam, void* ws, size_t ws_bytes, double* norm,
                          void* stream);
+
+/* Report a non-finite residual norm that no call has read back. Every residual
+ * norm the library computes on a device (each MGRIT iteration's rho_m, and
+ * lp_residual_norm) that is NaN or Inf sets a sticky flag on that device,
+ * whether or not the computing call read the norm back. This call waits for
+ * `stream`, reads the flag of the current device and clears it: LP_ENONFINITE
+ * if it was set, else LP_OK. Callers that run solves without a read-back (no
+ * stopping rule, no res_hist) call it where they next synchronise, e.g. once
+ * per training update, so that a diverging iterate is never used silently.
+ * The flag is shared by all streams on the device. */
+int32_t lp_check_finite(void* stream);
 
 /* ---- boundary helpers (outside the per-iteration hot path) ---- */
 

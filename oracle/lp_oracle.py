@@ -558,12 +558,13 @@ def mgrit_adjoint(U, Lam, K, b, h, kind, cf=4, max_levels=2, min_coarse=1, relax
 # ---------------------------------------------------------------------------
 
 def one_shot(y, onehot, L_in, K, b, W, mu, h, kind, opening, cf, max_levels, min_coarse,
-             relax, updates, lr, m1=1, m2=1):
+             relax, updates, lr, m1=1, m2=1, progress=None):
     """Algorithm 2: per design update, m1 state MGRIT iterations and m2 adjoint MGRIT
     iterations (both warm-started from the previous update's iterates), the reduced
     gradient with the inexact state and adjoint, then theta <- theta - lr * grad for
     K, b, L_in, W, mu. The loss J is evaluated on the state iterate used for the
-    gradient. Returns the list of losses (one per update) and the final weights."""
+    gradient. Returns the list of losses (one per update) and the final weights.
+    progress (optional) is called as progress(update, J) after each update."""
     L_in, K, b, W, mu = (None if a is None else np.array(a, dtype=np.float64, copy=True)
                          for a in (L_in, K, b, W, mu))
     y, onehot = _f64(y, onehot)
@@ -590,18 +591,21 @@ def one_shot(y, onehot, L_in, K, b, W, mu, h, kind, opening, cf, max_levels, min
         mu -= lr * dmu
         if dL is not None:
             L_in -= lr * dL
+        if progress is not None:
+            progress(it, J)
     return losses, dict(L_in=L_in, K=K, b=b, W=W, mu=mu)
 
 
-def serial_training(y, onehot, L_in, K, b, W, mu, h, kind, opening, updates, lr):
+def serial_training(y, onehot, L_in, K, b, W, mu, h, kind, opening, updates, lr, progress=None):
     """Layer-serial gradient descent on the same objective (the paper's baseline
-    method): exact forward propagation, backpropagation and the same update."""
+    method): exact forward propagation, backpropagation and the same update.
+    progress (optional) is called as progress(update, J) after each update."""
     L_in, K, b, W, mu = (None if a is None else np.array(a, dtype=np.float64, copy=True)
                          for a in (L_in, K, b, W, mu))
     y, onehot = _f64(y, onehot)
     N = K.shape[0]
     losses = []
-    for _ in range(updates):
+    for it in range(updates):
         u0 = open_forward(y, L_in, kind, opening)
         U = serial_forward(u0, K, b, h, kind)
         J, lamN, dW, dmu = loss_terminal(U[N], W, mu, onehot)
@@ -615,6 +619,8 @@ def serial_training(y, onehot, L_in, K, b, W, mu, h, kind, opening, updates, lr)
         mu -= lr * dmu
         if dL is not None:
             L_in -= lr * dL
+        if progress is not None:
+            progress(it, J)
     return losses, dict(L_in=L_in, K=K, b=b, W=W, mu=mu)
 
 

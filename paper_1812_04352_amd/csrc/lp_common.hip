@@ -24,6 +24,12 @@ __global__ __launch_bounds__(NT) void k_copy_rows(uint4* X, size_t units, long s
   }
 }
 
+// Sticky per-device record of a non-finite residual norm (any MGRIT solve or
+// residual-norm call on this device since the flag was last cleared). Set by the
+// reduction below with an ordinary global store; read and cleared by
+// lp_check_finite.
+__device__ uint32_t g_nonfinite = 0u;
+
 // out[0] = sqrt(sum of partial[0..n)), summed in a fixed order: thread t adds
 // partial[t], partial[t + NTR], ... in index order (eight loads issued at a time,
 // so the serial chain waits once per eight), then the workgroup tree.
@@ -41,7 +47,11 @@ __global__ __launch_bounds__(NTR) void k_norm_reduce(const double* partial, int 
   }
   for (; i < n; i += NTR) s += partial[i];
   s = block_sum<NTR>(s, sh);
-  if (threadIdx.x == 0) out[0] = sqrt(s);
+  if (threadIdx.x == 0) {
+    const double r = sqrt(s);
+    out[0] = r;
+    if (!isfinite(r)) g_nonfinite = 1u;
+  }
 }
 
 // dst[i] = src[i] over 16-byte units.
@@ -231,6 +241,18 @@ hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_
 hipError_t launch_norm_reduce(const double* partial, int n, double* out, hipStream_t st) {
   k_norm_reduce<<<1, NTR, 0, st>>>(partial, n, out);
   return hipGetLastError();
+}
+
+hipError_t read_nonfinite(uint32_t* flag, bool clear, hipStream_t st) {
+  hipError_t e = hipMemcpyFromSymbolAsync(flag, HIP_SYMBOL(g_nonfinite), sizeof(uint32_t), 0,
+                                          hipMemcpyDeviceToHost, st);
+  if (e != hipSuccess) return e;
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess || !clear || *flag == 0u) return e;
+  const uint32_t zero = 0u;
+  e = hipMemcpyToSymbolAsync(HIP_SYMBOL(g_nonfinite), &zero, sizeof(uint32_t), 0, hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(st);
 }
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t st) {

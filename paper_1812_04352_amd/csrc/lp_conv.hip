@@ -20,6 +20,8 @@
 // its channel axes swapped; the same product runs with that weight gather.
 // The weight gradient contracts over pair-pixels instead: dWbig[(co,dy)][k] =
 // sum_P s[co][2Y+dy][x] patch[P][k], then dK[co][ci][ty][tx] = sum_dy dWbig[(co,dy)][(ci, ty+dy, tx)].
+#include <algorithm>
+
 #include "lp_device.h"
 #include "lp_internal.h"
 
@@ -954,18 +956,18 @@ __global__ __launch_bounds__(NT) void k_grad_final(GradArgs a) {
   const size_t n = o / (KW + CH);
   const int r = (int)(o - n * (KW + CH));
   const float* p = static_cast<const float*>(a.partial) + n * a.nchunks * GOUT;
-  float s = 0.f;
+  double s = 0.0;  // chunk partials summed in fp64
   if (r < KW) {
     const int co = r / 72, ci = (r % 72) / 9, ty = (r % 9) / 3, tx = r % 3;
     for (int ch = 0; ch < a.nchunks; ++ch)
       for (int dy = 0; dy < 2; ++dy) {
         const int kk = ci * 12 + (ty + dy) * 3 + tx;
-        s += p[(size_t)ch * GOUT + (2 * co + dy) * 96 + kk];
+        s += (double)p[(size_t)ch * GOUT + (2 * co + dy) * 96 + kk];
       }
-    static_cast<float*>(a.dK)[n * KW + r] = s * (float)a.h;
+    static_cast<float*>(a.dK)[n * KW + r] = (float)(s * a.h);
   } else {
-    for (int ch = 0; ch < a.nchunks; ++ch) s += p[(size_t)ch * GOUT + 16 * 96 + (r - KW)];
-    static_cast<float*>(a.db)[n * CH + (r - KW)] = s * (float)a.h;
+    for (int ch = 0; ch < a.nchunks; ++ch) s += (double)p[(size_t)ch * GOUT + 16 * 96 + (r - KW)];
+    static_cast<float*>(a.db)[n * CH + (r - KW)] = (float)(s * a.h);
   }
 }
 
@@ -1041,9 +1043,15 @@ int conv_tile(const Shape&) { return 1; }
 
 size_t conv_dsig_block_bytes(const Shape& s) { return conv::rec_block_bytes(sweep_geo(s), s.act == ACT_RELU); }
 
+// Enough workgroups to fill the chip when N is small, and at most GRAD_EX
+// examples per chunk: a partial sums GRAD_EX x 784 pixels x 4 terms per matrix-core
+// accumulator in fp32, and the chunks are summed in fp64, which keeps the
+// gradient's rounding error near 1e-6 relative at any batch size.
+constexpr int GRAD_EX = 32;
 int conv_grad_chunks(int B, int N) {
-  const int want = (2048 + N - 1) / N;
-  const int ch = want < B ? want : B;
+  int ch = (2048 + N - 1) / N;
+  ch = std::max(ch, (B + GRAD_EX - 1) / GRAD_EX);
+  ch = std::min(ch, B);
   return ch < 1 ? 1 : ch;
 }
 

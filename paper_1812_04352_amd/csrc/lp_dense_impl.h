@@ -613,7 +613,7 @@ __global__ __launch_bounds__(NT) void k_grad_partial(GradArgs a) {
   if ((int)threadIdx.x < Q) out[Q * Q + threadIdx.x] = accb;
 }
 
-// Second pass: sum the chunk partials in chunk order and scale by h.
+// Second pass: sum the chunk partials in chunk order (in fp64) and scale by h.
 template <typename T>
 __global__ __launch_bounds__(NT) void k_grad_final(GradArgs a, int nw, int nbias) {
   const int nout = nw + nbias;
@@ -623,11 +623,11 @@ __global__ __launch_bounds__(NT) void k_grad_final(GradArgs a, int nw, int nbias
   const size_t n = o / nout;
   const size_t r = o - n * nout;
   const T* p = static_cast<const T*>(a.partial) + n * a.nchunks * nout + r;
-  T s = T(0);
-  for (int ch = 0; ch < a.nchunks; ++ch) s += p[(size_t)ch * nout];
-  s *= (T)a.h;
-  if (r < (size_t)nw) static_cast<T*>(a.dK)[n * nw + r] = s;
-  else static_cast<T*>(a.db)[n * nbias + (r - nw)] = s;
+  double s = 0.0;  // chunk partials summed in fp64
+  for (int ch = 0; ch < a.nchunks; ++ch) s += (double)p[(size_t)ch * nout];
+  const T v = (T)(s * a.h);
+  if (r < (size_t)nw) static_cast<T*>(a.dK)[n * nw + r] = v;
+  else static_cast<T*>(a.db)[n * nbias + (r - nw)] = v;
 }
 
 // ------------------------------------------------------------------ launchers

@@ -811,18 +811,18 @@ __global__ __launch_bounds__(NT) void k_grad(GradArgs a) {
   if (threadIdx.x < Q) out[(size_t)Q * Q + threadIdx.x] = dbacc;
 }
 
-// Sum the chunk partials in chunk order and scale by h.
+// Sum the chunk partials in chunk order in fp64 and scale by h.
 __global__ __launch_bounds__(256) void k_grad_final(GradArgs a, int nw, int nbias) {
   const int nout = nw + nbias;
   const size_t o = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (o >= (size_t)a.N * nout) return;
   const size_t n = o / nout, r = o - n * nout;
   const float* p = static_cast<const float*>(a.partial) + n * a.nchunks * nout + r;
-  float s = 0.f;
-  for (int ch = 0; ch < a.nchunks; ++ch) s += p[(size_t)ch * nout];
-  s *= (float)a.h;
-  if (r < (size_t)nw) static_cast<float*>(a.dK)[n * nw + r] = s;
-  else static_cast<float*>(a.db)[n * nbias + (r - nw)] = s;
+  double s = 0.0;
+  for (int ch = 0; ch < a.nchunks; ++ch) s += (double)p[(size_t)ch * nout];
+  const float v = (float)(s * a.h);
+  if (r < (size_t)nw) static_cast<float*>(a.dK)[n * nw + r] = v;
+  else static_cast<float*>(a.db)[n * nbias + (r - nw)] = v;
 }
 
 // ------------------------------------------------------------------ launchers

@@ -464,7 +464,8 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
   rc = s.finish();
   if (rc) return rc;
   // With neither a stopping rule nor a history to return, nothing is read back:
-  // the call returns with the work enqueued (and the norms are not checked).
+  // the call returns with the work enqueued; a non-finite norm stays recorded in
+  // the device flag that lp_check_finite reads.
   if (!early && res_hist) {
     hist.assign(it, 0.0);
     LP_TRY(hipMemcpyAsync(hist.data(), rho, it * sizeof(double), hipMemcpyDeviceToHost, st), "read residuals");
@@ -484,10 +485,13 @@ namespace lp {
 bool dense_width_supported(int q) { return q == 8 || q == 16 || q == 32 || q == 64; }
 
 int dense_grad_chunks(int B, int N) {
-  // enough workgroups to fill the chip when N is small; at least 64 examples per chunk
-  const int want = (2048 + N - 1) / N;
-  const int most = (B + 63) / 64;
-  const int ch = want < most ? want : most;
+  // enough workgroups to fill the chip when N is small, at least 64 and at most
+  // 2048 examples per chunk: each of a chunk's four waves then sums at most 512
+  // examples in fp32 before the chunks are summed in fp64, which keeps the
+  // gradient's rounding error near 1e-6 relative at any batch size
+  int ch = (2048 + N - 1) / N;
+  ch = std::max(ch, (B + 2047) / 2048);
+  ch = std::min(ch, (B + 63) / 64);
   return ch < 1 ? 1 : ch;
 }
 
@@ -577,7 +581,7 @@ const char* lp_last_error(void) { return g_err.c_str(); }
 
 size_t lp_workspace_bytes(const lp_problem* p, const lp_mgrit* m) {
   if (check_problem(p) != LP_OK) return 0;
-  size_t need = std::max({grad_bytes(p), resid_bytes(p), lp::loss_workspace_bytes(p->B, (int)qdim(p), 64)});
+  size_t need = std::max({grad_bytes(p), resid_bytes(p), lp::loss_workspace_bytes_max(esize(p), p->B, (int)qdim(p), 64)});
   if (m) {
     std::vector<int> sizes;
     if (check_mgrit(p, m, sizes) != LP_OK) return 0;
@@ -689,6 +693,13 @@ int32_t lp_residual_norm(const lp_problem* p, int32_t which, const void* K, cons
   return LP_OK;
 }
 
+int32_t lp_check_finite(void* stream) {
+  uint32_t flag = 0u;
+  LP_TRY(lp::read_nonfinite(&flag, true, static_cast<hipStream_t>(stream)), "read non-finite flag");
+  if (flag) return fail(LP_ENONFINITE, "a residual norm computed on this device was not finite");
+  return LP_OK;
+}
+
 int32_t lp_open_forward(const lp_problem* p, int32_t opening, int32_t nf, const void* y, const void* L_in,
                         void* u0, void* stream) {
   int rc = check_problem(p);
@@ -732,7 +743,7 @@ int32_t lp_loss_terminal(const lp_problem* p, int32_t nc, const void* uN, const 
   if (nc < 1 || nc > 64) return fail(LP_EINVAL, "need 1 <= nc <= 64, nc = %d", nc);
   if (!uN || !W || !mu || !c || !J || !lamN || !dW || !dmu) return fail(LP_EINVAL, "NULL array argument");
   if (p->B == 0) return fail(LP_EINVAL, "the mean loss needs B >= 1");
-  rc = check_ws(ws, ws_bytes, lp::loss_workspace_bytes(p->B, (int)qdim(p), nc));
+  rc = check_ws(ws, ws_bytes, lp::loss_workspace_bytes(esize(p), p->B, (int)qdim(p), nc));
   if (rc) return rc;
   LP_TRY(lp::launch_loss(p->dtype, p->B, (int)qdim(p), nc, uN, W, mu, c, J, lamN, dW, dmu, ws,
                          static_cast<hipStream_t>(stream)),
@@ -769,7 +780,7 @@ int32_t lp_accuracy(const lp_problem* p, int32_t nc, const void* uN, const void*
   if (nc < 1 || nc > 64) return fail(LP_EINVAL, "need 1 <= nc <= 64, nc = %d", nc);
   if (!uN || !W || !mu || !c || !acc) return fail(LP_EINVAL, "NULL array argument");
   if (p->B == 0) return fail(LP_EINVAL, "the accuracy needs B >= 1");
-  rc = check_ws(ws, ws_bytes, lp::loss_workspace_bytes(p->B, (int)qdim(p), nc));
+  rc = check_ws(ws, ws_bytes, lp::loss_workspace_bytes(esize(p), p->B, (int)qdim(p), nc));
   if (rc) return rc;
   LP_TRY(lp::launch_accuracy(p->dtype, p->B, (int)qdim(p), nc, uN, W, mu, c, acc, ws,
                              static_cast<hipStream_t>(stream)),

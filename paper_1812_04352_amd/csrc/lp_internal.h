@@ -169,6 +169,9 @@ size_t conv_dsig_block_bytes(const Shape& s);  // sigma' record bytes per (layer
 hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_row0,
                             long dst_step, long count, hipStream_t st);
 hipError_t launch_norm_reduce(const double* partial, int n, double* out, hipStream_t st);
+// Wait for st, then read the device's sticky non-finite-norm flag into *flag
+// (host); clear it when set and `clear` is true.
+hipError_t read_nonfinite(uint32_t* flag, bool clear, hipStream_t st);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);
 hipError_t launch_open_forward(const Shape& s, int opening, int nf, int B, const void* y, const void* L,
                                void* u0, hipStream_t st);
@@ -176,7 +179,8 @@ hipError_t launch_open_grad(const Shape& s, int opening, int nf, int B, const vo
                             const void* lam0, void* dL, hipStream_t st);
 hipError_t launch_loss(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,
                        const void* c, double* J, void* lamN, void* dW, void* dmu, void* ws, hipStream_t st);
-size_t loss_workspace_bytes(int B, int q, int nc);  // lp_loss.hip
+size_t loss_workspace_bytes(size_t esz, int B, int q, int nc);         // lp_loss.hip: one class count
+size_t loss_workspace_bytes_max(size_t esz, int B, int q, int nc_max);  // every class count <= nc_max
 hipError_t launch_sgd(int dtype, size_t n, double lr, const void* g, void* x, hipStream_t st);
 constexpr int DOT_BLOCKS = 256;  // partials of lp_vec_dot (out[1 .. DOT_BLOCKS])
 hipError_t launch_axpby(int dtype, size_t n, double a, const void* x, double b, void* y, hipStream_t st);

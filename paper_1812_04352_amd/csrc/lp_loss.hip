@@ -288,14 +288,24 @@ hipError_t launch_accuracy(int dtype, int B, int q, int nc, const void* uN, cons
                     : accuracy_t<double>(B, q, nc, uN, Wc, mu, c, acc, ws, st);
 }
 
-// Partials: one per CHUNK examples (k_wpart), or one per head workgroup of NT/S
-// examples (S the power of two >= nc, rows one double longer); the larger. Both counts grow
-// with nc, so the size for nc = 64 covers every smaller nc.
-size_t loss_workspace_bytes(int B, int q, int nc) {
+// Workspace of the loss for one class count: the logits (B nc doubles), the
+// per-example losses (B doubles) and the partials of the path loss_t takes: one
+// row of nc (q+1) + 1 doubles per head workgroup of NT/S examples when k_head
+// stages W and u^N in LDS, else one row of nc (q+1) doubles per CHUNK examples.
+size_t loss_workspace_bytes(size_t esz, int B, int q, int nc) {
   int S = 1;
   while (S < nc) S *= 2;
-  const size_t nch = std::max((size_t)(B + CHUNK - 1) / CHUNK, (size_t)(B + NT / S - 1) / (NT / S));
-  return up((size_t)B * nc * 8) + up((size_t)B * 8) + up(nch * (nc * (size_t)(q + 1) + 1) * 8);
+  const size_t nw = (size_t)nc * (q + 1);
+  const size_t part = head_lds(esz, q, nc, S) <= HEAD_LDS_MAX ? (size_t)((B + NT / S - 1) / (NT / S)) * (nw + 1)
+                                                              : (size_t)((B + CHUNK - 1) / CHUNK) * nw;
+  return up((size_t)B * nc * 8) + up((size_t)B * 8) + up(part * 8);
+}
+
+// The largest of the above over every class count 1 .. nc_max.
+size_t loss_workspace_bytes_max(size_t esz, int B, int q, int nc_max) {
+  size_t need = 0;
+  for (int nc = 1; nc <= nc_max; ++nc) need = std::max(need, loss_workspace_bytes(esz, B, q, nc));
+  return need;
 }
 
 hipError_t launch_loss(int dtype, int B, int q, int nc, const void* uN, const void* Wc, const void* mu,

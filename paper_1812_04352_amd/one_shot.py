@@ -60,6 +60,51 @@ class OneShotTrainer:
         out = [] if losses is None else losses
         for _ in range(updates):
             self.step(lr)
+            # the solves read nothing back: a diverging iterate shows up here
+            L.lp_check_finite()
+            out.append(float(self.J.item()))
+        return out
+
+
+class SerialTrainer:
+    """Layer-serial gradient descent on the same objective, the baseline method
+    the one-shot run is compared with (Section 5.3): per update the exact
+    forward propagation and backpropagation (the state and adjoint equations of
+    Section 2.3 solved by forward and backward substitution), the exact reduced
+    gradient, and the same plain gradient step as OneShotTrainer. Same
+    arguments as OneShotTrainer without the MGRIT schedules."""
+
+    def __init__(self, prob: L.LpProblem, params: Dict[str, torch.Tensor], y: torch.Tensor, c: torch.Tensor,
+                 n_classes: int, opening: int, n_features: int):
+        self.p, self.P = prob, params
+        self.y, self.c = y, c
+        self.nc, self.opening, self.nf = n_classes, opening, n_features
+        dt = params["K"].dtype
+        shape = (prob.N + 1, prob.B) + ((prob.C, prob.H, prob.W) if prob.layer == L.LP_CONV3X3 else (prob.q,))
+        self.U = torch.zeros(shape, device="cuda", dtype=dt)
+        self.Lam = torch.zeros_like(self.U)
+        self.ws = L.alloc_workspace(prob)
+        self.J = torch.zeros(1, device="cuda", dtype=torch.float64)
+        self.G = {k: torch.empty_like(v) for k, v in params.items()}
+        self.rec = L.alloc_dsig(prob) if L.lp_dsig_bytes(prob) else None
+
+    def step(self, lr: float) -> None:
+        P, G, p = self.P, self.G, self.p
+        L.lp_open_forward(p, self.opening, self.nf, self.y, P.get("L_in"), self.U[0])
+        L.lp_serial_forward(p, P["K"], P["b"], self.U, dsig=self.rec)
+        L.lp_loss_terminal(p, self.nc, self.U[-1], P["W"], P["mu"], self.c, self.J, self.Lam[-1], G["W"], G["mu"],
+                           self.ws)
+        L.lp_serial_adjoint(p, P["K"], P["b"], self.U, self.Lam, dsig=self.rec)
+        L.lp_gradient(p, P["K"], P["b"], self.U, self.Lam, G["K"], G["b"], self.ws, dsig=self.rec)
+        if "L_in" in P:
+            L.lp_open_grad(p, self.opening, self.nf, self.y, P["L_in"], self.Lam[0], G["L_in"])
+        for k in P:
+            L.lp_sgd_update(P[k], G[k], lr)
+
+    def run(self, updates: int, lr: float, losses: Optional[List[float]] = None) -> List[float]:
+        out = [] if losses is None else losses
+        for _ in range(updates):
+            self.step(lr)
             out.append(float(self.J.item()))
         return out
 
@@ -164,6 +209,8 @@ class LbfgsOneShotTrainer:
         L.lp_gradient(self.p, P["K"], P["b"], self.U, self.Lam, G["K"], G["b"], self.ws, dsig=self.rec)
         if "L_in" in P:
             L.lp_open_grad(self.p, self.opening, self.nf, self.y, P["L_in"], self.Lam[0], G["L_in"])
+        # the state and adjoint solves read nothing back: a diverging iterate shows up here
+        L.lp_check_finite()
         # curvature pair from the previous update
         if self.prev is not None:
             xp, gp = self.prev
@@ -196,6 +243,12 @@ class LbfgsOneShotTrainer:
             L.lp_vec_axpby(self.Ut, self.U, 1.0, 0.0)
             self._state_after(self.T, self.Ut, True)
             Jt = self._loss(self.T, self.Ut, self.lam_scratch, self.gW, self.gmu)
+            try:
+                L.lp_check_finite()
+            except L.LpError as err:  # the trial design's state solve diverged: reject it
+                if err.status != L.LP_ENONFINITE:
+                    raise
+                Jt = float("inf")
             if Jt <= J + self.c1 * alpha * gd or t == self.max_ls - 1:
                 break
             alpha *= self.shrink

@@ -173,3 +173,31 @@ def test_cycle_and_relaxation_options(monkeypatch):
     m = L.mgrit(4, 4, 1, "FCF", 2)
     m.relax = 3
     assert lib.lp_workspace_bytes(ctypes.byref(p), ctypes.byref(m)) == 0
+
+
+def test_loss_workspace_follows_the_head_path():
+    """The loss reserves partials for the path it takes: one row per head
+    workgroup when W and u^N fit in LDS (dense width 32), one row per 16 examples
+    otherwise (the convolutional head, q = 6272), for every class count <= 64."""
+    lib = L.load()
+
+    def up(x):
+        return (x + 255) // 256 * 256
+
+    conv = L.problem("f32", "conv3x3", "relu", 512, 1024, 8, H=28, W=28, h=5 / 512)
+    q, B = 8 * 28 * 28, 1024
+    unstaged64 = up(B * 64 * 8) + up(B * 8) + up((B // 16) * 64 * (q + 1) * 8)
+    got = L.lp_workspace_bytes(conv)
+    assert unstaged64 <= got <= unstaged64 + (128 << 20)  # the gradient's partials are smaller
+    assert got < 300 << 20  # not the staged size (four times as many rows)
+    # the loss itself checks the size for its class count
+    need10 = up(B * 10 * 8) + up(B * 8) + up((B // 16) * 10 * (q + 1) * 8)
+    J = ctypes.c_void_p(0x2000)
+    assert lib.lp_loss_terminal(ctypes.byref(conv), 10, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, FAKE,
+                                need10 - 1, None) == L.LP_EWORKSPACE
+    # dense width 32, 16 classes: staged head, 16 examples per workgroup, rows of nc (q+1) + 1
+    dense = L.problem("f32", "dense", "relu", 8, 4096, 32, h=0.1)
+    need16 = up(4096 * 16 * 8) + up(4096 * 8) + up((4096 // 16) * (16 * 33 + 1) * 8)
+    assert lib.lp_loss_terminal(ctypes.byref(dense), 16, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, FAKE,
+                                need16 - 1, None) == L.LP_EWORKSPACE
+    assert L.lp_workspace_bytes(dense) >= need16

@@ -1,10 +1,16 @@
 """GPU parity at the full workload sizes, in the launch configuration the
-benchmark uses. Examples are independent in the forward and adjoint MGRIT
-solves, so the oracle runs on a sample of examples (the first ones, the last
-ones of the ragged final workgroup, and seeded random ones) and is compared
-element by element with the same examples of the full GPU solve. The reduced
-gradient couples the batch: it is compared with the oracle in full where that
-is cheap, and otherwise checked for additivity over the batch on the GPU."""
+benchmark uses (the sigma' record kept where the kernels keep one). Examples are
+independent in the forward and adjoint MGRIT solves, so the oracle runs on a
+sample of examples (the first ones, the last ones of the ragged final
+workgroup, and seeded random ones) and is compared element by element with the
+same examples of the full GPU solve. The reduced gradient couples the batch:
+each layer's gradient depends only on U[n] and Lam[n+1] (Section 2.3, design
+equations), so the oracle evaluates it over the full batch from the GPU's own
+U and Lam upcast to fp64, for every layer (dense) or a seeded set of layers
+including the first and the last (convolution); this isolates the gradient
+kernels' own arithmetic, fp32 accumulation over the whole batch included.
+Where it is cheap the whole pipeline is also compared with an oracle run from
+the inputs."""
 import numpy as np
 import pytest
 import torch
@@ -38,26 +44,77 @@ def _stop_rule(wl, iters):
     return sched(wl, iters, rtol=wl.rtol, stag=wl.stag)
 
 
-def _check_relu_gradient(dK, db, dKr, dbr, U, Lam, d, wl, rel_tau=1e-5):
-    """ReLU gradient check. sigma'(z) = 1[z > 0] is a decision; the fp32 GPU run and
-    the fp64 oracle reach the trajectory with rounding-level differences, so
-    pre-activations within tau of 0 may be decided either way. The difference must
-    be within the parity bar plus the largest change those ambiguous sites can make,
-    |h sum_{|z| < tau} lam u^T| elementwise (tau = rel_tau * max|z| per layer)."""
+def _relu_slack(Kn, bn, Un, Lam1, h, rel_tau=1e-5):
+    """Largest change of one layer's gradient (dK, db) that the ReLU decisions
+    sigma'(z) = 1[z > 0] near the kink can make: the fp32 GPU trajectory and the
+    fp64 oracle may decide pre-activations within tau = rel_tau * max|z| of 0
+    either way. Returns |h sum_{|z| < tau} lam u^T| bounds elementwise."""
+    z = O.preact(Kn, bn, Un)
+    amb = np.abs(z) < rel_tau * np.abs(z).max()
+    lam = np.where(amb, np.abs(Lam1), 0.0)
+    if z.ndim == 4:
+        return h * O.conv3x3_weight_grad(lam, np.abs(Un)), h * lam.sum(axis=(0, 2, 3))
+    return h * (lam.T @ np.abs(Un)), h * lam.sum(axis=0)
+
+
+def _check_gradient(dK, db, dKr, dbr, wl, what, A=None, Ab=None):
+    """Normwise and element bars of the parity tolerance; for ReLU widened by
+    exactly the slack A, Ab of the ambiguous kink sites (see _relu_slack)."""
+    if A is None:
+        assert_close(dK, dKr, wl.dtype, f"{what} dK")
+        assert_close(db, dbr, wl.dtype, f"{what} db")
+        return
     tol = 1e-5
+    eK, eb = np.abs(dK - dKr), np.abs(db - dbr)
+    assert np.linalg.norm(eK) <= tol * np.linalg.norm(dKr) + np.linalg.norm(A), (what, np.linalg.norm(eK),
+                                                                                  np.linalg.norm(A))
+    assert np.all(eK <= 10 * tol * np.abs(dKr).max() + A), what
+    assert np.linalg.norm(eb) <= tol * np.linalg.norm(dbr) + np.linalg.norm(Ab), what
+    assert np.all(eb <= 10 * tol * np.abs(dbr).max() + Ab), what
+
+
+def _check_relu_gradient(dK, db, dKr, dbr, U, Lam, d, wl, rel_tau=1e-5):
+    """ReLU gradient check over all layers of an oracle trajectory (see _relu_slack)."""
     A = np.zeros_like(dKr)
     Ab = np.zeros_like(dbr)
     for n in range(wl.N):
-        z = O.preact(d["K"][n].astype(np.float64), d["b"][n].astype(np.float64), U[n])
-        amb = np.abs(z) < rel_tau * np.abs(z).max()
-        lam = np.where(amb, np.abs(Lam[n + 1]), 0.0)
-        A[n] = wl.h * lam.T @ np.abs(U[n])
-        Ab[n] = wl.h * lam.sum(axis=0)
-    eK, eb = np.abs(dK - dKr), np.abs(db - dbr)
-    assert np.linalg.norm(eK) <= tol * np.linalg.norm(dKr) + np.linalg.norm(A), (np.linalg.norm(eK), np.linalg.norm(A))
-    assert np.all(eK <= 10 * tol * np.abs(dKr).max() + A)
-    assert np.linalg.norm(eb) <= tol * np.linalg.norm(dbr) + np.linalg.norm(Ab)
-    assert np.all(eb <= 10 * tol * np.abs(dbr).max() + Ab)
+        A[n], Ab[n] = _relu_slack(d["K"][n].astype(np.float64), d["b"][n].astype(np.float64), U[n], Lam[n + 1],
+                                  wl.h, rel_tau)
+    _check_gradient(dK, db, dKr, dbr, wl, "full pipeline", A, Ab)
+
+
+def gradient_layers(wl):
+    """Layers whose gradient the oracle evaluates at full size: all of a dense
+    network; 16 of a convolutional one (first, last and 14 seeded others)."""
+    if wl.layer != "conv3x3":
+        return np.arange(wl.N)
+    r = np.random.default_rng(4000 + wl.cfg)
+    return np.array(sorted({0, wl.N - 1} | set(r.choice(np.arange(1, wl.N - 1), 14, replace=False).tolist())))
+
+
+def _oracle_layer_gradients(c, U, Lam, layers, block=64):
+    """Oracle dK, db of the given layers over the full batch, from the GPU's own
+    trajectory and adjoint (rows copied to the host a block of layers at a time
+    and upcast to fp64), with the ReLU slack of each layer."""
+    wl, d = c.wl, c.d
+    dKr = np.zeros((len(layers),) + d["K"].shape[1:])
+    dbr = np.zeros((len(layers),) + d["b"].shape[1:])
+    A = np.zeros_like(dKr) if wl.act == "relu" else None
+    Ab = np.zeros_like(dbr) if wl.act == "relu" else None
+    for j0 in range(0, len(layers), block):
+        ls = layers[j0:j0 + block]
+        sel = torch.from_numpy(ls).cuda()
+        Ub = U.index_select(0, sel).cpu().numpy().astype(np.float64)
+        Lb = Lam.index_select(0, sel + 1).cpu().numpy().astype(np.float64)
+        for i, n in enumerate(ls):
+            Kn = d["K"][n:n + 1].astype(np.float64)
+            bn = d["b"][n:n + 1].astype(np.float64)
+            Lpair = np.stack([np.zeros_like(Lb[i]), Lb[i]])
+            gK, gb = O.gradient(Ub[i][None], Lpair, Kn, bn, wl.h, wl.act)
+            dKr[j0 + i], dbr[j0 + i] = gK[0], gb[0]
+            if A is not None:
+                A[j0 + i], Ab[j0 + i] = _relu_slack(Kn[0], bn[0], Ub[i], Lb[i], wl.h)
+    return dKr, dbr, A, Ab
 
 
 def test_mgrit_forward_and_adjoint_full_size(full):
@@ -66,8 +123,11 @@ def test_mgrit_forward_and_adjoint_full_size(full):
     S = sample_of(wl.B, 8 if wl.layer == "conv3x3" else 12)
     mg = _stop_rule(wl, wl.fwd_iters)
     ws = L.alloc_workspace(c.p, mg)
+    # the benchmark's configuration: the forward keeps the sigma' record, the
+    # adjoint and the gradient read it
+    rec = L.alloc_dsig(c.p) if L.lp_dsig_bytes(c.p) else None
     U = c.new_traj()
-    itF, histF = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws)
+    itF, histF = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, dsig=rec)
     assert all(np.isfinite(histF))
     if wl.rtol > 0:
         assert histF[-1] <= wl.rtol * histF[0] or itF == wl.fwd_iters or histF[-1] > wl.stag * histF[-2]
@@ -85,7 +145,7 @@ def test_mgrit_forward_and_adjoint_full_size(full):
     dW, dmu = torch.empty_like(c.W), torch.empty_like(c.mu)
     L.lp_loss_terminal(c.p, wl.n_classes, U[-1], c.W, c.mu, c.onehot, J, Lam[-1], dW, dmu, ws)
     mgA = _stop_rule(wl, wl.adj_iters)
-    itA, histA = L.lp_mgrit_adjoint(c.p, mgA, c.K, c.b, U, Lam, ws)
+    itA, histA = L.lp_mgrit_adjoint(c.p, mgA, c.K, c.b, U, Lam, ws, dsig=rec)
     assert all(np.isfinite(histA))
     lamN = O.loss_terminal(Ur[-1], c.d["W"], c.d["mu"], c.d["onehot"][S])[1] * (len(S) / wl.B)
     Lr = np.zeros_like(Ur)
@@ -95,9 +155,22 @@ def test_mgrit_forward_and_adjoint_full_size(full):
     Lg = Lam[:, torch.from_numpy(S).cuda()].cpu().numpy()
     assert_close(Lg, Lr, wl.dtype, f"cfg{wl.cfg} Lam sample after {itA} iterations")
 
-    # gradient: full oracle comparison where cheap, else additivity over the batch
+    # gradient over the full batch, with the record (as benchmarked) and recomputing
+    # sigma' from U, against the oracle on the GPU's own U and Lam
     dK, db = torch.empty_like(c.K), torch.empty_like(c.b)
-    L.lp_gradient(c.p, c.K, c.b, U, Lam, dK, db, ws)
+    L.lp_gradient(c.p, c.K, c.b, U, Lam, dK, db, ws, dsig=rec)
+    dK2, db2 = torch.empty_like(c.K), torch.empty_like(c.b)
+    L.lp_gradient(c.p, c.K, c.b, U, Lam, dK2, db2, ws)
+    layers = gradient_layers(wl)
+    print(f"[fullsize] cfg{wl.cfg} oracle gradient of {len(layers)} layers", flush=True)
+    dKr, dbr, A, Ab = _oracle_layer_gradients(c, U, Lam, layers)
+    sel = torch.from_numpy(layers).cuda()
+    for what, gK, gb in (("record", dK, db), ("recompute", dK2, db2)):
+        _check_gradient(gK.index_select(0, sel).cpu().numpy(), gb.index_select(0, sel).cpu().numpy(), dKr, dbr,
+                        wl, f"cfg{wl.cfg} gradient ({what}, {len(layers)} layers, B = {wl.B})", A, Ab)
+    del dK2, db2
+
+    # the whole pipeline from the inputs, where the oracle finishes in seconds
     if wl.cfg in (1, 2, 6):
         Uf, _, _ = O.mgrit_forward(
             np.concatenate([c.u0_ref[None], np.zeros((wl.N,) + c.u0_ref.shape)]), c.d["K"], c.d["b"], wl.h,
@@ -113,44 +186,43 @@ def test_mgrit_forward_and_adjoint_full_size(full):
         else:
             assert_close(dK.cpu().numpy(), dKr, wl.dtype, "dK full size")
             assert_close(db.cpu().numpy(), dbr, wl.dtype, "db full size")
-    else:
-        half = wl.B // 2
-        parts = []
-        for lo, hi in ((0, half), (half, wl.B)):
-            p2 = L.problem(wl.dtype, wl.layer, wl.act, wl.N, hi - lo, wl.C, wl.H, wl.W, wl.h)
-            Uh, Lh = U[:, lo:hi].contiguous(), Lam[:, lo:hi].contiguous()
-            dKh, dbh = torch.empty_like(c.K), torch.empty_like(c.b)
-            L.lp_gradient(p2, c.K, c.b, Uh, Lh, dKh, dbh, L.alloc_workspace(p2))
-            parts.append((dKh.double(), dbh.double()))
-            del Uh, Lh
-        sK = (parts[0][0] + parts[1][0]).cpu().numpy()
-        sb = (parts[0][1] + parts[1][1]).cpu().numpy()
-        assert_close(dK.cpu().numpy(), sK, wl.dtype, "dK additivity", scale=10)
-        assert_close(db.cpu().numpy(), sb, wl.dtype, "db additivity", scale=10)
-    del U, Lam, ws
+    del U, Lam, ws, rec
 
 
 def test_one_shot_training_full_size_matches_golden():
     """Algorithm 2 on the one-shot workload at full size (N = 1024, B = 16384, one
-    forward and one adjoint MGRIT iteration per update, lr = 1e-2): the per-update
-    losses of the GPU run against the fp64 oracle's, stored by
-    tests/golden/make_one_shot_golden.py (oracle calls only)."""
+    forward and one adjoint MGRIT iteration per update, lr = 1e-2), and layer-serial
+    gradient descent from the same seed: the per-update losses of both GPU runs
+    against the fp64 oracle's, stored by tests/golden/make_one_shot_golden.py
+    (oracle calls only). Bar: 1e-4 relative at every update (fp32 rounding
+    differences compound over the updates)."""
     import os
-    from paper_1812_04352_amd.one_shot import OneShotTrainer
+    from paper_1812_04352_amd.one_shot import OneShotTrainer, SerialTrainer
     from workloads import ONE_SHOT_LR
     path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "one_shot_losses.txt")
     if not os.path.exists(path):
         pytest.skip("golden one-shot losses not generated")
     ref = np.loadtxt(path)
-    ref = ref[~np.isnan(ref[:, 1]), 1]
+    ref_os = ref[~np.isnan(ref[:, 1]), 1]
+    ref_se = ref[~np.isnan(ref[:, 2]), 2]
     wl = WORKLOADS[5]
-    print(f"[fullsize] one-shot {wl.name}, {len(ref)} updates", flush=True)
+    print(f"[fullsize] one-shot {wl.name}: {len(ref_os)} one-shot and {len(ref_se)} layer-serial updates", flush=True)
     c = Case(wl)
-    params = {k: getattr(c, k).clone() for k in ("K", "b", "W", "mu", "L_in")}
-    tr = OneShotTrainer(c.p, sched(wl, wl.fwd_iters), sched(wl, wl.adj_iters), params, c.y, c.onehot,
+
+    def params():
+        return {k: getattr(c, k).clone() for k in ("K", "b", "W", "mu", "L_in")}
+
+    tr = OneShotTrainer(c.p, sched(wl, wl.fwd_iters), sched(wl, wl.adj_iters), params(), c.y, c.onehot,
                         wl.n_classes, L.OPENING[wl.opening], wl.n_features)
-    losses = tr.run(len(ref), ONE_SHOT_LR)
-    for i, (a, b) in enumerate(zip(losses, ref)):
-        assert abs(a - b) <= 1e-4 * abs(b), (i, a, b)
-    del tr, c
+    losses = tr.run(len(ref_os), ONE_SHOT_LR)
+    del tr
+    for i, (a, b) in enumerate(zip(losses, ref_os)):
+        assert abs(a - b) <= 1e-4 * abs(b), ("one-shot", i, a, b)
+    if len(ref_se):
+        tr = SerialTrainer(c.p, params(), c.y, c.onehot, wl.n_classes, L.OPENING[wl.opening], wl.n_features)
+        losses = tr.run(len(ref_se), ONE_SHOT_LR)
+        del tr
+        for i, (a, b) in enumerate(zip(losses, ref_se)):
+            assert abs(a - b) <= 1e-4 * abs(b), ("layer-serial", i, a, b)
+    del c
     torch.cuda.empty_cache()

@@ -201,6 +201,80 @@ def test_stop_rules_and_errors():
     with pytest.raises(L.LpError) as e:
         L.lp_mgrit_forward(c.p, sched(wl, 2), c.K, c.b, U, ws)
     assert e.value.status == L.LP_ENONFINITE
+    # the device flag recorded it as well; the check reports it once and clears it
+    with pytest.raises(L.LpError) as e:
+        L.lp_check_finite()
+    assert e.value.status == L.LP_ENONFINITE
+    L.lp_check_finite()
+
+
+@pytest.mark.parametrize("name,wl", [DENSE[1], DENSE[6], DENSE[8]], ids=[DENSE[1][0], DENSE[6][0], DENSE[8][0]])
+def test_nonfinite_without_readback(name, wl):
+    """Solves that read nothing back (no stopping rule, no history) still record a
+    non-finite residual norm on the device; lp_check_finite reports it, and the
+    one-shot trainer, which runs that way, raises instead of training on NaN."""
+    from paper_1812_04352_amd.one_shot import OneShotTrainer
+    c = case(wl)
+    L.lp_check_finite()  # nothing pending
+    mg = sched(wl, 2)
+    ws = L.alloc_workspace(c.p, mg)
+    U = c.new_traj()
+    U[0].view(-1)[7] = float("nan")
+    assert L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, history=False) == (2, [])
+    with pytest.raises(L.LpError) as e:
+        L.lp_check_finite()
+    assert e.value.status == L.LP_ENONFINITE
+    L.lp_check_finite()  # cleared
+    # a finite solve sets nothing
+    U = c.new_traj()
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, history=False)
+    L.lp_check_finite()
+    # a diverging design in the one-shot trainer
+    P = {k: getattr(c, k).clone() for k in ("K", "b", "W", "mu") + (("L_in",) if c.L_in is not None else ())}
+    P["K"].view(-1)[3] = float("inf")
+    tr = OneShotTrainer(c.p, sched(wl, 1), sched(wl, 1), P, c.y, c.onehot, wl.n_classes, L.OPENING[wl.opening],
+                        wl.n_features)
+    with pytest.raises(L.LpError) as e:
+        tr.run(1, 1e-2)
+    assert e.value.status == L.LP_ENONFINITE
+    L.lp_check_finite()
+
+
+@pytest.mark.parametrize("name,wl", [DENSE[1], DENSE[2], DENSE[3], DENSE[6], DENSE[8]],
+                         ids=[DENSE[i][0] for i in (1, 2, 3, 6, 8)])
+def test_gradient_and_loss_are_bitwise_reproducible(name, wl):
+    """lp_gradient (with and without the sigma' record) and lp_loss_terminal give
+    bit-identical results when called twice on the same inputs, the second time
+    with a workspace pre-filled with NaN bytes (so no result may depend on what the
+    workspace held): every batch reduction runs in a fixed order."""
+    c = case(wl)
+    mg = sched(wl, 2)
+    ws = L.alloc_workspace(c.p, mg)
+    rec = L.alloc_dsig(c.p) if L.lp_dsig_bytes(c.p) else None
+    U = c.new_traj()
+    L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, dsig=rec)
+    Lam = torch.zeros_like(U)
+    outs = []
+    for t in range(2):
+        if t:
+            ws.fill_(0xFF)
+        J = torch.zeros(1, device="cuda", dtype=torch.float64)
+        lamN, dW, dmu = torch.empty_like(U[-1]), torch.empty_like(c.W), torch.empty_like(c.mu)
+        L.lp_loss_terminal(c.p, wl.n_classes, U[-1], c.W, c.mu, c.onehot, J, lamN, dW, dmu, ws)
+        if t == 0:
+            Lam[-1] = lamN
+            L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, Lam, ws, dsig=rec)
+        g = []
+        for r in (rec, None):
+            if t:
+                ws.fill_(0xFF)
+            dK, db = torch.empty_like(c.K), torch.empty_like(c.b)
+            L.lp_gradient(c.p, c.K, c.b, U, Lam, dK, db, ws, dsig=r)
+            g += [dK, db]
+        outs.append([J, lamN, dW, dmu] + g)
+    names = ["J", "lamN", "dW", "dmu", "dK (record)", "db (record)", "dK", "db"]
+    for n, a, b in zip(names, outs[0], outs[1]):
+        assert torch.equal(a, b), n
 
 
 @pytest.mark.parametrize("name,wl", [DENSE[1], DENSE[2], DENSE[7]], ids=[DENSE[1][0], DENSE[2][0], DENSE[7][0]])
