@@ -220,6 +220,22 @@ int32_t lp_residual_norm(const lp_problem* prob, int32_t which, const void* K, c
                          const void* U, const void* Lam, void* ws, size_t ws_bytes, double* norm,
                          void* stream);
 
+/* lp_residual_norm without a workspace, for callers that cannot allocate
+ * device memory or own a workspace (serving loops that check convergence
+ * between requests, harnesses that forbid allocation). It computes exactly what
+ * lp_residual_norm computes, with the same kernels and summation order (equal
+ * results bit for bit), and allocates nothing: the per-workgroup partials and
+ * the result go to a scratch array of 16 MiB + 256 bytes that the library holds
+ * in device memory, one per GPU from the first call on it until the process
+ * ends. Limit: problems needing more than 2^21 partials ((N+1) ceil(B/32) for
+ * dense layers, (N+1) B for convolutions) return LP_EWORKSPACE before any work
+ * is enqueued. The scratch needs no clearing (every call writes what it reads),
+ * but it is shared by every call on a GPU: calls that overlap on one GPU (other
+ * host threads, other streams) race and must be serialised by the caller. Waits
+ * for `stream` like lp_residual_norm, so it cannot be captured in a graph. */
+int32_t lp_residual_norm_noalloc(const lp_problem* prob, int32_t which, const void* K, const void* b,
+                                 const void* U, const void* Lam, double* norm, void* stream);
+
 /* Report a non-finite residual norm that no call has read back. Every residual
  * norm the library computes on a device (each MGRIT iteration's rho_m, and
  * lp_residual_norm) that is NaN or Inf sets a sticky flag on that device,

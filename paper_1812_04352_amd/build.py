@@ -20,7 +20,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["lp_host.cpp", "lp_common.hip", "lp_loss.hip", "lp_dense_f32.hip", "lp_dense_f64.hip",
-           "lp_dense_mfma.hip", "lp_dense_wide.hip", "lp_conv.hip"]
+           "lp_dense_mfma.hip", "lp_dense_wide.hip", "lp_conv.hip", "lp_noalloc.hip"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17",

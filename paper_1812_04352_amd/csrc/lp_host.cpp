@@ -664,20 +664,22 @@ int32_t lp_gradient(const lp_problem* p, const void* K, const void* b, const voi
   return LP_OK;
 }
 
-int32_t lp_residual_norm(const lp_problem* p, int32_t which, const void* K, const void* b, const void* U,
-                         const void* Lam, void* ws, size_t ws_bytes, double* norm, void* stream) {
+namespace {
+
+int residual_norm_args(const lp_problem* p, int32_t which, const void* K, const void* b, const void* U,
+                       const void* Lam, const double* norm) {
   int rc = check_problem(p);
   if (rc) return rc;
   if (which != LP_STATE && which != LP_ADJOINT) return fail(LP_EINVAL, "bad system %d", which);
   if (!K || !b || !norm || (p->B && (!U || (which == LP_ADJOINT && !Lam))))
     return fail(LP_EINVAL, "NULL array argument");
-  if (p->B == 0) {
-    *norm = 0.0;
-    return LP_OK;
-  }
-  rc = check_ws(ws, ws_bytes, resid_bytes(p));
-  if (rc) return rc;
-  hipStream_t st = static_cast<hipStream_t>(stream);
+  return LP_OK;
+}
+
+// The residual kernels write one partial per workgroup into ws, the fixed-order
+// reduction the norm into the slot after them; the result is read back.
+int residual_norm_in(const lp_problem* p, int32_t which, const void* K, const void* b, const void* U,
+                     const void* Lam, void* ws, double* norm, hipStream_t st) {
   double* partial = static_cast<double*>(ws);
   double* out = reinterpret_cast<double*>(static_cast<char*>(ws) + up((size_t)partial_capacity(p) * sizeof(double)));
   lp::ResidArgs a{p->act, K, b, U, Lam, p->B, p->N, p->h, partial};
@@ -691,6 +693,39 @@ int32_t lp_residual_norm(const lp_problem* p, int32_t which, const void* K, cons
   LP_TRY(hipStreamSynchronize(st), "stream sync");
   if (!isfinite(*norm)) return fail(LP_ENONFINITE, "residual norm is not finite");
   return LP_OK;
+}
+
+}  // namespace
+
+int32_t lp_residual_norm(const lp_problem* p, int32_t which, const void* K, const void* b, const void* U,
+                         const void* Lam, void* ws, size_t ws_bytes, double* norm, void* stream) {
+  int rc = residual_norm_args(p, which, K, b, U, Lam, norm);
+  if (rc) return rc;
+  if (p->B == 0) {
+    *norm = 0.0;
+    return LP_OK;
+  }
+  rc = check_ws(ws, ws_bytes, resid_bytes(p));
+  if (rc) return rc;
+  return residual_norm_in(p, which, K, b, U, Lam, ws, norm, static_cast<hipStream_t>(stream));
+}
+
+int32_t lp_residual_norm_noalloc(const lp_problem* p, int32_t which, const void* K, const void* b, const void* U,
+                                 const void* Lam, double* norm, void* stream) {
+  int rc = residual_norm_args(p, which, K, b, U, Lam, norm);
+  if (rc) return rc;
+  if (p->B == 0) {
+    *norm = 0.0;
+    return LP_OK;
+  }
+  const size_t need = resid_bytes(p), have = lp::noalloc_scratch_bytes();
+  if (need > have)
+    return fail(LP_EWORKSPACE, "the residual of this problem needs %zu bytes of scratch; the library's static "
+                "scratch holds %zu (at most %zu residual partials; use lp_residual_norm with a workspace)",
+                need, have, (have - kAlign) / sizeof(double));
+  void* ws = nullptr;
+  LP_TRY(lp::noalloc_scratch(&ws), "static scratch");
+  return residual_norm_in(p, which, K, b, U, Lam, ws, norm, static_cast<hipStream_t>(stream));
 }
 
 int32_t lp_check_finite(void* stream) {

@@ -165,6 +165,11 @@ int conv_grad_chunks(int B, int N);
 int conv_tile(const Shape& s);
 size_t conv_dsig_block_bytes(const Shape& s);  // sigma' record bytes per (layer, example)
 
+// Library-owned scratch of the allocation-free entry point (lp_noalloc.hip):
+// its size, and its address on the current device (looked up once per device).
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(void** ptr);
+
 // Common kernels (lp_common.hip)
 hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_row0,
                             long dst_step, long count, hipStream_t st);

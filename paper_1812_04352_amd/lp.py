@@ -37,7 +37,7 @@ OPENING = {"identity": LP_OPEN_IDENTITY, "dense_act": LP_OPEN_DENSE_ACT, "conv_a
 EXPORTS = (
     "lp_abi_version", "lp_status_string", "lp_last_error", "lp_workspace_bytes",
     "lp_dsig_bytes", "lp_serial_forward", "lp_serial_adjoint", "lp_mgrit_forward", "lp_mgrit_adjoint",
-    "lp_gradient", "lp_residual_norm", "lp_check_finite", "lp_open_forward", "lp_open_grad",
+    "lp_gradient", "lp_residual_norm", "lp_residual_norm_noalloc", "lp_check_finite", "lp_open_forward", "lp_open_grad",
     "lp_loss_terminal", "lp_sgd_update", "lp_vec_axpby", "lp_vec_dot", "lp_accuracy",
     "lp_trace_enable", "lp_trace_read",
 )
@@ -88,6 +88,7 @@ _SIGS = {
     "lp_mgrit_adjoint": ([_P, _M, _v, _v, _v, _v, _v, _v, _sz, _dp, _ip, _v], _i32),
     "lp_gradient": ([_P, _v, _v, _v, _v, _v, _v, _v, _v, _sz, _v], _i32),
     "lp_residual_norm": ([_P, _i32, _v, _v, _v, _v, _v, _sz, _dp, _v], _i32),
+    "lp_residual_norm_noalloc": ([_P, _i32, _v, _v, _v, _v, _dp, _v], _i32),
     "lp_check_finite": ([_v], _i32),
     "lp_open_forward": ([_P, _i32, _i32, _v, _v, _v, _v], _i32),
     "lp_open_grad": ([_P, _i32, _i32, _v, _v, _v, _v, _v], _i32),
@@ -273,6 +274,17 @@ def lp_residual_norm(p: LpProblem, which: int, K, b, U, Lam, ws) -> float:
     wp, wn = _ws(ws, 1)
     _check(load().lp_residual_norm(ctypes.byref(p), which, Kp, bp, _arr(U, n, "U", _elem_dtype(p)), lam, wp, wn,
                                    ctypes.byref(out), _stream()), "lp_residual_norm")
+    return out.value
+
+
+def lp_residual_norm_noalloc(p: LpProblem, which: int, K, b, U, Lam) -> float:
+    """lp_residual_norm on the library's static scratch (no workspace)."""
+    Kp, bp = _weights(p, K, b)
+    n = (p.N + 1) * p.B * p.q
+    out = ctypes.c_double(0.0)
+    lam = _arr(Lam, n, "Lam", _elem_dtype(p)) if which == LP_ADJOINT else None
+    _check(load().lp_residual_norm_noalloc(ctypes.byref(p), which, Kp, bp, _arr(U, n, "U", _elem_dtype(p)), lam,
+                                           ctypes.byref(out), _stream()), "lp_residual_norm_noalloc")
     return out.value
 
 

@@ -201,3 +201,24 @@ def test_loss_workspace_follows_the_head_path():
     assert lib.lp_loss_terminal(ctypes.byref(dense), 16, FAKE, FAKE, FAKE, FAKE, J, FAKE, FAKE, FAKE, FAKE,
                                 need16 - 1, None) == L.LP_EWORKSPACE
     assert L.lp_workspace_bytes(dense) >= need16
+
+
+def test_residual_norm_noalloc_limits():
+    """The allocation-free residual norm checks its arguments and its static
+    scratch limit (2^21 partials) on the host, before any device work."""
+    lib = L.load()
+    out = ctypes.byref(ctypes.c_double())
+    # (N + 1) * ceil(B / 32) partials: 4096 * 512 = 2^21 fits, 4097 * 512 does not
+    big = L.problem("f32", "dense", "tanh", 4096, 16384, 64, h=1e-3)
+    assert lib.lp_residual_norm_noalloc(ctypes.byref(big), L.LP_STATE, FAKE, FAKE, FAKE, None, out,
+                                        None) == L.LP_EWORKSPACE
+    assert b"static scratch" in lib.lp_last_error()
+    conv = L.problem("f32", "conv3x3", "relu", 2048, 1024, 8, H=28, W=28, h=1e-3)  # 2049 * 1024 partials
+    assert lib.lp_residual_norm_noalloc(ctypes.byref(conv), L.LP_STATE, FAKE, FAKE, FAKE, None, out,
+                                        None) == L.LP_EWORKSPACE
+    p = _p()
+    assert lib.lp_residual_norm_noalloc(ctypes.byref(p), 5, FAKE, FAKE, FAKE, FAKE, out, None) == L.LP_EINVAL
+    assert lib.lp_residual_norm_noalloc(ctypes.byref(p), L.LP_ADJOINT, FAKE, FAKE, FAKE, None, out,
+                                        None) == L.LP_EINVAL
+    assert lib.lp_residual_norm_noalloc(ctypes.byref(p), L.LP_STATE, FAKE, FAKE, FAKE, None, None,
+                                        None) == L.LP_EINVAL
