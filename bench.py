@@ -14,8 +14,14 @@ summed time in a traced warm-up step) is timed live with HIP events recorded by
 the library on the launch stream over the timed steps, and compared with its
 algorithmic bytes or flops (the model below) to give the roofline fraction.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--no-cpu]
+The default run measures the deep dense workload (N = 2048, B = 16384, width 64),
+the largest dense configuration, and then the convolutional workload, whose line
+goes under "extra" with its own roofline; the CPU oracle baseline is the deep
+workload's.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--extra 4 ...] [--no-cpu]
                        [--relax F|FCF|FCFCF] [--cycle V|F] [--cf C] [--no-record]
+       python bench.py --updates 100     (one-shot and layer-serial loss curves of the one-shot workload)
 """
 from __future__ import annotations
 
@@ -263,10 +269,28 @@ def summarize_traffic(workload: str, fetch_dir: str, write_dir: str, copy_fetch_
         fh.write("\n")
 
 
+def cpu_sample_size(wl) -> int:
+    """Examples the CPU oracle baseline runs on: the full batch of the small dense
+    workloads, fixed leading slices of the large ones (examples are independent
+    in every solve, so the rate per example carries over)."""
+    if wl.layer == "conv3x3":
+        return min(wl.B, 64)
+    if wl.q > 64:
+        return min(wl.B, 64)
+    if wl.cfg in (1, 2, 5):
+        return wl.B
+    return min(wl.B, 1024)
+
+
 def cpu_baseline(wl, budget_s: float = 12.0):
-    """The oracle (fp64 NumPy) timed on the host: one MGRIT forward iteration and
-    one adjoint iteration on a bounded batch sample, repeated until about
-    budget_s seconds have passed."""
+    """The oracle timed on the host cores, in the workload's own dtype, on a
+    bounded sample of the batch (cpu_sample_size), two legs, each repeated until
+    about budget_s / 2 seconds have passed:
+      MGRIT: one forward and one adjoint MGRIT iteration with the GPU's schedule
+             (the same metric as the GPU line, which is `value`);
+      layer-serial: forward propagation, backpropagation and the gradient (the
+             paper's baseline method), as layer-steps x examples per second of
+             one forward + backward pass."""
     import numpy as np
 
     import oracle as O
@@ -276,28 +300,41 @@ def cpu_baseline(wl, budget_s: float = 12.0):
     except ImportError:  # pragma: no cover
         threadpool_info = threadpool_limits = None
     ncores = len(os.sched_getaffinity(0))
-    # about 10-30 s of oracle work: wide dense layers and convolutions take a smaller sample
-    Bs = min(wl.B, (1024 if wl.q <= 64 else 64) if wl.layer == "dense" else 8)
+    Bs = cpu_sample_size(wl)
     d = generate(wl.with_overrides(B=Bs))
     ctx = threadpool_limits(ncores) if threadpool_limits else None
+    dt = np.float32 if wl.dtype == "f32" else np.float64
     try:
-        u0 = O.open_forward(d["y"], d["L_in"], wl.act, wl.opening)
-        U = np.zeros((wl.N + 1,) + u0.shape)
-        U[0] = u0
-        args = dict(cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=1,
-                    cycle=wl.cycle)
-        t0 = time.perf_counter()
-        reps = 0
-        while True:
-            Uo, _, _ = O.mgrit_forward(U, d["K"], d["b"], wl.h, wl.act, **args)
-            lamN = O.loss_terminal(Uo[-1], d["W"], d["mu"], d["onehot"])[1]
-            Lam = np.zeros_like(Uo)
-            Lam[-1] = lamN
-            O.mgrit_adjoint(Uo, Lam, d["K"], d["b"], wl.h, wl.act, **args)
-            reps += 1
-            if time.perf_counter() - t0 >= budget_s:
-                break
-        dt = time.perf_counter() - t0
+        with O.working_precision(dt):
+            u0 = O.open_forward(d["y"], d["L_in"], wl.act, wl.opening)
+            U = np.zeros((wl.N + 1,) + u0.shape, dtype=dt)
+            U[0] = u0
+            args = dict(cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=1,
+                        cycle=wl.cycle)
+            t0 = time.perf_counter()
+            reps = 0
+            while True:
+                Uo, _, _ = O.mgrit_forward(U, d["K"], d["b"], wl.h, wl.act, **args)
+                lamN = O.loss_terminal(Uo[-1], d["W"], d["mu"], d["onehot"])[1]
+                Lam = np.zeros_like(Uo)
+                Lam[-1] = lamN
+                O.mgrit_adjoint(Uo, Lam, d["K"], d["b"], wl.h, wl.act, **args)
+                reps += 1
+                if time.perf_counter() - t0 >= budget_s / 2:
+                    break
+            t_mg = time.perf_counter() - t0
+            t0 = time.perf_counter()
+            reps_s = 0
+            while True:
+                Us = O.serial_forward(u0, d["K"], d["b"], wl.h, wl.act)
+                lamN = O.loss_terminal(Us[-1], d["W"], d["mu"], d["onehot"])[1]
+                Ls = O.serial_adjoint(Us, lamN, d["K"], d["b"], wl.h, wl.act)
+                O.gradient(Us, Ls, d["K"], d["b"], wl.h, wl.act)
+                reps_s += 1
+                if time.perf_counter() - t0 >= budget_s / 2:
+                    break
+            t_se = time.perf_counter() - t0
+            assert Us.dtype == dt and Ls.dtype == dt
         threads = ncores
         if threadpool_info:
             th = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
@@ -305,63 +342,29 @@ def cpu_baseline(wl, budget_s: float = 12.0):
     finally:
         if ctx is not None:
             ctx.__exit__(None, None, None)
-    return {"value": wl.N * Bs * reps / dt, "unit": "layer-steps*examples/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {Bs} of {wl.B} examples, {reps} x (1 forward + 1 adjoint MGRIT iteration, "
-                      f"{wl.relax}, {len(level_sizes(wl.N, wl.cf, wl.max_levels, wl.min_coarse))} levels), "
-                      f"fp64 NumPy, {dt:.1f} s"}
+    levels = len(level_sizes(wl.N, wl.cf, wl.max_levels, wl.min_coarse))
+    sample = "full batch" if Bs == wl.B else f"first {Bs} of {wl.B} examples"
+    return {"value": wl.N * Bs * reps / t_mg, "unit": "layer-steps*examples/s", "cores": threads, "kind": "oracle",
+            "sample": f"{sample}, {reps} x (1 forward + 1 adjoint MGRIT iteration, {wl.relax}, {levels} levels), "
+                      f"NumPy in {wl.dtype}, {t_mg:.1f} s",
+            "layer_serial": {"value": wl.N * Bs * reps_s / t_se, "unit": "layer-steps*examples/s",
+                             "sample": f"{sample}, {reps_s} x (forward propagation + backpropagation + gradient), "
+                                       f"NumPy in {wl.dtype}, {t_se:.1f} s"}}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, help="workload 1..7 (default: the second workload)")
-    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--no-record", action="store_true",
-                    help="let the adjoint and the gradient recompute sigma' instead of reading the record")
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="only run a plain 1 GiB device copy 5 times (to scale HBM byte counters)")
-    ap.add_argument("--relax", choices=["F", "FCF", "FCFCF"], help="relaxation (default: the workload's)")
-    ap.add_argument("--cycle", choices=["V", "F"], help="MGRIT cycle (default: the workload's V-cycle)")
-    ap.add_argument("--cf", type=int, help="coarsening factor (default: the workload's, 4)")
-    ap.add_argument("--traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
-                    help="summarise rocprofv3 FETCH_SIZE / WRITE_SIZE runs of --config into profiles/traffic.json "
-                         "(no GPU needed)")
-    args = ap.parse_args()
-    if args.traffic:
-        summarize_traffic(f"cfg{args.config}", *args.traffic)
-        return
-    if args.copy_calibration:
-        import torch
-        n = 1 << 28  # fp32 values = 1 GiB
-        src = torch.ones(n, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(5):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes_read_per_launch": 4 * n, "copy_bytes_written_per_launch": 4 * n,
-                          "launches": 5}), flush=True)
-        return
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
-              file=sys.stderr)
-        sys.exit(2)
+def note(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
+
+def measure(wl, steps: int, warmup: int, no_record: bool = False):
+    """Time `steps` benchmark steps of one workload on the GPU (after `warmup`
+    untimed ones) and return its result line: value, ms per step, the dominant
+    kernel's live roofline and the per-kind times of a traced warm-up step."""
     import numpy as np
     import torch
 
     from paper_1812_04352_amd import lp as L
-    from workloads import WORKLOADS, generate
-
-    wl = WORKLOADS[args.config]
-    if args.relax or args.cycle or args.cf:
-        wl = wl.with_overrides(**{k: v for k, v in (("relax", args.relax), ("cycle", args.cycle), ("cf", args.cf))
-                                  if v})
-
-    def note(msg):
-        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+    from workloads import generate
 
     torch.cuda.set_device(0)
     dt = torch.float32 if wl.dtype == "f32" else torch.float64
@@ -382,7 +385,7 @@ def main():
 
     note(f"cfg{wl.cfg} inputs on the GPU")
     # the forward's final sweep keeps sigma'(z) for the adjoint and the gradient
-    rec_e = 0 if args.no_record else record_bytes(wl)
+    rec_e = 0 if no_record else record_bytes(wl)
     rec = L.alloc_dsig(p) if rec_e else None
     # iteration counts: fixed by the workload, or found once with its stop rule
     fwd_iters, adj_iters = wl.fwd_iters, wl.adj_iters
@@ -426,28 +429,30 @@ def main():
             per_kind[name] = ms
     dominant = max(per_kind, key=per_kind.get)
     lib.lp_trace_enable(0)
-    for _ in range(max(0, args.warmup - 2)):
+    for _ in range(max(0, warmup - 2)):
         step()
     torch.cuda.synchronize()
 
-    note(f"timed region: {args.steps} steps, dominant kernel {dominant}")
+    note(f"timed region: {steps} steps, dominant kernel {dominant}")
     # timed region: only the dominant kind is traced
     lib.lp_trace_enable(1 << KIND_NAMES.index(dominant))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     nl, kms = ctypes_read(lib, KIND_NAMES.index(dominant))
     lib.lp_trace_enable(0)
-    ms_step = (t1 - t0) * 1000.0 / args.steps
+    # the timed solves read nothing back: a non-finite residual norm shows up here
+    L.lp_check_finite()
+    ms_step = (t1 - t0) * 1000.0 / steps
     pairs = 0.5 * (fwd_iters + adj_iters)
     value = wl.N * wl.B * pairs / (ms_step / 1000.0)
 
     # roofline of the dominant kernel
     byts, flops, launches = kernel_model(wl, dominant, fwd_iters, adj_iters, rec_e)
-    assert nl == launches * args.steps, (dominant, nl, launches, args.steps)
+    assert nl == launches * steps, (dominant, nl, launches, steps)
     avg_ms = kms / nl
     intensity = flops / byts
     ridge = PEAK_TFLOPS[wl.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
@@ -477,20 +482,11 @@ def main():
         L.lp_serial_forward(p, K, b, Us)
     torch.cuda.synchronize()
     serial_ms = (time.perf_counter() - t0) * 200.0
-
-    out = {
-        "metric": "layer-steps*examples/s per MGRIT fwd+adjoint iteration",
+    del Us, U, Lam, ws, rec
+    torch.cuda.empty_cache()
+    return {
         "value": value,
-        "unit": "layer-steps*examples/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": ms_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": wl.dtype,
-        "data": "synthetic",
         "config": {"workload": f"cfg{wl.cfg}: {wl.name}", "N": wl.N, "B": wl.B, "width": wl.q,
                    "activation": wl.act, "mgrit": {"cf": wl.cf, "levels": len(level_sizes(
                        wl.N, wl.cf, wl.max_levels, wl.min_coarse)), "relax": wl.relax, "cycle": wl.cycle,
@@ -502,6 +498,141 @@ def main():
         "serial_forward_ms": serial_ms,
         "residual_history": {"fwd": hist["fwd"], "adj": hist["adj"]},
     }
+
+
+def one_shot_report(updates: int):
+    """Algorithm 2 on the one-shot workload (lr = 1e-2, one forward and one adjoint
+    MGRIT iteration per update) next to layer-serial gradient descent from the
+    same seed, both on the GPU: the per-update losses, the time per update, and
+    the largest relative deviation from the fp64 oracle's curves stored in
+    tests/golden/one_shot_losses.txt (where it holds them)."""
+    import numpy as np
+    import torch
+
+    from paper_1812_04352_amd import lp as L
+    from paper_1812_04352_amd.one_shot import OneShotTrainer, SerialTrainer
+    from workloads import ONE_SHOT_LR, WORKLOADS, generate
+
+    wl = WORKLOADS[5]
+    torch.cuda.set_device(0)
+    d = generate(wl)
+
+    def params():
+        return {k: torch.from_numpy(np.ascontiguousarray(d[k])).cuda() for k in ("K", "b", "W", "mu", "L_in")}
+
+    y, c = (torch.from_numpy(np.ascontiguousarray(d[k])).cuda() for k in ("y", "onehot"))
+    p = L.problem(wl.dtype, wl.layer, wl.act, wl.N, wl.B, wl.C, wl.H, wl.W, wl.h)
+
+    def mg(it):
+        return L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, it, cycle=wl.cycle)
+
+    curves, times = {}, {}
+    for name in ("one_shot", "layer_serial"):
+        note(f"{name}: {updates} updates")
+        tr = OneShotTrainer(p, mg(wl.fwd_iters), mg(wl.adj_iters), params(), y, c, wl.n_classes,
+                            L.OPENING[wl.opening], wl.n_features) if name == "one_shot" else \
+            SerialTrainer(p, params(), y, c, wl.n_classes, L.OPENING[wl.opening], wl.n_features)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        curves[name] = tr.run(updates, ONE_SHOT_LR)
+        times[name] = (time.perf_counter() - t0) * 1000.0 / updates
+        del tr
+        torch.cuda.empty_cache()
+    out = {"workload": f"cfg5: {wl.name}", "updates": updates, "lr": ONE_SHOT_LR,
+           "ms_per_update": times, "loss": curves}
+    path = os.path.join(ROOT, "tests", "golden", "one_shot_losses.txt")
+    if os.path.exists(path):
+        ref = np.loadtxt(path)
+        dev = {}
+        for col, name in ((1, "one_shot"), (2, "layer_serial")):
+            r = ref[~np.isnan(ref[:, col]), col][:updates]
+            if len(r):
+                dev[name] = {"updates_compared": int(len(r)),
+                             "max_rel_deviation": float(np.max(np.abs(np.array(curves[name][:len(r)]) - r) / np.abs(r)))}
+        out["vs_oracle"] = dev
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3,
+                    help="workload 1..7 (default: the third, the deep dense network, the largest dense one)")
+    ap.add_argument("--extra", type=int, nargs="*", default=None,
+                    help="workloads measured after the headline one and reported under 'extra' (default: 4, the "
+                         "convolutional network, when the headline is the default workload)")
+    ap.add_argument("--extra-steps", type=int, default=5)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-record", action="store_true",
+                    help="let the adjoint and the gradient recompute sigma' instead of reading the record")
+    ap.add_argument("--cpu-budget", type=float, default=16.0)
+    ap.add_argument("--updates", type=int, default=0,
+                    help="instead of the benchmark: run this many one-shot and layer-serial training updates of "
+                         "the one-shot workload and report both loss curves")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 5 times (to scale HBM byte counters)")
+    ap.add_argument("--relax", choices=["F", "FCF", "FCFCF"], help="relaxation (default: the workload's)")
+    ap.add_argument("--cycle", choices=["V", "F"], help="MGRIT cycle (default: the workload's V-cycle)")
+    ap.add_argument("--cf", type=int, help="coarsening factor (default: the workload's, 4)")
+    ap.add_argument("--traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="summarise rocprofv3 FETCH_SIZE / WRITE_SIZE runs of --config into profiles/traffic.json "
+                         "(no GPU needed)")
+    args = ap.parse_args()
+    if args.traffic:
+        summarize_traffic(f"cfg{args.config}", *args.traffic)
+        return
+    if args.copy_calibration:
+        import torch
+        n = 1 << 28  # fp32 values = 1 GiB
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read_per_launch": 4 * n, "copy_bytes_written_per_launch": 4 * n,
+                          "launches": 5}), flush=True)
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.updates:
+        print(json.dumps(one_shot_report(args.updates)), flush=True)
+        return
+
+    from workloads import WORKLOADS
+
+    def variant(wl):
+        ov = {k: v for k, v in (("relax", args.relax), ("cycle", args.cycle), ("cf", args.cf)) if v}
+        return wl.with_overrides(**ov) if ov else wl
+
+    wl = variant(WORKLOADS[args.config])
+    extra = args.extra if args.extra is not None else ([4] if args.config == 3 else [])
+    res = measure(wl, args.steps, args.warmup, args.no_record)
+    out = {
+        "metric": "layer-steps*examples/s per MGRIT fwd+adjoint iteration",
+        "value": res["value"],
+        "unit": "layer-steps*examples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+    }
+    out.update({k: v for k, v in res.items() if k not in ("value", "ms_per_step")})
+    if extra:
+        out["extra"] = {}
+        for cfg in extra:
+            wx = variant(WORKLOADS[cfg])
+            rx = measure(wx, args.extra_steps, min(args.warmup, 3), args.no_record)
+            rx["steps"], rx["dtype"] = args.extra_steps, wx.dtype
+            out["extra"][f"cfg{cfg}"] = rx
     if not args.no_cpu:
         note("CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)

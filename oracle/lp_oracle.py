@@ -28,9 +28,33 @@ from __future__ import annotations
 import numpy as np
 
 
+# Working precision of every function below: fp64 for all parity uses. Only the
+# benchmark's CPU timing switches it (working_precision) to time the oracle in a
+# workload's own dtype; the arithmetic is the same either way.
+_DT = np.float64
+
+
+class working_precision:
+    """Context manager: run the oracle in the given numpy float dtype."""
+
+    def __init__(self, dtype):
+        self.dtype = np.dtype(dtype).type
+
+    def __enter__(self):
+        global _DT
+        self.prev, _DT = _DT, self.dtype
+        return self
+
+    def __exit__(self, *exc):
+        global _DT
+        _DT = self.prev
+        return False
+
+
 def _f64(*arrays):
-    """Upcast inputs (typically already rounded to the workload dtype) to fp64."""
-    out = tuple(None if a is None else np.asarray(a, dtype=np.float64) for a in arrays)
+    """Upcast inputs (typically already rounded to the workload dtype) to fp64
+    (to the working precision when the benchmark has changed it)."""
+    out = tuple(None if a is None else np.asarray(a, dtype=_DT) for a in arrays)
     return out if len(out) > 1 else out[0]
 
 
@@ -65,9 +89,9 @@ def dact(z, kind):
         t = np.tanh(z)
         return 1.0 - t * t
     if kind == "relu":
-        return (z > 0.0).astype(np.float64)
+        return (z > 0.0).astype(z.dtype)
     if kind == "smoothrelu":
-        return np.where(np.abs(z) <= 0.1, 5.0 * z + 0.5, (z > 0.0).astype(np.float64))
+        return np.where(np.abs(z) <= 0.1, 5.0 * z + 0.5, (z > 0.0).astype(z.dtype))
     if kind == "identity":
         return np.ones_like(z)
     raise ValueError(kind)
@@ -80,9 +104,9 @@ def dact(z, kind):
 def conv3x3(Kn, v):
     """z[b,co,y,x] = sum_{ci,dy,dx} Kn[co,ci,dy+1,dx+1] v[b,ci,y+dy,x+dx], zero padded."""
     Bn, C, H, W = v.shape
-    vp = np.zeros((Bn, C, H + 2, W + 2))
+    vp = np.zeros((Bn, C, H + 2, W + 2), dtype=v.dtype)
     vp[:, :, 1:H + 1, 1:W + 1] = v
-    z = np.zeros((Bn, Kn.shape[0], H, W))
+    z = np.zeros((Bn, Kn.shape[0], H, W), dtype=v.dtype)
     for ty in range(3):
         for tx in range(3):
             z += np.einsum("oc,bcyx->boyx", Kn[:, :, ty, tx], vp[:, :, ty:ty + H, tx:tx + W])
@@ -93,7 +117,7 @@ def conv3x3_transpose(Kn, s):
     """Adjoint of conv3x3 with respect to its input: scatter every output back to
     the inputs that produced it, then drop the padding."""
     Bn, Co, H, W = s.shape
-    gp = np.zeros((Bn, Kn.shape[1], H + 2, W + 2))
+    gp = np.zeros((Bn, Kn.shape[1], H + 2, W + 2), dtype=s.dtype)
     for ty in range(3):
         for tx in range(3):
             gp[:, :, ty:ty + H, tx:tx + W] += np.einsum("oc,boyx->bcyx", Kn[:, :, ty, tx], s)
@@ -103,9 +127,9 @@ def conv3x3_transpose(Kn, s):
 def conv3x3_weight_grad(s, v):
     """d/dKn of sum(s * conv3x3(Kn, v)): [Co][Ci][3][3]."""
     Bn, C, H, W = v.shape
-    vp = np.zeros((Bn, C, H + 2, W + 2))
+    vp = np.zeros((Bn, C, H + 2, W + 2), dtype=v.dtype)
     vp[:, :, 1:H + 1, 1:W + 1] = v
-    g = np.zeros((s.shape[1], C, 3, 3))
+    g = np.zeros((s.shape[1], C, 3, 3), dtype=v.dtype)
     for ty in range(3):
         for tx in range(3):
             g[:, :, ty, tx] = np.einsum("boyx,bcyx->oc", s, vp[:, :, ty:ty + H, tx:tx + W])
@@ -161,7 +185,7 @@ def serial_forward(u0, K, b, h, kind):
     solved by forward substitution. Returns U [N+1][...]."""
     u0, K, b = _f64(u0, K, b)
     N = K.shape[0]
-    U = np.empty((N + 1,) + u0.shape)
+    U = np.empty((N + 1,) + u0.shape, dtype=_DT)
     U[0] = u0
     for n in range(N):
         U[n + 1] = phi(U[n], K[n], b[n], h, kind)
@@ -187,8 +211,8 @@ def gradient(U, Lam, K, b, h, kind):
     Returns (dK like K, db like b)."""
     U, Lam, K, b = _f64(U, Lam, K, b)
     N = K.shape[0]
-    dK = np.empty(K.shape)
-    db = np.empty(b.shape)
+    dK = np.empty(K.shape, dtype=_DT)
+    db = np.empty(b.shape, dtype=_DT)
     for n in range(N):
         s = dact(preact(K[n], b[n], U[n]), kind) * Lam[n + 1]
         if _is_conv(K[n]):
@@ -395,7 +419,7 @@ def _fwd_cycle(H, K, b, kind, relax, l, rho_out, cycle="V"):
         acc += float(np.sum(r * r))
     if l == 0:
         rho_out.append(np.sqrt(acc))
-    uc = np.empty((Nc + 1,) + u.shape[1:])
+    uc = np.empty((Nc + 1,) + u.shape[1:], dtype=u.dtype)
     gc = np.empty_like(uc)
     for k in range(Nc + 1):
         uc[k] = u[k * c]
@@ -433,7 +457,7 @@ def mgrit_forward(U, K, b, h, kind, cf=4, max_levels=2, min_coarse=1, relax="FCF
     N = K.shape[0]
     sizes = level_sizes(N, cf, max_levels, min_coarse)
     H = _Hierarchy(sizes, cf, h)
-    u = np.array(U, dtype=np.float64, copy=True)
+    u = np.array(U, dtype=_DT, copy=True)
     if not warm_start and len(sizes) > 1:
         for k in range(1, N // cf + 1):
             u[k * cf] = u[0]
@@ -504,7 +528,7 @@ def _adj_cycle(H, U, K, b, kind, relax, l, rho_out, cycle="V"):
         acc += float(np.sum(r * r))
     if l == 0:
         rho_out.append(np.sqrt(acc))
-    lc = np.empty((Nc + 1,) + lam.shape[1:])
+    lc = np.empty((Nc + 1,) + lam.shape[1:], dtype=lam.dtype)
     gc = np.empty_like(lc)
     for k in range(Nc + 1):
         lc[k] = lam[k * c]
@@ -531,7 +555,7 @@ def mgrit_adjoint(U, Lam, K, b, h, kind, cf=4, max_levels=2, min_coarse=1, relax
     N = K.shape[0]
     sizes = level_sizes(N, cf, max_levels, min_coarse)
     H = _Hierarchy(sizes, cf, h)
-    lam = np.array(Lam, dtype=np.float64, copy=True)
+    lam = np.array(Lam, dtype=_DT, copy=True)
     if not warm_start and len(sizes) > 1:
         for k in range(N // cf):
             lam[k * cf] = lam[N]

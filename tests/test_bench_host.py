@@ -101,3 +101,17 @@ def test_source_hashes_are_per_family_and_stable():
     fams = [h("lp::conv::k"), h("lp::mfma::k"), h("lp::dense::k"), h("lp::wide::k"), h()]
     assert len(set(fams)) == len(fams)
     assert h("void lp::conv::k_adj<1>") == h("lp::conv::") and h() == h("")
+
+
+def test_cpu_baseline_legs():
+    """The CPU baseline times both oracle legs (MGRIT iteration, layer-serial
+    forward + backward + gradient) in the workload's dtype on the full batch of
+    the small dense workloads and on a leading slice of the large ones."""
+    from workloads import WORKLOADS
+    assert bench.cpu_sample_size(WORKLOADS[2]) == WORKLOADS[2].B
+    assert bench.cpu_sample_size(WORKLOADS[5]) == WORKLOADS[5].B
+    assert bench.cpu_sample_size(WORKLOADS[3]) == 1024
+    assert bench.cpu_sample_size(WORKLOADS[4]) == 64
+    r = bench.cpu_baseline(WORKLOADS[2].with_overrides(N=16, B=64), budget_s=0.2)
+    assert r["value"] > 0 and r["layer_serial"]["value"] > 0 and r["cores"] >= 1
+    assert "full batch" in r["sample"] and "f32" in r["sample"]

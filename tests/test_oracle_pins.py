@@ -779,3 +779,28 @@ def test_one_shot_lbfgs_with_exact_inner_solves_takes_exact_gradients():
     _, wo = O.serial_training(*args, updates=1, lr=0.25)
     for k in ("K", "b", "W", "mu", "L_in"):
         assert rel(r["weights"][k], wo[k]) < 1e-10, k
+
+
+def test_working_precision_changes_only_the_rounding():
+    """The benchmark times the oracle in a workload's own dtype. Under
+    working_precision(float32) every result is float32 and agrees with the fp64
+    default to fp32 rounding; leaving the context restores fp64."""
+    from workloads import WORKLOADS, generate
+    wl = WORKLOADS[2].with_overrides(N=16, B=64, max_levels=2)
+    d = generate(wl)
+    u0 = O.open_forward(d["y"], d["L_in"], wl.act, wl.opening)
+    U64 = O.serial_forward(u0, d["K"], d["b"], wl.h, wl.act)
+    M64, h64, _ = O.mgrit_forward(np.concatenate([u0[None], np.zeros((wl.N,) + u0.shape)]), d["K"], d["b"], wl.h,
+                                  wl.act, cf=4, max_levels=2, max_iter=2)
+    with O.working_precision(np.float32):
+        U32 = O.serial_forward(u0, d["K"], d["b"], wl.h, wl.act)
+        lam = O.loss_terminal(U32[-1], d["W"], d["mu"], d["onehot"])[1]
+        L32 = O.serial_adjoint(U32, lam, d["K"], d["b"], wl.h, wl.act)
+        dK32, _ = O.gradient(U32, L32, d["K"], d["b"], wl.h, wl.act)
+        M32, h32, _ = O.mgrit_forward(np.concatenate([u0[None], np.zeros((wl.N,) + u0.shape)]), d["K"], d["b"],
+                                      wl.h, wl.act, cf=4, max_levels=2, max_iter=2)
+    assert U32.dtype == L32.dtype == dK32.dtype == M32.dtype == np.float32
+    assert np.linalg.norm(U32 - U64) <= 1e-5 * np.linalg.norm(U64)
+    assert np.linalg.norm(M32 - M64) <= 1e-5 * np.linalg.norm(M64)
+    assert abs(h32[-1] - h64[-1]) <= 1e-4 * h64[-1]
+    assert O.serial_forward(u0, d["K"], d["b"], wl.h, wl.act).dtype == np.float64
