@@ -39,6 +39,53 @@ def _compile(src: str) -> str:
     return obj
 
 
+# Host-code sanitizers (AddressSanitizer, UndefinedBehaviorSanitizer) for the
+# CPU-side checks: every flag goes to the host compilation only (-Xarch_host), the
+# GPU code objects are the ordinary ones.
+SAN_FLAGS = ["-O1", "-g", "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+             "-Xarch_host", "-shared-libasan"]
+SAN_SOURCES = ["lp_host.cpp", "lp_noalloc.hip"]  # the translation units with host logic beyond launches
+SAN_OUT = os.path.join(OBJ, "liblp_san.so")
+
+
+def sanitizer_runtime() -> str:
+    """Path of the shared AddressSanitizer runtime (to be preloaded into a host
+    process that is not itself instrumented, e.g. python)."""
+    r = subprocess.run([HIPCC, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    return r.stdout.strip()
+
+
+def build_sanitized(verbose: bool = True) -> str:
+    """Build _build/liblp_san.so: the library with its host logic (argument
+    checks, workspace layout, MGRIT schedule) compiled with AddressSanitizer and
+    UndefinedBehaviorSanitizer; the kernel translation units are the ordinary
+    objects (built first if missing)."""
+    os.makedirs(os.path.join(OBJ, "san"), exist_ok=True)
+    objs = []
+    for src in SOURCES:
+        if src in SAN_SOURCES:
+            obj = os.path.join(OBJ, "san", os.path.splitext(src)[0] + ".o")
+            flags = [f for f in FLAGS if f != "-O3"] + SAN_FLAGS
+            cmd = [HIPCC, *flags, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+            r = subprocess.run(cmd, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"hipcc failed on {src} (sanitized):\n{r.stdout}\n{r.stderr}")
+        else:
+            obj = os.path.join(OBJ, os.path.splitext(src)[0] + ".o")
+            if not os.path.exists(obj):
+                obj = _compile(src)
+        objs.append(obj)
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Xarch_host", "-fsanitize=address",
+           "-Xarch_host", "-fsanitize=undefined", "-Xarch_host", "-shared-libasan", *objs, "-o", SAN_OUT]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{r.stdout}\n{r.stderr}")
+    if verbose:
+        print(f"built {SAN_OUT}")
+    return SAN_OUT
+
+
 def build(verbose: bool = True) -> str:
     """Compile every source (always: this is the build check) and link liblp.so."""
     os.makedirs(OBJ, exist_ok=True)
@@ -57,5 +104,8 @@ def build(verbose: bool = True) -> str:
 
 
 if __name__ == "__main__":
-    build()
+    if len(sys.argv) > 1 and sys.argv[1] == "--sanitize":
+        build_sanitized()
+    else:
+        build()
     sys.exit(0)
