@@ -78,7 +78,7 @@ def record_bytes(wl) -> int:
     return 1 if wl.act == "relu" else 4
 
 
-def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
+def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0, cpt: bool = False):
     """Algorithmic HBM bytes and flops of every launch of one kernel kind in one
     step (summed over MGRIT levels and iterations), and the launch count.
 
@@ -96,7 +96,12 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
     adjoint reads one record row per step instead of a primal row and skips the
     forward product (2q^2 flops per step), the gradient (width 64) reads the
     record instead of K_n and takes no forward product, and the final finest CORRF writes c
-    record rows per interval and takes one more product."""
+    record rows per interval and takes one more product.
+    With C-point storage (cpt) the finest adjoint sweeps read one primal row (the
+    lower C-point) per interval and recompute the interval's states with c forward
+    products; the finest forward CORRF only corrects the C-points (read 2, write 1,
+    no products); the gradient reads the C-points, writes and reads back the
+    recomputed states of every layer ((c-1)/c N forward products), and reads Lam."""
     q, B, c = wl.q, wl.B, wl.cf
     e = 4 if wl.dtype == "f32" else 8
     row = B * q * e
@@ -115,6 +120,9 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
     arow = (rrow / row) if rec else 1.0
     fstep = (2 if adj and rec else 4 if adj else 2) * mac
     byts = flops = launches = 0
+    if kind == "gradient" and cpt:
+        return ((wl.N // c + 3 * wl.N) * row + 3 * wl.N * nweights * e,
+                (4.0 + 2.0 * (c - 1) / c) * mac * B * wl.N, 1)
     if kind == "gradient":
         if rec and (wl.layer != "dense" or q >= 64):  # the dense width-32 kernel recomputes sigma'
             return 2 * wl.N * row + wl.N * rrow + wl.N * nweights * e, 2.0 * mac * B * wl.N, 1
@@ -136,21 +144,31 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0):
             Nc = Nl // c
             xn = (1.0 / c) if (l + 1 < L - 1) else 0.0
             deferred = l == 0 and fcf
+            # primal rows the adjoint reads per interval, and the extra recompute products
+            prow = (1.0 if cpt and l == 0 else c * arow) if adj else 0.0
+            if kind.endswith("_corrf") and cpt and l == 0 and not adj:
+                if not deferred or m == iters - 1:
+                    byts += nv * Nc * 3 * row
+                    launches += nv
+                continue
             if kind.endswith("_fc") and fcf:
                 # the first FC sweep reads the pending correction on the finest level
                 # from the second cycle on; a second one (FCFCF) reads staged C-points
-                first = Nc * (2 + g * c + (c * arow if adj else 0) + (1 if deferred and m > 0 else 0)) * row
-                again = Nc * (2 + g * c + (c * arow if adj else 0)) * row
+                first = Nc * (2 + g * c + prow + (1 if deferred and m > 0 else 0)) * row
+                again = Nc * (2 + g * c + prow) * row
                 byts += nv * (first + (nfc - 1) * again + nfc * wbytes)
                 flops += nv * nfc * Nc * c * fstep * B
                 launches += nv * nfc
             elif kind.endswith("_fres"):
-                byts += nv * (Nc * (3 + xn + g * c + (c * arow if adj else 0)) * row + wbytes)
+                byts += nv * (Nc * (3 + xn + g * c + prow) * row + wbytes)
                 flops += nv * Nc * (c * fstep + (2 * mac if adj else 0)) * B
                 launches += nv
             elif kind.endswith("_corrf") and (not deferred or m == iters - 1):
-                byts += nv * (Nc * (2 + c + g * (c - 1) + ((c - 1) * arow if adj else 0)) * row + wbytes)
+                byts += nv * (Nc * (2 + c + g * (c - 1) + ((1.0 if cpt and l == 0 else (c - 1) * arow)
+                                                           if adj else 0)) * row + wbytes)
                 flops += nv * Nc * (c - 1) * fstep * B
+                if cpt and adj and l == 0:
+                    flops += nv * Nc * 2 * mac * B  # the recompute also needs the interval's first product
                 if rec and not adj and l == 0:
                     # the final finest sweep keeps the record of all c layers
                     byts += Nc * c * rrow
@@ -356,10 +374,12 @@ def note(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def measure(wl, steps: int, warmup: int, no_record: bool = False):
+def measure(wl, steps: int, warmup: int, no_record: bool = False, storage: str = "all"):
     """Time `steps` benchmark steps of one workload on the GPU (after `warmup`
     untimed ones) and return its result line: value, ms per step, the dominant
-    kernel's live roofline and the per-kind times of a traced warm-up step."""
+    kernel's live roofline and the per-kind times of a traced warm-up step.
+    storage "cpoints": the primal trajectory keeps the C-points only (no record;
+    the adjoint and the gradient recompute the F-point states)."""
     import numpy as np
     import torch
 
@@ -367,8 +387,10 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False):
     from workloads import generate
 
     torch.cuda.set_device(0)
+    torch.cuda.reset_peak_memory_stats()
     dt = torch.float32 if wl.dtype == "f32" else torch.float64
     d = generate(wl)
+    cpt = storage == "cpoints"
 
     def g(x):
         return torch.from_numpy(np.ascontiguousarray(x)).to(device="cuda", dtype=dt)
@@ -376,31 +398,31 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False):
     K, b, W, mu, y, c = (g(d[k]) for k in ("K", "b", "W", "mu", "y", "onehot"))
     Lin = g(d["L_in"]) if d["L_in"] is not None else None
     p = L.problem(wl.dtype, wl.layer, wl.act, wl.N, wl.B, wl.C, wl.H, wl.W, wl.h)
-    U = torch.zeros((wl.N + 1, wl.B, wl.q), device="cuda", dtype=dt)
+    U = torch.zeros(((wl.N // wl.cf if cpt else wl.N) + 1, wl.B, wl.q), device="cuda", dtype=dt)
     L.lp_open_forward(p, L.OPENING[wl.opening], wl.n_features, y, Lin, U[0])
-    Lam = torch.zeros_like(U)
+    Lam = torch.zeros((wl.N + 1, wl.B, wl.q), device="cuda", dtype=dt)
     J = torch.zeros(1, device="cuda", dtype=torch.float64)
     dW, dmu = torch.empty_like(W), torch.empty_like(mu)
     dK, db = torch.empty_like(K), torch.empty_like(b)
 
     note(f"cfg{wl.cfg} inputs on the GPU")
     # the forward's final sweep keeps sigma'(z) for the adjoint and the gradient
-    rec_e = 0 if no_record else record_bytes(wl)
+    rec_e = 0 if (no_record or cpt) else record_bytes(wl)
     rec = L.alloc_dsig(p) if rec_e else None
     # iteration counts: fixed by the workload, or found once with its stop rule
     fwd_iters, adj_iters = wl.fwd_iters, wl.adj_iters
     if wl.rtol > 0 or wl.stag > 0:
         mg = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, wl.fwd_iters, False, wl.rtol, wl.stag,
-                     wl.cycle)
+                     wl.cycle, storage)
         ws = L.alloc_workspace(p, mg)
         fwd_iters, _ = L.lp_mgrit_forward(p, mg, K, b, U, ws, dsig=rec)
         L.lp_loss_terminal(p, wl.n_classes, U[-1], W, mu, c, J, Lam[-1], dW, dmu, ws)
         adj_iters, _ = L.lp_mgrit_adjoint(p, L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax,
-                                                     wl.adj_iters, False, wl.rtol, wl.stag, wl.cycle), K, b, U, Lam, ws,
-                                          dsig=rec)
+                                                     wl.adj_iters, False, wl.rtol, wl.stag, wl.cycle, storage), K, b,
+                                          U, Lam, ws, dsig=rec)
         del ws
-    mgF = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, fwd_iters, cycle=wl.cycle)
-    mgA = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, adj_iters, cycle=wl.cycle)
+    mgF = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, fwd_iters, cycle=wl.cycle, storage=storage)
+    mgA = L.mgrit(wl.cf, wl.max_levels, wl.min_coarse, wl.relax, adj_iters, cycle=wl.cycle, storage=storage)
     ws = L.alloc_workspace(p, mgF if fwd_iters >= adj_iters else mgA)
     hist = {}
 
@@ -409,7 +431,10 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False):
         _, hf = L.lp_mgrit_forward(p, mgF, K, b, U, ws, history=history, dsig=rec)
         L.lp_loss_terminal(p, wl.n_classes, U[-1], W, mu, c, J, Lam[-1], dW, dmu, ws)
         _, ha = L.lp_mgrit_adjoint(p, mgA, K, b, U, Lam, ws, history=history, dsig=rec)
-        L.lp_gradient(p, K, b, U, Lam, dK, db, ws, dsig=rec)
+        if cpt:
+            L.lp_gradient_cpoints(p, wl.cf, K, b, U, Lam, dK, db, ws)
+        else:
+            L.lp_gradient(p, K, b, U, Lam, dK, db, ws, dsig=rec)
         if history:
             hist["fwd"], hist["adj"] = hf, ha
 
@@ -450,8 +475,9 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False):
     pairs = 0.5 * (fwd_iters + adj_iters)
     value = wl.N * wl.B * pairs / (ms_step / 1000.0)
 
+    peak_gb = torch.cuda.max_memory_allocated() / 1e9
     # roofline of the dominant kernel
-    byts, flops, launches = kernel_model(wl, dominant, fwd_iters, adj_iters, rec_e)
+    byts, flops, launches = kernel_model(wl, dominant, fwd_iters, adj_iters, rec_e, cpt)
     assert nl == launches * steps, (dominant, nl, launches, steps)
     avg_ms = kms / nl
     intensity = flops / byts
@@ -474,7 +500,8 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False):
     roof["algorithmic_flops_per_launch"] = flops / launches
 
     # single-GPU context: the layer-serial forward pass (the baseline method)
-    Us = U.clone()
+    Us = torch.empty_like(Lam)
+    Us[0] = U[0]
     L.lp_serial_forward(p, K, b, Us)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -492,7 +519,9 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False):
                        wl.N, wl.cf, wl.max_levels, wl.min_coarse)), "relax": wl.relax, "cycle": wl.cycle,
                        "fwd_iters": fwd_iters, "adj_iters": adj_iters},
                    "sigma_record": {0: None, 1: "u8", 4: "f32"}[rec_e],
+                   "storage": "C-points only (F-point states recomputed)" if cpt else "every layer",
                    "step": "MGRIT forward iterations + loss + MGRIT adjoint iterations + gradient"},
+        "device_memory_gb": peak_gb,
         "roofline": roof,
         "kernel_ms_per_step": {k: v for k, v in sorted(per_kind.items(), key=lambda t: -t[1])},
         "serial_forward_ms": serial_ms,
@@ -567,6 +596,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-record", action="store_true",
                     help="let the adjoint and the gradient recompute sigma' instead of reading the record")
+    ap.add_argument("--storage", choices=["all", "cpoints"], default="all",
+                    help="primal trajectory storage: every layer, or the C-points only (dense widths 32/64)")
     ap.add_argument("--cpu-budget", type=float, default=16.0)
     ap.add_argument("--updates", type=int, default=0,
                     help="instead of the benchmark: run this many one-shot and layer-serial training updates of "
@@ -610,7 +641,7 @@ def main():
 
     wl = variant(WORKLOADS[args.config])
     extra = args.extra if args.extra is not None else ([4] if args.config == 3 else [])
-    res = measure(wl, args.steps, args.warmup, args.no_record)
+    res = measure(wl, args.steps, args.warmup, args.no_record, args.storage)
     out = {
         "metric": "layer-steps*examples/s per MGRIT fwd+adjoint iteration",
         "value": res["value"],
@@ -630,7 +661,8 @@ def main():
         out["extra"] = {}
         for cfg in extra:
             wx = variant(WORKLOADS[cfg])
-            rx = measure(wx, args.extra_steps, min(args.warmup, 3), args.no_record)
+            rx = measure(wx, args.extra_steps, min(args.warmup, 3), args.no_record,
+                         args.storage if wx.layer == "dense" and wx.q in (32, 64) else "all")
             rx["steps"], rx["dtype"] = args.extra_steps, wx.dtype
             out["extra"][f"cfg{cfg}"] = rx
     if not args.no_cpu:

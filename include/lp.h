@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LP_ABI_VERSION 3
+#define LP_ABI_VERSION 4
 
 typedef enum {
   LP_OK = 0,
@@ -65,6 +65,7 @@ enum { LP_RELAX_F = 0, LP_RELAX_FCF = 1, LP_RELAX_FCFCF = 2 }; /* MGRIT relaxati
 enum { LP_CYCLE_V = 0, LP_CYCLE_F = 1 };               /* MGRIT cycle */
 enum { LP_STATE = 0, LP_ADJOINT = 1 };                 /* which system */
 enum { LP_OPEN_IDENTITY = 0, LP_OPEN_DENSE_ACT = 1, LP_OPEN_CONV_ACT = 2 }; /* opening layer */
+enum { LP_STORE_ALL = 0, LP_STORE_CPOINTS = 1 };       /* primal trajectory storage */
 
 /* The network and batch (Section 2.2). Dense: C = width q, H = W = 1.
  * Conv: C channels of H x W pixels. h = T / N is the step size.
@@ -105,7 +106,22 @@ typedef struct {
   double rtol;           /* stop after iteration m when rho_m <= rtol * rho_1 (0: off) */
   double stag;           /* stop after iteration m > 1 when rho_m > stag * rho_{m-1} (0: off) */
   int32_t cycle;         /* LP_CYCLE_V | LP_CYCLE_F */
+  int32_t storage;       /* LP_STORE_ALL | LP_STORE_CPOINTS: how the primal trajectory is kept (below) */
 } lp_mgrit;
+
+/* Primal storage (Section 3.2, remark on storing or recomputing the states the
+ * adjoint equations depend on). LP_STORE_ALL: the state trajectory U is
+ * [N+1][B][q], every layer stored. LP_STORE_CPOINTS: U holds the fine C-points
+ * only, Uc [N/cf + 1][B][q] with row k = u^{k cf} (a checkpoint per coarse
+ * interval, cf times less memory). lp_mgrit_forward then writes only Uc (the
+ * F-points of the returned iterate are the F-relaxation of its C-points, never
+ * stored); lp_mgrit_adjoint, given Uc, recomputes each interval's F-point states
+ * and sigma' from its lower C-point on the finest level (coarse levels use only
+ * C-points); lp_gradient_cpoints does the same for the gradient. The recomputed
+ * states equal the stored ones bit for bit, so both storages give the same
+ * iterates and gradients. Implemented for fp32 dense widths 32 and 64 (the
+ * matrix-core kernels) with cf = 4 and at least two levels; other problems
+ * return LP_EUNSUPPORTED. No sigma' record is kept or read (dsig is ignored). */
 
 int32_t lp_abi_version(void);
 const char* lp_status_string(int32_t status);
@@ -114,7 +130,8 @@ const char* lp_last_error(void);
 
 /* Workspace bytes that lp_mgrit_forward, lp_mgrit_adjoint, lp_gradient,
  * lp_residual_norm and lp_loss_terminal need for this problem and schedule (mg
- * may be NULL: then the MGRIT hierarchy is not counted). Returns 0 for an invalid
+ * may be NULL: then the MGRIT hierarchy is not counted; with mg->storage =
+ * LP_STORE_CPOINTS lp_gradient_cpoints is covered too). Returns 0 for an invalid
  * problem. The workspace holds the coarse levels (U_l and the FAS right-hand
  * side G_l for l >= 1), the relaxed C-points of every non-coarsest level,
  * per-workgroup residual partials (fp64) and per-chunk gradient partials. */
@@ -160,7 +177,9 @@ int32_t lp_serial_adjoint(const lp_problem* prob, const void* K, const void* b, 
  * U [N+1][B][q]: row 0 is u^0 (read, never written); with warm_start the other
  * rows are the initial guess (only rows at multiples of cf are read), else they
  * are ignored; on return they hold the iterate after *iters V-cycles (every row
- * written, the last sweep being an F-relaxation).
+ * written, the last sweep being an F-relaxation). With mg->storage =
+ * LP_STORE_CPOINTS, U is Uc [N/cf + 1][B][q] (row k = C-point k cf) and only
+ * those rows are read and written.
  * res_hist (host, nullable, length >= max_iter): rho_m, m = 1..*iters, the fp64
  * norm ||G - A(U)|| over all examples and features, taken at the finest level's
  * C-points after the relaxation of iteration m (Algorithm 1, step 2).
@@ -185,7 +204,9 @@ int32_t lp_mgrit_forward(const lp_problem* prob, const lp_mgrit* mg, const void*
  * adjoint step of size cf^l h linearised at the injected fine state U[i cf^l].
  * res_hist, iters as for lp_mgrit_forward, on the adjoint residual.
  * dsig (nullable): the sigma' record of U; every level then reads sigma' of the
- * injected fine state from it. */
+ * injected fine state from it. With mg->storage = LP_STORE_CPOINTS, U is the
+ * C-point trajectory Uc [N/cf + 1][B][q] of lp_mgrit_forward (Lam stays
+ * [N+1][B][q]). */
 int32_t lp_mgrit_adjoint(const lp_problem* prob, const lp_mgrit* mg, const void* K,
                          const void* b, const void* U, const void* dsig, void* Lam, void* ws,
                          size_t ws_bytes, double* res_hist, int32_t* iters, void* stream);
@@ -204,6 +225,16 @@ int32_t lp_mgrit_adjoint(const lp_problem* prob, const lp_mgrit* mg, const void*
 int32_t lp_gradient(const lp_problem* prob, const void* K, const void* b, const void* U,
                     const void* dsig, const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes,
                     void* stream);
+
+/* lp_gradient from a C-point-only trajectory (LP_STORE_CPOINTS, Section 3.2
+ * remark): Uc [N/cf + 1][B][q] holds u^{k cf}; the states of every layer are
+ * recomputed by forward steps from the C-points (a block of at most 64
+ * intervals at a time, staged in the workspace) and the gradient is the one
+ * lp_gradient gives for the full trajectory, bit for bit. cf must be 4 and the
+ * problem an fp32 dense width 32 or 64 (else LP_EUNSUPPORTED). ws: at least
+ * lp_workspace_bytes(prob, mg) bytes for an mg with storage = LP_STORE_CPOINTS. */
+int32_t lp_gradient_cpoints(const lp_problem* prob, int32_t cf, const void* K, const void* b, const void* Uc,
+                            const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes, void* stream);
 
 /* Full-grid residual norm ||G - A(U)|| of the space-time system, the quantity
  * whose drop stops the MGRIT iteration (Algorithm 1, step 6; Section 3.1.1 for

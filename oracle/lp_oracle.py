@@ -204,6 +204,24 @@ def serial_adjoint(U, lamN, K, b, h, kind):
     return Lam
 
 
+def expand_cpoints(Uc, K, b, h, kind, cf):
+    """The trajectory implied by C-point storage (Section 3.2, remark on storing or
+    recomputing the primal states the adjoint depends on): row k of Uc is the state
+    at the C-point k*cf; each F-point is the forward step from the one before,
+    u^{kc+j} = Phi(u^{kc+j-1}, theta^{kc+j-1}), j = 1..cf-1 (the F-relaxation, eq.
+    Frelax, on the finest level). Returns U [N+1][...]."""
+    Uc, K, b = _f64(Uc, K, b)
+    N = K.shape[0]
+    U = np.empty((N + 1,) + Uc.shape[1:], dtype=_DT)
+    for k in range(N // cf):
+        U[k * cf] = Uc[k]
+        for j in range(1, cf):
+            n = k * cf + j
+            U[n] = phi(U[n - 1], K[n - 1], b[n - 1], h, kind)
+    U[N] = Uc[N // cf]
+    return U
+
+
 def gradient(U, Lam, K, b, h, kind):
     """Design equations for theta^n (Section 2.3, item 3) with R = 0:
     dJ/dK_n = sum_k (d_K Phi(u_k^n))^T lam_k^{n+1} = h sum_k (sigma'(z_k^n) * lam_k^{n+1}) u_k^n^T,

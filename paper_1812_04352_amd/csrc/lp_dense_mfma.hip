@@ -558,7 +558,7 @@ __attribute__((amdgpu_waves_per_eu(Q == 64 && REC ? (MODE == SWEEP_FRES ? 3 : 4)
       V u[NB];
 #pragma unroll
       for (int mb = 0; mb < NB; ++mb) u[mb] = 0.f;
-      if (on) Lt::load(u, Uf + (size_t)i * a.stride * slice + row);
+      if (on) Lt::load(u, Uf + (size_t)i * a.ustride * slice + row);
       Lt::template prod<C::LD>(d, u, W[j & 1], lane);
       apply<V, NB, NV>(d, a.act, true);
     }
@@ -745,13 +745,31 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
   const float hl = (float)a.hl, hc = (float)a.hc;
   const long kc = (long)k * IV_CF;
 
+  if (MODE == SWEEP_CORRF && !HASG && a.cpt) {
+    // C-point storage: the corrected C-points are the whole result (the F-points
+    // are not stored; the adjoint and the gradient recompute them from these)
+    if (on) {
+      V v[NB];
+      if (k > 0) {
+        correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+        Lt::store(X + (size_t)k * slice + row, v);
+      }
+      if (k == Nc - 1) {
+        correct<Lt>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
+        Lt::store(X + (size_t)Nc * slice + row, v);
+      }
+    }
+    return;
+  }
+
   WAll<Q, NL, WAVES> wr;
   wall_fetch<Q, NL, WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), kc, 1, a.stride);
   V v[NB], cn[NB], g[HASG ? NS : 1][NB];
   if (MODE == SWEEP_FC) {
-    // a pending coarse-grid correction of the previous cycle is applied on the fly
+    // a pending coarse-grid correction of the previous cycle is applied on the fly;
+    // with C-point storage C-point k is row k of the level-0 trajectory
     if (Vn) correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
-    else Lt::load(v, X + kc * slice + row);
+    else Lt::load(v, X + (a.cpt ? (long)k : kc) * slice + row);
   } else if (MODE == SWEEP_FRES) {
     Lt::load(v, Cs + (size_t)k * a.cs_stride * slice + row);
     Lt::load(cn, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
@@ -829,16 +847,22 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
 
 // REC: sigma' comes from the record (ReLU: RBYTES, one byte per value) instead of
 // the layer product at the primal state.
-template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG>
+// CPT (finest level, C-point storage): Uf holds the fine C-points only (row k is
+// u^{kc}); the interval first recomputes its F-point states and sigma'(z_n) for
+// n = kc .. kc + 3 by forward steps from its lower C-point, with the arithmetic of
+// the forward F-relaxation (so the results equal those of full storage bit for bit).
+template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG, bool CPT = false>
 __global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(Q == 32 && !HASG && REC && RBYTES ? 8 : 1, 8)))
 void k_adj_iv(SweepArgs a) {
+  static_assert(!(CPT && (REC || HASG)), "C-point storage is a finest-level mode without a record");
   constexpr int EX = 16;
   using C = Cfg<Q, WAVES>;
   using Lt = Lay<Q, EX>;
   using V = typename Lt::V;
   constexpr int NB = Lt::NB, NV = Lt::NV;
   constexpr int NS = MODE == SWEEP_CORRF ? IV_CF - 1 : IV_CF;
-  __shared__ float W[NS * C::WSZ];
+  constexpr int NW = CPT ? IV_CF : NS;  // layers staged: the recompute needs all of the interval's
+  __shared__ float W[NW * C::WSZ];
   __shared__ double red[WAVES];
   const int lane = threadIdx.x & 63;
   const int k = blockIdx.y;
@@ -855,8 +879,8 @@ void k_adj_iv(SweepArgs a) {
   const float hl = (float)a.hl, hc = (float)a.hc;
   const long top = (long)(k + 1) * IV_CF;
 
-  WAll<Q, NS, WAVES> wr;
-  wall_fetch<Q, NS, WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), top - 1, -1,
+  WAll<Q, NW, WAVES> wr;  // slot j holds layer top - 1 - j
+  wall_fetch<Q, NW, WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), top - 1, -1,
                            a.stride);
   V v[NB], cu[NB], ck[NB];
   if (MODE == SWEEP_FC) {
@@ -870,23 +894,43 @@ void k_adj_iv(SweepArgs a) {
   } else {
     correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
   }
-  // step j is linearised at fine index (top - 1 - j) * stride
+  // step j is linearised at fine index (top - 1 - j) * stride, the primal state of
+  // which is row (top - 1 - j) * ustride of Uf
   RecRow<Lt, RBYTES> rr[REC ? NS : 1];
-  V u[REC ? 1 : NS][NB];
+  V u[(REC || CPT) ? 1 : NS][NB];
   if constexpr (REC) {
 #pragma unroll
     for (int j = 0; j < NS; ++j) rr[j].load(a.dsig, (size_t)(top - 1 - j) * a.stride * slice + row);
+  } else if constexpr (CPT) {
+    Lt::load(u[0], Uf + (size_t)k * slice + row);  // u^{kc}
   } else {
 #pragma unroll
-    for (int j = 0; j < NS; ++j) Lt::load(u[j], Uf + (size_t)(top - 1 - j) * a.stride * slice + row);
+    for (int j = 0; j < NS; ++j) Lt::load(u[j], Uf + (size_t)(top - 1 - j) * a.ustride * slice + row);
   }
   V g[HASG ? NS : 1][NB];
   if constexpr (HASG) {
 #pragma unroll
     for (int j = 0; j < NS; ++j) Lt::load(g[j], G + (size_t)(top - 1 - j) * slice + row);
   }
-  wall_put<Q, NS, WAVES>(W, wr);
+  wall_put<Q, NW, WAVES>(W, wr);
   __syncthreads();
+  // C-point storage: dz[jf] = sigma'(z_{kc+jf}) along u^{kc+jf+1} = u^{kc+jf} + h sigma(z_{kc+jf})
+  V dz[CPT ? IV_CF : 1][NB];
+  if constexpr (CPT) {
+#pragma unroll
+    for (int jf = 0; jf < IV_CF; ++jf) {
+      V sz[NB];
+      Lt::template prod<C::LD>(sz, u[0], W + (IV_CF - 1 - jf) * C::WSZ, lane);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) dz[jf][mb] = sz[mb];
+      apply<V, NB, NV>(dz[jf], a.act, true);
+      if (jf + 1 < IV_CF) {
+        apply<V, NB, NV>(sz, a.act, false);
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) u[0][mb] = u[0][mb] + hl * sz[mb];
+      }
+    }
+  }
   if (MODE == SWEEP_FRES) {
 #pragma unroll
     for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb];
@@ -902,6 +946,9 @@ void k_adj_iv(SweepArgs a) {
     V d[NB], w[NB];
     if constexpr (REC) {
       rr[j].get(d);
+    } else if constexpr (CPT) {
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) d[mb] = dz[IV_CF - 1 - j][mb];
     } else {
       Lt::template prod<C::LD>(d, u[j], Wj, lane);
       apply<V, NB, NV>(d, a.act, true);
@@ -973,12 +1020,13 @@ __global__ __launch_bounds__(64 * GRAD_WAVES) void k_grad(GradArgs a) {
   __shared__ float tile[GRAD_WAVES][2][32 * TL];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int h = lane >> 5, li = lane & 31;
-  const int n = blockIdx.x, chunk = blockIdx.y;
+  const long n = a.n0 + blockIdx.x;  // layer; its state is row blockIdx.x of U
+  const int chunk = blockIdx.y;
   const int per = (((a.B + a.nchunks - 1) / a.nchunks) + 32 * GRAD_WAVES - 1) / (32 * GRAD_WAVES) *
                   (32 * GRAD_WAVES);
   const int e0 = chunk * per, e1 = min(a.B, e0 + per);
   const size_t slice = (size_t)a.B * Q;
-  const float* U = static_cast<const float*>(a.U) + (size_t)n * slice;
+  const float* U = static_cast<const float*>(a.U) + (size_t)blockIdx.x * slice;
   const float* L = static_cast<const float*>(a.Lam) + (size_t)(n + 1) * slice;
   {
     WRegs<Q, GRAD_WAVES> wr;
@@ -1079,18 +1127,69 @@ __global__ __launch_bounds__(256) void k_grad_final(GradArgs a, int nw, int nbia
   else static_cast<float*>(a.db)[n * nbias + (r - nw)] = v;
 }
 
+// First pass over `nl` layers starting at a.n0 (grid: layers x chunks).
 template <int Q>
-hipError_t grad(const GradArgs& a, hipStream_t st) {
+hipError_t grad_partials(const GradArgs& a, long nl, hipStream_t st) {
   // at width 32 the kernel is HBM-bound and a third row read per layer costs more
   // than the forward product it replaces
   constexpr bool REC_OK = Q >= 64;
-  if (REC_OK && a.dsig) launch(k_grad<Q, REC_OK>, dim3(a.N, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
-  else launch(k_grad<Q, false>, dim3(a.N, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  if (REC_OK && a.dsig) launch(k_grad<Q, REC_OK>, dim3((unsigned)nl, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
+  else launch(k_grad<Q, false>, dim3((unsigned)nl, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
+  return hipGetLastError();
+}
+
+template <int Q>
+hipError_t grad_finish(const GradArgs& a, hipStream_t st) {
   const size_t tot = (size_t)a.N * (Q * Q + Q);
   launch(k_grad_final, (unsigned)((tot + 255) / 256), 256, 0, st, a, Q * Q, Q);
   return hipGetLastError();
+}
+
+template <int Q>
+hipError_t grad(const GradArgs& a, hipStream_t st) {
+  hipError_t err = grad_partials<Q>(a, a.N, st);
+  if (err != hipSuccess) return err;
+  return grad_finish<Q>(a, st);
+}
+
+// C-point storage: the F-relaxation of interval k0 + blockIdx.y from its lower
+// C-point Uc[k0 + blockIdx.y], written to rows 4 blockIdx.y .. 4 blockIdx.y + 3 of Y
+// (the C-point, then its three F-points), with the arithmetic of the forward
+// sweeps' F-relaxation on the finest level (k_fwd_iv), so the states are those a
+// full-storage solve stores.
+template <int Q>
+__global__ __launch_bounds__(64 * 4) void k_expand(const float* __restrict__ K, const float* __restrict__ bias,
+                                                   const float* __restrict__ Uc, float* __restrict__ Y, int B,
+                                                   long k0, float hl, int act) {
+  constexpr int WAVES = 4, EX = 16, NL = IV_CF - 1;
+  using C = Cfg<Q, WAVES>;
+  using Lt = Lay<Q, EX>;
+  using V = typename Lt::V;
+  constexpr int NB = Lt::NB, NV = Lt::NV;
+  __shared__ float W[NL * C::WSZ];
+  const int lane = threadIdx.x & 63;
+  const long k = k0 + blockIdx.y, kc = k * IV_CF;
+  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * EX + (lane % EX);
+  const bool on = e < B;
+  const size_t slice = (size_t)B * Q;
+  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane / EX);
+  float* Yk = Y + (size_t)blockIdx.y * IV_CF * slice;
+  WAll<Q, NL, WAVES> wr;
+  wall_fetch<Q, NL, WAVES>(wr, K, bias, kc, 1, 1);
+  V v[NB];
+  Lt::load(v, Uc + (size_t)k * slice + row);
+  wall_put<Q, NL, WAVES>(W, wr);
+  __syncthreads();
+  if (on) Lt::store(Yk + row, v);
+#pragma unroll
+  for (int j = 0; j < NL; ++j) {
+    V s[NB];
+    Lt::template prod<C::LD>(s, v, W + j * C::WSZ, lane);
+    apply<V, NB, NV>(s, act, false);
+#pragma unroll
+    for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * s[mb];
+    if (on) Lt::store(Yk + (size_t)(j + 1) * slice + row, v);
+  }
 }
 
 // ------------------------------------------------------------------ serial solves
@@ -1178,8 +1277,8 @@ __global__ __launch_bounds__(64) void k_ser_fwd(SweepArgs a) {
 }
 
 // Adjoint: Lam[i] = Lam[i+1] + h_l K_i^T (sigma'(K_i U_f[i] + b_i) * Lam[i+1]) (+ G[i]),
-// i = N_l - 1 .. 0, the primal state (or the record, RK = 1 bytes, 2 fp32) at
-// fine index i * stride.
+// i = N_l - 1 .. 0, the primal state (row i * ustride of Uf, or the record at fine
+// index i * stride, RK = 1 bytes, 2 fp32).
 template <int Q, int RK>
 __global__ __launch_bounds__(64) void k_ser_adj(SweepArgs a) {
   using C = Cfg<Q, 1>;
@@ -1216,7 +1315,7 @@ __global__ __launch_bounds__(64) void k_ser_adj(SweepArgs a) {
       const int i = max(Nl - 1 - u, 0);  // every lane reads a valid row
       w_fetch<Q, 1>(wr[u], K, bb, (size_t)max(i - 1, 0) * a.stride);
       if constexpr (REC) rr[u].load(a.dsig, (size_t)i * a.stride * slice + row);
-      else Lt::load(ur[u], Uf + (size_t)i * a.stride * slice + row);
+      else Lt::load(ur[u], Uf + (size_t)i * a.ustride * slice + row);
       if (G) Lt::load(gr[u], G + (size_t)i * slice + row);
     }
     w_put<Q, 1>(W[0], w0);
@@ -1241,7 +1340,7 @@ __global__ __launch_bounds__(64) void k_ser_adj(SweepArgs a) {
       } else {
         Lt::template prod<C::LD>(d, ur[u], Wj, lane);
         apply<V, NB, NV>(d, a.act, true);
-        Lt::load(ur[u], Uf + (size_t)ip * a.stride * slice + row);
+        Lt::load(ur[u], Uf + (size_t)ip * a.ustride * slice + row);
       }
 #pragma unroll
       for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * v[mb];
@@ -1283,7 +1382,8 @@ void sweep_iv(int dir, const SweepArgs& a, dim3 grid, hipStream_t st) {
   }
 #define LP_ADJ_IV(MODE)                                                                                    \
   do {                                                                                                     \
-    if (!rec) launch(k_adj_iv<Q, MODE, W4, false, false, HASG>, grid, 64 * W4, 0, st, a);                  \
+    if (!HASG && a.cpt) launch(k_adj_iv<Q, MODE, W4, false, false, false, true>, grid, 64 * W4, 0, st, a); \
+    else if (!rec) launch(k_adj_iv<Q, MODE, W4, false, false, HASG>, grid, 64 * W4, 0, st, a);             \
     else if (bytes) launch(k_adj_iv<Q, MODE, W4, true, true, HASG>, grid, 64 * W4, 0, st, a);              \
     else launch(k_adj_iv<Q, MODE, W4, true, false, HASG>, grid, 64 * W4, 0, st, a);                        \
   } while (0)
@@ -1315,8 +1415,11 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   // sweep, whose per-step kernel with the record requested a step ahead was
   // measured faster (56.3 against 60.9 ms per step on the deep workload; the
   // other modes gain 1-6 %).
+  // C-point storage (a.cpt, finest level) has interval-resident kernels only.
   if constexpr (Q == 32 || Q == 64) {
-    if (a.c == IV_CF && iv_enabled() && !(Q == 64 && dir == DIR_ADJ && a.mode == SWEEP_FRES)) {
+    if (a.cpt && a.c != IV_CF) return hipErrorNotSupported;
+    if (a.c == IV_CF &&
+        (a.cpt || (iv_enabled() && !(Q == 64 && dir == DIR_ADJ && a.mode == SWEEP_FRES)))) {
       if (a.G) sweep_iv<Q, true>(dir, a, grid, st);
       else sweep_iv<Q, false>(dir, a, grid, st);
       return hipGetLastError();
@@ -1357,6 +1460,7 @@ hipError_t serial(int dir, const SerialArgs& s, hipStream_t st) {
   a.X = s.X;
   a.G = s.G;
   a.dsig = s.dsig;
+  a.ustride = s.ustride;
   const dim3 grid((s.B + 15) / 16, 1);
   if (dir == DIR_FWD) {
     if (s.dsig) launch(k_ser_fwd<Q, true>, grid, 64, 0, st, a);
@@ -1388,6 +1492,33 @@ hipError_t mfma_serial(int q, int dir, const SerialArgs& a, hipStream_t st) {
 hipError_t mfma_grad(int q, const GradArgs& a, hipStream_t st) {
   if (q == 32) return mfma::grad<32>(a, st);
   if (q == 64) return mfma::grad<64>(a, st);
+  return hipErrorNotSupported;
+}
+
+hipError_t mfma_expand(int q, int act, const void* K, const void* b, const void* Uc, void* Y, int B, long k0,
+                       long nk, double h, hipStream_t st) {
+  if (nk <= 0 || B <= 0) return hipSuccess;
+  if (nk > 65535) return hipErrorNotSupported;
+  const dim3 grid((unsigned)((B + 63) / 64), (unsigned)nk);
+  const float* Kp = static_cast<const float*>(K);
+  const float* bp = static_cast<const float*>(b);
+  const float* up = static_cast<const float*>(Uc);
+  float* yp = static_cast<float*>(Y);
+  if (q == 32) launch(mfma::k_expand<32>, grid, 256, 0, st, Kp, bp, up, yp, B, k0, (float)h, act);
+  else if (q == 64) launch(mfma::k_expand<64>, grid, 256, 0, st, Kp, bp, up, yp, B, k0, (float)h, act);
+  else return hipErrorNotSupported;
+  return hipGetLastError();
+}
+
+hipError_t mfma_grad_partials(int q, const GradArgs& a, long nl, hipStream_t st) {
+  if (q == 32) return mfma::grad_partials<32>(a, nl, st);
+  if (q == 64) return mfma::grad_partials<64>(a, nl, st);
+  return hipErrorNotSupported;
+}
+
+hipError_t mfma_grad_finish(int q, const GradArgs& a, hipStream_t st) {
+  if (q == 32) return mfma::grad_finish<32>(a, st);
+  if (q == 64) return mfma::grad_finish<64>(a, st);
   return hipErrorNotSupported;
 }
 

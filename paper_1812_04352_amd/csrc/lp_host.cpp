@@ -147,6 +147,7 @@ int check_mgrit(const lp_problem* p, const lp_mgrit* m, std::vector<int>& sizes)
   if (m->relax != LP_RELAX_F && m->relax != LP_RELAX_FCF && m->relax != LP_RELAX_FCFCF)
     return fail(LP_EINVAL, "bad relax %d", m->relax);
   if (m->cycle != LP_CYCLE_V && m->cycle != LP_CYCLE_F) return fail(LP_EINVAL, "bad cycle %d", m->cycle);
+  if (m->storage != LP_STORE_ALL && m->storage != LP_STORE_CPOINTS) return fail(LP_EINVAL, "bad storage %d", m->storage);
   if (m->max_iter < 1) return fail(LP_EINVAL, "max_iter %d < 1", m->max_iter);
   if (!(m->rtol >= 0.0) || !(m->stag >= 0.0)) return fail(LP_EINVAL, "rtol and stag must be >= 0");
   sizes.assign(1, p->N);
@@ -155,6 +156,11 @@ int check_mgrit(const lp_problem* p, const lp_mgrit* m, std::vector<int>& sizes)
       return fail(LP_EINVAL, "level %d has N_l = %d, not divisible by cf = %d", (int)sizes.size() - 1,
                   sizes.back(), m->cf);
     sizes.push_back(sizes.back() / m->cf);
+  }
+  if (m->storage == LP_STORE_CPOINTS) {
+    if (!lp::cpoints_supported(shape_of(p)) || m->cf != 4)
+      return fail(LP_EUNSUPPORTED, "C-point storage needs an fp32 dense width 32 or 64 and cf = 4");
+    if (sizes.size() < 2) return fail(LP_EINVAL, "C-point storage needs at least two levels");
   }
   return LP_OK;
 }
@@ -220,6 +226,14 @@ size_t grad_bytes(const lp_problem* p) {
   return up((size_t)p->N * nch * lp::grad_partial_floats(s) * esize(p));
 }
 
+// lp_gradient_cpoints: the gradient partials, then the states of one block of at
+// most kExpandIntervals coarse intervals recomputed from their C-points.
+constexpr long kExpandIntervals = 64;
+long expand_block(const lp_problem* p, int cf) { return std::min<long>(p->N / cf, kExpandIntervals); }
+size_t grad_cpoints_bytes(const lp_problem* p, int cf) {
+  return grad_bytes(p) + up((size_t)expand_block(p, cf) * cf * slice_bytes(p));
+}
+
 size_t resid_bytes(const lp_problem* p) {
   return up((size_t)partial_capacity(p) * sizeof(double)) + up(sizeof(double));
 }
@@ -243,6 +257,7 @@ struct Solver {
   const void* Uf;  // fine primal trajectory (adjoint)
   void* dsig = nullptr;  // sigma' record (written by the forward's final level-0 F-relaxation, read by the adjoint)
   std::vector<int> sizes;
+  bool cpt = false;  // C-point storage: the finest trajectory (forward X[0], adjoint Uf) holds C-points only
   std::vector<void*> X, G, S, S2;
   void* S0[2] = {nullptr, nullptr};  // finest-level staging buffers (FCF, FCFCF), used alternately
   int cur0 = 0;
@@ -257,6 +272,10 @@ struct Solver {
     return s;
   }
 
+  // row step of the adjoint's primal trajectory per level-l point (the C-point
+  // trajectory holds fine index n at row n / cf; level l >= 1 points are C-points)
+  long ustride(int l) const { return cpt ? stride(l) / m->cf : stride(l); }
+
   // One cycle on level l (Algorithm 1 with step 3 recursive): cyc is LP_CYCLE_V or
   // LP_CYCLE_F (coarse problem solved by an F-cycle and then a V-cycle, the latter
   // left out above the coarsest level, whose solve is exact).
@@ -266,7 +285,7 @@ struct Solver {
     const int kb = dir == lp::DIR_FWD ? LP_TRACE_FWD_FC : LP_TRACE_ADJ_FC;  // first kind of this direction
     if (l == L - 1) {
       lp::SerialArgs a{p->act, K, b, Uf, p->B, sizes[l], stride(l), hl, X[l], G[l],
-                       dir == lp::DIR_ADJ || l == 0 ? dsig : nullptr};
+                       dir == lp::DIR_ADJ || l == 0 ? dsig : nullptr, ustride(l)};
       TraceScope ts(kb + 3, l, st);
       LP_TRY(lp::launch_serial(sh, dir, a, st), "coarsest-level solve");
       return LP_OK;
@@ -281,6 +300,8 @@ struct Solver {
     a.Nl = sizes[l];
     a.c = m->cf;
     a.stride = stride(l);
+    a.ustride = ustride(l);
+    a.cpt = cpt && l == 0;
     a.hl = hl;
     a.hc = hl * (double)m->cf;
     a.X = X[l];
@@ -323,7 +344,8 @@ struct Solver {
     }
     a.V = nullptr;
     a.Cs = fcf ? Sl : X[l];
-    a.cs_stride = fcf ? 1 : m->cf;
+    // C-points of the level trajectory: every cf-th row (row k with C-point storage)
+    a.cs_stride = fcf || (a.cpt && dir == lp::DIR_FWD) ? 1 : m->cf;
     a.Xn = X[l + 1];
     a.Gn = G[l + 1];
     a.xn_every = (l + 1 < L - 1) ? m->cf : 0;
@@ -369,6 +391,8 @@ struct Solver {
     a.Nl = sizes[0];
     a.c = m->cf;
     a.stride = 1;
+    a.ustride = ustride(0);
+    a.cpt = cpt;
     a.hl = p->h;
     a.hc = p->h * (double)m->cf;
     a.X = X[0];
@@ -412,7 +436,8 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
   s.K = K;
   s.b = b;
   s.Uf = U;
-  s.dsig = lp::dsig_supported(shape_of(p)) ? dsig : nullptr;
+  s.cpt = m->storage == LP_STORE_CPOINTS;
+  s.dsig = lp::dsig_supported(shape_of(p)) && !s.cpt ? dsig : nullptr;
   s.sizes = sizes;
   s.X.assign(L, nullptr);
   s.G.assign(L, nullptr);
@@ -439,7 +464,8 @@ int mgrit_solve(const lp_problem* p, const lp_mgrit* m, int dir, const void* K, 
 
   if (!m->warm_start && L > 1) {
     // cold start: every C-point is a copy of the fixed boundary row
-    if (dir == lp::DIR_FWD) LP_TRY(lp::launch_copy_rows(Xuser, sl, 0, c, c, Nc, st), "cold start");
+    if (dir == lp::DIR_FWD && s.cpt) LP_TRY(lp::launch_copy_rows(Xuser, sl, 0, 1, 1, Nc, st), "cold start");
+    else if (dir == lp::DIR_FWD) LP_TRY(lp::launch_copy_rows(Xuser, sl, 0, c, c, Nc, st), "cold start");
     else LP_TRY(lp::launch_copy_rows(Xuser, sl, p->N, 0, c, Nc, st), "cold start");
   }
   const bool early = m->rtol > 0.0 || m->stag > 0.0;
@@ -523,6 +549,9 @@ bool use_mfma(const Shape& s) {
   return !(e && strcmp(e, "valu") == 0);
 }
 
+// C-point storage: the matrix-core kernels of widths 32 and 64 recompute F-point states
+bool cpoints_supported(const Shape& s) { return use_mfma(s); }
+
 // fp32 dense layers too wide for the per-thread and whole-layer-in-LDS kernels
 bool use_wide(const Shape& s) { return s.layer == 0 && s.dtype == 0 && wide_width_supported(s.C); }
 
@@ -586,6 +615,7 @@ size_t lp_workspace_bytes(const lp_problem* p, const lp_mgrit* m) {
     std::vector<int> sizes;
     if (check_mgrit(p, m, sizes) != LP_OK) return 0;
     need = std::max(need, mgrit_layout(p, m, sizes).total);
+    if (m->storage == LP_STORE_CPOINTS) need = std::max(need, grad_cpoints_bytes(p, m->cf));
   }
   g_err.clear();
   return need;
@@ -611,7 +641,7 @@ int32_t lp_serial_forward(const lp_problem* p, const void* K, const void* b, voi
   if (rc) return rc;
   if (!K || !b || (p->B && !U)) return fail(LP_EINVAL, "NULL array argument");
   if (p->B == 0) return LP_OK;
-  lp::SerialArgs a{p->act, K, b, nullptr, p->B, p->N, 1, p->h, U, nullptr, dsig_for(p, dsig)};
+  lp::SerialArgs a{p->act, K, b, nullptr, p->B, p->N, 1, p->h, U, nullptr, dsig_for(p, dsig), 1};
   TraceScope ts(LP_TRACE_SERIAL, 0, static_cast<hipStream_t>(stream));
   LP_TRY(lp::launch_serial(shape_of(p), lp::DIR_FWD, a, static_cast<hipStream_t>(stream)), "serial forward");
   return LP_OK;
@@ -624,7 +654,7 @@ int32_t lp_serial_adjoint(const lp_problem* p, const void* K, const void* b, con
   if (!K || !b || (p->B && (!U || !Lam))) return fail(LP_EINVAL, "NULL array argument");
   if (p->B && U == Lam) return fail(LP_EINVAL, "U and Lam alias");
   if (p->B == 0) return LP_OK;
-  lp::SerialArgs a{p->act, K, b, U, p->B, p->N, 1, p->h, Lam, nullptr, dsig_for(p, dsig)};
+  lp::SerialArgs a{p->act, K, b, U, p->B, p->N, 1, p->h, Lam, nullptr, dsig_for(p, dsig), 1};
   TraceScope ts(LP_TRACE_SERIAL, 1, static_cast<hipStream_t>(stream));
   LP_TRY(lp::launch_serial(shape_of(p), lp::DIR_ADJ, a, static_cast<hipStream_t>(stream)), "serial adjoint");
   return LP_OK;
@@ -658,7 +688,7 @@ int32_t lp_gradient(const lp_problem* p, const void* K, const void* b, const voi
   rc = check_ws(ws, ws_bytes, grad_bytes(p));
   if (rc) return rc;
   lp::GradArgs a{p->act, K, b, U, Lam, p->B, p->N, p->h, ws, lp::grad_chunks(s, p->B, p->N), dK, db,
-                 dsig_for(p, dsig)};
+                 dsig_for(p, dsig), 0};
   TraceScope ts(LP_TRACE_GRADIENT, 0, st);
   LP_TRY(lp::launch_grad(s, a, st), "gradient");
   return LP_OK;
@@ -696,6 +726,37 @@ int residual_norm_in(const lp_problem* p, int32_t which, const void* K, const vo
 }
 
 }  // namespace
+
+int32_t lp_gradient_cpoints(const lp_problem* p, int32_t cf, const void* K, const void* b, const void* Uc,
+                            const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_problem(p);
+  if (rc) return rc;
+  const lp::Shape s = shape_of(p);
+  if (!lp::cpoints_supported(s) || cf != 4)
+    return fail(LP_EUNSUPPORTED, "C-point storage needs an fp32 dense width 32 or 64 and cf = 4");
+  if (p->N % cf) return fail(LP_EINVAL, "N = %d is not divisible by cf = %d", p->N, cf);
+  if (!K || !b || !dK || !db || (p->B && (!Uc || !Lam))) return fail(LP_EINVAL, "NULL array argument");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (p->B == 0) {
+    LP_TRY(lp::launch_zero(dK, (size_t)p->N * p->C * p->C * esize(p), st), "zero gradient");
+    LP_TRY(lp::launch_zero(db, (size_t)p->N * p->C * esize(p), st), "zero gradient");
+    return LP_OK;
+  }
+  rc = check_ws(ws, ws_bytes, grad_cpoints_bytes(p, cf));
+  if (rc) return rc;
+  void* Y = static_cast<char*>(ws) + grad_bytes(p);  // states of one block of intervals
+  const long Nc = p->N / cf, blk = expand_block(p, cf);
+  lp::GradArgs a{p->act, K, b, Y, Lam, p->B, p->N, p->h, ws, lp::grad_chunks(s, p->B, p->N), dK, db, nullptr, 0};
+  TraceScope ts(LP_TRACE_GRADIENT, 0, st);
+  for (long k0 = 0; k0 < Nc; k0 += blk) {
+    const long nk = std::min(blk, Nc - k0);
+    LP_TRY(lp::mfma_expand(p->C, p->act, K, b, Uc, Y, p->B, k0, nk, p->h, st), "gradient: recompute states");
+    a.n0 = k0 * cf;
+    LP_TRY(lp::mfma_grad_partials(p->C, a, nk * cf, st), "gradient");
+  }
+  LP_TRY(lp::mfma_grad_finish(p->C, a, st), "gradient");
+  return LP_OK;
+}
 
 int32_t lp_residual_norm(const lp_problem* p, int32_t which, const void* K, const void* b, const void* U,
                          const void* Lam, void* ws, size_t ws_bytes, double* norm, void* stream) {

@@ -64,6 +64,11 @@ struct SweepArgs {
   int finest;          // 1 on level 0: the fixed boundary row (u^0 or lam^N) is never written
   void* dsig;          // sigma' record (nullable; dense [N][B][q], conv per-(layer, example) tile blocks): forward level-0 CORRF writes it
                        // (every layer of its intervals), the adjoint reads it at i*stride
+  long ustride;        // adjoint: the primal state of level point i is Uf row i*ustride (stride, or
+                       // stride / c when Uf holds the fine C-points only)
+  int cpt;             // level 0 with C-point storage: forward, X holds C-point k at row k (F-points are
+                       // not stored); adjoint, Uf holds the C-points and each interval recomputes its
+                       // F-point states (and sigma') by forward steps from its lower C-point
 };
 
 // Serial (coarsest level or layer-serial) solve of X over Nl steps.
@@ -79,6 +84,7 @@ struct SerialArgs {
   void* X;
   const void* G;       // nullable
   void* dsig;          // sigma' record (nullable): written by a level-0 forward solve, read by the adjoint
+  long ustride;        // adjoint: primal state of level point i at Uf row i*ustride
 };
 
 struct ResidArgs {
@@ -107,6 +113,8 @@ struct GradArgs {
   void* dK;
   void* db;
   const void* dsig;    // sigma' record of U (nullable)
+  long n0;             // first layer of this launch: grid x runs over layers n0 .. n0 + gridDim.x - 1,
+                       // U row j is layer n0 + j (Lam, K, b, dsig and the partials use absolute indices)
 };
 
 struct Shape {
@@ -125,6 +133,7 @@ hipError_t launch_resid(const Shape& s, int dir, const ResidArgs& a, hipStream_t
 hipError_t launch_grad(const Shape& s, const GradArgs& a, hipStream_t st);
 int grad_chunks(const Shape& s, int B, int N);  // batch chunks of the gradient's first pass
 bool dsig_supported(const Shape& s);            // kernels that write and read the sigma' record
+bool cpoints_supported(const Shape& s);         // kernels with C-point storage (recomputed F-point states)
 int grad_nout(const Shape& s);            // weights + bias entries per layer
 int grad_partial_floats(const Shape& s);  // values per (layer, chunk) gradient partial
 bool shape_supported(const Shape& s);
@@ -146,6 +155,14 @@ hipError_t mfma_sweep(int q, int dir, const SweepArgs& a, hipStream_t st, int* p
 hipError_t mfma_serial(int q, int dir, const SerialArgs& a, hipStream_t st);
 hipError_t mfma_grad(int q, const GradArgs& a, hipStream_t st);
 int dense_grad_chunks(int B, int N);
+// C-point storage (c = 4): forward F-relaxation of intervals k0 .. k0 + nk - 1 from the
+// C-points Uc[k] (row k), writing fine layers 4 k0 .. 4 (k0 + nk) - 1 to rows 0 .. 4 nk - 1
+// of Y, with the arithmetic of the sweeps (the F-point states a full-storage solve stores)
+hipError_t mfma_expand(int q, int act, const void* K, const void* b, const void* Uc, void* Y, int B, long k0,
+                       long nk, double h, hipStream_t st);
+// the first pass of the gradient only (GradArgs.n0 selects the layers), and its second pass
+hipError_t mfma_grad_partials(int q, const GradArgs& a, long nl, hipStream_t st);
+hipError_t mfma_grad_finish(int q, const GradArgs& a, hipStream_t st);
 
 // Dense fp32 matrix-core family for wide layers (lp_dense_wide.hip), width 220:
 // the layer weights stream through LDS in panels

@@ -17,7 +17,7 @@ from typing import Optional, Sequence, Tuple
 # compare kernel variants under the same tests)
 LIB_PATH = os.environ.get("LP_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblp.so")
 
-LP_ABI_VERSION = 3
+LP_ABI_VERSION = 4
 LP_OK, LP_EINVAL, LP_EUNSUPPORTED, LP_EWORKSPACE, LP_EHIP, LP_ENONFINITE = range(6)
 LP_F32, LP_F64 = 0, 1
 LP_DENSE, LP_CONV3X3 = 0, 1
@@ -26,6 +26,7 @@ LP_RELAX_F, LP_RELAX_FCF, LP_RELAX_FCFCF = 0, 1, 2
 LP_CYCLE_V, LP_CYCLE_F = 0, 1
 LP_STATE, LP_ADJOINT = 0, 1
 LP_OPEN_IDENTITY, LP_OPEN_DENSE_ACT, LP_OPEN_CONV_ACT = 0, 1, 2
+LP_STORE_ALL, LP_STORE_CPOINTS = 0, 1
 
 ACT = {"tanh": LP_TANH, "relu": LP_RELU, "smoothrelu": LP_SMOOTHRELU, "identity": LP_IDENTITY}
 LAYER = {"dense": LP_DENSE, "conv3x3": LP_CONV3X3}
@@ -37,7 +38,7 @@ OPENING = {"identity": LP_OPEN_IDENTITY, "dense_act": LP_OPEN_DENSE_ACT, "conv_a
 EXPORTS = (
     "lp_abi_version", "lp_status_string", "lp_last_error", "lp_workspace_bytes",
     "lp_dsig_bytes", "lp_serial_forward", "lp_serial_adjoint", "lp_mgrit_forward", "lp_mgrit_adjoint",
-    "lp_gradient", "lp_residual_norm", "lp_residual_norm_noalloc", "lp_check_finite", "lp_open_forward", "lp_open_grad",
+    "lp_gradient", "lp_gradient_cpoints", "lp_residual_norm", "lp_residual_norm_noalloc", "lp_check_finite", "lp_open_forward", "lp_open_grad",
     "lp_loss_terminal", "lp_sgd_update", "lp_vec_axpby", "lp_vec_dot", "lp_accuracy",
     "lp_trace_enable", "lp_trace_read",
 )
@@ -57,7 +58,8 @@ class LpProblem(ctypes.Structure):
 class LpMgrit(ctypes.Structure):
     _fields_ = [("cf", ctypes.c_int32), ("max_levels", ctypes.c_int32), ("min_coarse", ctypes.c_int32),
                 ("relax", ctypes.c_int32), ("max_iter", ctypes.c_int32), ("warm_start", ctypes.c_int32),
-                ("rtol", ctypes.c_double), ("stag", ctypes.c_double), ("cycle", ctypes.c_int32)]
+                ("rtol", ctypes.c_double), ("stag", ctypes.c_double), ("cycle", ctypes.c_int32),
+                ("storage", ctypes.c_int32)]
 
 
 class LpError(RuntimeError):
@@ -87,6 +89,7 @@ _SIGS = {
     "lp_mgrit_forward": ([_P, _M, _v, _v, _v, _v, _v, _sz, _dp, _ip, _v], _i32),
     "lp_mgrit_adjoint": ([_P, _M, _v, _v, _v, _v, _v, _v, _sz, _dp, _ip, _v], _i32),
     "lp_gradient": ([_P, _v, _v, _v, _v, _v, _v, _v, _v, _sz, _v], _i32),
+    "lp_gradient_cpoints": ([_P, _i32, _v, _v, _v, _v, _v, _v, _v, _sz, _v], _i32),
     "lp_residual_norm": ([_P, _i32, _v, _v, _v, _v, _v, _sz, _dp, _v], _i32),
     "lp_residual_norm_noalloc": ([_P, _i32, _v, _v, _v, _v, _dp, _v], _i32),
     "lp_check_finite": ([_v], _i32),
@@ -132,9 +135,19 @@ def problem(dtype: str, layer: str, act: str, N: int, B: int, C: int, H: int = 1
 
 
 def mgrit(cf: int = 4, max_levels: int = 2, min_coarse: int = 1, relax: str = "FCF", max_iter: int = 1,
-          warm_start: bool = False, rtol: float = 0.0, stag: float = 0.0, cycle: str = "V") -> LpMgrit:
+          warm_start: bool = False, rtol: float = 0.0, stag: float = 0.0, cycle: str = "V",
+          storage: str = "all") -> LpMgrit:
+    """storage: "all" (every layer of U stored) or "cpoints" (U holds the fine C-points only)."""
     return LpMgrit(cf, max_levels, min_coarse, RELAX[relax], max_iter, int(bool(warm_start)), rtol, stag,
-                   CYCLE[cycle])
+                   CYCLE[cycle], {"all": LP_STORE_ALL, "cpoints": LP_STORE_CPOINTS}[storage])
+
+
+def traj_rows(p: "LpProblem", mg: Optional[LpMgrit] = None) -> int:
+    """Rows of the primal trajectory U under the schedule's storage: N + 1, or
+    N / cf + 1 C-points."""
+    if mg is not None and mg.storage == LP_STORE_CPOINTS:
+        return p.N // mg.cf + 1
+    return p.N + 1
 
 
 # ---------------------------------------------------------------- tensor marshalling
@@ -238,7 +251,7 @@ def lp_mgrit_forward(p: LpProblem, mg: LpMgrit, K, b, U, ws, history: bool = Tru
     it = ctypes.c_int32(0)
     wp, wn = _ws(ws, 1)
     _check(load().lp_mgrit_forward(ctypes.byref(p), ctypes.byref(mg), Kp, bp,
-                                   _arr(U, (p.N + 1) * p.B * p.q, "U", _elem_dtype(p)), _dsig(p, dsig), wp, wn,
+                                   _arr(U, traj_rows(p, mg) * p.B * p.q, "U", _elem_dtype(p)), _dsig(p, dsig), wp, wn,
                                    hist, ctypes.byref(it), _stream()), "lp_mgrit_forward")
     return it.value, list(hist[:it.value]) if history else []
 
@@ -251,7 +264,8 @@ def lp_mgrit_adjoint(p: LpProblem, mg: LpMgrit, K, b, U, Lam, ws, history: bool 
     hist = (ctypes.c_double * max(1, mg.max_iter))() if history else None
     it = ctypes.c_int32(0)
     wp, wn = _ws(ws, 1)
-    _check(load().lp_mgrit_adjoint(ctypes.byref(p), ctypes.byref(mg), Kp, bp, _arr(U, n, "U", _elem_dtype(p)),
+    _check(load().lp_mgrit_adjoint(ctypes.byref(p), ctypes.byref(mg), Kp, bp,
+                                   _arr(U, traj_rows(p, mg) * p.B * p.q, "U", _elem_dtype(p)),
                                    _dsig(p, dsig), _arr(Lam, n, "Lam", _elem_dtype(p)), wp, wn, hist,
                                    ctypes.byref(it), _stream()), "lp_mgrit_adjoint")
     return it.value, list(hist[:it.value]) if history else []
@@ -264,6 +278,17 @@ def lp_gradient(p: LpProblem, K, b, U, Lam, dK, db, ws, dsig=None) -> None:
     wp, wn = _ws(ws, 1)
     _check(load().lp_gradient(ctypes.byref(p), Kp, bp, _arr(U, n, "U", _elem_dtype(p)), _dsig(p, dsig),
                               _arr(Lam, n, "Lam", _elem_dtype(p)), dKp, dbp, wp, wn, _stream()), "lp_gradient")
+
+
+def lp_gradient_cpoints(p: LpProblem, cf: int, K, b, Uc, Lam, dK, db, ws) -> None:
+    """lp_gradient from the C-point trajectory Uc [N/cf + 1][B][q]."""
+    Kp, bp = _weights(p, K, b)
+    dKp, dbp = _weights(p, dK, db)
+    wp, wn = _ws(ws, 1)
+    _check(load().lp_gradient_cpoints(ctypes.byref(p), cf, Kp, bp,
+                                      _arr(Uc, (p.N // cf + 1) * p.B * p.q, "Uc", _elem_dtype(p)),
+                                      _arr(Lam, (p.N + 1) * p.B * p.q, "Lam", _elem_dtype(p)), dKp, dbp, wp, wn,
+                                      _stream()), "lp_gradient_cpoints")
 
 
 def lp_residual_norm(p: LpProblem, which: int, K, b, U, Lam, ws) -> float:

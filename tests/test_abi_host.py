@@ -222,3 +222,35 @@ def test_residual_norm_noalloc_limits():
                                         None) == L.LP_EINVAL
     assert lib.lp_residual_norm_noalloc(ctypes.byref(p), L.LP_STATE, FAKE, FAKE, FAKE, None, None,
                                         None) == L.LP_EINVAL
+
+
+def test_cpoint_storage_validation():
+    """C-point storage is accepted for the fp32 matrix-core widths with cf = 4 and
+    two or more levels, refused (LP_EUNSUPPORTED) elsewhere; its workspace also
+    covers the gradient's recompute block."""
+    lib = L.load()
+    hist = (ctypes.c_double * 4)()
+    it = ctypes.c_int32(0)
+
+    def fwd(p, mg):
+        return lib.lp_mgrit_forward(ctypes.byref(p), ctypes.byref(mg), FAKE, FAKE, FAKE, None, None, 0, hist,
+                                    ctypes.byref(it), None)
+
+    p = L.problem("f32", "dense", "tanh", 2048, 16384, 64, h=1 / 256)
+    mg = L.mgrit(cf=4, max_levels=5, min_coarse=8, max_iter=2, storage="cpoints")
+    full = L.lp_workspace_bytes(p, L.mgrit(cf=4, max_levels=5, min_coarse=8, max_iter=2))
+    need = L.lp_workspace_bytes(p, mg)
+    assert need >= 64 * 4 * 16384 * 64 * 4 and need >= full
+    assert fwd(p, mg) == L.LP_EWORKSPACE  # valid schedule: only the (absent) workspace is refused
+    assert fwd(p, L.mgrit(cf=2, max_levels=5, max_iter=2, storage="cpoints")) == L.LP_EUNSUPPORTED
+    assert fwd(p, L.mgrit(cf=4, max_levels=1, max_iter=2, storage="cpoints")) == L.LP_EINVAL
+    for q in (_p(C=8), _p(dtype="f64")):
+        assert fwd(q, L.mgrit(cf=4, max_levels=2, max_iter=2, storage="cpoints")) == L.LP_EUNSUPPORTED
+    bad = L.mgrit(cf=4, max_levels=2, max_iter=2)
+    bad.storage = 2
+    assert fwd(p, bad) == L.LP_EINVAL
+    out = ctypes.c_void_p(0x3000)
+    assert lib.lp_gradient_cpoints(ctypes.byref(p), 2, FAKE, FAKE, FAKE, FAKE, out, out, FAKE, 1 << 40,
+                                   None) == L.LP_EUNSUPPORTED
+    assert lib.lp_gradient_cpoints(ctypes.byref(p), 4, FAKE, FAKE, FAKE, FAKE, out, out, FAKE, 1024,
+                                   None) == L.LP_EWORKSPACE

@@ -115,3 +115,18 @@ def test_cpu_baseline_legs():
     r = bench.cpu_baseline(WORKLOADS[2].with_overrides(N=16, B=64), budget_s=0.2)
     assert r["value"] > 0 and r["layer_serial"]["value"] > 0 and r["cores"] >= 1
     assert "full batch" in r["sample"] and "f32" in r["sample"]
+
+
+def test_kernel_model_cpoint_storage():
+    """With C-point storage the finest adjoint sweeps read one primal row per
+    interval instead of c, and the final finest forward correction moves three rows
+    per interval with no products."""
+    from workloads import WORKLOADS
+    wl = WORKLOADS[3].with_overrides(N=64, B=256, max_levels=2)
+    full = bench.kernel_model(wl, "adj_fc", 1, 1)
+    cpt = bench.kernel_model(wl, "adj_fc", 1, 1, cpt=True)
+    row = wl.B * wl.q * 4
+    assert full[2] == cpt[2] and full[1] == cpt[1]
+    assert full[0] - cpt[0] == (wl.N // wl.cf) * (wl.cf - 1) * row
+    b, f, n = bench.kernel_model(wl, "fwd_corrf", 1, 1, cpt=True)
+    assert (b, f, n) == ((wl.N // wl.cf) * 3 * row, 0, 1)

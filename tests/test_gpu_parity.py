@@ -785,3 +785,64 @@ def test_loss_head_class_counts(q, nc, B):
     assert_close(lamN.cpu().numpy(), lamNr, "f32", "lamN")
     assert_close(dW.cpu().numpy(), dWr, "f32", "dW")
     assert_close(dmu.cpu().numpy(), dmur, "f32", "dmu")
+
+
+CPT_CASES = [DENSE[1], DENSE[2], DENSE[3], ("tanh64_l3", WORKLOADS[3].with_overrides(N=64, B=77, max_levels=3))]
+
+
+@pytest.mark.parametrize("name,wl", CPT_CASES, ids=[n for n, _ in CPT_CASES])
+@pytest.mark.parametrize("relax", ["F", "FCF"])
+def test_cpoint_storage(name, wl, relax):
+    """C-point storage (Section 3.2 remark: states stored or recomputed). The
+    forward keeps the C-points only, the adjoint and the gradient recompute the
+    F-point states by forward steps from them. The C-points, the adjoint iterate,
+    the residual histories and the gradient must equal those of full storage bit
+    for bit (the recompute repeats the forward F-relaxation's arithmetic), and the
+    adjoint and gradient match the oracle run on the oracle's expansion of its own
+    C-points."""
+    c = case(wl)
+    cf = wl.cf
+    mgA = sched(wl, 2, relax=relax)
+    mgC = L.mgrit(cf=cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=relax, max_iter=2,
+                  storage="cpoints")
+    ws = L.alloc_workspace(c.p, mgC)
+    U = c.new_traj()
+    _, hA = L.lp_mgrit_forward(c.p, mgA, c.K, c.b, U, ws)
+    Uc = torch.zeros((wl.N // cf + 1,) + tuple(U.shape[1:]), device="cuda", dtype=U.dtype)
+    Uc[0] = c.u0
+    _, hC = L.lp_mgrit_forward(c.p, mgC, c.K, c.b, Uc, ws)
+    assert hA == hC
+    assert torch.equal(Uc, U[::cf].contiguous())
+    lamN = _lamN(c, U)[0]
+    LA = torch.zeros_like(U)
+    LA[-1] = lamN
+    LC = LA.clone()
+    _, gA = L.lp_mgrit_adjoint(c.p, mgA, c.K, c.b, U, LA, ws)
+    _, gC = L.lp_mgrit_adjoint(c.p, mgC, c.K, c.b, Uc, LC, ws)
+    assert gA == gC
+    assert torch.equal(LA, LC)
+    dKA, dbA = torch.empty_like(c.K), torch.empty_like(c.b)
+    L.lp_gradient(c.p, c.K, c.b, U, LA, dKA, dbA, ws)
+    dKC, dbC = torch.empty_like(c.K), torch.empty_like(c.b)
+    L.lp_gradient_cpoints(c.p, cf, c.K, c.b, Uc, LC, dKC, dbC, ws)
+    assert torch.equal(dKA, dKC) and torch.equal(dbA, dbC)
+    # oracle: C-points of its own MGRIT iterate, expanded, then the adjoint and gradient
+    Ur, _, _ = O.mgrit_forward(c.ref_traj(), c.d["K"], c.d["b"], wl.h, wl.act, cf=cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=relax, max_iter=2)
+    assert_close(Uc.cpu().numpy(), Ur[::cf], wl.dtype, "C-points")
+    Ue = O.expand_cpoints(Ur[::cf], c.d["K"], c.d["b"], wl.h, wl.act, cf)
+    Lr = np.zeros_like(Ue)
+    Lr[-1] = O.loss_terminal(Ue[-1], c.d["W"], c.d["mu"], c.d["onehot"])[1]
+    Lr, _, _ = O.mgrit_adjoint(Ue, Lr, c.d["K"], c.d["b"], wl.h, wl.act, cf=cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=relax, max_iter=2)
+    assert_close(LC.cpu().numpy(), Lr, wl.dtype, "Lam from C-points")
+    dKr, dbr = O.gradient(Ue, Lr, c.d["K"], c.d["b"], wl.h, wl.act)
+    if wl.act != "relu":
+        assert_close(dKC.cpu().numpy(), dKr, wl.dtype, "dK from C-points")
+        assert_close(dbC.cpu().numpy(), dbr, wl.dtype, "db from C-points")
+    # warm start from the stored C-points: one more iteration, same on both sides
+    mgA.warm_start = mgC.warm_start = 1
+    mgA.max_iter = mgC.max_iter = 1
+    L.lp_mgrit_forward(c.p, mgA, c.K, c.b, U, ws)
+    L.lp_mgrit_forward(c.p, mgC, c.K, c.b, Uc, ws)
+    assert torch.equal(Uc, U[::cf].contiguous())

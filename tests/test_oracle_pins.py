@@ -804,3 +804,23 @@ def test_working_precision_changes_only_the_rounding():
     assert np.linalg.norm(M32 - M64) <= 1e-5 * np.linalg.norm(M64)
     assert abs(h32[-1] - h64[-1]) <= 1e-4 * h64[-1]
     assert O.serial_forward(u0, d["K"], d["b"], wl.h, wl.act).dtype == np.float64
+
+
+def test_expand_cpoints_reproduces_stored_trajectories():
+    """C-point storage keeps u^{kc} only; the F-points follow by forward steps. From
+    the C-points of the serial solution this is the serial solution (the state
+    equations, Section 2.3), and from those of an MGRIT iterate it is that iterate,
+    whose last sweep is an F-relaxation (Algorithm 1, step 5)."""
+    from workloads import WORKLOADS, generate
+    for wl in (WORKLOADS[1], WORKLOADS[2].with_overrides(N=32, B=20)):
+        d = generate(wl)
+        u0 = O.open_forward(d["y"], d["L_in"], wl.act, wl.opening)
+        S = O.serial_forward(u0, d["K"], d["b"], wl.h, wl.act)
+        E = O.expand_cpoints(S[::wl.cf], d["K"], d["b"], wl.h, wl.act, wl.cf)
+        assert np.array_equal(E, S)
+        U0 = np.concatenate([u0[None], np.zeros((wl.N,) + u0.shape)])
+        M, _, _ = O.mgrit_forward(U0, d["K"], d["b"], wl.h, wl.act, cf=wl.cf, max_levels=2, max_iter=1)
+        E = O.expand_cpoints(M[::wl.cf], d["K"], d["b"], wl.h, wl.act, wl.cf)
+        assert np.max(np.abs(E - M)) <= 1e-15 * np.max(np.abs(M))
+        # a non-converged iterate: its F-points are not the serial ones
+        assert np.max(np.abs(M - S)) > 1e-8
