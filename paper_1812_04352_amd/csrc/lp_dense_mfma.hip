@@ -18,6 +18,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include "lp_device.h"
 #include "lp_internal.h"
 
@@ -218,42 +220,96 @@ struct Lay<Q, 16> {
     }
   }
 
-  // z = K_n v + b_n: A operand of slice (ib, r) in lane l is K[16ob + l%16][16ib + 4(l/16) + r]
-  template <int LD>
+  // z = K_n v + b_n: A operand of slice (ib, r) in lane l is K[16ob + l%16][16ib + 4(l/16) + r].
+  // At width 64 (DB) the A operands (and bias) of output block ob + 1 are read
+  // from LDS while block ob's products run, so the products do not wait on LDS
+  // latency; the extra registers are what DB = false saves.
+  template <int LD, bool DB = true>
   __device__ static void prod(V (&z)[NB], const V (&v)[NB], const float* W, int lane) {
     const int g = lane >> 4, i = lane & 15;
+    if constexpr (NB < 4 || !DB) {
+      // width 32: two blocks, few registers to spare (up to eight waves per SIMD)
 #pragma unroll
-    for (int ob = 0; ob < NB; ++ob) {
-      z[ob] = *reinterpret_cast<const f32x4*>(W + Q * LD + 16 * ob + 4 * g);
+      for (int ob = 0; ob < NB; ++ob) {
+        z[ob] = *reinterpret_cast<const f32x4*>(W + Q * LD + 16 * ob + 4 * g);
+        const float* rowp = W + (16 * ob + i) * LD + 4 * g;
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib) {
+          const f32x4 a4 = *reinterpret_cast<const f32x4*>(rowp + 16 * ib);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) z[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[r], v[ib][r], z[ob], 0, 0, 0);
+        }
+      }
+      return;
+    }
+    f32x4 A[2][NB], bz[2];
+    auto rd = [&](int buf, int ob) {
+      bz[buf] = *reinterpret_cast<const f32x4*>(W + Q * LD + 16 * ob + 4 * g);
       const float* rowp = W + (16 * ob + i) * LD + 4 * g;
 #pragma unroll
-      for (int ib = 0; ib < NB; ++ib) {
-        const f32x4 a4 = *reinterpret_cast<const f32x4*>(rowp + 16 * ib);
+      for (int ib = 0; ib < NB; ++ib) A[buf][ib] = *reinterpret_cast<const f32x4*>(rowp + 16 * ib);
+    };
+    rd(0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NB + 1, 0);  // block 0's LDS reads
 #pragma unroll
-        for (int r = 0; r < 4; ++r) z[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[r], v[ib][r], z[ob], 0, 0, 0);
-      }
+    for (int ob = 0; ob < NB; ++ob) {
+      const int cb = ob & 1;
+      if (ob + 1 < NB) rd(cb ^ 1, ob + 1);
+      z[ob] = bz[cb];
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) z[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[cb][ib][r], v[ib][r], z[ob], 0, 0, 0);
+      if (ob + 1 < NB) __builtin_amdgcn_sched_group_barrier(0x100, NB + 1, 0);  // next block's LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);                 // then this block's products
     }
   }
 
   // w = K_n^T s: A operand of slice (ib, r) in lane l is K[16ib + 4(l/16) + r][16ob + l%16]
-  template <int LD>
+  // (column reads of the staged K_n), double-buffered across output blocks as in prod.
+  template <int LD, bool DB = true>
   __device__ static void prod_t(V (&w)[NB], const V (&s)[NB], const float* W, int lane) {
     const int g = lane >> 4, i = lane & 15;
+    if constexpr (NB < 4 || !DB) {
+#pragma unroll
+      for (int ob = 0; ob < NB; ++ob) {
+        w[ob] = 0.f;
+        const float* colp = W + 16 * ob + i + 4 * g * LD;
+        float a[NB][4];
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) a[ib][r] = colp[(16 * ib + r) * LD];
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) w[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ib][r], s[ib][r], w[ob], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 4 * NB, 0);  // LDS reads
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);  // then the products
+      }
+      return;
+    }
+    float A[2][NB][4];
+    auto rd = [&](int buf, int ob) {
+      const float* colp = W + 16 * ob + i + 4 * g * LD;
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) A[buf][ib][r] = colp[(16 * ib + r) * LD];
+    };
+    rd(0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4 * NB, 0);  // block 0's LDS reads
 #pragma unroll
     for (int ob = 0; ob < NB; ++ob) {
+      const int cb = ob & 1;
+      if (ob + 1 < NB) rd(cb ^ 1, ob + 1);
       w[ob] = 0.f;
-      const float* colp = W + 16 * ob + i + 4 * g * LD;
-      float a[NB][4];
 #pragma unroll
       for (int ib = 0; ib < NB; ++ib)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) a[ib][r] = colp[(16 * ib + r) * LD];
-#pragma unroll
-      for (int ib = 0; ib < NB; ++ib)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) w[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ib][r], s[ib][r], w[ob], 0, 0, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 4 * NB, 0);  // LDS reads
-      __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);  // then the products
+        for (int r = 0; r < 4; ++r) w[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[cb][ib][r], s[ib][r], w[ob], 0, 0, 0);
+      if (ob + 1 < NB) __builtin_amdgcn_sched_group_barrier(0x100, 4 * NB, 0);  // next block's LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);                 // then this block's products
     }
   }
 };
@@ -717,9 +773,33 @@ struct RecRow<Lt, false> {
   }
 };
 
+// The interval kernels can walk batch tiles: workgroup (g, k) stages the weights
+// of interval k once and runs tiles g, g + gridDim.x, ... of 64 examples (tile
+// mode TM = 1), so the weights are read from L2 once per workgroup instead of once
+// per tile; with TM = 2 the rows of its next tile are requested before the current
+// tile's steps (the index is clamped, so every load is issued unconditionally and
+// the waits stay exact) and a tile's loads overlap the previous tile's products.
+// TM = 0 is one tile per workgroup.
+__device__ __forceinline__ size_t iv_row(int t, int waves, int ex, int B, int Q, bool& on) {
+  const int lane = threadIdx.x & 63;
+  const int e = (t * waves + (threadIdx.x >> 6)) * ex + (lane % ex);
+  on = e < B;
+  return (size_t)(on ? e : 0) * Q + 4 * (lane / ex);
+}
+
+// Rows of one tile for a forward interval sweep: two state rows (FC: the C-point,
+// or the staged C-point and the coarse value of a pending correction; FRES: the
+// lower and the upper C-point; CORRF: the C-point and its coarse value) and the
+// level's right-hand-side rows.
+template <typename Lt, int NS, bool HASG>
+struct FwdRows {
+  typename Lt::V a[Lt::NB], c[Lt::NB];
+  typename Lt::V g[HASG ? NS : 1][Lt::NB];
+};
+
 // REC: the final F-relaxation writes the sigma' record (CORRF only).
 // HASG: the level has right-hand-side rows (every level but the finest).
-template <int Q, int MODE, int WAVES, bool REC, bool HASG>
+template <int Q, int MODE, int WAVES, bool REC, bool HASG, int TM, bool CORR>
 __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
   constexpr int EX = 16;
   using C = Cfg<Q, WAVES>;
@@ -729,15 +809,14 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
   constexpr bool rec = REC && MODE == SWEEP_CORRF;
   constexpr int NS = MODE == SWEEP_CORRF ? IV_CF - 1 : IV_CF;
   constexpr int NL = NS + (rec ? 1 : 0);
+  using Rows = FwdRows<Lt, NS, HASG>;
   __shared__ float W[NL * C::WSZ];
   __shared__ double red[WAVES];
   const int lane = threadIdx.x & 63;
   const int k = blockIdx.y;
   const int Nc = gridDim.y;
-  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * EX + (lane % EX);
-  const bool on = e < a.B;
+  const int ntiles = (a.B + EX * WAVES - 1) / (EX * WAVES);
   const size_t slice = (size_t)a.B * Q;
-  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane / EX);
   float* X = static_cast<float*>(a.X);
   const float* G = static_cast<const float*>(a.G);
   const float* Cs = static_cast<const float*>(a.Cs);
@@ -748,102 +827,167 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
   if (MODE == SWEEP_CORRF && !HASG && a.cpt) {
     // C-point storage: the corrected C-points are the whole result (the F-points
     // are not stored; the adjoint and the gradient recompute them from these)
-    if (on) {
-      V v[NB];
-      if (k > 0) {
-        correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
-        Lt::store(X + (size_t)k * slice + row, v);
-      }
-      if (k == Nc - 1) {
-        correct<Lt>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
-        Lt::store(X + (size_t)Nc * slice + row, v);
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+      bool on;
+      const size_t row = iv_row(t, WAVES, EX, a.B, Q, on);
+      if (on) {
+        V v[NB];
+        if (k > 0) {
+          correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
+          Lt::store(X + (size_t)k * slice + row, v);
+        }
+        if (k == Nc - 1) {
+          correct<Lt>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
+          Lt::store(X + (size_t)Nc * slice + row, v);
+        }
       }
     }
     return;
   }
 
+  // FC with CORR (a.V set) reads its C-points as C + (V - C): a pending coarse-grid
+  // correction of the previous cycle applied on the fly, or (the second FC sweep of
+  // FCFCF) staged C-points read as C + (C - C); with C-point storage C-point k is
+  // row k of the level-0 trajectory
+  constexpr bool pair = MODE != SWEEP_FC || CORR;
+  auto load_rows = [&](Rows& r, size_t row) {
+    if (MODE == SWEEP_FC && !pair) {
+      Lt::load(r.a, X + (a.cpt ? (long)k : kc) * slice + row);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) r.c[mb] = 0.f;  // unused; initialised so the rows stay in registers
+    } else {
+      Lt::load(r.a, Cs + (size_t)k * a.cs_stride * slice + row);
+      if (MODE == SWEEP_FRES) Lt::load(r.c, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
+      else Lt::load(r.c, Vn + (size_t)k * slice + row);
+    }
+    if constexpr (HASG) {
+#pragma unroll
+      for (int j = 0; j < NS; ++j) Lt::load(r.g[j], G + (kc + j + 1) * slice + row);
+    }
+  };
+
   WAll<Q, NL, WAVES> wr;
   wall_fetch<Q, NL, WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), kc, 1, a.stride);
-  V v[NB], cn[NB], g[HASG ? NS : 1][NB];
-  if (MODE == SWEEP_FC) {
-    // a pending coarse-grid correction of the previous cycle is applied on the fly;
-    // with C-point storage C-point k is row k of the level-0 trajectory
-    if (Vn) correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
-    else Lt::load(v, X + (a.cpt ? (long)k : kc) * slice + row);
-  } else if (MODE == SWEEP_FRES) {
-    Lt::load(v, Cs + (size_t)k * a.cs_stride * slice + row);
-    Lt::load(cn, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
-  } else {
-    correct<Lt>(v, Cs + (size_t)k * a.cs_stride * slice + row, Vn + (size_t)k * slice + row);
-  }
-  if constexpr (HASG) {
-#pragma unroll
-    for (int j = 0; j < NS; ++j) Lt::load(g[j], G + (kc + j + 1) * slice + row);
+  Rows cur;
+  {
+    bool on0;
+    load_rows(cur, iv_row(blockIdx.x, WAVES, EX, a.B, Q, on0));
   }
   wall_put<Q, NL, WAVES>(W, wr);
   __syncthreads();
-  if (on) {
-    if (MODE == SWEEP_FC && k == 0) Lt::store(static_cast<float*>(a.S) + row, v);
-    if (MODE == SWEEP_CORRF && k > 0) Lt::store(X + kc * slice + row, v);
-  }
 
-  V coarse[NB];
+  double acc = 0.0;
+  // the work of one tile t, reading the staged weights through Wt
+  auto tile = [&](Rows& cur, int t, const float* Wt) {
+    bool on;
+    const size_t row = iv_row(t, WAVES, EX, a.B, Q, on);
+    V v[NB];
+    if (MODE == SWEEP_FC && !pair) {
 #pragma unroll
-  for (int j = 0; j < NS; ++j) {
-    V s[NB];
-    Lt::template prod<C::LD>(s, v, W + j * C::WSZ, lane);
-    if constexpr (rec) {
-      V dz[NB];
+      for (int mb = 0; mb < NB; ++mb) v[mb] = cur.a[mb];
+    } else if (MODE == SWEEP_FRES) {
 #pragma unroll
-      for (int mb = 0; mb < NB; ++mb) dz[mb] = s[mb];
-      apply<V, NB, NV>(dz, a.act, true);
-      if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + j) * a.stride * slice + row, a.act, dz);
+      for (int mb = 0; mb < NB; ++mb) v[mb] = cur.a[mb];
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) v[mb] = cur.a[mb] + (cur.c[mb] - cur.a[mb]);  // C + (V - C)
     }
-    apply<V, NB, NV>(s, a.act, false);
-    if (MODE == SWEEP_FRES && j == 0) {
-#pragma unroll
-      for (int mb = 0; mb < NB; ++mb) coarse[mb] = v[mb] + hc * s[mb];
-    }
-#pragma unroll
-    for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * s[mb];
-    if constexpr (HASG) add_to<V, NB>(v, g[j]);
-    if (MODE == SWEEP_CORRF && on) Lt::store(X + (kc + j + 1) * slice + row, v);
-  }
-
-  if constexpr (rec) {
-    // sigma' of the layer before the next C-point, from the last F-point
-    V z[NB];
-    Lt::template prod<C::LD>(z, v, W + NS * C::WSZ, lane);
-    apply<V, NB, NV>(z, a.act, true);
-    if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + NS) * a.stride * slice + row, a.act, z);
-  }
-  if (MODE == SWEEP_FC) {
-    if (on) Lt::store(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
-  } else if (MODE == SWEEP_FRES) {
-    double acc = 0.0;
     if (on) {
-      acc = sq_diff<V, NB, NV>(v, cn);
+      if (MODE == SWEEP_FC && k == 0) Lt::store(static_cast<float*>(a.S) + row, v);
+      if (MODE == SWEEP_CORRF && k > 0) Lt::store(X + kc * slice + row, v);
+    }
+
+    V coarse[NB];
 #pragma unroll
-      for (int mb = 0; mb < NB; ++mb) coarse[mb] = v[mb] - coarse[mb];  // g_{l+1}^{k+1}
-      Lt::store(static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + row, coarse);
-      if (a.xn_every > 0 && (k + 1) % a.xn_every == 0)
-        Lt::store(static_cast<float*>(a.Xn) + (size_t)(k + 1) * slice + row, cn);
-      if (k == 0) {
-        Lt::load(cn, Cs + row);
-        Lt::store(static_cast<float*>(a.Xn) + row, cn);
+    for (int j = 0; j < NS; ++j) {
+      V s[NB];
+      Lt::template prod<C::LD>(s, v, Wt + j * C::WSZ, lane);
+      if constexpr (rec) {
+        V dz[NB];
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) dz[mb] = s[mb];
+        apply<V, NB, NV>(dz, a.act, true);
+        if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + j) * a.stride * slice + row, a.act, dz);
+      }
+      apply<V, NB, NV>(s, a.act, false);
+      if (MODE == SWEEP_FRES && j == 0) {
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) coarse[mb] = v[mb] + hc * s[mb];
+      }
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * s[mb];
+      if constexpr (HASG) add_to<V, NB>(v, cur.g[j]);
+      if (MODE == SWEEP_CORRF && on) Lt::store(X + (kc + j + 1) * slice + row, v);
+    }
+
+    if constexpr (rec) {
+      // sigma' of the layer before the next C-point, from the last F-point
+      V z[NB];
+      Lt::template prod<C::LD>(z, v, Wt + NS * C::WSZ, lane);
+      apply<V, NB, NV>(z, a.act, true);
+      if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + NS) * a.stride * slice + row, a.act, z);
+    }
+    if (MODE == SWEEP_FC) {
+      if (on) Lt::store(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
+    } else if (MODE == SWEEP_FRES) {
+      if (on) {
+        acc += sq_diff<V, NB, NV>(v, cur.c);
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) coarse[mb] = v[mb] - coarse[mb];  // g_{l+1}^{k+1}
+        Lt::store(static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + row, coarse);
+        if (a.xn_every > 0 && (k + 1) % a.xn_every == 0)
+          Lt::store(static_cast<float*>(a.Xn) + (size_t)(k + 1) * slice + row, cur.c);
+        if (k == 0) {
+          V c0[NB];
+          Lt::load(c0, Cs + row);
+          Lt::store(static_cast<float*>(a.Xn) + row, c0);
+        }
+      }
+    } else if (MODE == SWEEP_CORRF) {
+      if (on && k == Nc - 1) {
+        correct<Lt>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
+        Lt::store(X + (size_t)a.Nl * slice + row, v);
       }
     }
-    if (a.partial) {
-      const double s = wg_sum<WAVES>(acc, red);
-      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
-    }
-  } else if (MODE == SWEEP_CORRF) {
-    if (on && k == Nc - 1) {
-      correct<Lt>(v, Cs + (size_t)Nc * a.cs_stride * slice + row, Vn + (size_t)Nc * slice + row);
-      Lt::store(X + (size_t)a.Nl * slice + row, v);
+  };
+  if constexpr (TM == 0) {
+    tile(cur, blockIdx.x, W);
+  } else {
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+      // the products read the staged weights from LDS in every tile: an offset
+      // the compiler cannot see through keeps it from hoisting those reads out of
+      // the loop into registers
+      int woff = 0;
+      asm volatile("" : "+v"(woff));
+      Rows nxt;
+      if constexpr (TM == 2) {
+        bool on1;
+        load_rows(nxt, iv_row(min(t + (int)gridDim.x, ntiles - 1), WAVES, EX, a.B, Q, on1));
+      } else if (t != (int)blockIdx.x) {
+        bool on1;
+        load_rows(cur, iv_row(t, WAVES, EX, a.B, Q, on1));
+      }
+      tile(cur, t, W + woff);
+      if constexpr (TM == 2) cur = nxt;
     }
   }
+  if (MODE == SWEEP_FRES && a.partial) {
+    const double s = wg_sum<WAVES>(acc, red);
+    if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
+  }
 }
+
+// Rows of one tile for an adjoint interval sweep: the two state rows (the upper
+// C-point, or the staged C-point and coarse value of a correction; FRES: the upper
+// and the lower C-point), what each step is linearised at (record rows, primal
+// rows, or the lower primal C-point), and the right-hand-side rows.
+template <typename Lt, int NS, bool REC, bool RBYTES, bool CPT, bool HASG>
+struct AdjRows {
+  typename Lt::V a[Lt::NB], c[Lt::NB];
+  RecRow<Lt, RBYTES> rr[REC ? NS : 1];
+  typename Lt::V u[(REC || CPT) ? 1 : NS][Lt::NB];
+  typename Lt::V g[HASG ? NS : 1][Lt::NB];
+};
 
 // REC: sigma' comes from the record (ReLU: RBYTES, one byte per value) instead of
 // the layer product at the primal state.
@@ -851,8 +995,10 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
 // u^{kc}); the interval first recomputes its F-point states and sigma'(z_n) for
 // n = kc .. kc + 3 by forward steps from its lower C-point, with the arithmetic of
 // the forward F-relaxation (so the results equal those of full storage bit for bit).
-template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG, bool CPT = false>
-__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(Q == 32 && !HASG && REC && RBYTES ? 8 : 1, 8)))
+// TM: tiles per workgroup (0: one; 1: several; 2: several, each one's rows
+// requested during the previous one's steps). CORR: FC reads C + (V - C).
+template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG, bool CPT, int TM, bool CORR>
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(Q == 32 && !HASG && REC && RBYTES && TM == 0 ? 8 : 1, 8)))
 void k_adj_iv(SweepArgs a) {
   static_assert(!(CPT && (REC || HASG)), "C-point storage is a finest-level mode without a record");
   constexpr int EX = 16;
@@ -862,15 +1008,17 @@ void k_adj_iv(SweepArgs a) {
   constexpr int NB = Lt::NB, NV = Lt::NV;
   constexpr int NS = MODE == SWEEP_CORRF ? IV_CF - 1 : IV_CF;
   constexpr int NW = CPT ? IV_CF : NS;  // layers staged: the recompute needs all of the interval's
+  // at eight waves per SIMD (width 32, finest level, byte record, no prefetch) the
+  // registers go to occupancy, and FRES reads its lower C-point after the steps
+  constexpr bool LATE_CK = MODE == SWEEP_FRES && Q == 32 && !HASG && REC && RBYTES && TM == 0;
+  using Rows = AdjRows<Lt, NS, REC, RBYTES, CPT, HASG>;
   __shared__ float W[NW * C::WSZ];
   __shared__ double red[WAVES];
   const int lane = threadIdx.x & 63;
   const int k = blockIdx.y;
   const int Nc = gridDim.y;
-  const int e = (blockIdx.x * WAVES + (threadIdx.x >> 6)) * EX + (lane % EX);
-  const bool on = e < a.B;
+  const int ntiles = (a.B + EX * WAVES - 1) / (EX * WAVES);
   const size_t slice = (size_t)a.B * Q;
-  const size_t row = (size_t)(on ? e : 0) * Q + 4 * (lane / EX);
   const float* Uf = static_cast<const float*>(a.Uf);
   float* X = static_cast<float*>(a.X);
   const float* G = static_cast<const float*>(a.G);
@@ -879,124 +1027,165 @@ void k_adj_iv(SweepArgs a) {
   const float hl = (float)a.hl, hc = (float)a.hc;
   const long top = (long)(k + 1) * IV_CF;
 
+  // step j is linearised at fine index (top - 1 - j) * stride, the primal state of
+  // which is row (top - 1 - j) * ustride of Uf
+  constexpr bool pair = MODE != SWEEP_FC || CORR;  // FC reading C + (V - C), as in k_fwd_iv
+  auto load_rows = [&](Rows& r, size_t row) {
+    if (MODE == SWEEP_FC && !pair) {
+      Lt::load(r.a, X + top * slice + row);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) r.c[mb] = 0.f;  // unused; initialised so the rows stay in registers
+    } else {
+      Lt::load(r.a, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
+      if (MODE == SWEEP_FRES) {
+        if (!LATE_CK) Lt::load(r.c, Cs + (size_t)k * a.cs_stride * slice + row);
+      } else {
+        Lt::load(r.c, Vn + (size_t)(k + 1) * slice + row);
+      }
+    }
+    if constexpr (REC) {
+#pragma unroll
+      for (int j = 0; j < NS; ++j) r.rr[j].load(a.dsig, (size_t)(top - 1 - j) * a.stride * slice + row);
+    } else if constexpr (CPT) {
+      Lt::load(r.u[0], Uf + (size_t)k * slice + row);  // u^{kc}
+    } else {
+#pragma unroll
+      for (int j = 0; j < NS; ++j) Lt::load(r.u[j], Uf + (size_t)(top - 1 - j) * a.ustride * slice + row);
+    }
+    if constexpr (HASG) {
+#pragma unroll
+      for (int j = 0; j < NS; ++j) Lt::load(r.g[j], G + (size_t)(top - 1 - j) * slice + row);
+    }
+  };
+
   WAll<Q, NW, WAVES> wr;  // slot j holds layer top - 1 - j
   wall_fetch<Q, NW, WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), top - 1, -1,
                            a.stride);
-  V v[NB], cu[NB], ck[NB];
-  if (MODE == SWEEP_FC) {
-    if (Vn) correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
-    else Lt::load(v, X + top * slice + row);
-  } else if (MODE == SWEEP_FRES) {
-    Lt::load(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row);
-    // at eight waves per SIMD (finest level, byte record) the registers go to
-    // occupancy, and the lower C-point is read after the steps
-    if (!(Q == 32 && !HASG && REC && RBYTES)) Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
-  } else {
-    correct<Lt>(v, Cs + (size_t)(k + 1) * a.cs_stride * slice + row, Vn + (size_t)(k + 1) * slice + row);
-  }
-  // step j is linearised at fine index (top - 1 - j) * stride, the primal state of
-  // which is row (top - 1 - j) * ustride of Uf
-  RecRow<Lt, RBYTES> rr[REC ? NS : 1];
-  V u[(REC || CPT) ? 1 : NS][NB];
-  if constexpr (REC) {
-#pragma unroll
-    for (int j = 0; j < NS; ++j) rr[j].load(a.dsig, (size_t)(top - 1 - j) * a.stride * slice + row);
-  } else if constexpr (CPT) {
-    Lt::load(u[0], Uf + (size_t)k * slice + row);  // u^{kc}
-  } else {
-#pragma unroll
-    for (int j = 0; j < NS; ++j) Lt::load(u[j], Uf + (size_t)(top - 1 - j) * a.ustride * slice + row);
-  }
-  V g[HASG ? NS : 1][NB];
-  if constexpr (HASG) {
-#pragma unroll
-    for (int j = 0; j < NS; ++j) Lt::load(g[j], G + (size_t)(top - 1 - j) * slice + row);
+  Rows cur;
+  {
+    bool on0;
+    load_rows(cur, iv_row(blockIdx.x, WAVES, EX, a.B, Q, on0));
   }
   wall_put<Q, NW, WAVES>(W, wr);
   __syncthreads();
-  // C-point storage: dz[jf] = sigma'(z_{kc+jf}) along u^{kc+jf+1} = u^{kc+jf} + h sigma(z_{kc+jf})
-  V dz[CPT ? IV_CF : 1][NB];
-  if constexpr (CPT) {
+
+  double acc = 0.0;
+  // the work of one tile t, reading the staged weights through Wt
+  auto tile = [&](Rows& cur, int t, const float* Wt) {
+    bool on;
+    const size_t row = iv_row(t, WAVES, EX, a.B, Q, on);
+    // C-point storage: dz[jf] = sigma'(z_{kc+jf}) along u^{kc+jf+1} = u^{kc+jf} + h sigma(z_{kc+jf})
+    V dz[CPT ? IV_CF : 1][NB];
+    if constexpr (CPT) {
 #pragma unroll
-    for (int jf = 0; jf < IV_CF; ++jf) {
-      V sz[NB];
-      Lt::template prod<C::LD>(sz, u[0], W + (IV_CF - 1 - jf) * C::WSZ, lane);
+      for (int jf = 0; jf < IV_CF; ++jf) {
+        V sz[NB];
+        Lt::template prod<C::LD, !HASG>(sz, cur.u[0], Wt + (IV_CF - 1 - jf) * C::WSZ, lane);
 #pragma unroll
-      for (int mb = 0; mb < NB; ++mb) dz[jf][mb] = sz[mb];
-      apply<V, NB, NV>(dz[jf], a.act, true);
-      if (jf + 1 < IV_CF) {
-        apply<V, NB, NV>(sz, a.act, false);
+        for (int mb = 0; mb < NB; ++mb) dz[jf][mb] = sz[mb];
+        apply<V, NB, NV>(dz[jf], a.act, true);
+        if (jf + 1 < IV_CF) {
+          apply<V, NB, NV>(sz, a.act, false);
 #pragma unroll
-        for (int mb = 0; mb < NB; ++mb) u[0][mb] = u[0][mb] + hl * sz[mb];
+          for (int mb = 0; mb < NB; ++mb) cur.u[0][mb] = cur.u[0][mb] + hl * sz[mb];
+        }
       }
     }
-  }
-  if (MODE == SWEEP_FRES) {
+    V v[NB], cu[NB];
+    if (MODE == SWEEP_FC && !pair) {
 #pragma unroll
-    for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb];
-  }
-  if (on) {
-    if (MODE == SWEEP_FC && k == Nc - 1) Lt::store(static_cast<float*>(a.S) + (size_t)Nc * slice + row, v);
-    if (MODE == SWEEP_CORRF && k + 1 < Nc) Lt::store(X + top * slice + row, v);
-  }
-
+      for (int mb = 0; mb < NB; ++mb) v[mb] = cur.a[mb];
+    } else if (MODE == SWEEP_FRES) {
 #pragma unroll
-  for (int j = 0; j < NS; ++j) {
-    const float* Wj = W + j * C::WSZ;
-    V d[NB], w[NB];
-    if constexpr (REC) {
-      rr[j].get(d);
-    } else if constexpr (CPT) {
-#pragma unroll
-      for (int mb = 0; mb < NB; ++mb) d[mb] = dz[IV_CF - 1 - j][mb];
+      for (int mb = 0; mb < NB; ++mb) v[mb] = cu[mb] = cur.a[mb];
     } else {
-      Lt::template prod<C::LD>(d, u[j], Wj, lane);
-      apply<V, NB, NV>(d, a.act, true);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) v[mb] = cur.a[mb] + (cur.c[mb] - cur.a[mb]);  // C + (V - C)
     }
-    if (MODE == SWEEP_FRES && j == NS - 1) {
-      // coarse adjoint step from the upper C-point, linearised at the same fine state
-      V s2[NB];
-#pragma unroll
-      for (int mb = 0; mb < NB; ++mb) s2[mb] = d[mb] * cu[mb];
-      Lt::template prod_t<C::LD>(w, s2, Wj, lane);
-#pragma unroll
-      for (int mb = 0; mb < NB; ++mb) cu[mb] = cu[mb] + hc * w[mb];
-    }
-#pragma unroll
-    for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * v[mb];
-    Lt::template prod_t<C::LD>(w, d, Wj, lane);
-#pragma unroll
-    for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * w[mb];
-    if constexpr (HASG) add_to<V, NB>(v, g[j]);
-    if (MODE == SWEEP_CORRF && on) Lt::store(X + (size_t)(top - 1 - j) * slice + row, v);
-  }
-
-  if (MODE == SWEEP_FC) {
-    if (on) Lt::store(static_cast<float*>(a.S) + (size_t)k * slice + row, v);
-  } else if (MODE == SWEEP_FRES) {
-    double acc = 0.0;
     if (on) {
-      if (Q == 32 && !HASG && REC && RBYTES) Lt::load(ck, Cs + (size_t)k * a.cs_stride * slice + row);
-      acc = sq_diff<V, NB, NV>(v, ck);
+      if (MODE == SWEEP_FC && k == Nc - 1) Lt::store(static_cast<float*>(a.S) + (size_t)Nc * slice + row, v);
+      if (MODE == SWEEP_CORRF && k + 1 < Nc) Lt::store(X + top * slice + row, v);
+    }
+
 #pragma unroll
-      for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb] - cu[mb];  // g_{l+1}^k
-      Lt::store(static_cast<float*>(a.Gn) + (size_t)k * slice + row, cu);
-      if (a.xn_every > 0 && k % a.xn_every == 0)
-        Lt::store(static_cast<float*>(a.Xn) + (size_t)k * slice + row, ck);
-      if (k == Nc - 1) {
-        Lt::load(ck, Cs + (size_t)Nc * a.cs_stride * slice + row);
-        Lt::store(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, ck);
+    for (int j = 0; j < NS; ++j) {
+      const float* Wj = Wt + j * C::WSZ;
+      V d[NB], w[NB];
+      if constexpr (REC) {
+        cur.rr[j].get(d);
+      } else if constexpr (CPT) {
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) d[mb] = dz[IV_CF - 1 - j][mb];
+      } else {
+        Lt::template prod<C::LD, !HASG>(d, cur.u[j], Wj, lane);
+        apply<V, NB, NV>(d, a.act, true);
+      }
+      if (MODE == SWEEP_FRES && j == NS - 1) {
+        // coarse adjoint step from the upper C-point, linearised at the same fine state
+        V s2[NB];
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) s2[mb] = d[mb] * cu[mb];
+        Lt::template prod_t<C::LD, !HASG>(w, s2, Wj, lane);
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) cu[mb] = cu[mb] + hc * w[mb];
+      }
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) d[mb] = d[mb] * v[mb];
+      Lt::template prod_t<C::LD, !HASG>(w, d, Wj, lane);
+#pragma unroll
+      for (int mb = 0; mb < NB; ++mb) v[mb] = v[mb] + hl * w[mb];
+      if constexpr (HASG) add_to<V, NB>(v, cur.g[j]);
+      if (MODE == SWEEP_CORRF && on) Lt::store(X + (size_t)(top - 1 - j) * slice + row, v);
+    }
+
+    if (MODE == SWEEP_FC) {
+      if (on) Lt::store(static_cast<float*>(a.S) + (size_t)k * slice + row, v);
+    } else if (MODE == SWEEP_FRES) {
+      if (on) {
+        if (LATE_CK) Lt::load(cur.c, Cs + (size_t)k * a.cs_stride * slice + row);
+        acc += sq_diff<V, NB, NV>(v, cur.c);
+#pragma unroll
+        for (int mb = 0; mb < NB; ++mb) cu[mb] = v[mb] - cu[mb];  // g_{l+1}^k
+        Lt::store(static_cast<float*>(a.Gn) + (size_t)k * slice + row, cu);
+        if (a.xn_every > 0 && k % a.xn_every == 0)
+          Lt::store(static_cast<float*>(a.Xn) + (size_t)k * slice + row, cur.c);
+        if (k == Nc - 1) {
+          V cN[NB];
+          Lt::load(cN, Cs + (size_t)Nc * a.cs_stride * slice + row);
+          Lt::store(static_cast<float*>(a.Xn) + (size_t)Nc * slice + row, cN);
+        }
+      }
+    } else if (MODE == SWEEP_CORRF) {
+      if (on && k == 0) {
+        correct<Lt>(v, Cs + row, Vn + row);
+        Lt::store(X + row, v);
       }
     }
-    if (a.partial) {
-      const double s = wg_sum<WAVES>(acc, red);
-      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
+  };
+  if constexpr (TM == 0) {
+    tile(cur, blockIdx.x, W);
+  } else {
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+      // the products read the staged weights from LDS in every tile: an offset
+      // the compiler cannot see through keeps it from hoisting those reads out of
+      // the loop into registers
+      int woff = 0;
+      asm volatile("" : "+v"(woff));
+      Rows nxt;
+      if constexpr (TM == 2) {
+        bool on1;
+        load_rows(nxt, iv_row(min(t + (int)gridDim.x, ntiles - 1), WAVES, EX, a.B, Q, on1));
+      } else if (t != (int)blockIdx.x) {
+        bool on1;
+        load_rows(cur, iv_row(t, WAVES, EX, a.B, Q, on1));
+      }
+      tile(cur, t, W + woff);
+      if constexpr (TM == 2) cur = nxt;
     }
-  } else if (MODE == SWEEP_CORRF) {
-    if (on && k == 0) {
-      correct<Lt>(v, Cs + row, Vn + row);
-      Lt::store(X + row, v);
-    }
+  }
+  if (MODE == SWEEP_FRES && a.partial) {
+    const double s = wg_sum<WAVES>(acc, red);
+    if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
   }
 }
 
@@ -1367,29 +1556,31 @@ constexpr int SWEEP_WAVES = 4;   // waves per interval workgroup (2 and 8 measur
 // per wave and twice the waves.
 constexpr int SWEEP_EX = 16;
 
-// Interval-resident sweeps (c = 4): the level's right-hand side and the record
-// kind select the instantiation.
-template <int Q, bool HASG>
+// Interval-resident sweeps (c = 4): the level's right-hand side, the record kind
+// and whether a workgroup prefetches its next tile select the instantiation.
+template <int Q, bool HASG, int TM>
 void sweep_iv(int dir, const SweepArgs& a, dim3 grid, hipStream_t st) {
   constexpr int W4 = SWEEP_WAVES;
-  const bool rec = a.dsig != nullptr, bytes = a.act == ACT_RELU;
+  const bool rec = a.dsig != nullptr, bytes = a.act == ACT_RELU, corr = a.V != nullptr;
   if (dir == DIR_FWD) {
-    if (a.mode == SWEEP_FC) launch(k_fwd_iv<Q, SWEEP_FC, W4, false, HASG>, grid, 64 * W4, 0, st, a);
-    else if (a.mode == SWEEP_FRES) launch(k_fwd_iv<Q, SWEEP_FRES, W4, false, HASG>, grid, 64 * W4, 0, st, a);
-    else if (rec) launch(k_fwd_iv<Q, SWEEP_CORRF, W4, true, HASG>, grid, 64 * W4, 0, st, a);
-    else launch(k_fwd_iv<Q, SWEEP_CORRF, W4, false, HASG>, grid, 64 * W4, 0, st, a);
+    if (a.mode == SWEEP_FC && corr) launch(k_fwd_iv<Q, SWEEP_FC, W4, false, HASG, TM, true>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FC) launch(k_fwd_iv<Q, SWEEP_FC, W4, false, HASG, TM, false>, grid, 64 * W4, 0, st, a);
+    else if (a.mode == SWEEP_FRES) launch(k_fwd_iv<Q, SWEEP_FRES, W4, false, HASG, TM, false>, grid, 64 * W4, 0, st, a);
+    else if (rec) launch(k_fwd_iv<Q, SWEEP_CORRF, W4, true, HASG, TM, false>, grid, 64 * W4, 0, st, a);
+    else launch(k_fwd_iv<Q, SWEEP_CORRF, W4, false, HASG, TM, false>, grid, 64 * W4, 0, st, a);
     return;
   }
-#define LP_ADJ_IV(MODE)                                                                                    \
-  do {                                                                                                     \
-    if (!HASG && a.cpt) launch(k_adj_iv<Q, MODE, W4, false, false, false, true>, grid, 64 * W4, 0, st, a); \
-    else if (!rec) launch(k_adj_iv<Q, MODE, W4, false, false, HASG>, grid, 64 * W4, 0, st, a);             \
-    else if (bytes) launch(k_adj_iv<Q, MODE, W4, true, true, HASG>, grid, 64 * W4, 0, st, a);              \
-    else launch(k_adj_iv<Q, MODE, W4, true, false, HASG>, grid, 64 * W4, 0, st, a);                        \
+#define LP_ADJ_IV(MODE, CORR)                                                                                         \
+  do {                                                                                                                \
+    if (!HASG && a.cpt) launch(k_adj_iv<Q, MODE, W4, false, false, false, true, TM, CORR>, grid, 64 * W4, 0, st, a);  \
+    else if (!rec) launch(k_adj_iv<Q, MODE, W4, false, false, HASG, false, TM, CORR>, grid, 64 * W4, 0, st, a);       \
+    else if (bytes) launch(k_adj_iv<Q, MODE, W4, true, true, HASG, false, TM, CORR>, grid, 64 * W4, 0, st, a);        \
+    else launch(k_adj_iv<Q, MODE, W4, true, false, HASG, false, TM, CORR>, grid, 64 * W4, 0, st, a);                  \
   } while (0)
-  if (a.mode == SWEEP_FC) LP_ADJ_IV(SWEEP_FC);
-  else if (a.mode == SWEEP_FRES) LP_ADJ_IV(SWEEP_FRES);
-  else LP_ADJ_IV(SWEEP_CORRF);
+  if (a.mode == SWEEP_FC && corr) LP_ADJ_IV(SWEEP_FC, true);
+  else if (a.mode == SWEEP_FC) LP_ADJ_IV(SWEEP_FC, false);
+  else if (a.mode == SWEEP_FRES) LP_ADJ_IV(SWEEP_FRES, false);
+  else LP_ADJ_IV(SWEEP_CORRF, false);
 #undef LP_ADJ_IV
 }
 
@@ -1403,28 +1594,79 @@ bool iv_enabled() {
   return on;
 }
 
+// Which width-64 adjoint FRES sweeps run on the interval-resident kernel instead of
+// the per-step one: LP_IV_FRES64 = 0 none, 1 the finest level's (the default:
+// 51.1 against 55.7 ms per step on the deep workload; on coarse levels its record
+// and right-hand-side rows leave one wave per SIMD), 2 every level's.
+int iv_fres64() {
+  static const int v = [] {
+    const char* e = getenv("LP_IV_FRES64");
+    return e ? atoi(e) : 1;
+  }();
+  return v;
+}
+
+// LP_IV_CORRF_WALK=1 lets the correction sweeps walk several tiles per workgroup
+// as the other sweeps do (for comparison; they write c rows per tile).
+bool iv_corrf_walk() {
+  static const bool on = [] {
+    const char* e = getenv("LP_IV_CORRF_WALK");
+    return e && strcmp(e, "1") == 0;
+  }();
+  return on;
+}
+
+// Workgroups per interval of an interval-resident sweep: enough for about
+// iv_target() workgroups in all (a few per resident slot), each walking
+// ntiles / groups batch tiles; LP_IV_WG overrides the target.
+int iv_target(int q) {
+  static const int env = [] {
+    const char* e = getenv("LP_IV_WG");
+    return e ? atoi(e) : 0;
+  }();
+  if (env > 0) return env;
+  return q == 64 ? 2048 : 1 << 30;
+}
+
+int iv_groups(int q, int ntiles, long Nc) {
+  const long g = (iv_target(q) + Nc - 1) / Nc;
+  return (int)std::max<long>(1, std::min<long>(ntiles, g));
+}
+
 template <int Q>
 hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   constexpr int W4 = SWEEP_WAVES, EX = SWEEP_EX;
   const long Nc = a.Nl / a.c;
   if (Nc > 65535) return hipErrorNotSupported;  // intervals index the grid's y dimension
-  const dim3 grid((a.B + EX * W4 - 1) / (EX * W4), (unsigned)Nc);
-  if (partials) *partials = (int)(grid.x * grid.y);
+  const int ntiles = (a.B + EX * W4 - 1) / (EX * W4);
+  const dim3 grid(ntiles, (unsigned)Nc);
   // Interval-resident kernels: every sweep at width 32; at width 64 (four layers,
   // 70 KB of LDS per workgroup, two waves per SIMD) all but the adjoint FRES
   // sweep, whose per-step kernel with the record requested a step ahead was
   // measured faster (56.3 against 60.9 ms per step on the deep workload; the
-  // other modes gain 1-6 %).
-  // C-point storage (a.cpt, finest level) has interval-resident kernels only.
+  // other modes gain 1-6 %). C-point storage (a.cpt, finest level) has
+  // interval-resident kernels only.
   if constexpr (Q == 32 || Q == 64) {
     if (a.cpt && a.c != IV_CF) return hipErrorNotSupported;
     if (a.c == IV_CF &&
-        (a.cpt || (iv_enabled() && !(Q == 64 && dir == DIR_ADJ && a.mode == SWEEP_FRES)))) {
-      if (a.G) sweep_iv<Q, true>(dir, a, grid, st);
-      else sweep_iv<Q, false>(dir, a, grid, st);
+        (a.cpt || (iv_enabled() && (iv_fres64() > (a.G ? 1 : 0) ||
+                                     !(Q == 64 && dir == DIR_ADJ && a.mode == SWEEP_FRES))))) {
+      const int tg = a.mode == SWEEP_CORRF && !iv_corrf_walk() ? ntiles : iv_groups(Q, ntiles, Nc);
+      const dim3 gi(tg, (unsigned)Nc);
+      if (partials) *partials = (int)(gi.x * gi.y);
+      // the next tile's rows are prefetched on the finest level only: with the
+      // right-hand-side rows of a coarse level they would cost half the occupancy
+      if (tg == ntiles) {
+        if (a.G) sweep_iv<Q, true, 0>(dir, a, gi, st);
+        else sweep_iv<Q, false, 0>(dir, a, gi, st);
+      } else {
+        if (a.G) sweep_iv<Q, true, 1>(dir, a, gi, st);
+        else sweep_iv<Q, false, 2>(dir, a, gi, st);
+      }
       return hipGetLastError();
     }
   }
+  if (partials) *partials = (int)(grid.x * grid.y);
   const bool rec = a.dsig != nullptr;
   if (dir == DIR_FWD) {
     // only the final F-relaxation writes the sigma' record
