@@ -292,7 +292,7 @@ def cpu_sample_size(wl) -> int:
     workloads, fixed leading slices of the large ones (examples are independent
     in every solve, so the rate per example carries over)."""
     if wl.layer == "conv3x3":
-        return min(wl.B, 64)
+        return min(wl.B, 8)  # one MGRIT iteration pair over 8 examples takes about 14 s
     if wl.q > 64:
         return min(wl.B, 64)
     if wl.cfg in (1, 2, 5):

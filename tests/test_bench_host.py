@@ -111,7 +111,7 @@ def test_cpu_baseline_legs():
     assert bench.cpu_sample_size(WORKLOADS[2]) == WORKLOADS[2].B
     assert bench.cpu_sample_size(WORKLOADS[5]) == WORKLOADS[5].B
     assert bench.cpu_sample_size(WORKLOADS[3]) == 1024
-    assert bench.cpu_sample_size(WORKLOADS[4]) == 64
+    assert bench.cpu_sample_size(WORKLOADS[4]) == 8
     r = bench.cpu_baseline(WORKLOADS[2].with_overrides(N=16, B=64), budget_s=0.2)
     assert r["value"] > 0 and r["layer_serial"]["value"] > 0 and r["cores"] >= 1
     assert "full batch" in r["sample"] and "f32" in r["sample"]
