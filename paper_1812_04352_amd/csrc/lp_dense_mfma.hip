@@ -997,8 +997,22 @@ struct AdjRows {
 // the forward F-relaxation (so the results equal those of full storage bit for bit).
 // TM: tiles per workgroup (0: one; 1: several; 2: several, each one's rows
 // requested during the previous one's steps). CORR: FC reads C + (V - C).
+//
+// Resident waves per SIMD the compiler must allow for. Width 32, finest level, byte
+// record, one tile: eight. Width 64: two, which is what LDS allows (70 KB of weights
+// per workgroup, two workgroups per CU); left to itself the compiler gives the
+// fp32-record sweeps 260 registers, one wave per SIMD. The recomputing FRES sweeps
+// that walk tiles are left free: held to 256 registers they spill.
+template <int Q, int MODE, bool REC, bool RBYTES, bool HASG, bool CPT, int TM>
+constexpr int adj_iv_waves() {
+  if (Q == 32) return !HASG && REC && RBYTES && TM == 0 ? 8 : 1;
+  if (Q == 64) return MODE == SWEEP_FRES && !REC && !CPT && TM != 0 ? 1 : 2;
+  return 1;
+}
+
 template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG, bool CPT, int TM, bool CORR>
-__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(Q == 32 && !HASG && REC && RBYTES && TM == 0 ? 8 : 1, 8)))
+__global__ __launch_bounds__(64 * WAVES)
+__attribute__((amdgpu_waves_per_eu(adj_iv_waves<Q, MODE, REC, RBYTES, HASG, CPT, TM>(), 8)))
 void k_adj_iv(SweepArgs a) {
   static_assert(!(CPT && (REC || HASG)), "C-point storage is a finest-level mode without a record");
   constexpr int EX = 16;
@@ -1641,11 +1655,9 @@ hipError_t sweep(int dir, const SweepArgs& a, hipStream_t st, int* partials) {
   const int ntiles = (a.B + EX * W4 - 1) / (EX * W4);
   const dim3 grid(ntiles, (unsigned)Nc);
   // Interval-resident kernels: every sweep at width 32; at width 64 (four layers,
-  // 70 KB of LDS per workgroup, two waves per SIMD) all but the adjoint FRES
-  // sweep, whose per-step kernel with the record requested a step ahead was
-  // measured faster (56.3 against 60.9 ms per step on the deep workload; the
-  // other modes gain 1-6 %). C-point storage (a.cpt, finest level) has
-  // interval-resident kernels only.
+  // 70 KB of LDS per workgroup) every sweep but the coarse levels' adjoint FRES
+  // (iv_fres64). C-point storage (a.cpt, finest level) has interval-resident
+  // kernels only.
   if constexpr (Q == 32 || Q == 64) {
     if (a.cpt && a.c != IV_CF) return hipErrorNotSupported;
     if (a.c == IV_CF &&

@@ -846,3 +846,64 @@ def test_cpoint_storage(name, wl, relax):
     L.lp_mgrit_forward(c.p, mgA, c.K, c.b, U, ws)
     L.lp_mgrit_forward(c.p, mgC, c.K, c.b, Uc, ws)
     assert torch.equal(Uc, U[::cf].contiguous())
+
+
+# More batch tiles than a width-64 sweep's workgroup budget (about 2048 workgroups):
+# N = 128 gives 32 finest intervals, so 64 workgroups per interval each walk about
+# 11 of the 701 tiles (and request the next tile's rows during the current one's
+# steps); on the 8 intervals of level 1, 256 workgroups walk about 3 tiles each.
+# The last tile holds 29 examples.
+WALK_CASES = [
+    ("tanh64_walk", WORKLOADS[3].with_overrides(N=128, B=64 * 700 + 29, max_levels=3)),
+    ("relu64_walk", WORKLOADS[3].with_overrides(act="relu", N=128, B=64 * 700 + 29, max_levels=3)),
+]
+
+
+@pytest.mark.parametrize("name,wl", WALK_CASES, ids=[n for n, _ in WALK_CASES])
+def test_tile_walking_sweeps(name, wl):
+    """Width-64 interval sweeps whose workgroups walk several batch tiles, the
+    launch configuration of the deep workload at full size. Sampled examples (the
+    first ones, the ragged last tile, both sides of tile boundaries that are a
+    walk step apart, seeded others) against the oracle run on those examples
+    alone (examples are independent in the solves; the oracle's terminal value
+    is rescaled from the sample mean to the batch mean). The adjoint linearised
+    through the sigma' record, through recomputed sigma', and from C-point
+    storage must agree bit for bit."""
+    c = Case(wl)
+    B, cf = wl.B, wl.cf
+    r = np.random.default_rng(7)
+    S = {0, 1, 2, 3, B - 29, B - 2, B - 1, 64 * 64 - 1, 64 * 64, 64 * 128, 64 * 256 - 1, 64 * 256}
+    S = np.array(sorted(S | set(r.choice(B, 12, replace=False).tolist())))
+    Sg = torch.from_numpy(S).cuda()
+    mg = sched(wl, 2)
+    mgC = L.mgrit(cf=cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax, max_iter=2,
+                  storage="cpoints")
+    ws = L.alloc_workspace(c.p, mgC)
+    rec = L.alloc_dsig(c.p)
+    U = c.new_traj()
+    _, hF = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, dsig=rec)
+    Ur = np.zeros((wl.N + 1, len(S), wl.q))
+    Ur[0] = c.u0_ref[S]
+    Ur, _, _ = O.mgrit_forward(Ur, c.d["K"], c.d["b"], wl.h, wl.act, cf=cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=wl.relax, max_iter=2)
+    assert_close(U.index_select(1, Sg).cpu().numpy(), Ur, wl.dtype, f"{name} U sample")
+    Uc = torch.zeros((wl.N // cf + 1, B, wl.q), device="cuda", dtype=U.dtype)
+    Uc[0] = c.u0
+    _, hC = L.lp_mgrit_forward(c.p, mgC, c.K, c.b, Uc, ws)
+    assert hC == hF
+    assert torch.equal(Uc, U[::cf].contiguous())
+
+    lamN = _lamN(c, U)[0]
+    LR = torch.zeros_like(U)
+    LR[-1] = lamN
+    LP, LC = LR.clone(), LR.clone()
+    _, hR = L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, LR, ws, dsig=rec)
+    _, hP = L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, LP, ws)
+    _, hCa = L.lp_mgrit_adjoint(c.p, mgC, c.K, c.b, Uc, LC, ws)
+    assert hR == hP == hCa
+    assert torch.equal(LR, LP) and torch.equal(LR, LC)
+    Lr = np.zeros_like(Ur)
+    Lr[-1] = O.loss_terminal(Ur[-1], c.d["W"], c.d["mu"], c.d["onehot"][S])[1] * (len(S) / B)
+    Lr, _, _ = O.mgrit_adjoint(Ur, Lr, c.d["K"], c.d["b"], wl.h, wl.act, cf=cf, max_levels=wl.max_levels,
+                               min_coarse=wl.min_coarse, relax=wl.relax, max_iter=2)
+    assert_close(LR.index_select(1, Sg).cpu().numpy(), Lr, wl.dtype, f"{name} Lam sample")
