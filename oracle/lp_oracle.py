@@ -694,9 +694,70 @@ def lbfgs_direction(g, pairs):
     return r
 
 
+def strong_wolfe_search(phi, dphi, J, gd, alpha_start, c1, c2, max_ls):
+    """A step length meeting the strong Wolfe conditions (Section 4 names them as
+    one choice for the line search) by the textbook method: bracketing with step
+    doubling, then zoom by bisection (Nocedal and Wright, Numerical Optimization,
+    2nd ed., Algorithms 3.5 and 3.6, bisection as the interpolation).
+    phi(a) -> (phi value, context), dphi(context) -> phi'(a); J = phi(0),
+    gd = phi'(0) < 0. Conditions: phi(a) <= J + c1 a gd and |phi'(a)| <= c2 |gd|.
+    At most max_ls evaluations of phi. Returns (alpha, phi evaluations, met): the
+    first step found meeting both; else the lower end of the last bracket (the
+    best step meeting sufficient decrease), or, if no step met it, the last one
+    tried."""
+    evals = [0]
+    last = [alpha_start]
+
+    def ev(a):
+        evals[0] += 1
+        last[0] = a
+        return phi(a)
+
+    def decrease(a, Ja):
+        return Ja <= J + c1 * a * gd
+
+    def zoom(lo, Jlo, hi):
+        while evals[0] < max_ls:
+            a = 0.5 * (lo + hi)
+            Ja, ctx = ev(a)
+            if not decrease(a, Ja) or Ja >= Jlo:
+                hi = a
+                continue
+            da = dphi(ctx)
+            if abs(da) <= c2 * abs(gd):
+                return a, True
+            if da * (hi - lo) >= 0.0:
+                hi = lo
+            lo, Jlo = a, Ja
+        return lo, False
+
+    prev_a, prev_J = 0.0, J
+    a = alpha_start
+    while True:
+        Ja, ctx = ev(a)
+        if not decrease(a, Ja) or (prev_a > 0.0 and Ja >= prev_J):
+            res, met = zoom(prev_a, prev_J, a)
+            break
+        da = dphi(ctx)
+        if abs(da) <= c2 * abs(gd):
+            res, met = a, True
+            break
+        if da >= 0.0:
+            res, met = zoom(a, Ja, prev_a)
+            break
+        if evals[0] >= max_ls:
+            res, met = a, False
+            break
+        prev_a, prev_J = a, Ja
+        a = 2.0 * a
+    if res == 0.0:
+        res = last[0]
+    return res, evals[0], met
+
+
 def one_shot_lbfgs(y, onehot, L_in, K, b, W, mu, h, kind, opening, cf, max_levels, min_coarse, relax,
                    updates, m1=2, m2=2, memory=5, alpha0=1e-2, c1=1e-4, shrink=0.5, max_ls=8,
-                   y_val=None, onehot_val=None, target_acc=None, cycle="V"):
+                   y_val=None, onehot_val=None, target_acc=None, cycle="V", line_search="armijo", c2=0.9):
     """Algorithm 2 with its Hessian approximated by limited-memory BFGS. Per design
     update: m1 state and m2 adjoint MGRIT iterations, warm-started from the previous
     update's iterates (cold at the first); the reduced gradient g of J at those
@@ -710,8 +771,16 @@ def one_shot_lbfgs(y, onehot, L_in, K, b, W, mu, h, kind, opening, cf, max_level
     state becomes the current one. With validation data, the validation accuracy of
     the new design (its exact forward propagation) is taken after every update and the
     run stops once it reaches target_acc.
+    line_search = "wolfe" replaces the backtracking by strong_wolfe_search, with
+    phi(a) the trial loss above and phi'(a) = g_a.d, g_a the reduced gradient after
+    m2 adjoint MGRIT iterations at the trial state warm-started from this update's
+    adjoint iterate (the inexact gradient the one-shot method sees), starting from
+    alpha_start; the accepted step's state is the state after m1 iterations at that
+    design, as for every trial.
     Design vector order: L_in (unless the opening is the identity), K, b, W, mu.
-    Returns dict(losses, alphas, trials, accuracies, weights)."""
+    Returns dict(losses, alphas, trials, accuracies, weights, and with
+    line_search = "wolfe" also wolfe: whether each accepted step met both
+    conditions); trials counts the loss evaluations of each update."""
     L_in, K, b, W, mu = (None if a is None else np.array(a, dtype=np.float64, copy=True)
                          for a in (L_in, K, b, W, mu))
     y, onehot = _f64(y, onehot)
@@ -757,13 +826,37 @@ def one_shot_lbfgs(y, onehot, L_in, K, b, W, mu, h, kind, opening, cf, max_level
         d = [-v for v in lbfgs_direction(g, pairs)]
         gd = _vdot(g, d)
         alpha = alpha0 if it == 0 else 1.0
-        for t in range(max_ls):
+        if line_search == "wolfe":
+            def phi(a):
+                Lt, Kt, bt, Wt, mut = unpack([v + a * w for v, w in zip(x, d)])
+                Ut = state_after(Lt, Kt, bt, U, True)
+                Jt, lamNt, dWt, dmut = loss_terminal(Ut[N], Wt, mut, onehot)
+                return Jt, (Lt, Kt, bt, Ut, lamNt, dWt, dmut)
+
+            def dphi(ctx):
+                # the reduced gradient at the trial state: m2 adjoint iterations warm-started
+                # from this update's adjoint iterate
+                Lt, Kt, bt, Ut, lamNt, dWt, dmut = ctx
+                La = Lam.copy()
+                La[N] = lamNt
+                La, _, _ = mgrit_adjoint(Ut, La, Kt, bt, h, kind, max_iter=m2, warm_start=True, **sched)
+                dKt, dbt = gradient(Ut, La, Kt, bt, h, kind)
+                ga = ([open_grad(y, Lt, La[0], kind, opening)] if has_open else []) + [dKt, dbt, dWt, dmut]
+                return _vdot(ga, d)
+
+            alpha, t, met = strong_wolfe_search(phi, dphi, J, gd, alpha, c1, c2, max_ls)
+            t -= 1  # trials below counts t + 1
+            out.setdefault("wolfe", []).append(met)
             Lt, Kt, bt, Wt, mut = unpack([a + alpha * v for a, v in zip(x, d)])
             Ut = state_after(Lt, Kt, bt, U, True)
-            Jt = loss_terminal(Ut[N], Wt, mut, onehot)[0]
-            if Jt <= J + c1 * alpha * gd or t == max_ls - 1:
-                break
-            alpha *= shrink
+        else:
+            for t in range(max_ls):
+                Lt, Kt, bt, Wt, mut = unpack([a + alpha * v for a, v in zip(x, d)])
+                Ut = state_after(Lt, Kt, bt, U, True)
+                Jt = loss_terminal(Ut[N], Wt, mut, onehot)[0]
+                if Jt <= J + c1 * alpha * gd or t == max_ls - 1:
+                    break
+                alpha *= shrink
         prev = (x, g)
         L_in, K, b, W, mu = Lt, Kt, bt, Wt, mut
         U = Ut

@@ -121,7 +121,10 @@ class LbfgsOneShotTrainer:
     theta + alpha d, alpha = alpha_start * shrink^t (alpha_start = alpha0 at the
     first update, 1 afterwards), each judged by the loss of the state after m1
     MGRIT iterations warm-started from the current state: the first with
-    J_t <= J + c1 alpha g.d is taken (the last trial if none is). With validation
+    J_t <= J + c1 alpha g.d is taken (the last trial if none is). line_search =
+    "wolfe" searches instead for a step meeting the strong Wolfe conditions
+    (_wolfe_search; the slope at a trial is the reduced gradient after m2 adjoint
+    iterations at the trial state, dotted with d). With validation
     data the accuracy of the new design (exact forward propagation) is taken after
     every update and the run stops once it reaches target_acc.
 
@@ -133,7 +136,10 @@ class LbfgsOneShotTrainer:
                  y: torch.Tensor, c: torch.Tensor, n_classes: int, opening: int, n_features: int,
                  memory: int = 5, alpha0: float = 1e-2, c1: float = 1e-4, shrink: float = 0.5, max_ls: int = 8,
                  y_val: Optional[torch.Tensor] = None, c_val: Optional[torch.Tensor] = None,
-                 target_acc: Optional[float] = None):
+                 target_acc: Optional[float] = None, line_search: str = "armijo", c2: float = 0.9):
+        if line_search not in ("armijo", "wolfe"):
+            raise ValueError(f"line_search must be 'armijo' or 'wolfe', not {line_search!r}")
+        self.line_search, self.c2 = line_search, c2
         self.p, self.mgF, self.mgA = prob, mg_fwd, mg_adj
         self.P = params
         self.names = (["L_in"] if "L_in" in params else []) + ["K", "b", "W", "mu"]
@@ -154,6 +160,10 @@ class LbfgsOneShotTrainer:
             return {k: torch.empty_like(params[k]) for k in self.names}
 
         self.G, self.T, self.D, self.Q = like(), like(), like(), like()
+        # the strong Wolfe search's trial gradient and trial adjoint
+        self.GT = like() if line_search == "wolfe" else None
+        self.LamT = torch.zeros_like(self.U) if line_search == "wolfe" else None
+        self.wolfe: List[bool] = []
         self.gW, self.gmu = torch.empty_like(params["W"]), torch.empty_like(params["mu"])
         self.prev = None  # (design copy, gradient copy) of the previous update
         self.pairs: List[tuple] = []
@@ -198,6 +208,96 @@ class LbfgsOneShotTrainer:
         L.lp_loss_terminal(self.p, self.nc, U[-1], design["W"], design["mu"], self.c, self.J, lamN, dW, dmu, self.ws)
         return float(self.J.item())
 
+    def _trial(self, alpha: float) -> float:
+        """T <- P + alpha D, Ut <- the state after m1 MGRIT iterations at T from U;
+        returns the trial loss (inf if the state solve diverged). Leaves the
+        trial's terminal adjoint and head gradients in lam_scratch, gW, gmu."""
+        self._axpby(self.T, self.P, 1.0, 0.0)
+        self._axpby(self.T, self.D, alpha, 1.0)
+        L.lp_vec_axpby(self.Ut, self.U, 1.0, 0.0)
+        self._state_after(self.T, self.Ut, True)
+        Jt = self._loss(self.T, self.Ut, self.lam_scratch, self.gW, self.gmu)
+        try:
+            L.lp_check_finite()
+        except L.LpError as err:  # the trial design's state solve diverged: reject it
+            if err.status != L.LP_ENONFINITE:
+                raise
+            Jt = float("inf")
+        return Jt
+
+    def _trial_slope(self) -> float:
+        """phi'(alpha) = g_T . D for the trial just taken: the reduced gradient at the
+        trial state after m2 adjoint MGRIT iterations warm-started from this update's
+        adjoint iterate."""
+        T, GT = self.T, self.GT
+        L.lp_vec_axpby(self.LamT, self.Lam, 1.0, 0.0)
+        L.lp_vec_axpby(self.LamT[-1], self.lam_scratch, 1.0, 0.0)
+        self.mgA.warm_start = 1
+        L.lp_mgrit_adjoint(self.p, self.mgA, T["K"], T["b"], self.Ut, self.LamT, self.ws, history=False)
+        L.lp_gradient(self.p, T["K"], T["b"], self.Ut, self.LamT, GT["K"], GT["b"], self.ws)
+        if "L_in" in T:
+            L.lp_open_grad(self.p, self.opening, self.nf, self.y, T["L_in"], self.LamT[0], GT["L_in"])
+        L.lp_vec_axpby(GT["W"], self.gW, 1.0, 0.0)
+        L.lp_vec_axpby(GT["mu"], self.gmu, 1.0, 0.0)
+        return self._dot(GT, self.D)
+
+    def _wolfe_search(self, J: float, gd: float, alpha0: float):
+        """Step length meeting the strong Wolfe conditions, phi(a) <= J + c1 a gd and
+        |phi'(a)| <= c2 |gd| (Section 4): bracketing with step doubling, then zoom by
+        bisection (Nocedal and Wright, Numerical Optimization, Algorithms 3.5, 3.6),
+        at most max_ls trial losses. Returns (alpha, trials - 1, last trial's alpha);
+        records in self.wolfe whether alpha meets both conditions. Without such a
+        step: the lower end of the last bracket (the best step with sufficient
+        decrease), else the last trial."""
+        c1, c2, cap = self.c1, self.c2, self.max_ls
+        n, last = 0, alpha0
+
+        def ok_decrease(a, Ja):
+            return Ja <= J + c1 * a * gd
+
+        def curvature(slope):
+            return abs(slope) <= c2 * abs(gd)
+
+        def zoom(lo, J_lo, hi):
+            nonlocal n, last
+            while n < cap:
+                a = 0.5 * (lo + hi)
+                Ja = self._trial(a)
+                n, last = n + 1, a
+                if not ok_decrease(a, Ja) or Ja >= J_lo:
+                    hi = a
+                    continue
+                slope = self._trial_slope()
+                if curvature(slope):
+                    return a, True
+                if slope * (hi - lo) >= 0.0:
+                    hi = lo
+                lo, J_lo = a, Ja
+            return lo, False
+
+        a_prev, J_prev, a = 0.0, J, alpha0
+        while True:
+            Ja = self._trial(a)
+            n, last = n + 1, a
+            if not ok_decrease(a, Ja) or (a_prev > 0.0 and Ja >= J_prev):
+                res, met = zoom(a_prev, J_prev, a)
+                break
+            slope = self._trial_slope()
+            if curvature(slope):
+                res, met = a, True
+                break
+            if slope >= 0.0:
+                res, met = zoom(a, Ja, a_prev)
+                break
+            if n >= cap:
+                res, met = a, False
+                break
+            a_prev, J_prev, a = a, Ja, 2.0 * a
+        if res == 0.0:
+            res = last
+        self.wolfe.append(met)
+        return res, n - 1, last
+
     def step(self) -> bool:
         """One design update; returns False once the validation target is reached."""
         P, G = self.P, self.G
@@ -235,23 +335,18 @@ class LbfgsOneShotTrainer:
             self._axpby(self.Q, s, a - beta, 1.0)
         self._axpby(self.D, self.Q, -1.0, 0.0)
         gd = self._dot(G, self.D)
-        # backtracking line search on the objective at trial designs
         alpha = self.alpha0 if first else 1.0
-        for t in range(self.max_ls):
-            self._axpby(self.T, P, 1.0, 0.0)
-            self._axpby(self.T, self.D, alpha, 1.0)
-            L.lp_vec_axpby(self.Ut, self.U, 1.0, 0.0)
-            self._state_after(self.T, self.Ut, True)
-            Jt = self._loss(self.T, self.Ut, self.lam_scratch, self.gW, self.gmu)
-            try:
-                L.lp_check_finite()
-            except L.LpError as err:  # the trial design's state solve diverged: reject it
-                if err.status != L.LP_ENONFINITE:
-                    raise
-                Jt = float("inf")
-            if Jt <= J + self.c1 * alpha * gd or t == self.max_ls - 1:
-                break
-            alpha *= self.shrink
+        if self.line_search == "wolfe":
+            alpha, t, last = self._wolfe_search(J, gd, alpha)
+            if alpha != last:  # T and Ut hold the last trial: take the accepted one again
+                self._trial(alpha)
+        else:
+            # backtracking line search on the objective at trial designs
+            for t in range(self.max_ls):
+                Jt = self._trial(alpha)
+                if Jt <= J + self.c1 * alpha * gd or t == self.max_ls - 1:
+                    break
+                alpha *= self.shrink
         self.prev = (self._copy(P), self._copy(G))
         self._axpby(P, self.T, 1.0, 0.0)
         self.U, self.Ut = self.Ut, self.U

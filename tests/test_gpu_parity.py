@@ -657,13 +657,9 @@ LBFGS = [
 ]
 
 
-@pytest.mark.parametrize("name,wl", LBFGS, ids=[n for n, _ in LBFGS])
-def test_one_shot_lbfgs_matches_oracle(name, wl):
-    """Algorithm 2 with the L-BFGS Hessian approximation, line search and validation
-    accuracy: per update the trial count, accepted step, loss and validation accuracy
-    against the oracle's run on the same train/validation split, then the final
-    weights. The line search's accept/reject test and the curvature-pair test are
-    taken on each side in its own arithmetic, so the discrete decisions must agree."""
+def _lbfgs_runs(wl, line_search, c2=0.9):
+    """The GPU trainer and the oracle's Algorithm 2 with L-BFGS on the same train /
+    validation split, 6 updates of m1 = m2 = 2 iterations."""
     from paper_1812_04352_amd.one_shot import LbfgsOneShotTrainer
     from workloads import generate
     from lp_testutil import dev, prob
@@ -674,15 +670,18 @@ def test_one_shot_lbfgs_matches_oracle(name, wl):
     updates, m1, m2, alpha0 = 6, 2, 2, 0.5
     names = [k for k in ("L_in", "K", "b", "W", "mu") if d[k] is not None]
     params = {k: dev(d[k], wl) for k in names}
-    mgF = sched(wl, m1)
-    mgA = sched(wl, m2)
-    trn = LbfgsOneShotTrainer(prob(wl), mgF, mgA, params, dev(tr["y"], wl), dev(tr["onehot"], wl), wl.n_classes,
-                              L.OPENING[wl.opening], wl.n_features, alpha0=alpha0,
-                              y_val=dev(va["y"], wl), c_val=dev(va["onehot"], wl))
+    trn = LbfgsOneShotTrainer(prob(wl), sched(wl, m1), sched(wl, m2), params, dev(tr["y"], wl), dev(tr["onehot"], wl),
+                              wl.n_classes, L.OPENING[wl.opening], wl.n_features, alpha0=alpha0,
+                              y_val=dev(va["y"], wl), c_val=dev(va["onehot"], wl), line_search=line_search, c2=c2)
     trn.run(updates)
     r = O.one_shot_lbfgs(tr["y"], tr["onehot"], d["L_in"], d["K"], d["b"], d["W"], d["mu"], wl.h, wl.act,
                          wl.opening, cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax,
-                         updates=updates, m1=m1, m2=m2, alpha0=alpha0, y_val=va["y"], onehot_val=va["onehot"])
+                         updates=updates, m1=m1, m2=m2, alpha0=alpha0, y_val=va["y"], onehot_val=va["onehot"],
+                         line_search=line_search, c2=c2)
+    return trn, r, names, params, Bv
+
+
+def _check_lbfgs(wl, trn, r, names, params, Bv):
     assert trn.trials == r["trials"], (trn.trials, r["trials"])
     assert trn.alphas == r["alphas"], (trn.alphas, r["alphas"])
     ltol = {"f32": 1e-4, "f64": 1e-10}[wl.dtype]
@@ -694,8 +693,35 @@ def test_one_shot_lbfgs_matches_oracle(name, wl):
     for i, (a, b) in enumerate(zip(trn.accuracies, r["accuracies"])):
         assert abs(a - b) <= atol, (i, a, b)
     for k in names:
-        assert_close(params[k].cpu().numpy(), r["weights"][k], wl.dtype, f"{k} after {updates} updates",
+        assert_close(params[k].cpu().numpy(), r["weights"][k], wl.dtype, f"{k} after {len(trn.losses)} updates",
                      scale={"f32": 100, "f64": 1000}[wl.dtype])
+
+
+@pytest.mark.parametrize("name,wl", LBFGS, ids=[n for n, _ in LBFGS])
+def test_one_shot_lbfgs_matches_oracle(name, wl):
+    """Algorithm 2 with the L-BFGS Hessian approximation, line search and validation
+    accuracy: per update the trial count, accepted step, loss and validation accuracy
+    against the oracle's run on the same train/validation split, then the final
+    weights. The line search's accept/reject test and the curvature-pair test are
+    taken on each side in its own arithmetic, so the discrete decisions must agree."""
+    _check_lbfgs(wl, *_lbfgs_runs(wl, "armijo"))
+
+
+# c2 = 0.9 (the usual quasi-Newton value) already doubles and bisects steps here;
+# c2 = 0.1 takes longer bracketing and zoom paths (fp64 only, where every discrete
+# decision must agree)
+WOLFE = [(LBFGS[0][0], LBFGS[0][1], 0.9), (LBFGS[1][0], LBFGS[1][1], 0.9), (LBFGS[0][0], LBFGS[0][1], 0.1)]
+
+
+@pytest.mark.parametrize("name,wl,c2", WOLFE, ids=[f"{n}-c2={c}" for n, _, c in WOLFE])
+def test_one_shot_lbfgs_strong_wolfe_matches_oracle(name, wl, c2):
+    """The strong Wolfe line search (Section 4): the slope at each trial is the
+    reduced gradient after m2 adjoint iterations at the trial state. Per update the
+    loss evaluations, the accepted step and whether it met both conditions, then
+    losses, accuracies and weights as above."""
+    trn, r, names, params, Bv = _lbfgs_runs(wl, "wolfe", c2)
+    assert trn.wolfe == r["wolfe"], (trn.wolfe, r["wolfe"])
+    _check_lbfgs(wl, trn, r, names, params, Bv)
 
 
 def test_one_shot_lbfgs_validation_stop():

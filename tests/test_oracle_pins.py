@@ -824,3 +824,66 @@ def test_expand_cpoints_reproduces_stored_trajectories():
         assert np.max(np.abs(E - M)) <= 1e-15 * np.max(np.abs(M))
         # a non-converged iterate: its F-points are not the serial ones
         assert np.max(np.abs(M - S)) > 1e-8
+
+
+def _line(f, df):
+    return (lambda a: (f(a), a)), df
+
+
+@pytest.mark.parametrize("c2", [0.9, 0.1])
+def test_strong_wolfe_search_on_analytic_lines(c2):
+    """The line search the paper names (strong Wolfe conditions, Section 4) on 1-D
+    functions whose acceptable steps are known in closed form: a quadratic with its
+    minimum beyond the first trial (doubling, then zoom), one with its minimum far
+    inside it (zoom by bisection from the overshoot), a smooth multi-modal
+    function, and a first step that lowers phi while overshooting; each accepted
+    step meets both conditions evaluated here directly."""
+    c1 = 1e-4
+    cases = [
+        (lambda a: (a - 3.0) ** 2, lambda a: 2.0 * (a - 3.0)),
+        (lambda a: (a - 0.1) ** 2, lambda a: 2.0 * (a - 0.1)),
+        # the first step decreases phi but overshoots with a large positive slope: the
+        # weak curvature condition would take it, the strong one (c2 = 0.1) does not
+        (lambda a: (a - 0.6) ** 2, lambda a: 2.0 * (a - 0.6)),
+        (lambda a: -np.exp(-(a - 1.7) ** 2) - 0.2 * np.sin(4.0 * a),
+         lambda a: 2.0 * (a - 1.7) * np.exp(-(a - 1.7) ** 2) - 0.8 * np.cos(4.0 * a)),
+    ]
+    for f, df in cases:
+        J, gd = f(0.0), df(0.0)
+        assert gd < 0.0
+        phi, dphi = _line(f, df)
+        a, n, met = O.strong_wolfe_search(phi, dphi, J, gd, 1.0, c1, c2, 30)
+        assert met and 1 <= n <= 30
+        assert f(a) <= J + c1 * a * gd
+        assert abs(df(a)) <= c2 * abs(gd)
+    # the quadratic's acceptable set is |2 (a - 3)| <= 6 c2 (sufficient decrease holds there)
+    phi, dphi = _line(*cases[0])
+    a, _, _ = O.strong_wolfe_search(phi, dphi, 9.0, -6.0, 1.0, c1, c2, 30)
+    assert abs(a - 3.0) <= 3.0 * c2
+    if c2 == 0.1:
+        assert a == 3.0  # 1, 2, 4 (no decrease from 2), then the bracket's midpoint
+
+
+def test_strong_wolfe_search_limits():
+    """Without an acceptable step within max_ls evaluations: a line that keeps
+    descending ends at the last doubled step; a minimum far below every trial
+    ends at the last bisected step (nothing met sufficient decrease)."""
+    phi, dphi = _line(lambda a: -a, lambda a: -1.0)
+    a, n, met = O.strong_wolfe_search(phi, dphi, 0.0, -1.0, 1.0, 1e-4, 0.9, 8)
+    assert (a, n, met) == (128.0, 8, False)
+    phi, dphi = _line(lambda a: (a - 1e-6) ** 2, lambda a: 2.0 * (a - 1e-6))
+    a, n, met = O.strong_wolfe_search(phi, dphi, 1e-12, -2e-6, 1.0, 1e-4, 0.9, 3)
+    assert (a, n, met) == (0.25, 3, False)
+
+
+def test_one_shot_lbfgs_with_strong_wolfe_steps():
+    """Algorithm 2 with the strong Wolfe line search on a small Peaks-shaped
+    problem: every update finds a step meeting both conditions and the loss falls."""
+    wl = WORKLOADS[1].with_overrides(N=16, B=60, max_levels=2)
+    d = generate(wl)
+    r = O.one_shot_lbfgs(d["y"], d["onehot"], d["L_in"], d["K"], d["b"], d["W"], d["mu"], wl.h, wl.act,
+                         wl.opening, cf=wl.cf, max_levels=wl.max_levels, min_coarse=wl.min_coarse, relax=wl.relax,
+                         updates=5, alpha0=0.5, line_search="wolfe")
+    assert r["wolfe"] == [True] * 5
+    assert r["losses"][-1] < r["losses"][0]
+    assert all(1 <= t <= 8 for t in r["trials"])
