@@ -680,17 +680,30 @@ void k_adj(SweepArgs a, SGeo ga) {
     }
   } else if (MODE == SWEEP_FRES) {
     // coarse adjoint step from the upper C-point, linearised at the fine state of
-    // the interval's last step (its weights are in both layer slots)
-    f32x4 cu[TPW];
+    // the interval's last step (its weights are in both layer slots); the lower
+    // C-point, for the residual, is requested with the upper one (one wait for
+    // both) and used before the coarse step's product, so it is not live there
+    const float* ck = Cs + (size_t)k * a.cs_stride * slice + eo;
+    f32x4 cu[TPW], cl[TPW];
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
       const Px p = px_of(g, t0 + tt, lane);
       cu[tt] = ld_px(src, g, p);
-      // with the record, sigma' of the last step is read again rather than kept
-      // live in registers through the loop
-      const f32x4 d = REC ? rec_get<RB>(a.dsig, (size_t)(top - nsteps) * a.stride * a.B + blockIdx.y, g, t0 + tt, lane)
-                          : dd[tt];
-      if (p.ok) put_px(buf, d * cu[tt], g, p);
+      cl[tt] = ld_px(ck, g, p);
+    }
+    double acc = 0.0;
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      const Px p = px_of(g, t0 + tt, lane);
+      // with the record, sigma' of the last step comes from its words, still in
+      // registers (the loop requests no further step after the last)
+      const f32x4 d = REC ? rec_val<RB>(rn[tt]) : dd[tt];
+      if (p.ok) {
+        put_px(buf, d * cu[tt], g, p);
+        const f32x4 rr = lam[tt] - cl[tt];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
+      }
     }
     float wt[24];
     gather_w<true>(wt, sw, lane);
@@ -699,18 +712,11 @@ void k_adj(SweepArgs a, SGeo ga) {
     conv_tiles(w, wt, buf, g, t0, lane, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) cu[tt] += hc * w[tt];
-    const float* ck = Cs + (size_t)k * a.cs_stride * slice + eo;
     float* gn = static_cast<float*>(a.Gn) + (size_t)k * slice + eo;
-    double acc = 0.0;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
       const Px p = px_of(g, t0 + tt, lane);
-      if (p.ok) {
-        const f32x4 rr = lam[tt] - ld_px(ck, g, p);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
-        st_px(gn, lam[tt] - cu[tt], g, p);  // g_{l+1}^k = f_k - Phibar_{l+1}(C_{k+1})
-      }
+      if (p.ok) st_px(gn, lam[tt] - cu[tt], g, p);  // g_{l+1}^k = f_k - Phibar_{l+1}(C_{k+1})
     }
     if (a.xn_every > 0 && k % a.xn_every == 0) row_copy(static_cast<float*>(a.Xn) + (size_t)k * slice + eo, ck, g.q, nt);
     if (k == Nc - 1)
