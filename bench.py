@@ -71,11 +71,14 @@ def level_visits(L: int, cycle: str):
     return v
 
 
-def record_bytes(wl) -> int:
-    """Bytes per value of the sigma' record the step keeps (0: none is kept)."""
+def record_bytes(wl) -> float:
+    """Bytes per value of the sigma' record the step keeps (0: none is kept): ReLU
+    one byte per value (dense) or one bit (convolution), fp32 otherwise."""
     if wl.dtype != "f32" or wl.act == "identity" or (wl.layer == "dense" and wl.q not in MATRIX_CORE_WIDTHS):
         return 0
-    return 1 if wl.act == "relu" else 4
+    if wl.act == "relu":
+        return 1 if wl.layer == "dense" else 0.125
+    return 4
 
 
 def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0, cpt: bool = False):
@@ -518,7 +521,7 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False, storage: str =
                    "activation": wl.act, "mgrit": {"cf": wl.cf, "levels": len(level_sizes(
                        wl.N, wl.cf, wl.max_levels, wl.min_coarse)), "relax": wl.relax, "cycle": wl.cycle,
                        "fwd_iters": fwd_iters, "adj_iters": adj_iters},
-                   "sigma_record": {0: None, 1: "u8", 4: "f32"}[rec_e],
+                   "sigma_record": {0: None, 0.125: "bits", 1: "u8", 4: "f32"}[rec_e],
                    "storage": "C-points only (F-point states recomputed)" if cpt else "every layer",
                    "step": "MGRIT forward iterations + loss + MGRIT adjoint iterations + gradient"},
         "device_memory_gb": peak_gb,

@@ -143,9 +143,10 @@ size_t lp_workspace_bytes(const lp_problem* prob, const lp_mgrit* mg);
  * Dense: layout [N][B][q] in the problem's element order, one value per
  * element: a byte 0 or 1 for LP_RELU, the problem dtype for LP_TANH and
  * LP_SMOOTHRELU. Convolution: one block per (layer n, example e) at index
- * n B + e, in the convolution kernels' own tile order (each lane of each tile of
- * 16 pair-pixels holds its four values as one word of 0/1 bytes for LP_RELU, or
- * as four fp32 values); the record is only meaningful to this library. No
+ * n B + e, in the convolution kernels' own tile order (LP_RELU: one 32-bit word
+ * of decision bits per lane of each wave, covering its tiles of 16 pair-pixels;
+ * else four fp32 values per lane of each tile); the record is only meaningful to
+ * this library. No
  * storage for LP_IDENTITY (sigma' = 1). A forward call given `dsig` writes the
  * record of the trajectory it returns; an adjoint or gradient call given `dsig`
  * uses it instead of recomputing K_n U[n] + b_n from U (saving one layer

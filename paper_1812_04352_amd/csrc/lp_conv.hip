@@ -275,12 +275,13 @@ __device__ __forceinline__ float dact_one(float z, int act) {
 // tile, ghost tiles included, writes its slot, so a block is whole once written
 // and each lane reads its values with one vector load. Blocks are indexed by
 // layer * B + example.
-__host__ __device__ constexpr size_t rec_block_bytes(const SGeo& g, bool bytes) {
-  return (size_t)g.NW * TPW * 64 * (bytes ? 4 : 16);
+__host__ __device__ constexpr size_t rec_block_bytes(const SGeo& g, bool bits) {
+  return (size_t)g.NW * 64 * (bits ? 4 : TPW * 16);
 }
 
-// The record values of one lane and tile as loaded (kept packed until used):
-// RB, ReLU's four 0/1 bytes in one word; else four fp32 values.
+// One lane's record of one step, all of its TPW tiles, as loaded (kept packed
+// until used): RB, ReLU's TPW x 4 decisions as bits 4 tt + r of one word (one
+// word per lane and step); else TPW quadruples of fp32 values.
 template <bool RB>
 struct RecW;
 template <>
@@ -289,52 +290,59 @@ struct RecW<true> {
 };
 template <>
 struct RecW<false> {
-  f32x4 f;
+  f32x4 f[TPW];
 };
 
+// slots: RB, lane of wave t0 / TPW; else, lane of tile t0 + tt
 __device__ __forceinline__ size_t rec_slot(int t, int lane) { return (size_t)t * 64 + lane; }
 
-// rec_put takes the pre-activation of the lane's four values in tile t
+// rec_put takes the pre-activations of the lane's four values in each of its tiles
 template <bool RB>
-__device__ __forceinline__ void rec_put(void* rec, size_t blk, const SGeo& g, int t, int lane, f32x4 z, int act) {
+__device__ __forceinline__ void rec_put(void* rec, size_t blk, const SGeo& g, int t0, int lane, const f32x4 (&z)[TPW],
+                                        int act) {
   uint8_t* base = static_cast<uint8_t*>(rec) + blk * rec_block_bytes(g, RB);
   if constexpr (RB) {
     uint32_t w = 0;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) w |= (z[r] > 0.f ? 1u : 0u) << (8 * r);
-    reinterpret_cast<uint32_t*>(base)[rec_slot(t, lane)] = w;
-  } else {
-    f32x4 d;
+    for (int tt = 0; tt < TPW; ++tt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) d[r] = dact_one(z[r], act);
-    reinterpret_cast<f32x4*>(base)[rec_slot(t, lane)] = d;
+      for (int r = 0; r < 4; ++r) w |= (z[tt][r] > 0.f ? 1u : 0u) << (4 * tt + r);
+    reinterpret_cast<uint32_t*>(base)[rec_slot(t0 / TPW, lane)] = w;
+  } else {
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      f32x4 d;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) d[r] = dact_one(z[tt][r], act);
+      reinterpret_cast<f32x4*>(base)[rec_slot(t0 + tt, lane)] = d;
+    }
   }
 }
 
 template <bool RB>
-__device__ __forceinline__ RecW<RB> rec_load(const void* rec, size_t blk, const SGeo& g, int t, int lane) {
+__device__ __forceinline__ RecW<RB> rec_load(const void* rec, size_t blk, const SGeo& g, int t0, int lane) {
   const uint8_t* base = static_cast<const uint8_t*>(rec) + blk * rec_block_bytes(g, RB);
   RecW<RB> r;
-  if constexpr (RB) r.w = reinterpret_cast<const uint32_t*>(base)[rec_slot(t, lane)];
-  else r.f = reinterpret_cast<const f32x4*>(base)[rec_slot(t, lane)];
+  if constexpr (RB) {
+    r.w = reinterpret_cast<const uint32_t*>(base)[rec_slot(t0 / TPW, lane)];
+  } else {
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) r.f[tt] = reinterpret_cast<const f32x4*>(base)[rec_slot(t0 + tt, lane)];
+  }
   return r;
 }
 
+// sigma' of the lane's four values in its tile tt
 template <bool RB>
-__device__ __forceinline__ f32x4 rec_val(const RecW<RB>& r) {
+__device__ __forceinline__ f32x4 rec_val(const RecW<RB>& r, int tt) {
   if constexpr (!RB) {
-    return r.f;
+    return r.f[tt];
   } else {
     f32x4 d;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) d[q] = (r.w >> (8 * q)) & 0xffu ? 1.f : 0.f;
+    for (int q = 0; q < 4; ++q) d[q] = (r.w >> (4 * tt + q)) & 1u ? 1.f : 0.f;
     return d;
   }
-}
-
-template <bool RB>
-__device__ __forceinline__ f32x4 rec_get(const void* rec, size_t blk, const SGeo& g, int t, int lane) {
-  return rec_val<RB>(rec_load<RB>(rec, blk, g, t, lane));
 }
 
 __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
@@ -445,8 +453,7 @@ void k_fwd(SweepArgs a, SGeo ga) {
     }
     if constexpr (rec) {
       const size_t blk = (size_t)(kc + j) * a.stride * a.B + blockIdx.y;
-#pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) rec_put<RB>(a.dsig, blk, g, t0 + tt, lane, z[tt], a.act);
+      rec_put<RB>(a.dsig, blk, g, t0, lane, z, a.act);
     }
     act_tiles<false>(z, a.act);
     // (without HG the kernel keeps the form it was tuned in: a run-time test that
@@ -482,8 +489,7 @@ void k_fwd(SweepArgs a, SGeo ga) {
     gather_w<false>(wr, swc, lane);
     conv_tiles(z, wr, buf, g, t0, lane, bias_px(swc, lane));
     const size_t blk = (size_t)(kc + nsteps) * a.stride * a.B + blockIdx.y;
-#pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) rec_put<RB>(a.dsig, blk, g, t0 + tt, lane, z[tt], a.act);
+    rec_put<RB>(a.dsig, blk, g, t0, lane, z, a.act);
   }
   if (MODE == SWEEP_FC) {
     float* so = static_cast<float*>(a.S) + (size_t)(k + 1) * slice + eo;
@@ -592,11 +598,8 @@ void k_adj(SweepArgs a, SGeo ga) {
 
   f32x4 dd[TPW];  // sigma'(z) of the step (after the loop: of the last one)
   // with the record, the words of step j + 1 are requested during step j
-  RecW<RB> rn[REC ? TPW : 1];
-  if constexpr (REC) {
-#pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) rn[tt] = rec_load<RB>(a.dsig, (size_t)(top - 1) * a.stride * a.B + blockIdx.y, g, t0 + tt, lane);
-  }
+  RecW<RB> rn;
+  if constexpr (REC) rn = rec_load<RB>(a.dsig, (size_t)(top - 1) * a.stride * a.B + blockIdx.y, g, t0, lane);
   for (int j = 0; j < nsteps; ++j) {
     // tile offsets recomputed each step (see k_fwd) where that lowers the
     // register count (compiler-measured per variant)
@@ -613,11 +616,8 @@ void k_adj(SweepArgs a, SGeo ga) {
     // d = sigma'(K u + b)
     if constexpr (REC) {
 #pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) dd[tt] = rec_val<RB>(rn[tt]);
-      if (more) {
-#pragma unroll
-        for (int tt = 0; tt < TPW; ++tt) rn[tt] = rec_load<RB>(a.dsig, (size_t)(i - 1) * a.stride * a.B + blockIdx.y, g, t0 + tt, lane);
-      }
+      for (int tt = 0; tt < TPW; ++tt) dd[tt] = rec_val<RB>(rn, tt);
+      if (more) rn = rec_load<RB>(a.dsig, (size_t)(i - 1) * a.stride * a.B + blockIdx.y, g, t0, lane);
     } else {
       float wr[24];
       gather_w<false>(wr, swc, lane);
@@ -697,7 +697,7 @@ void k_adj(SweepArgs a, SGeo ga) {
       const Px p = px_of(g, t0 + tt, lane);
       // with the record, sigma' of the last step comes from its words, still in
       // registers (the loop requests no further step after the last)
-      const f32x4 d = REC ? rec_val<RB>(rn[tt]) : dd[tt];
+      const f32x4 d = REC ? rec_val<RB>(rn, tt) : dd[tt];
       if (p.ok) {
         put_px(buf, d * cu[tt], g, p);
         const f32x4 rr = lam[tt] - cl[tt];
@@ -877,9 +877,9 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
       lam[tt] = ld_px(Lm + (size_t)e * g.q, g, p);
     }
     if constexpr (REC) {
+      const RecW<RB> r = rec_load<RB>(a.dsig, (size_t)n * a.B + e, g, t0, lane);
 #pragma unroll
-      for (int tt = 0; tt < TPW; ++tt)
-        z[tt] = rec_get<RB>(a.dsig, (size_t)n * a.B + e, g, t0 + tt, lane);
+      for (int tt = 0; tt < TPW; ++tt) z[tt] = rec_val<RB>(r, tt);
     } else {
       conv_tiles(z, wf, bu, g, t0, lane, bias);
       act_tiles<true>(z, a.act);

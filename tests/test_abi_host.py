@@ -115,10 +115,12 @@ def test_dsig_record_sizes(monkeypatch):
     # kernels that keep no record
     assert L.lp_dsig_bytes(_p(act="smoothrelu", dtype="f64")) == 0
     assert L.lp_dsig_bytes(_p(C=8)) == 0
-    # conv: one block per (layer, example) in the kernels' tile order, a 4-byte word
-    # (ReLU) or four fp32 values per lane of every tile: 12 x 12 -> 72 pair-pixels,
+    # conv: one block per (layer, example) in the kernels' tile order: ReLU, one 32-bit
+    # word of decision bits per lane of every wave (7 tiles x 4 values); smooth
+    # activations, four fp32 values per lane of every tile. 12 x 12 -> 72 pair-pixels,
     # 5 tiles of 16, one wave of 7 tiles; 28 x 28 -> 392 pair-pixels, 25 tiles, 4 waves
-    assert L.lp_dsig_bytes(L.problem("f32", "conv3x3", "relu", 16, 5, 8, H=12, W=12, h=0.1)) == 16 * 5 * 7 * 64 * 4
+    assert L.lp_dsig_bytes(L.problem("f32", "conv3x3", "relu", 16, 5, 8, H=12, W=12, h=0.1)) == 16 * 5 * 1 * 64 * 4
+    assert L.lp_dsig_bytes(L.problem("f32", "conv3x3", "relu", 16, 5, 8, H=28, W=28, h=0.1)) == 16 * 5 * 4 * 64 * 4
     assert L.lp_dsig_bytes(L.problem("f32", "conv3x3", "tanh", 16, 5, 8, H=28, W=28, h=0.1)) == 16 * 5 * 28 * 64 * 16
     assert L.lp_dsig_bytes(L.problem("f64", "conv3x3", "tanh", 16, 5, 8, H=28, W=28, h=0.1)) == 0
     monkeypatch.setenv("LP_DENSE_PATH", "valu")

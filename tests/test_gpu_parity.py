@@ -520,11 +520,20 @@ def _conv_record(rec, N, B, C, H, W, relu):
     lp_dsig_bytes in include/lp.h) rearranged to [N][B][C][H][W]: tile t of 16
     pair-pixels, lane l: pair-pixel P = 16 t + l % 16 (ghost lanes P >= H/2 W are
     skipped), value r of the lane = channel 2 (l // 16) + r // 2, row 2 (P // W) +
-    r % 2, column P % W."""
+    r % 2, column P % W. ReLU: one 32-bit word per lane of each wave w (tiles
+    7 w .. 7 w + 6), bit 4 (t - 7 w) + r; smooth activations: four fp32 values per
+    tile and lane."""
     npp = H // 2 * W
     T = -(-(-(-npp // 16)) // 7) * 7
-    raw = rec[: N * B * T * 64 * (4 if relu else 16)].cpu()
-    vals = (raw if relu else raw.view(torch.float32)).numpy().reshape(N, B, T, 64, 4)
+    if relu:
+        words = rec[: N * B * (T // 7) * 64 * 4].cpu().view(torch.int32).numpy().view(np.uint32)
+        words = words.reshape(N, B, T // 7, 64)
+        vals = np.zeros((N, B, T, 64, 4), dtype=np.uint8)
+        for t in range(T):
+            for r in range(4):
+                vals[:, :, t, :, r] = (words[:, :, t // 7, :] >> (4 * (t % 7) + r)) & 1
+    else:
+        vals = rec[: N * B * T * 64 * 16].cpu().view(torch.float32).numpy().reshape(N, B, T, 64, 4)
     out = np.zeros((N, B, C, H, W), dtype=vals.dtype)
     for t in range(T):
         for l in range(64):
@@ -539,7 +548,7 @@ def _conv_record(rec, N, B, C, H, W, relu):
 
 def _check_record(c, U, rec):
     """The record against sigma'(K_n u_n + b_n) evaluated by the oracle in fp64 at
-    the trajectory the GPU returned. ReLU's 0/1 bytes may differ from the fp64
+    the trajectory the GPU returned. ReLU's 0/1 decisions may differ from the fp64
     decision only where the pre-activation is within fp32 rounding of zero."""
     wl = c.wl
     Uh = U.double().cpu().numpy()
@@ -550,7 +559,7 @@ def _check_record(c, U, rec):
         if wl.act == "relu":
             assert set(np.unique(got)) <= {0, 1}
             bad = got != want
-            assert np.all(np.abs(z[bad]) <= 1e-5 * np.abs(z).max()), f"{bad.sum()} wrong record bytes"
+            assert np.all(np.abs(z[bad]) <= 1e-5 * np.abs(z).max()), f"{bad.sum()} wrong record bits"
         else:
             np.testing.assert_allclose(got, want, rtol=0, atol=2e-5)
         return
