@@ -73,11 +73,11 @@ def level_visits(L: int, cycle: str):
 
 def record_bytes(wl) -> float:
     """Bytes per value of the sigma' record the step keeps (0: none is kept): ReLU
-    one byte per value (dense) or one bit (convolution), fp32 otherwise."""
+    one bit per value (one byte at width 220), fp32 otherwise."""
     if wl.dtype != "f32" or wl.act == "identity" or (wl.layer == "dense" and wl.q not in MATRIX_CORE_WIDTHS):
         return 0
     if wl.act == "relu":
-        return 1 if wl.layer == "dense" else 0.125
+        return 1 if wl.layer == "dense" and wl.q == 220 else 0.125
     return 4
 
 

@@ -141,8 +141,9 @@ size_t lp_workspace_bytes(const lp_problem* prob, const lp_mgrit* mg);
  * every call that takes `dsig`): sigma'(K_n U[n] + b_n) for n = 0..N-1, the
  * factor the adjoint steps and the gradient apply (Section 3.2, Section 2.3).
  * Dense: layout [N][B][q] in the problem's element order, one value per
- * element: a byte 0 or 1 for LP_RELU, the problem dtype for LP_TANH and
- * LP_SMOOTHRELU. Convolution: one block per (layer n, example e) at index
+ * element: for LP_RELU one bit (widths 32 and 64: bit f of example e's q-bit
+ * word, N B q / 8 bytes) or one byte 0 or 1 (width 220); the problem dtype for
+ * LP_TANH and LP_SMOOTHRELU. Convolution: one block per (layer n, example e) at index
  * n B + e, in the convolution kernels' own tile order (LP_RELU: one 32-bit word
  * of decision bits per lane of each wave, covering its tiles of 16 pair-pixels;
  * else four fp32 values per lane of each tile); the record is only meaningful to

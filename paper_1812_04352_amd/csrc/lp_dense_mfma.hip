@@ -19,6 +19,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "lp_device.h"
 #include "lp_internal.h"
@@ -95,6 +96,37 @@ __device__ __forceinline__ void w_put(float* sh, const WRegs<Q, WAVES>& r) {
 // steps never move state between lanes. A wave of the 16-example shape does half
 // the work per step with half the latency and needs about two thirds of the
 // registers; the sweeps and the serial solve use it, the gradient the other.
+// ReLU's sigma' record: one bit per element in element order ([N][B][q], bit f of
+// example e's q-bit word, q = 32 or 64), so an example's decisions are one 32- or
+// 64-bit word. off is an element offset inside the example's row; the row starts
+// at off - off % Q, a multiple of 32 elements, so the word is aligned.
+template <int Q>
+struct MaskWord {
+  static_assert(Q == 32 || Q == 64, "bit records exist for widths 32 and 64");
+  using T = typename std::conditional<Q == 64, unsigned long long, uint32_t>::type;
+  __device__ static T load(const uint8_t* rec, size_t off) {
+    return *reinterpret_cast<const T*>(rec + (off - off % Q) / 8);
+  }
+  __device__ static void store(uint8_t* rec, size_t off, T w) { *reinterpret_cast<T*>(rec + (off - off % Q) / 8) = w; }
+  // 32-bit half i of the word (bits 32 i .. 32 i + 31), shifted right by s: lanes
+  // shift once by their own offset and then read bits at constant positions
+  __device__ static uint32_t half(T w, int i, int s) { return (uint32_t)(i ? (uint64_t)w >> 32 : w) >> s; }
+  // the word from its halves, after an OR over lanes l, l ^ 16, l ^ 32, l ^ 48 (the
+  // lanes of one example)
+  __device__ static T combine(uint32_t lo, uint32_t hi) {
+    lo |= __shfl_xor(lo, 16, 64);
+    lo |= __shfl_xor(lo, 32, 64);
+    if constexpr (Q == 64) {
+      hi |= __shfl_xor(hi, 16, 64);
+      hi |= __shfl_xor(hi, 32, 64);
+      return ((T)hi << 32) | lo;
+    } else {
+      return lo;
+    }
+  }
+};
+__device__ __forceinline__ float mask_bit(uint32_t h, int b) { return (h >> b) & 1u ? 1.f : 0.f; }
+
 template <int Q, int EX>
 struct Lay;
 
@@ -124,16 +156,19 @@ struct Lay<Q, 32> {
             f32x4{v[mb][4 * g + 0], v[mb][4 * g + 1], v[mb][4 * g + 2], v[mb][4 * g + 3]};
   }
 
-  // sigma' record of ReLU (one byte per element, 0 or 1), p at the element offset
-  __device__ static void load_mask(V (&v)[NB], const uint8_t* __restrict__ p) {
+  // sigma' record of ReLU (bits, MaskWord), off at the lane's element offset
+  // e Q + 4 (lane / 32): value (mb, 4 g + t) is feature 32 mb + 8 g + 4 (lane / 32) + t
+  __device__ static void load_mask(V (&v)[NB], const uint8_t* __restrict__ rec, size_t off) {
+    const auto w = MaskWord<Q>::load(rec, off);
+    const int h4 = (int)(off % Q);
 #pragma unroll
-    for (int mb = 0; mb < NB; ++mb)
+    for (int mb = 0; mb < NB; ++mb) {
+      const uint32_t h = MaskWord<Q>::half(w, mb, h4);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(p + 32 * mb + 8 * g);
+      for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) v[mb][4 * g + t] = (w >> (8 * t)) & 0xffu ? 1.f : 0.f;
-      }
+        for (int t = 0; t < 4; ++t) v[mb][4 * g + t] = mask_bit(h, 8 * g + t);
+    }
   }
 
   // z = K_n v + b_n (W: staged weights, row-major with row pitch LD, bias row last)
@@ -200,24 +235,34 @@ struct Lay<Q, 16> {
     for (int mb = 0; mb < NB; ++mb) *reinterpret_cast<f32x4*>(p + 16 * mb) = v[mb];
   }
 
-  // sigma' record of ReLU (one byte per element, 0 or 1), p at the element offset
-  __device__ static void load_mask(V (&v)[NB], const uint8_t* __restrict__ p) {
+  // sigma' record of ReLU (bits, MaskWord), off at the lane's element offset
+  // e Q + 4 (lane / 16): value (mb, r) is feature 16 mb + 4 (lane / 16) + r
+  __device__ static void load_mask(V (&v)[NB], const uint8_t* __restrict__ rec, size_t off) {
+    unpack_mask(v, MaskWord<Q>::load(rec, off), (int)(off % Q));
+  }
+  // g4 = 4 (lane / 16): value (mb, r) is bit 16 (mb % 2) + r of half mb / 2, shifted by g4
+  __device__ static void unpack_mask(V (&v)[NB], typename MaskWord<Q>::T w, int g4) {
 #pragma unroll
-    for (int mb = 0; mb < NB; ++mb) {
-      const uint32_t w = *reinterpret_cast<const uint32_t*>(p + 16 * mb);
+    for (int i = 0; i < (NB + 1) / 2; ++i) {
+      const uint32_t h = MaskWord<Q>::half(w, i, g4);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[mb][r] = (w >> (8 * r)) & 0xffu ? 1.f : 0.f;
+      for (int mb = 2 * i; mb < NB && mb < 2 * i + 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[mb][r] = mask_bit(h, 16 * (mb % 2) + r);
     }
   }
 
-  __device__ static void store_mask(uint8_t* __restrict__ p, const V (&v)[NB]) {
+  // the four lanes of an example hold disjoint bits of its word: they are combined
+  // across lanes (every lane of the wave must call this) and one of them stores it
+  __device__ static void store_mask(uint8_t* __restrict__ rec, size_t off, const V (&v)[NB], bool on) {
+    const int g4 = (int)(off % Q);
+    uint32_t h[2] = {0u, 0u};
 #pragma unroll
-    for (int mb = 0; mb < NB; ++mb) {
-      uint32_t w = 0;
+    for (int mb = 0; mb < NB; ++mb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) w |= (v[mb][r] != 0.f ? 1u : 0u) << (8 * r);
-      *reinterpret_cast<uint32_t*>(p + 16 * mb) = w;
-    }
+      for (int r = 0; r < 4; ++r) h[mb / 2] |= (v[mb][r] != 0.f ? 1u : 0u) << (16 * (mb % 2) + r);
+    const auto w = MaskWord<Q>::combine(h[0] << g4, h[1] << g4);
+    if (on && g4 == 0) MaskWord<Q>::store(rec, off, w);
   }
 
   // z = K_n v + b_n: A operand of slice (ib, r) in lane l is K[16ob + l%16][16ib + 4(l/16) + r].
@@ -381,17 +426,19 @@ __device__ __forceinline__ double sq_diff(const V (&a)[NB], const V (&b)[NB]) {
   return acc;
 }
 
-// The sigma' record at element offset off: bytes for ReLU, fp32 otherwise.
+// The sigma' record at element offset off: bits for ReLU (MaskWord), fp32 otherwise.
 template <typename Lt>
 __device__ __forceinline__ void load_dsig(typename Lt::V (&d)[Lt::NB], const void* rec, size_t off, int act) {
-  if (act == ACT_RELU) Lt::load_mask(d, static_cast<const uint8_t*>(rec) + off);
+  if (act == ACT_RELU) Lt::load_mask(d, static_cast<const uint8_t*>(rec), off);
   else Lt::load(d, static_cast<const float*>(rec) + off);
 }
 
+// on: whether the lane's example exists; every lane of the wave calls this (the
+// ReLU bits of an example are gathered across its lanes)
 template <typename Lt>
-__device__ __forceinline__ void store_dsig(void* rec, size_t off, int act, const typename Lt::V (&d)[Lt::NB]) {
-  if (act == ACT_RELU) Lt::store_mask(static_cast<uint8_t*>(rec) + off, d);
-  else Lt::store(static_cast<float*>(rec) + off, d);
+__device__ __forceinline__ void store_dsig(void* rec, size_t off, int act, const typename Lt::V (&d)[Lt::NB], bool on) {
+  if (act == ACT_RELU) Lt::store_mask(static_cast<uint8_t*>(rec), off, d, on);
+  else if (on) Lt::store(static_cast<float*>(rec) + off, d);
 }
 
 // Fixed-order workgroup sum of one double per lane; result in thread 0.
@@ -477,7 +524,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
 #pragma unroll
       for (int mb = 0; mb < NB; ++mb) dz[mb] = s[mb];
       apply<V, NB, NV>(dz, a.act, true);
-      if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + j) * a.stride * slice + row, a.act, dz);
+      store_dsig<Lt>(a.dsig, (size_t)(kc + j) * a.stride * slice + row, a.act, dz, on);
     }
     apply<V, NB, NV>(s, a.act, false);
     if (MODE == SWEEP_FRES && j == 0) {
@@ -503,7 +550,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd(SweepArgs a) {
     V z[NB];
     Lt::template prod<C::LD>(z, v, W[nsteps & 1], lane);
     apply<V, NB, NV>(z, a.act, true);
-    if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + nsteps) * a.stride * slice + row, a.act, z);
+    store_dsig<Lt>(a.dsig, (size_t)(kc + nsteps) * a.stride * slice + row, a.act, z, on);
   }
   if (MODE == SWEEP_FC) {
     if (on) Lt::store(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
@@ -744,24 +791,16 @@ __device__ __forceinline__ void wall_put(float* sh, const WAll<Q, NL, WAVES>& r)
   }
 }
 
-// A sigma' record row as loaded: the raw bytes of ReLU's 0/1 record (one word per
-// block) or the fp32 values of the smooth activations.
-template <typename Lt, bool BYTES>
+// A sigma' record row as loaded (16-example lanes): the example's word of ReLU's
+// decision bits (MaskWord) or the fp32 values of the smooth activations.
+template <typename Lt, bool BITS>
 struct RecRow;
 template <typename Lt>
 struct RecRow<Lt, true> {
-  uint32_t w[Lt::NB];
-  __device__ void load(const void* rec, size_t off) {
-    const uint8_t* p = static_cast<const uint8_t*>(rec) + off;
-#pragma unroll
-    for (int mb = 0; mb < Lt::NB; ++mb) w[mb] = *reinterpret_cast<const uint32_t*>(p + 16 * mb);
-  }
-  __device__ void get(typename Lt::V (&d)[Lt::NB]) const {
-#pragma unroll
-    for (int mb = 0; mb < Lt::NB; ++mb)
-#pragma unroll
-      for (int r = 0; r < Lt::NV; ++r) d[mb][r] = (w[mb] >> (8 * r)) & 0xffu ? 1.f : 0.f;
-  }
+  static constexpr int Q = 16 * Lt::NB;
+  typename MaskWord<Q>::T w;
+  __device__ void load(const void* rec, size_t off) { w = MaskWord<Q>::load(static_cast<const uint8_t*>(rec), off); }
+  __device__ void get(typename Lt::V (&d)[Lt::NB]) const { Lt::unpack_mask(d, w, 4 * ((threadIdx.x & 63) >> 4)); }
 };
 template <typename Lt>
 struct RecRow<Lt, false> {
@@ -907,7 +946,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
 #pragma unroll
         for (int mb = 0; mb < NB; ++mb) dz[mb] = s[mb];
         apply<V, NB, NV>(dz, a.act, true);
-        if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + j) * a.stride * slice + row, a.act, dz);
+        store_dsig<Lt>(a.dsig, (size_t)(kc + j) * a.stride * slice + row, a.act, dz, on);
       }
       apply<V, NB, NV>(s, a.act, false);
       if (MODE == SWEEP_FRES && j == 0) {
@@ -925,7 +964,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
       V z[NB];
       Lt::template prod<C::LD>(z, v, Wt + NS * C::WSZ, lane);
       apply<V, NB, NV>(z, a.act, true);
-      if (on) store_dsig<Lt>(a.dsig, (size_t)(kc + NS) * a.stride * slice + row, a.act, z);
+      store_dsig<Lt>(a.dsig, (size_t)(kc + NS) * a.stride * slice + row, a.act, z, on);
     }
     if (MODE == SWEEP_FC) {
       if (on) Lt::store(static_cast<float*>(a.S) + (size_t)(k + 1) * slice + row, v);
@@ -989,7 +1028,7 @@ struct AdjRows {
   typename Lt::V g[HASG ? NS : 1][Lt::NB];
 };
 
-// REC: sigma' comes from the record (ReLU: RBYTES, one byte per value) instead of
+// REC: sigma' comes from the record (ReLU: RBYTES, one bit per value) instead of
 // the layer product at the primal state.
 // CPT (finest level, C-point storage): Uf holds the fine C-points only (row k is
 // u^{kc}); the interval first recomputes its F-point states and sigma'(z_n) for
@@ -1461,7 +1500,7 @@ __global__ __launch_bounds__(64) void k_ser_fwd(SweepArgs a) {
 #pragma unroll
         for (int mb = 0; mb < NB; ++mb) dz[mb] = s[mb];
         apply<V, NB, NV>(dz, a.act, true);
-        if (on) store_dsig<Lt>(a.dsig, (size_t)j * a.stride * slice + row, a.act, dz);
+        store_dsig<Lt>(a.dsig, (size_t)j * a.stride * slice + row, a.act, dz, on);
       }
       apply<V, NB, NV>(s, a.act, false);
 #pragma unroll

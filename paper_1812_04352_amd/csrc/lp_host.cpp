@@ -626,8 +626,10 @@ size_t lp_dsig_bytes(const lp_problem* p) {
   g_err.clear();
   if (!lp::dsig_supported(shape_of(p))) return 0;
   if (p->layer == LP_CONV3X3) return (size_t)p->N * p->B * lp::conv_dsig_block_bytes(shape_of(p));
-  const size_t per = p->act == LP_RELU ? 1 : esize(p);
-  return (size_t)p->N * p->B * qdim(p) * per;
+  const size_t vals = (size_t)p->N * p->B * qdim(p);
+  // ReLU: one bit per value at widths 32 and 64, one byte at width 220
+  if (p->act == LP_RELU) return qdim(p) == 220 ? vals : vals / 8;
+  return vals * esize(p);
 }
 
 // The record is only written and read where the kernels support it, so a

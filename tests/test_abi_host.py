@@ -107,8 +107,11 @@ def test_workspace_sizes():
 
 
 def test_dsig_record_sizes(monkeypatch):
-    # one byte per value for ReLU, fp32 for smooth activations, none for the identity
-    assert L.lp_dsig_bytes(_p(act="relu")) == 64 * 100 * 32
+    # one bit per value for ReLU (one byte at width 220), fp32 for smooth activations,
+    # none for the identity
+    assert L.lp_dsig_bytes(_p(act="relu")) == 64 * 100 * 32 // 8
+    assert L.lp_dsig_bytes(_p(act="relu", C=64)) == 64 * 100 * 64 // 8
+    assert L.lp_dsig_bytes(_p(act="relu", C=220)) == 64 * 100 * 220
     assert L.lp_dsig_bytes(_p(act="tanh")) == 64 * 100 * 32 * 4
     assert L.lp_dsig_bytes(_p(act="smoothrelu", C=64)) == 64 * 100 * 64 * 4
     assert L.lp_dsig_bytes(_p(act="identity")) == 0

@@ -88,7 +88,7 @@ def test_kernel_model_closed_forms():
 
 def test_record_bytes():
     assert bench.record_bytes(WORKLOADS[1]) == 0          # fp64 keeps no record
-    assert bench.record_bytes(WORKLOADS[2]) == 1          # ReLU: one byte per value
+    assert bench.record_bytes(WORKLOADS[2]) == 0.125      # ReLU: one bit per value
     assert bench.record_bytes(WORKLOADS[3]) == 4          # tanh: fp32
     assert bench.record_bytes(WORKLOADS[4]) == 0.125      # conv ReLU: one bit per value
     assert bench.record_bytes(WORKLOADS[7]) == 4          # width 220, smoothed ReLU

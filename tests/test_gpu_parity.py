@@ -564,11 +564,14 @@ def _check_record(c, U, rec):
             np.testing.assert_allclose(got, want, rtol=0, atol=2e-5)
         return
     if wl.act == "relu":
-        got = rec[: z.size].cpu().numpy().reshape(z.shape)
+        if wl.q == 220:  # one byte per element
+            got = rec[: z.size].cpu().numpy().reshape(z.shape)
+        else:  # one bit per element in element order, least significant bit first
+            got = np.unpackbits(rec[: z.size // 8].cpu().numpy(), bitorder="little").reshape(z.shape)
         assert set(np.unique(got)) <= {0, 1}
         bad = got != want
         scale = np.abs(z).max()
-        assert np.all(np.abs(z[bad]) <= 1e-5 * scale), f"{bad.sum()} wrong record bytes"
+        assert np.all(np.abs(z[bad]) <= 1e-5 * scale), f"{bad.sum()} wrong record values"
     else:
         got = rec.view(torch.float32)[: z.size].cpu().numpy().reshape(z.shape)
         np.testing.assert_allclose(got, want, rtol=0, atol=2e-5)
