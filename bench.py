@@ -502,6 +502,16 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False, storage: str =
     roof["algorithmic_bytes_per_launch"] = byts / launches
     roof["algorithmic_flops_per_launch"] = flops / launches
 
+    # executed layer evaluations: every K v product the solves ran (a step Phi, an
+    # adjoint step with the record, the coarse step of an FRES sweep; an adjoint step
+    # that recomputes sigma' counts its two products), per second of solve time (the
+    # step without the gradient)
+    mac = wl.q * wl.q if wl.layer == "dense" else 9 * wl.C * wl.C * wl.H * wl.W
+    solve_flops = sum(kernel_model(wl, k, fwd_iters, adj_iters, rec_e, cpt)[1]
+                      for k in KIND_NAMES if k != "gradient")
+    solve_ms = ms_step - per_kind.get("gradient", 0.0)
+    products_per_s = solve_flops / (2.0 * mac) / (solve_ms / 1e3)
+
     # single-GPU context: the layer-serial forward pass (the baseline method)
     Us = torch.empty_like(Lam)
     Us[0] = U[0]
@@ -527,6 +537,7 @@ def measure(wl, steps: int, warmup: int, no_record: bool = False, storage: str =
         "device_memory_gb": peak_gb,
         "roofline": roof,
         "kernel_ms_per_step": {k: v for k, v in sorted(per_kind.items(), key=lambda t: -t[1])},
+        "layer_products_per_s": products_per_s,
         "serial_forward_ms": serial_ms,
         "residual_history": {"fwd": hist["fwd"], "adj": hist["adj"]},
     }
