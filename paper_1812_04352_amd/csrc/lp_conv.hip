@@ -427,7 +427,14 @@ void k_fwd(SweepArgs a, SGeo ga) {
   // layer; CORRF then also takes the product of the layer before the next C-point
   constexpr bool rec = REC && (MODE == SWEEP_CORRF || MODE == MODE_SERIAL);
   constexpr int extra = MODE == SWEEP_CORRF && rec ? 1 : 0;
-  f32x4 coarse[TPW];
+  // FRES on a coarse level parks the coarse step's value Phi_{l+1}(C_k) in its
+  // output row (the next level's right-hand side) instead of holding it in
+  // registers through the interval: with the level's right-hand-side rows also in
+  // flight, holding it spills, and each reload from scratch would wait for those
+  // rows too. The epilogue reads it back together with the upper C-point.
+  constexpr bool PARK = MODE == SWEEP_FRES && HG;
+  float* const gn = MODE == SWEEP_FRES ? static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + eo : nullptr;
+  f32x4 coarse[PARK ? 1 : TPW];
   for (int j = 0; j < nsteps; ++j) {
     // an empty asm statement makes the lane index opaque to the optimiser, so the
     // tile offsets derived from it are recomputed each step instead of being kept
@@ -461,7 +468,14 @@ void k_fwd(SweepArgs a, SGeo ga) {
     const float* gi = !HG && G ? G + (kc + j + 1) * slice + eo : nullptr;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      if (MODE == SWEEP_FRES && j == 0) coarse[tt] = v[tt] + hc * z[tt];
+      if (MODE == SWEEP_FRES && j == 0) {
+        if constexpr (PARK) {
+          const Px p = px_of(g, t0 + tt, lane);
+          if (p.ok) st_px(gn, v[tt] + hc * z[tt], g, p);
+        } else {
+          coarse[tt] = v[tt] + hc * z[tt];
+        }
+      }
       v[tt] = v[tt] + hl * z[tt];
       if constexpr (HG) v[tt] += gv[tt];
       else if (gi) v[tt] += ld_px(gi, g, px_of(g, t0 + tt, lane));
@@ -500,16 +514,36 @@ void k_fwd(SweepArgs a, SGeo ga) {
     }
   } else if (MODE == SWEEP_FRES) {
     const float* cn = Cs + (size_t)(k + 1) * a.cs_stride * slice + eo;
-    float* gn = static_cast<float*>(a.Gn) + (size_t)(k + 1) * slice + eo;
     double acc = 0.0;
+    if constexpr (PARK) {
+      asm volatile("" ::: "memory");  // read the parked row back from memory
+      f32x4 cv[TPW], pk[TPW];
 #pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) {
-      const Px p = px_of(g, t0 + tt, lane);
-      if (p.ok) {
-        const f32x4 rr = v[tt] - ld_px(cn, g, p);
+      for (int tt = 0; tt < TPW; ++tt) {
+        const Px p = px_of(g, t0 + tt, lane);
+        cv[tt] = ld_px(cn, g, p);
+        pk[tt] = ld_px(gn, g, p);  // this lane's own step-0 stores (ghost lanes: unused)
+      }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
-        st_px(gn, v[tt] - coarse[tt], g, p);  // g_{l+1}^{k+1} = f_{k+1} - Phi_{l+1}(C_k)
+      for (int tt = 0; tt < TPW; ++tt) {
+        const Px p = px_of(g, t0 + tt, lane);
+        if (p.ok) {
+          const f32x4 rr = v[tt] - cv[tt];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
+          st_px(gn, v[tt] - pk[tt], g, p);  // g_{l+1}^{k+1} = f_{k+1} - Phi_{l+1}(C_k)
+        }
+      }
+    } else {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        const Px p = px_of(g, t0 + tt, lane);
+        if (p.ok) {
+          const f32x4 rr = v[tt] - ld_px(cn, g, p);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc += (double)rr[r] * (double)rr[r];
+          st_px(gn, v[tt] - coarse[tt], g, p);  // g_{l+1}^{k+1} = f_{k+1} - Phi_{l+1}(C_k)
+        }
       }
     }
     if (a.xn_every > 0 && (k + 1) % a.xn_every == 0)
