@@ -410,11 +410,26 @@ void k_fwd(SweepArgs a, SGeo ga) {
     if (MODE == SWEEP_CORRF) vsrc = Vn + (size_t)k * slice + eo;
   }
   f32x4 v[TPW];
+  if constexpr (MODE == SWEEP_CORRF) {
+    // every load of the starting state is issued before the first use: a test of
+    // vsrc inside the tile loop splits it into one wait per tile (measured 4.8 %
+    // faster here; the FC sweep measured slower with it and keeps the tile loop)
 #pragma unroll
-  for (int tt = 0; tt < TPW; ++tt) {
-    const Px p = px_of(g, t0 + tt, lane);
-    v[tt] = ld_px(src, g, p);
-    if (vsrc) v[tt] = v[tt] + (ld_px(vsrc, g, p) - v[tt]);
+    for (int tt = 0; tt < TPW; ++tt) v[tt] = ld_px(src, g, px_of(g, t0 + tt, lane));
+    if (vsrc) {
+      f32x4 cv[TPW];
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) cv[tt] = ld_px(vsrc, g, px_of(g, t0 + tt, lane));
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) v[tt] = v[tt] + (cv[tt] - v[tt]);
+    }
+  } else {
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      const Px p = px_of(g, t0 + tt, lane);
+      v[tt] = ld_px(src, g, p);
+      if (vsrc) v[tt] = v[tt] + (ld_px(vsrc, g, p) - v[tt]);
+    }
   }
   __syncthreads();  // halo zeroed
 #pragma unroll
@@ -621,13 +636,22 @@ void k_adj(SweepArgs a, SGeo ga) {
     src = Cs + (size_t)(k + 1) * a.cs_stride * slice + eo;
     if (MODE == SWEEP_CORRF) vsrc = Vn + (size_t)(k + 1) * slice + eo;
   }
+  // every load of the starting values is issued before the first use: a test of
+  // vsrc inside the tile loop splits it into one wait per tile (measured: adjoint
+  // CORRF 6.6 % faster, FC unchanged)
   f32x4 lam[TPW], un[TPW];
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt) {
     const Px p = px_of(g, t0 + tt, lane);
     lam[tt] = ld_px(src, g, p);
-    if (vsrc) lam[tt] = lam[tt] + (ld_px(vsrc, g, p) - lam[tt]);
     if (!REC) un[tt] = ld_px(Uf + (size_t)(top - 1) * ustep + eo, g, p);
+  }
+  if (vsrc) {
+    f32x4 cv[TPW];
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) cv[tt] = ld_px(vsrc, g, px_of(g, t0 + tt, lane));
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) lam[tt] = lam[tt] + (cv[tt] - lam[tt]);
   }
   __syncthreads();  // halo zeroed
 #pragma unroll
