@@ -1253,12 +1253,17 @@ void k_adj_iv(SweepArgs a) {
 // scales by h (deterministic).
 constexpr int GRAD_WAVES = 4;
 
+// With the record (REC) the layer weights are not needed (no forward product), so
+// they are not staged: the workgroup then takes 67 KB of LDS, two fit on a CU, and
+// the kernel is held to two waves per SIMD (left free it takes about 276
+// registers, one wave, and each chunk's loads are waited on in full).
 template <int Q, bool REC>
-__global__ __launch_bounds__(64 * GRAD_WAVES) void k_grad(GradArgs a) {
+__global__ __launch_bounds__(64 * GRAD_WAVES) __attribute__((amdgpu_waves_per_eu(REC ? 2 : 1, 8)))
+void k_grad(GradArgs a) {
   using C = Cfg<Q, GRAD_WAVES>;
   constexpr int MB = C::MB;
   constexpr int TL = Q + 1;  // tile row (floats)
-  __shared__ float W[C::WSZ];
+  __shared__ float W[REC ? 1 : C::WSZ];
   __shared__ float tile[GRAD_WAVES][2][32 * TL];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int h = lane >> 5, li = lane & 31;
@@ -1270,12 +1275,12 @@ __global__ __launch_bounds__(64 * GRAD_WAVES) void k_grad(GradArgs a) {
   const size_t slice = (size_t)a.B * Q;
   const float* U = static_cast<const float*>(a.U) + (size_t)blockIdx.x * slice;
   const float* L = static_cast<const float*>(a.Lam) + (size_t)(n + 1) * slice;
-  {
+  if constexpr (!REC) {
     WRegs<Q, GRAD_WAVES> wr;
     w_fetch<Q, GRAD_WAVES>(wr, static_cast<const float*>(a.K), static_cast<const float*>(a.b), n);
     w_put<Q, GRAD_WAVES>(W, wr);
+    __syncthreads();
   }
-  __syncthreads();
   f32x16 acc[MB][MB];
 #pragma unroll
   for (int x = 0; x < MB; ++x)
