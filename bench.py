@@ -97,9 +97,10 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0, cp
     Each launch also reads the weights of its level once: N_l (q^2 + q) values.
     With a sigma' record of rec bytes per value (rrow per example row), the
     adjoint reads one record row per step instead of a primal row and skips the
-    forward product (2q^2 flops per step), the gradient (width 64) reads the
-    record instead of K_n and takes no forward product, and the final finest CORRF writes c
-    record rows per interval and takes one more product.
+    forward product (2q^2 flops per step), the gradient (width 64, width 32 with
+    ReLU's bit record, convolution) reads the record instead of K_n and takes no
+    forward product, and the final finest CORRF writes c record rows per interval
+    and takes one more product.
     With C-point storage (cpt) the finest adjoint sweeps read one primal row (the
     lower C-point) per interval and recompute the interval's states with c forward
     products; the finest forward CORRF only corrects the C-points (read 2, write 1,
@@ -127,8 +128,11 @@ def kernel_model(wl, kind: str, fwd_iters: int, adj_iters: int, rec: int = 0, cp
         return ((wl.N // c + 3 * wl.N) * row + 3 * wl.N * nweights * e,
                 (4.0 + 2.0 * (c - 1) / c) * mac * B * wl.N, 1)
     if kind == "gradient":
-        if rec and (wl.layer != "dense" or q >= 64):  # the dense width-32 kernel recomputes sigma'
-            return 2 * wl.N * row + wl.N * rrow + wl.N * nweights * e, 2.0 * mac * B * wl.N, 1
+        # the dense width-32 kernel recomputes sigma' for smooth activations
+        if rec and (wl.layer != "dense" or q >= 64 or wl.act == "relu"):
+            # (with the record, the dense kernels stage no weights)
+            return 2 * wl.N * row + wl.N * rrow + (wl.N * nweights * e if wl.layer != "dense" else 0), \
+                2.0 * mac * B * wl.N, 1
         return 2 * wl.N * row + 2 * wl.N * nweights * e, 4.0 * mac * B * wl.N, 1
     # With FCF the finest level's correction is applied inside the next cycle's FC
     # sweep (one more row read per interval from the second cycle on) and its

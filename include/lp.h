@@ -221,9 +221,9 @@ int32_t lp_mgrit_adjoint(const lp_problem* prob, const lp_mgrit* mg, const void*
  * summed over the batch in a fixed order (bitwise reproducible).
  * dK like K, db like b; both written. The 1/B factor of the mean loss is
  * expected inside Lam (it is part of the terminal value). dsig (nullable): the
- * sigma' record of U; the width-32 kernel recomputes sigma' even when given one
- * (there the extra record read costs more HBM time than the product it saves),
- * with results equal to rounding. */
+ * sigma' record of U; the width-32 kernel with a smooth activation recomputes
+ * sigma' even when given one (there an fp32 record row costs more HBM time than
+ * the product it saves), with results equal to rounding. */
 int32_t lp_gradient(const lp_problem* prob, const void* K, const void* b, const void* U,
                     const void* dsig, const void* Lam, void* dK, void* db, void* ws, size_t ws_bytes,
                     void* stream);

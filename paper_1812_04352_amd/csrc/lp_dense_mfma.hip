@@ -1254,11 +1254,11 @@ void k_adj_iv(SweepArgs a) {
 constexpr int GRAD_WAVES = 4;
 
 // With the record (REC) the layer weights are not needed (no forward product), so
-// they are not staged: the workgroup then takes 67 KB of LDS, two fit on a CU, and
-// the kernel is held to two waves per SIMD (left free it takes about 276
-// registers, one wave, and each chunk's loads are waited on in full).
+// they are not staged: at width 64 the workgroup then takes 67 KB of LDS, two fit
+// on a CU, and the kernel is held to two waves per SIMD (left free it takes about
+// 276 registers, one wave, and each chunk's loads are waited on in full).
 template <int Q, bool REC>
-__global__ __launch_bounds__(64 * GRAD_WAVES) __attribute__((amdgpu_waves_per_eu(REC ? 2 : 1, 8)))
+__global__ __launch_bounds__(64 * GRAD_WAVES) __attribute__((amdgpu_waves_per_eu(REC && Q == 64 ? 2 : 1, 8)))
 void k_grad(GradArgs a) {
   using C = Cfg<Q, GRAD_WAVES>;
   constexpr int MB = C::MB;
@@ -1377,10 +1377,11 @@ __global__ __launch_bounds__(256) void k_grad_final(GradArgs a, int nw, int nbia
 // First pass over `nl` layers starting at a.n0 (grid: layers x chunks).
 template <int Q>
 hipError_t grad_partials(const GradArgs& a, long nl, hipStream_t st) {
-  // at width 32 the kernel is HBM-bound and a third row read per layer costs more
-  // than the forward product it replaces
-  constexpr bool REC_OK = Q >= 64;
-  if (REC_OK && a.dsig) launch(k_grad<Q, REC_OK>, dim3((unsigned)nl, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
+  // at width 32 the kernel is HBM-bound: an fp32 record row read per layer costs
+  // more than the forward product it replaces, ReLU's bit record (1/32 of a row)
+  // does not
+  const bool rec = a.dsig && (Q >= 64 || a.act == ACT_RELU);
+  if (rec) launch(k_grad<Q, true>, dim3((unsigned)nl, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
   else launch(k_grad<Q, false>, dim3((unsigned)nl, a.nchunks), 64 * GRAD_WAVES, 0, st, a);
   return hipGetLastError();
 }
