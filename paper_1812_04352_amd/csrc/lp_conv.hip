@@ -883,8 +883,9 @@ __global__ __launch_bounds__(64 * MAXW) void k_resid(ResidArgs a, SGeo g) {
 // dWbig[(co,dy)][k] += s[co][2Y+dy][x] * patch[P][k] with the pair-pixels as
 // contraction index (k-slice = 4 pair-pixels, lane group = one of them): A = s
 // (rows (co,dy)), B = patches of u (96 columns in 6 blocks of 16). db sums s
-// from registers. The next example's u is loaded during the contraction. Waves
-// and lanes are combined in a fixed order.
+// from registers. The next example's u (and, with a record, its lambda and
+// record word) is loaded during the contraction. Waves and lanes are combined in
+// a fixed order.
 constexpr int GOUT = 16 * 96 + CH;  // dWbig then db per chunk
 
 template <int GH, int GW, int RK>
@@ -918,12 +919,16 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   for (int nb = 0; nb < 6; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float db0 = 0.f, db1 = 0.f;  // channels 2*(lane/16) and 2*(lane/16)+1
   const int nsl = (g.NPP + 3) / 4;  // pair-pixel slices of 4
-  f32x4 un[TPW];
+  f32x4 un[TPW], lam[TPW];
+  RecW<RB> rw;
   if (e0 < e1) {
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-      un[tt] = ld_px(U + (size_t)e0 * g.q, g, px_of(g, t0 + tt, lane));
+      const Px p = px_of(g, t0 + tt, lane);
+      un[tt] = ld_px(U + (size_t)e0 * g.q, g, p);
+      if constexpr (REC) lam[tt] = ld_px(Lm + (size_t)e0 * g.q, g, p);
     }
+    if constexpr (REC) rw = rec_load<RB>(a.dsig, (size_t)n * a.B + e0, g, t0, lane);
   }
   __syncthreads();  // buffers zeroed, weights staged
   float wf[24];
@@ -939,17 +944,13 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   __syncthreads();
   for (int e = e0; e < e1; ++e) {
     const bool more = e + 1 < e1;
-    f32x4 z[TPW], lam[TPW];
-#pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) {
-      const Px p = px_of(g, t0 + tt, lane);
-      lam[tt] = ld_px(Lm + (size_t)e * g.q, g, p);
-    }
+    f32x4 z[TPW];
     if constexpr (REC) {
-      const RecW<RB> r = rec_load<RB>(a.dsig, (size_t)n * a.B + e, g, t0, lane);
 #pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) z[tt] = rec_val<RB>(r, tt);
+      for (int tt = 0; tt < TPW; ++tt) z[tt] = rec_val<RB>(rw, tt);
     } else {
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) lam[tt] = ld_px(Lm + (size_t)e * g.q, g, px_of(g, t0 + tt, lane));
       conv_tiles(z, wf, bu, g, t0, lane, bias);
       act_tiles<true>(z, a.act);
     }
@@ -964,10 +965,16 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
       }
     }
     __syncthreads();
-    // the next example's primal state arrives while the contraction runs
+    // the next example's primal state, adjoint and record arrive while the
+    // contraction runs
     if (more) {
 #pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) un[tt] = ld_px(U + (size_t)(e + 1) * g.q, g, px_of(g, t0 + tt, lane));
+      for (int tt = 0; tt < TPW; ++tt) {
+        const Px p = px_of(g, t0 + tt, lane);
+        un[tt] = ld_px(U + (size_t)(e + 1) * g.q, g, p);
+        if constexpr (REC) lam[tt] = ld_px(Lm + (size_t)(e + 1) * g.q, g, p);
+      }
+      if constexpr (REC) rw = rec_load<RB>(a.dsig, (size_t)n * a.B + e + 1, g, t0, lane);
     }
     // contraction over pair-pixels
     for (int sl = wave; sl < nsl; sl += g.NW) {
