@@ -356,7 +356,26 @@ __device__ __forceinline__ double wg_sum_n(double v, double* red, int nw) {
   return s;
 }
 
-// RK: the sigma' record kind (0 none, 1 ReLU bytes, 2 fp32 values). HG: the level
+// The sweeps' workgroup for (interval, example). Workgroups go to the eight XCDs
+// in turn by linear id, and each XCD has its own L2. This mapping hands each XCD
+// one contiguous range of the interval-fastest order instead, so the intervals
+// of one example, which share their C-points, run on one XCD at about the same
+// time, and the eight XCDs work on examples far apart. It is a bijection of the
+// grid for any size. (Measured on 28x28 images, 1024 examples, 512 layers: the
+// correction sweeps run 8-14 % faster; a mapping that gives each XCD a block of
+// intervals for every example cuts the fetched bytes further but runs no faster
+// than the plain order.)
+struct Blk {
+  int k, ex;
+};
+__device__ __forceinline__ Blk sweep_block() {
+  const unsigned nx = gridDim.x, T = nx * gridDim.y;
+  const unsigned p = blockIdx.x + blockIdx.y * nx, x = p % 8u;
+  const unsigned L = x * (T / 8u) + min(x, T % 8u) + p / 8u;
+  return {(int)(L % nx), (int)(L / nx)};
+}
+
+// RK: the sigma' record kind (0 none, 1 ReLU bits, 2 fp32 values). HG: the level
 // has right-hand-side rows (every level but the finest); a step requests its row
 // before the product, so the load overlaps the matrix-core work (three waves per
 // SIMD leave room for it).
@@ -379,8 +398,9 @@ void k_fwd(SweepArgs a, SGeo ga) {
   constexpr bool UNIF = MODE == SWEEP_CORRF;
   const int wave = threadIdx.x >> 6;
   const int t0 = (UNIF ? __builtin_amdgcn_readfirstlane(wave) : wave) * TPW, nt = blockDim.x;
-  const int k = blockIdx.x, Nc = gridDim.x;
-  const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
+  const Blk wb = sweep_block();
+  const int k = wb.k, Nc = gridDim.x;
+  const size_t slice = (size_t)a.B * g.q, eo = (size_t)wb.ex * g.q;
   const float* K = static_cast<const float*>(a.K);
   const float* bb = static_cast<const float*>(a.b);
   float* X = static_cast<float*>(a.X);
@@ -479,7 +499,7 @@ void k_fwd(SweepArgs a, SGeo ga) {
       conv_tiles(z, wr, buf, g, t0, lane, bias);
     }
     if constexpr (rec) {
-      const size_t blk = (size_t)(kc + j) * a.stride * a.B + blockIdx.y;
+      const size_t blk = (size_t)(kc + j) * a.stride * a.B + wb.ex;
       rec_put<RB>(a.dsig, blk, g, t0, lane, z, a.act);
     }
     act_tiles<false>(z, a.act);
@@ -522,7 +542,7 @@ void k_fwd(SweepArgs a, SGeo ga) {
     float wr[24];
     gather_w<false>(wr, swc, lane);
     conv_tiles(z, wr, buf, g, t0, lane, bias_px(swc, lane));
-    const size_t blk = (size_t)(kc + nsteps) * a.stride * a.B + blockIdx.y;
+    const size_t blk = (size_t)(kc + nsteps) * a.stride * a.B + wb.ex;
     rec_put<RB>(a.dsig, blk, g, t0, lane, z, a.act);
   }
   if (MODE == SWEEP_FC) {
@@ -571,7 +591,7 @@ void k_fwd(SweepArgs a, SGeo ga) {
     if (k == 0) row_copy(static_cast<float*>(a.Xn) + eo, Cs + eo, g.q, nt);
     if (a.partial) {
       const double s = wg_sum_n(acc, red, g.NW);
-      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
+      if (threadIdx.x == 0) a.partial[(size_t)k * gridDim.y + wb.ex] = s;
     }
   } else if (MODE == SWEEP_CORRF) {
     if (k == Nc - 1) {
@@ -606,8 +626,9 @@ void k_adj(SweepArgs a, SGeo ga) {
   constexpr bool UNIF = MODE == SWEEP_FRES && RK != 0;
   const int wave = threadIdx.x >> 6;
   const int t0 = (UNIF ? __builtin_amdgcn_readfirstlane(wave) : wave) * TPW, nt = blockDim.x;
-  const int k = blockIdx.x, Nc = gridDim.x;
-  const size_t slice = (size_t)a.B * g.q, eo = (size_t)blockIdx.y * g.q;
+  const Blk wb = sweep_block();
+  const int k = wb.k, Nc = gridDim.x;
+  const size_t slice = (size_t)a.B * g.q, eo = (size_t)wb.ex * g.q;
   const float* K = static_cast<const float*>(a.K);
   const float* bb = static_cast<const float*>(a.b);
   const float* Uf = static_cast<const float*>(a.Uf);
@@ -668,7 +689,7 @@ void k_adj(SweepArgs a, SGeo ga) {
   f32x4 dd[TPW];  // sigma'(z) of the step (after the loop: of the last one)
   // with the record, the words of step j + 1 are requested during step j
   RecW<RB> rn;
-  if constexpr (REC) rn = rec_load<RB>(a.dsig, (size_t)(top - 1) * a.stride * a.B + blockIdx.y, g, t0, lane);
+  if constexpr (REC) rn = rec_load<RB>(a.dsig, (size_t)(top - 1) * a.stride * a.B + wb.ex, g, t0, lane);
   for (int j = 0; j < nsteps; ++j) {
     // tile offsets recomputed each step (see k_fwd) where that lowers the
     // register count (compiler-measured per variant)
@@ -686,7 +707,7 @@ void k_adj(SweepArgs a, SGeo ga) {
     if constexpr (REC) {
 #pragma unroll
       for (int tt = 0; tt < TPW; ++tt) dd[tt] = rec_val<RB>(rn, tt);
-      if (more) rn = rec_load<RB>(a.dsig, (size_t)(i - 1) * a.stride * a.B + blockIdx.y, g, t0, lane);
+      if (more) rn = rec_load<RB>(a.dsig, (size_t)(i - 1) * a.stride * a.B + wb.ex, g, t0, lane);
     } else {
       float wr[24];
       gather_w<false>(wr, swc, lane);
@@ -792,7 +813,7 @@ void k_adj(SweepArgs a, SGeo ga) {
       row_copy(static_cast<float*>(a.Xn) + (size_t)Nc * slice + eo, Cs + (size_t)Nc * a.cs_stride * slice + eo, g.q, nt);
     if (a.partial) {
       const double s = wg_sum_n(acc, red, g.NW);
-      if (threadIdx.x == 0) a.partial[(size_t)blockIdx.x * gridDim.y + blockIdx.y] = s;
+      if (threadIdx.x == 0) a.partial[(size_t)k * gridDim.y + wb.ex] = s;
     }
   } else if (MODE == SWEEP_CORRF) {
     if (k == 0) {
