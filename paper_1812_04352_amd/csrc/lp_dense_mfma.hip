@@ -1020,15 +1020,15 @@ __global__ __launch_bounds__(64 * WAVES) void k_fwd_iv(SweepArgs a) {
 // C-point, or the staged C-point and coarse value of a correction; FRES: the upper
 // and the lower C-point), what each step is linearised at (record rows, primal
 // rows, or the lower primal C-point), and the right-hand-side rows.
-template <typename Lt, int NS, bool REC, bool RBYTES, bool CPT, bool HASG>
+template <typename Lt, int NS, bool REC, bool RBITS, bool CPT, bool HASG>
 struct AdjRows {
   typename Lt::V a[Lt::NB], c[Lt::NB];
-  RecRow<Lt, RBYTES> rr[REC ? NS : 1];
+  RecRow<Lt, RBITS> rr[REC ? NS : 1];
   typename Lt::V u[(REC || CPT) ? 1 : NS][Lt::NB];
   typename Lt::V g[HASG ? NS : 1][Lt::NB];
 };
 
-// REC: sigma' comes from the record (ReLU: RBYTES, one bit per value) instead of
+// REC: sigma' comes from the record (ReLU: RBITS, one bit per value) instead of
 // the layer product at the primal state.
 // CPT (finest level, C-point storage): Uf holds the fine C-points only (row k is
 // u^{kc}); the interval first recomputes its F-point states and sigma'(z_n) for
@@ -1037,21 +1037,21 @@ struct AdjRows {
 // TM: tiles per workgroup (0: one; 1: several; 2: several, each one's rows
 // requested during the previous one's steps). CORR: FC reads C + (V - C).
 //
-// Resident waves per SIMD the compiler must allow for. Width 32, finest level, byte
+// Resident waves per SIMD the compiler must allow for. Width 32, finest level, bit
 // record, one tile: eight. Width 64: two, which is what LDS allows (70 KB of weights
 // per workgroup, two workgroups per CU); left to itself the compiler gives the
 // fp32-record sweeps 260 registers, one wave per SIMD. The recomputing FRES sweeps
 // that walk tiles are left free: held to 256 registers they spill.
-template <int Q, int MODE, bool REC, bool RBYTES, bool HASG, bool CPT, int TM>
+template <int Q, int MODE, bool REC, bool RBITS, bool HASG, bool CPT, int TM>
 constexpr int adj_iv_waves() {
-  if (Q == 32) return !HASG && REC && RBYTES && TM == 0 ? 8 : 1;
+  if (Q == 32) return !HASG && REC && RBITS && TM == 0 ? 8 : 1;
   if (Q == 64) return MODE == SWEEP_FRES && !REC && !CPT && TM != 0 ? 1 : 2;
   return 1;
 }
 
-template <int Q, int MODE, int WAVES, bool REC, bool RBYTES, bool HASG, bool CPT, int TM, bool CORR>
+template <int Q, int MODE, int WAVES, bool REC, bool RBITS, bool HASG, bool CPT, int TM, bool CORR>
 __global__ __launch_bounds__(64 * WAVES)
-__attribute__((amdgpu_waves_per_eu(adj_iv_waves<Q, MODE, REC, RBYTES, HASG, CPT, TM>(), 8)))
+__attribute__((amdgpu_waves_per_eu(adj_iv_waves<Q, MODE, REC, RBITS, HASG, CPT, TM>(), 8)))
 void k_adj_iv(SweepArgs a) {
   static_assert(!(CPT && (REC || HASG)), "C-point storage is a finest-level mode without a record");
   constexpr int EX = 16;
@@ -1061,10 +1061,10 @@ void k_adj_iv(SweepArgs a) {
   constexpr int NB = Lt::NB, NV = Lt::NV;
   constexpr int NS = MODE == SWEEP_CORRF ? IV_CF - 1 : IV_CF;
   constexpr int NW = CPT ? IV_CF : NS;  // layers staged: the recompute needs all of the interval's
-  // at eight waves per SIMD (width 32, finest level, byte record, no prefetch) the
+  // at eight waves per SIMD (width 32, finest level, bit record, no prefetch) the
   // registers go to occupancy, and FRES reads its lower C-point after the steps
-  constexpr bool LATE_CK = MODE == SWEEP_FRES && Q == 32 && !HASG && REC && RBYTES && TM == 0;
-  using Rows = AdjRows<Lt, NS, REC, RBYTES, CPT, HASG>;
+  constexpr bool LATE_CK = MODE == SWEEP_FRES && Q == 32 && !HASG && REC && RBITS && TM == 0;
+  using Rows = AdjRows<Lt, NS, REC, RBITS, CPT, HASG>;
   __shared__ float W[NW * C::WSZ];
   __shared__ double red[WAVES];
   const int lane = threadIdx.x & 63;
