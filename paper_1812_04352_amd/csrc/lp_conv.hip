@@ -905,8 +905,10 @@ __global__ __launch_bounds__(64 * MAXW) void k_resid(ResidArgs a, SGeo g) {
 // contraction index (k-slice = 4 pair-pixels, lane group = one of them): A = s
 // (rows (co,dy)), B = patches of u (96 columns in 6 blocks of 16). db sums s
 // from registers. The next example's u (and, with a record, its lambda and
-// record word) is loaded during the contraction. Waves and lanes are combined in
-// a fixed order.
+// record word) is loaded during the contraction; with a record its s is written
+// to LDS together with its u, so an example takes two barriers instead of three.
+// The contraction loop is wave-uniform and reads each slice's operands while the
+// previous slice's products run. Waves and lanes are combined in a fixed order.
 constexpr int GOUT = 16 * 96 + CH;  // dWbig then db per chunk
 
 template <int GH, int GW, int RK>
@@ -955,26 +957,8 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
   float wf[24];
   gather_w<false>(wf, sw, lane);
   const f32x4 bias = bias_px(sw, lane);
-  if (e0 < e1) {
-#pragma unroll
-    for (int tt = 0; tt < TPW; ++tt) {
-      const Px p = px_of(g, t0 + tt, lane);
-      if (p.ok) put_px(bu, un[tt], g, p);
-    }
-  }
-  __syncthreads();
-  for (int e = e0; e < e1; ++e) {
-    const bool more = e + 1 < e1;
-    f32x4 z[TPW];
-    if constexpr (REC) {
-#pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) z[tt] = rec_val<RB>(rw, tt);
-    } else {
-#pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) lam[tt] = ld_px(Lm + (size_t)e * g.q, g, px_of(g, t0 + tt, lane));
-      conv_tiles(z, wf, bu, g, t0, lane, bias);
-      act_tiles<true>(z, a.act);
-    }
+  // s = sigma' * lam at the lane's own pixels into the s image, and into db
+  auto put_s = [&](const f32x4 (&z)[TPW]) {
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
       const Px p = px_of(g, t0 + tt, lane);
@@ -985,7 +969,49 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
         db1 += s[2] + s[3];
       }
     }
-    __syncthreads();
+  };
+  // matrix-core operands of pair-pixel slice sl: A = s at (co, dy) = lane % 16 of
+  // pair-pixel 4 sl + lane / 16, B = its patch entries 16 nb + lane % 16 (zero A
+  // past the last pair-pixel, whose address is clamped)
+  auto ld_slice = [&](int sl, float& av, float (&bv)[6]) {
+    const int P = 4 * sl + (lane >> 4);
+    const bool ok = P < g.NPP;
+    const int Pc = ok ? P : g.NPP - 1;
+    const int Y = Pc / g.W, x = Pc - Y * g.W;
+    const int nA = lane & 15, co = nA >> 1, dy = nA & 1;
+    av = ok ? bs[co * g.CS + (2 * Y + dy + 1) * g.PW + x + 1] : 0.f;
+    const int pb = 2 * Y * g.PW + x;  // (row 2Y-1+r, col x-1+tx) padded = (2Y+r, x+tx)
+#pragma unroll
+    for (int nb = 0; nb < 6; ++nb) bv[nb] = bu[pb + koff[nb]];
+  };
+  // with a record, s of an example needs no product, so it is written together
+  // with the example's u, before one barrier (two barriers per example, not three)
+  auto put_rec_s = [&]() {
+    f32x4 z[TPW];
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) z[tt] = rec_val<RB>(rw, tt);
+    put_s(z);
+  };
+  if (e0 < e1) {
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      const Px p = px_of(g, t0 + tt, lane);
+      if (p.ok) put_px(bu, un[tt], g, p);
+    }
+    if constexpr (REC) put_rec_s();
+  }
+  __syncthreads();
+  for (int e = e0; e < e1; ++e) {
+    const bool more = e + 1 < e1;
+    if constexpr (!REC) {
+      f32x4 z[TPW];
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) lam[tt] = ld_px(Lm + (size_t)e * g.q, g, px_of(g, t0 + tt, lane));
+      conv_tiles(z, wf, bu, g, t0, lane, bias);
+      act_tiles<true>(z, a.act);
+      put_s(z);
+      __syncthreads();
+    }
     // the next example's primal state, adjoint and record arrive while the
     // contraction runs
     if (more) {
@@ -997,18 +1023,22 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
       }
       if constexpr (REC) rw = rec_load<RB>(a.dsig, (size_t)n * a.B + e + 1, g, t0, lane);
     }
-    // contraction over pair-pixels
-    for (int sl = wave; sl < nsl; sl += g.NW) {
-      const int P = 4 * sl + (lane >> 4);
-      const bool ok = P < g.NPP;
-      const int Pc = ok ? P : g.NPP - 1;
-      const int Y = Pc / g.W, x = Pc - Y * g.W;
-      const int nA = lane & 15, co = nA >> 1, dy = nA & 1;
-      const float av = ok ? bs[co * g.CS + (2 * Y + dy + 1) * g.PW + x + 1] : 0.f;
-      const int pb = 2 * Y * g.PW + x;  // (row 2Y-1+r, col x-1+tx) padded = (2Y+r, x+tx)
+    // contraction over pair-pixels, wave-uniform and pipelined: a slice's operands
+    // are read from LDS while the previous slice's products run (a slice past the
+    // end reads in bounds and contributes zero)
+    {
+      const int wv = __builtin_amdgcn_readfirstlane(wave);
+      float av, bv[6];
+      ld_slice(wv, av, bv);
+      for (int sl = wv; sl < nsl; sl += g.NW) {
+        float an, bn[6];
+        ld_slice(sl + g.NW, an, bn);
 #pragma unroll
-      for (int nb = 0; nb < 6; ++nb)
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bu[pb + koff[nb]], acc[nb], 0, 0, 0);
+        for (int nb = 0; nb < 6; ++nb) acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[nb], acc[nb], 0, 0, 0);
+        av = an;
+#pragma unroll
+        for (int nb = 0; nb < 6; ++nb) bv[nb] = bn[nb];
+      }
     }
     __syncthreads();
     if (more) {
@@ -1017,6 +1047,7 @@ __global__ __launch_bounds__(64 * MAXW) void k_grad(GradArgs a, SGeo ga) {
         const Px p = px_of(g, t0 + tt, lane);
         if (p.ok) put_px(bu, un[tt], g, p);
       }
+      if constexpr (REC) put_rec_s();
     }
     __syncthreads();
   }
