@@ -1257,6 +1257,15 @@ constexpr int GRAD_WAVES = 4;
 // they are not staged: at width 64 the workgroup then takes 67 KB of LDS, two fit
 // on a CU, and the kernel is held to two waves per SIMD (left free it takes about
 // 276 registers, one wave, and each chunk's loads are waited on in full).
+// Lanes of one wave exchanging data through LDS: a wave's LDS instructions run in
+// order, so a compiler fence and a wave barrier are enough between the writes and
+// the reads.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int Q, bool REC>
 __global__ __launch_bounds__(64 * GRAD_WAVES) __attribute__((amdgpu_waves_per_eu(REC && Q == 64 ? 2 : 1, 8)))
 void k_grad(GradArgs a) {
@@ -1291,17 +1300,35 @@ void k_grad(GradArgs a) {
   float dbacc = 0.f;  // lane < Q: column sum of s over this wave's examples
   float* st = tile[wave][0];
   float* ut = tile[wave][1];
-  for (int base = e0; base < e1; base += 32 * GRAD_WAVES) {
+  using Lt = Lay<Q, 32>;
+  // the rows of the wave's 32 examples from base on (zero past the chunk)
+  auto ld_rows = [&](int base, f32x16 (&u)[MB], f32x16 (&s)[MB]) {
     const int e = base + wave * 32 + li;
-    const bool on = e < e1;
-    const size_t row = (size_t)(on ? e : 0) * Q + 4 * h;
-    using Lt = Lay<Q, 32>;
-    f32x16 u[MB], s[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) u[mb] = s[mb] = 0.f;
-    if (on) {
-      Lt::load(u, U + row);
-      Lt::load(s, L + row);
+    if (e < e1) {
+      Lt::load(u, U + (size_t)e * Q + 4 * h);
+      Lt::load(s, L + (size_t)e * Q + 4 * h);
+    }
+  };
+  // At width 32 the next examples' rows are requested during the contraction
+  // (their registers cost no occupancy there); the tiles are the wave's own, so
+  // its lanes meet at wave barriers only.
+  constexpr bool PF = Q == 32;
+  f32x16 un[PF ? MB : 1], sn[PF ? MB : 1];
+  if constexpr (PF) ld_rows(e0, un, sn);
+  for (int base = e0; base < e1; base += 32 * GRAD_WAVES) {
+    const int e = base + wave * 32 + li;
+    const size_t row = (size_t)(e < e1 ? e : 0) * Q + 4 * h;
+    f32x16 u[MB], s[MB];
+    if constexpr (PF) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        u[mb] = un[mb];
+        s[mb] = sn[mb];
+      }
+    } else {
+      ld_rows(base, u, s);
     }
     {
       f32x16 z[MB];
@@ -1323,7 +1350,12 @@ void k_grad(GradArgs a) {
         st[li * TL + f] = s[mb][r];
         ut[li * TL + f] = u[mb][r];
       }
-    __syncthreads();
+    if constexpr (PF) {
+      wave_lds_sync();
+      if (base + 32 * GRAD_WAVES < e1) ld_rows(base + 32 * GRAD_WAVES, un, sn);
+    } else {
+      __syncthreads();
+    }
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       const int er = (2 * t + h) * TL + li;
@@ -1337,8 +1369,10 @@ void k_grad(GradArgs a) {
     }
     if (lane < Q)
       for (int t = 0; t < 32; ++t) dbacc += st[t * TL + lane];
-    __syncthreads();
+    if constexpr (PF) wave_lds_sync();
+    else __syncthreads();
   }
+  if constexpr (PF) __syncthreads();  // the combine below reuses every wave's tiles
   // combine the waves in order: wave w adds its accumulators into a Q x Q buffer
   float* red = &tile[0][0][0];  // Q*Q + Q floats fit in the tiles
   for (int w = 0; w < GRAD_WAVES; ++w) {
