@@ -14,13 +14,14 @@ namespace {
 
 constexpr int NT = 256;
 
-// X[dst_row0 + t*dst_step] = X[src_row] for t = 0..count-1 (16-byte units).
+// X[dst_row0 + t*dst_step] = X[src_row] for t = 0..count-1 (16-byte units; the
+// source row is not among the destinations). Each thread reads its units of the
+// source row once and writes them to every destination row.
 __global__ __launch_bounds__(NT) void k_copy_rows(uint4* X, size_t units, long src_row,
                                                   long dst_row0, long dst_step, long count) {
-  const size_t tot = units * (size_t)count;
-  for (size_t i = (size_t)blockIdx.x * NT + threadIdx.x; i < tot; i += (size_t)gridDim.x * NT) {
-    const size_t t = i / units, u = i - t * units;
-    X[(size_t)(dst_row0 + (long)t * dst_step) * units + u] = X[(size_t)src_row * units + u];
+  for (size_t u = (size_t)blockIdx.x * NT + threadIdx.x; u < units; u += (size_t)gridDim.x * NT) {
+    const uint4 v = X[(size_t)src_row * units + u];
+    for (long t = 0; t < count; ++t) X[(size_t)(dst_row0 + t * dst_step) * units + u] = v;
   }
 }
 
@@ -233,8 +234,7 @@ hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_
                             long count, hipStream_t st) {
   if (count <= 0 || slice_bytes == 0) return hipSuccess;
   const size_t units = slice_bytes / 16;
-  k_copy_rows<<<grid_for(units * (size_t)count), NT, 0, st>>>(static_cast<uint4*>(X), units, src_row,
-                                                              dst_row0, dst_step, count);
+  k_copy_rows<<<grid_for(units), NT, 0, st>>>(static_cast<uint4*>(X), units, src_row, dst_row0, dst_step, count);
   return hipGetLastError();
 }
 

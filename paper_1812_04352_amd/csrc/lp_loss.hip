@@ -259,8 +259,13 @@ hipError_t loss_t(int B, int q, int nc, const void* uN, const void* Wc, const vo
                                                                    nc);
     return hipGetLastError();
   }
-  k_head<T, false><<<(B + per - 1) / per, NT, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu, (const T*)c, z,
-                                                       loss, (T*)lamN, nullptr, B, q, nc, S);
+  // W and u^N do not fit in LDS (wide states): a whole wave per example, so its
+  // dot products split over 64 lanes and the batch gives NT/64 examples per
+  // workgroup (a segment as narrow as the class count would leave most CUs idle)
+  const int Sw = nc <= 64 ? 64 : S;
+  k_head<T, false><<<(B + NT / Sw - 1) / (NT / Sw), NT, 0, st>>>((const T*)uN, (const T*)Wc, (const T*)mu,
+                                                                 (const T*)c, z, loss, (T*)lamN, nullptr, B, q,
+                                                                 nc, Sw);
   k_mean<<<1, NT_MEAN, 0, st>>>(loss, B, J);
   k_wpart<T><<<dim3(nch, (unsigned)((nw + NT - 1) / NT)), NT, 0, st>>>((const T*)uN, z, part, B, q, nc);
   k_wfinal<T><<<(unsigned)((nw + FO - 1) / FO), NT, 0, st>>>(part, nch, nw, (T*)dW, (T*)dmu, nullptr, B, q, nc);
