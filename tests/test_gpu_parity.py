@@ -802,18 +802,24 @@ def test_accuracy(name, wl):
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("q,nc,B", [(32, 1, 45), (32, 3, 257), (32, 17, 45), (32, 64, 45), (220, 10, 33),
-                                    (220, 64, 7), (8, 5, 1)])
+                                    (220, 64, 7), (8, 5, 1), (1152, 10, 37), (1152, 64, 5), (6272, 10, 9)])
 def test_loss_head_class_counts(q, nc, B):
     """Softmax head, loss, terminal adjoint and classifier gradient against the
     oracle (Section 2.1 loss, Section 2.3 terminal condition) over class counts
     that set the lanes per example (1 .. 64) and batches that leave the last
-    workgroup partly empty; width 220 with 64 classes still stages W in LDS."""
+    workgroup partly empty; width 220 with 64 classes still stages W in LDS, and
+    the widths 1152 and 6272 (convolution states) take the path that does not,
+    one wave per example."""
     rng = np.random.default_rng(1000 * q + nc + B)
     uN = rng.standard_normal((B, q)).astype(np.float32)
     W = (0.3 * rng.standard_normal((nc, q))).astype(np.float32)
     mu = (0.1 * rng.standard_normal(nc)).astype(np.float32)
     onehot = np.eye(nc, dtype=np.float32)[rng.integers(0, nc, B)]
-    p = L.problem("f32", "dense", "relu", N=4, B=B, C=q, h=0.25)
+    if q % 72 == 0 or q == 6272:  # a convolution state: 8 channels of an H x H image
+        hw = int(round((q // 8) ** 0.5))
+        p = L.problem("f32", "conv3x3", "relu", N=4, B=B, C=8, H=hw, W=hw, h=0.25)
+    else:
+        p = L.problem("f32", "dense", "relu", N=4, B=B, C=q, h=0.25)
     g = {k: torch.from_numpy(v).cuda() for k, v in dict(uN=uN, W=W, mu=mu, c=onehot).items()}
     J = torch.zeros(1, device="cuda", dtype=torch.float64)
     lamN, dW, dmu = torch.empty_like(g["uN"]), torch.empty_like(g["W"]), torch.empty_like(g["mu"])
