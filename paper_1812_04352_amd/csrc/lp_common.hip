@@ -4,6 +4,7 @@
 // outside the per-iteration hot path. The loss helper lives in lp_loss.hip.
 #include <math.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "lp_device.h"
@@ -15,13 +16,15 @@ namespace {
 constexpr int NT = 256;
 
 // X[dst_row0 + t*dst_step] = X[src_row] for t = 0..count-1 (16-byte units; the
-// source row is not among the destinations). Each thread reads its units of the
-// source row once and writes them to every destination row.
+// source row is not among the destinations). Workgroup row blockIdx.y takes
+// destination rows rows * blockIdx.y .. + rows - 1: each thread reads its units
+// of the source row once and writes them to those rows.
 __global__ __launch_bounds__(NT) void k_copy_rows(uint4* X, size_t units, long src_row,
-                                                  long dst_row0, long dst_step, long count) {
+                                                  long dst_row0, long dst_step, long count, long rows) {
+  const long t0 = (long)blockIdx.y * rows, t1 = min(count, t0 + rows);
   for (size_t u = (size_t)blockIdx.x * NT + threadIdx.x; u < units; u += (size_t)gridDim.x * NT) {
     const uint4 v = X[(size_t)src_row * units + u];
-    for (long t = 0; t < count; ++t) X[(size_t)(dst_row0 + t * dst_step) * units + u] = v;
+    for (long t = t0; t < t1; ++t) X[(size_t)(dst_row0 + t * dst_step) * units + u] = v;
   }
 }
 
@@ -234,7 +237,14 @@ hipError_t launch_copy_rows(void* X, size_t slice_bytes, long src_row, long dst_
                             long count, hipStream_t st) {
   if (count <= 0 || slice_bytes == 0) return hipSuccess;
   const size_t units = slice_bytes / 16;
-  k_copy_rows<<<grid_for(units), NT, 0, st>>>(static_cast<uint4*>(X), units, src_row, dst_row0, dst_step, count);
+  // about 8192 workgroups: the rows are split into groups when one row's
+  // workgroups are fewer
+  const unsigned gx = grid_for(units);
+  const long want = std::max<long>(1, std::min<long>(count, (8192 + gx - 1) / gx));
+  const long rows = (count + want - 1) / want, groups = (count + rows - 1) / rows;
+  if (groups > 65535) return hipErrorInvalidValue;  // the grid's y dimension
+  k_copy_rows<<<dim3(gx, (unsigned)groups), NT, 0, st>>>(static_cast<uint4*>(X), units, src_row, dst_row0,
+                                                         dst_step, count, rows);
   return hipGetLastError();
 }
 
