@@ -277,6 +277,37 @@ def test_gradient_and_loss_are_bitwise_reproducible(name, wl):
         assert torch.equal(a, b), n
 
 
+@pytest.mark.parametrize("name,wl", [DENSE[1], DENSE[2], DENSE[6], DENSE[7]],
+                         ids=[DENSE[i][0] for i in (1, 2, 6, 7)])
+def test_solves_are_bitwise_reproducible(name, wl):
+    """Two forward and two adjoint MGRIT solves from the same cold start give
+    bit-identical iterates and residual histories (Algorithm 1; the residual norms
+    are reduced in a fixed order), the second time with a workspace pre-filled with
+    NaN bytes. The conv cases run grids whose size is not a multiple of eight, the
+    uneven branch of the sweeps' workgroup order."""
+    c = case(wl)
+    mg = sched(wl, 2)
+    ws = L.alloc_workspace(c.p, mg)
+    rec = L.alloc_dsig(c.p) if L.lp_dsig_bytes(c.p) else None
+    outs = []
+    for t in range(2):
+        if t:
+            ws.fill_(0xFF)
+        U = c.new_traj()
+        _, hf = L.lp_mgrit_forward(c.p, mg, c.K, c.b, U, ws, history=True, dsig=rec)
+        J = torch.zeros(1, device="cuda", dtype=torch.float64)
+        Lam = torch.zeros_like(U)
+        dW, dmu = torch.empty_like(c.W), torch.empty_like(c.mu)
+        L.lp_loss_terminal(c.p, wl.n_classes, U[-1], c.W, c.mu, c.onehot, J, Lam[-1], dW, dmu, ws)
+        _, ha = L.lp_mgrit_adjoint(c.p, mg, c.K, c.b, U, Lam, ws, history=True, dsig=rec)
+        outs.append((U, Lam, list(hf), list(ha)))
+    (U0, L0, f0, a0), (U1, L1, f1, a1) = outs
+    assert torch.equal(U0, U1), "U"
+    assert torch.equal(L0, L1), "Lam"
+    assert f0 == f1 and a0 == a1, (f0, f1, a0, a1)
+    assert len(f0) == 2 and len(a0) == 2
+
+
 @pytest.mark.parametrize("name,wl", [DENSE[1], DENSE[2], DENSE[7]], ids=[DENSE[1][0], DENSE[2][0], DENSE[7][0]])
 def test_solves_without_history_match(name, wl):
     """With no residual history and no stopping rule the solves return without
